@@ -1,0 +1,111 @@
+"""Brute-force checks for tiny inputs -- TEST INFRASTRUCTURE ONLY.
+
+Two algorithms that differ from the sequential reference in ``hbf_oracle.c``
+and are used to pin it (they take the request->resource assignment as given;
+the address mapping is pinned separately):
+
+* :func:`time_stepped` advances a clock 1 ns at a time over the two-station
+  system (die read, then channel transfer).  Within a tick, completions are
+  processed before starts, so a resource freed at t can start a waiting
+  request at t and a page finishing its die read at t can start its channel
+  transfer at t.  Dies serve their queue first come first served by
+  (issue, index); channels by (arrival at the channel, index).
+* :func:`enumerate_orders` lists every service order of a single server with
+  identical service times and keeps the work-conserving ones: with identical
+  services they all share one multiset of departure epochs, and the
+  first-come-first-served order minimises the largest flow time.
+"""
+import itertools
+from collections import deque
+
+
+def time_stepped(issue, die_key, chan, t_read, xfer, die_free=None, chan_free=None):
+    """Return (die_done, complete) lists; ``None`` entries for die_key < 0.
+
+    ``die_free`` / ``chan_free``: dict resource -> time it is busy until
+    (missing = idle since minus infinity).
+    """
+    n = len(issue)
+    die_free = dict(die_free or {})
+    chan_free = dict(chan_free or {})
+    die_done = [None] * n
+    complete = [None] * n
+    live = [i for i in range(n) if die_key[i] >= 0]
+    if not live:
+        return die_done, complete
+    die_q, chan_q = {}, {}
+    die_job, chan_job = {}, {}      # resource -> (request, finish time)
+    pending = deque(sorted(live, key=lambda i: (issue[i], i)))
+    t = min(issue[i] for i in live)
+    left = len(live)
+    t_stop = t + 10 * (max(issue[i] for i in live) - t + 1) + (n + 2) * (t_read + xfer) * 4 \
+        + max(list(die_free.values()) + list(chan_free.values()) + [0])
+    while left:
+        if t > t_stop:
+            raise RuntimeError("time-stepped simulation did not drain")
+        # 1. die completions -> channel queue
+        for d, (i, fin) in list(die_job.items()):
+            if fin == t:
+                del die_job[d]
+                die_done[i] = t
+                chan_q.setdefault(chan[i], []).append((t, i))
+        # 2. channel completions
+        for c, (i, fin) in list(chan_job.items()):
+            if fin == t:
+                del chan_job[c]
+                complete[i] = t
+                left -= 1
+        # 3. arrivals
+        while pending and issue[pending[0]] == t:
+            i = pending.popleft()
+            die_q.setdefault(die_key[i], deque()).append(i)
+        # 4. die starts (FCFS by (issue, index): queue order)
+        for d, q in die_q.items():
+            if q and d not in die_job and die_free.get(d, t) <= t:
+                i = q.popleft()
+                die_job[d] = (i, t + t_read)
+        # 5. channel starts (FCFS by (arrival, index))
+        for c, q in chan_q.items():
+            if q and c not in chan_job and chan_free.get(c, t) <= t:
+                q.sort()
+                _, i = q.pop(0)
+                chan_job[c] = (i, t + xfer)
+        t += 1
+    return die_done, complete
+
+
+def single_server(order, arrival, service, free=None):
+    """Serve ``order`` on one server; returns (start, finish) dicts."""
+    start, finish = {}, {}
+    f = free
+    for i in order:
+        s = arrival[i] if f is None else max(arrival[i], f)
+        start[i], finish[i] = s, s + service
+        f = s + service
+    return start, finish
+
+
+def work_conserving(order, arrival, start, finish, free=None):
+    """True if the server never idles while an unserved request has arrived."""
+    prev_end = float("-inf") if free is None else free
+    for k, i in enumerate(order):
+        if start[i] > prev_end:
+            # idle in (prev_end, start): nobody unserved may have arrived before start
+            for j in order[k:]:
+                if arrival[j] < start[i]:
+                    return False
+        prev_end = finish[i]
+    return True
+
+
+def enumerate_orders(arrival, service, free=None):
+    """All work-conserving service orders of requests 0..n-1.
+
+    Returns a list of (order, finish-dict)."""
+    n = len(arrival)
+    out = []
+    for order in itertools.permutations(range(n)):
+        s, f = single_server(order, arrival, service, free)
+        if work_conserving(order, arrival, s, f, free):
+            out.append((order, f))
+    return out

@@ -1,0 +1,387 @@
+/*
+ * hbf_oracle.c -- plain, slow, sequential CPU reference of the HBF service
+ * model.  TEST INFRASTRUCTURE ONLY: nothing in the product path may link,
+ * load or call this file; only the test-suite, the smoke check and the
+ * benchmark's CPU-baseline leg do.  It shares no code, header, constant or
+ * table with the HIP implementation.
+ *
+ * What it computes (paper: HBFSim, arXiv 2609.09800):
+ *  - Explicit range registration and fail-closed classification of an
+ *    address against the sorted snapshot of registered ranges
+ *    (Section "D1: An Explicit and Fail-Closed Boundary").  An address
+ *    outside every range takes the native path: zero modeled delay.
+ *  - Each in-range access becomes one foreground media request (a page
+ *    read) that is timed by an online media model (Section "Design",
+ *    opening paragraph: each foreground request is placed into the online
+ *    media-model instance and its completion is returned to the request).
+ *    The paper delegates the media model to MQSim and publishes no timing
+ *    parameters (Section "Motivation": the specification defers every
+ *    time quantity to vendor datasheets).  This oracle therefore takes the
+ *    reading used throughout the project: a die-read stage (service tR,
+ *    FCFS in (issue, index) order, one queue per die) followed by a
+ *    channel-transfer stage (service xfer, FCFS in (die-done, index) order,
+ *    one queue per channel), both with infinite buffers and resource clocks
+ *    that persist across calls.
+ *
+ * Readings where the paper is silent (each is a documented choice):
+ *  - address -> device page: p = dev_page_base(range) + (addr-base)/page,
+ *    dev_page_base = pages of earlier-registered ranges, in registration
+ *    order.
+ *  - page -> (channel, die, plane, page-in-plane): channel-first striping,
+ *    ch = p mod C, die = (p / C) mod D, plane = (p / (C*D)) mod P,
+ *    pg = p / (C*D*P).
+ *  - die queue key = (ch, die); with the plane-parallel flag (ch, die, plane).
+ *  - xfer = ceil(page_bytes * 1e9 / channel_bytes_per_s) in integer ns.
+ *  - times are int64 ns; "idle since minus infinity" at create/reset.
+ *
+ * Every step below is written in the order the model defines it, with no
+ * blocking, fusion or reordering: validate, classify, map, die stage in
+ * request order, sort by (die_done, index), channel stage in that order.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <math.h>
+
+/* Status codes of the public contract (values fixed by the C ABI docs). */
+#define ORC_OK             0
+#define ORC_EINVAL        -1
+#define ORC_EALIGN        -2
+#define ORC_EOVERLAP      -3
+#define ORC_ENOWORKSPACE  -4
+#define ORC_EUNSORTED     -5
+#define ORC_ERANGE_TIME   -6
+#define ORC_EHIP          -7
+#define ORC_ENOMEM        -8
+
+#define ORC_TIME_ERROR    INT64_MIN
+#define ORC_FLAG_PLANE_PARALLEL 1u
+#define ORC_MAX_RANGES    64
+
+/* Issue times must lie in [0, 2^61); any modeled time reaching 2^62 is an
+ * overflow of the model's time domain and fails the whole call. */
+#define ORC_ISSUE_LIMIT   ((int64_t)1 << 61)
+#define ORC_TIME_LIMIT    ((int64_t)1 << 62)
+#define ORC_SERVICE_LIMIT ((int64_t)1 << 29)
+#define ORC_N_LIMIT       ((int64_t)1 << 31)
+
+typedef struct {
+  uint32_t channels, dies_per_channel, planes_per_die, page_bytes;
+  int64_t  t_read_ns;
+  uint64_t channel_bytes_per_s;
+  uint32_t flags;
+} orc_params;
+
+typedef struct {
+  uint64_t base, bytes, dev_page_base;
+} orc_range;
+
+typedef struct {
+  orc_params p;
+  int64_t xfer_ns;
+  int n_ranges;
+  orc_range ranges[ORC_MAX_RANGES];   /* in registration order */
+  uint64_t total_pages;
+  int64_t *die_free;    /* per die queue key; idle = has_die_free 0 */
+  uint8_t *die_busy;    /* 0 = idle since -inf */
+  int64_t *chan_free;
+  uint8_t *chan_busy;
+  uint32_t n_die_keys;
+} orc_model;
+
+uint32_t orc_n_die_keys(const orc_params *p) {
+  uint64_t k = (uint64_t)p->channels * p->dies_per_channel;
+  if (p->flags & ORC_FLAG_PLANE_PARALLEL) k *= p->planes_per_die;
+  return (uint32_t)k;
+}
+
+int orc_create(const orc_params *p, orc_model **out) {
+  if (!p || !out) return ORC_EINVAL;
+  if (p->channels == 0 || p->dies_per_channel == 0 || p->planes_per_die == 0) return ORC_EINVAL;
+  if (p->page_bytes == 0) return ORC_EINVAL;
+  if (p->t_read_ns < 1 || p->t_read_ns > ORC_SERVICE_LIMIT) return ORC_EINVAL;
+  if (p->channel_bytes_per_s == 0) return ORC_EINVAL;
+  if (p->flags & ~ORC_FLAG_PLANE_PARALLEL) return ORC_EINVAL;
+  if ((uint64_t)p->channels * p->dies_per_channel * p->planes_per_die > 65536u) return ORC_EINVAL;
+  /* transfer time: ceil(page_bytes * 1e9 / bytes_per_s), exact integers */
+  unsigned __int128 num = (unsigned __int128)p->page_bytes * 1000000000u;
+  unsigned __int128 q = (num + p->channel_bytes_per_s - 1) / p->channel_bytes_per_s;
+  if (q < 1 || q > (unsigned __int128)ORC_SERVICE_LIMIT) return ORC_EINVAL;
+  orc_model *m = (orc_model *)calloc(1, sizeof(orc_model));
+  if (!m) return ORC_ENOMEM;
+  m->p = *p;
+  m->xfer_ns = (int64_t)q;
+  m->n_die_keys = orc_n_die_keys(p);
+  m->die_free = (int64_t *)calloc(m->n_die_keys, sizeof(int64_t));
+  m->die_busy = (uint8_t *)calloc(m->n_die_keys, 1);
+  m->chan_free = (int64_t *)calloc(p->channels, sizeof(int64_t));
+  m->chan_busy = (uint8_t *)calloc(p->channels, 1);
+  if (!m->die_free || !m->die_busy || !m->chan_free || !m->chan_busy) {
+    free(m->die_free); free(m->die_busy); free(m->chan_free); free(m->chan_busy); free(m);
+    return ORC_ENOMEM;
+  }
+  *out = m;
+  return ORC_OK;
+}
+
+void orc_destroy(orc_model *m) {
+  if (!m) return;
+  free(m->die_free); free(m->die_busy); free(m->chan_free); free(m->chan_busy);
+  free(m);
+}
+
+int64_t orc_xfer_ns(const orc_model *m) { return m->xfer_ns; }
+
+/* Return every resource to "idle since minus infinity". */
+void orc_reset(orc_model *m) {
+  memset(m->die_busy, 0, m->n_die_keys);
+  memset(m->chan_busy, 0, m->p.channels);
+  memset(m->die_free, 0, sizeof(int64_t) * m->n_die_keys);
+  memset(m->chan_free, 0, sizeof(int64_t) * m->p.channels);
+}
+
+/* Range registration (Section D1): explicit [base, base+bytes) intervals,
+ * page aligned, never overlapping. */
+int orc_register_range(orc_model *m, uint64_t base, uint64_t bytes) {
+  if (!m || bytes == 0) return ORC_EINVAL;
+  if (m->n_ranges >= ORC_MAX_RANGES) return ORC_EINVAL;
+  if (base % m->p.page_bytes != 0 || bytes % m->p.page_bytes != 0) return ORC_EALIGN;
+  if (base + bytes < base) return ORC_EINVAL;             /* wraps past 2^64 */
+  for (int r = 0; r < m->n_ranges; r++) {
+    uint64_t b = m->ranges[r].base, e = m->ranges[r].base + m->ranges[r].bytes;
+    if (base < e && b < base + bytes) return ORC_EOVERLAP;
+  }
+  m->ranges[m->n_ranges].base = base;
+  m->ranges[m->n_ranges].bytes = bytes;
+  m->ranges[m->n_ranges].dev_page_base = m->total_pages;
+  m->total_pages += bytes / m->p.page_bytes;
+  m->n_ranges++;
+  return ORC_OK;
+}
+
+/* Classification (Section D1): the index of the range containing addr, or
+ * -1 for the native path.  A linear scan is the plain definition. */
+static int orc_classify(const orc_model *m, uint64_t addr) {
+  for (int r = 0; r < m->n_ranges; r++)
+    if (addr >= m->ranges[r].base && addr - m->ranges[r].base < m->ranges[r].bytes) return r;
+  return -1;
+}
+
+typedef struct { uint32_t ch, die, plane; uint64_t page; uint32_t key; } orc_loc;
+
+/* Device page and its (channel, die, plane, page) by channel-first striping. */
+static orc_loc orc_map(const orc_model *m, int r, uint64_t addr) {
+  const orc_params *p = &m->p;
+  uint64_t dp = m->ranges[r].dev_page_base + (addr - m->ranges[r].base) / p->page_bytes;
+  orc_loc L;
+  L.ch = (uint32_t)(dp % p->channels);
+  L.die = (uint32_t)((dp / p->channels) % p->dies_per_channel);
+  L.plane = (uint32_t)((dp / ((uint64_t)p->channels * p->dies_per_channel)) % p->planes_per_die);
+  L.page = dp / ((uint64_t)p->channels * p->dies_per_channel * p->planes_per_die);
+  L.key = L.ch * p->dies_per_channel + L.die;
+  if (p->flags & ORC_FLAG_PLANE_PARALLEL) L.key = L.key * p->planes_per_die + L.plane;
+  return L;
+}
+
+/* Packed classification word (documented format of hbf_classify_map):
+ * bit 63 in-range; bits 62..56 range index; 55..50 plane; 49..42 die;
+ * 41..32 channel; 31..0 page within the plane.  Out of range: 0. */
+static uint64_t orc_pack(int r, orc_loc L) {
+  return (1ull << 63) | ((uint64_t)r << 56) | ((uint64_t)L.plane << 50) |
+         ((uint64_t)L.die << 42) | ((uint64_t)L.ch << 32) | (L.page & 0xffffffffull);
+}
+
+int orc_classify_map(const orc_model *m, const uint64_t *addr, int64_t n, uint64_t *map_out) {
+  if (!m || n < 0 || (n > 0 && (!addr || !map_out))) return ORC_EINVAL;
+  const orc_params *p = &m->p;
+  if (p->channels > 1024 || p->dies_per_channel > 256 || p->planes_per_die > 64) return ORC_EINVAL;
+  for (int64_t i = 0; i < n; i++) {
+    int r = orc_classify(m, addr[i]);
+    if (r < 0) { map_out[i] = 0; continue; }
+    orc_loc L = orc_map(m, r, addr[i]);
+    if (L.page > 0xffffffffull) return ORC_EINVAL;
+    map_out[i] = orc_pack(r, L);
+  }
+  return ORC_OK;
+}
+
+typedef struct { int64_t dd; int64_t idx; } orc_pair;
+
+static int orc_cmp_pair(const void *a, const void *b) {
+  const orc_pair *x = (const orc_pair *)a, *y = (const orc_pair *)b;
+  if (x->dd != y->dd) return x->dd < y->dd ? -1 : 1;
+  if (x->idx != y->idx) return x->idx < y->idx ? -1 : 1;
+  return 0;
+}
+
+static int64_t orc_max(int64_t a, int64_t b) { return a > b ? a : b; }
+
+/*
+ * The timing call.  Steps, in the model's order:
+ *  1. validate every issue time (0 <= t < 2^61, nondecreasing in index);
+ *  2. classify + map every request;
+ *  3. die stage, requests in index order (= FCFS by (issue, index)):
+ *       start = max(issue, die_free), die_done = start + tR;
+ *  4. sort the in-range requests by (die_done, index);
+ *  5. channel stage in that order:
+ *       start = max(die_done, chan_free), complete = start + xfer;
+ *  6. out-of-range requests: complete = issue (native path, no delay).
+ * On a validation or time-domain error every output is ORC_TIME_ERROR and the
+ * resource clocks keep their values from before the call.
+ */
+int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, int64_t n,
+                      int64_t *complete) {
+  if (!m || n < 0 || n > ORC_N_LIMIT || (n > 0 && (!addr || !issue || !complete))) return ORC_EINVAL;
+  if (n == 0) return ORC_OK;
+  const orc_params *p = &m->p;
+  const int64_t tR = p->t_read_ns, xfer = m->xfer_ns;
+
+  /* 1. validation; a bad time range takes precedence over disorder */
+  int bad_range = 0, bad_order = 0;
+  for (int64_t i = 0; i < n; i++) {
+    if (issue[i] < 0 || issue[i] >= ORC_ISSUE_LIMIT) bad_range = 1;
+    if (i > 0 && issue[i] < issue[i - 1]) bad_order = 1;
+  }
+  if (bad_range || bad_order) {
+    for (int64_t i = 0; i < n; i++) complete[i] = ORC_TIME_ERROR;
+    return bad_range ? ORC_ERANGE_TIME : ORC_EUNSORTED;
+  }
+
+  /* working copies of the clocks: committed only if the call succeeds */
+  int64_t *df = (int64_t *)malloc(sizeof(int64_t) * m->n_die_keys);
+  uint8_t *db = (uint8_t *)malloc(m->n_die_keys);
+  int64_t *cf = (int64_t *)malloc(sizeof(int64_t) * p->channels);
+  uint8_t *cb = (uint8_t *)malloc(p->channels);
+  int64_t *dd = (int64_t *)malloc(sizeof(int64_t) * n);
+  uint32_t *chan = (uint32_t *)malloc(sizeof(uint32_t) * n);
+  int8_t *in = (int8_t *)malloc(n);
+  orc_pair *ord = (orc_pair *)malloc(sizeof(orc_pair) * n);
+  if (!df || !db || !cf || !cb || !dd || !chan || !in || !ord) {
+    free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord);
+    return ORC_ENOMEM;
+  }
+  memcpy(df, m->die_free, sizeof(int64_t) * m->n_die_keys);
+  memcpy(db, m->die_busy, m->n_die_keys);
+  memcpy(cf, m->chan_free, sizeof(int64_t) * p->channels);
+  memcpy(cb, m->chan_busy, p->channels);
+
+  int overflow = 0;
+  int64_t n_in = 0;
+  /* 2.+3. classify, map and serve each request at its die, in index order */
+  for (int64_t i = 0; i < n; i++) {
+    int r = orc_classify(m, addr[i]);
+    if (r < 0) { in[i] = 0; continue; }
+    in[i] = 1;
+    orc_loc L = orc_map(m, r, addr[i]);
+    int64_t start = db[L.key] ? orc_max(issue[i], df[L.key]) : issue[i];
+    dd[i] = start + tR;
+    if (dd[i] >= ORC_TIME_LIMIT) overflow = 1;
+    df[L.key] = dd[i];
+    db[L.key] = 1;
+    chan[i] = L.ch;
+    ord[n_in].dd = dd[i];
+    ord[n_in].idx = i;
+    n_in++;
+  }
+  /* 4. channel service order: by (die_done, index) */
+  qsort(ord, (size_t)n_in, sizeof(orc_pair), orc_cmp_pair);
+  /* 5. channel stage */
+  for (int64_t k = 0; k < n_in; k++) {
+    int64_t i = ord[k].idx;
+    uint32_t c = chan[i];
+    int64_t start = cb[c] ? orc_max(dd[i], cf[c]) : dd[i];
+    complete[i] = start + xfer;
+    if (complete[i] >= ORC_TIME_LIMIT) overflow = 1;
+    cf[c] = complete[i];
+    cb[c] = 1;
+  }
+  /* 6. native path */
+  for (int64_t i = 0; i < n; i++)
+    if (!in[i]) complete[i] = issue[i];
+
+  int rc = ORC_OK;
+  if (overflow) {
+    for (int64_t i = 0; i < n; i++) complete[i] = ORC_TIME_ERROR;
+    rc = ORC_ERANGE_TIME;
+  } else {
+    memcpy(m->die_free, df, sizeof(int64_t) * m->n_die_keys);
+    memcpy(m->die_busy, db, m->n_die_keys);
+    memcpy(m->chan_free, cf, sizeof(int64_t) * p->channels);
+    memcpy(m->chan_busy, cb, p->channels);
+  }
+  free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord);
+  return rc;
+}
+
+/* Die-stage completion times alone (a diagnostic used by the tests): the
+ * same step 3 as above, without touching the model's clocks.  Out-of-range
+ * requests get ORC_TIME_ERROR. */
+int orc_die_done(const orc_model *m, const uint64_t *addr, const int64_t *issue, int64_t n,
+                 int64_t *dd) {
+  if (!m || n < 0) return ORC_EINVAL;
+  int64_t *df = (int64_t *)malloc(sizeof(int64_t) * (m->n_die_keys ? m->n_die_keys : 1));
+  uint8_t *db = (uint8_t *)malloc(m->n_die_keys ? m->n_die_keys : 1);
+  if (!df || !db) { free(df); free(db); return ORC_ENOMEM; }
+  memcpy(df, m->die_free, sizeof(int64_t) * m->n_die_keys);
+  memcpy(db, m->die_busy, m->n_die_keys);
+  for (int64_t i = 0; i < n; i++) {
+    int r = orc_classify(m, addr[i]);
+    if (r < 0) { dd[i] = ORC_TIME_ERROR; continue; }
+    orc_loc L = orc_map(m, r, addr[i]);
+    int64_t start = db[L.key] ? orc_max(issue[i], df[L.key]) : issue[i];
+    dd[i] = start + m->p.t_read_ns;
+    df[L.key] = dd[i];
+    db[L.key] = 1;
+  }
+  free(df); free(db);
+  return ORC_OK;
+}
+
+/* Resource clocks, idle encoded as INT64_MIN (for state comparisons). */
+void orc_get_state(const orc_model *m, int64_t *die_free, int64_t *chan_free) {
+  for (uint32_t k = 0; k < m->n_die_keys; k++) die_free[k] = m->die_busy[k] ? m->die_free[k] : INT64_MIN;
+  for (uint32_t c = 0; c < m->p.channels; c++) chan_free[c] = m->chan_busy[c] ? m->chan_free[c] : INT64_MIN;
+}
+
+/* Restore resource clocks (checkpoint / resume of an online model).  Idle is
+ * INT64_MIN; any other value must lie in [0, 2^62). */
+int orc_set_state(orc_model *m, const int64_t *die_free, const int64_t *chan_free) {
+  for (uint32_t k = 0; k < m->n_die_keys; k++)
+    if (die_free[k] != INT64_MIN && (die_free[k] < 0 || die_free[k] >= ORC_TIME_LIMIT)) return ORC_EINVAL;
+  for (uint32_t c = 0; c < m->p.channels; c++)
+    if (chan_free[c] != INT64_MIN && (chan_free[c] < 0 || chan_free[c] >= ORC_TIME_LIMIT)) return ORC_EINVAL;
+  for (uint32_t k = 0; k < m->n_die_keys; k++) {
+    m->die_busy[k] = die_free[k] != INT64_MIN;
+    m->die_free[k] = m->die_busy[k] ? die_free[k] : 0;
+  }
+  for (uint32_t c = 0; c < m->p.channels; c++) {
+    m->chan_busy[c] = chan_free[c] != INT64_MIN;
+    m->chan_free[c] = m->chan_busy[c] ? chan_free[c] : 0;
+  }
+  return ORC_OK;
+}
+
+/* bf16 -> double, exact: a bf16 is the top 16 bits of an IEEE binary32. */
+static double orc_bf16(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+/* Grouped GEMV of the instrumented kernel, in double precision over the exact
+ * bf16 inputs:  Y[e][b][nn] = sum_k X[e][b][k] * W[e][nn][k].
+ * W is [E][N][K] (each output row's K weights contiguous), X is [E][B][K]. */
+int orc_gemv_bf16(const uint16_t *W, int E, int K, int N, const uint16_t *X, int B, double *Y) {
+  if (!W || !X || !Y || E <= 0 || K <= 0 || N <= 0 || B <= 0) return ORC_EINVAL;
+  for (int e = 0; e < E; e++)
+    for (int b = 0; b < B; b++)
+      for (int nn = 0; nn < N; nn++) {
+        const uint16_t *w = W + ((size_t)e * N + nn) * K;
+        const uint16_t *x = X + ((size_t)e * B + b) * K;
+        double s = 0.0;
+        for (int k = 0; k < K; k++) s += orc_bf16(x[k]) * orc_bf16(w[k]);
+        Y[((size_t)e * B + b) * N + nn] = s;
+      }
+  return ORC_OK;
+}

@@ -1,0 +1,192 @@
+"""ctypes front end of the plain C reference model (``hbf_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py`` may import this module.  It shares no
+code with the HIP implementation: it loads its own shared object, built from
+``hbf_oracle.c`` by :func:`build`, and defines its own constants.
+
+The model it exposes is the HBF service model of HBFSim (arXiv 2609.09800):
+registered address ranges with fail-closed classification (Section D1) and an
+online per-request media model (Section "Design"), read as a die-read queue
+followed by a channel-transfer queue.  See ``hbf_oracle.c`` for every reading.
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "hbf_oracle.c")
+LIB = os.path.join(HERE, "libhbf_oracle.so")
+
+OK, EINVAL, EALIGN, EOVERLAP, ENOWORKSPACE, EUNSORTED, ERANGE_TIME, EHIP, ENOMEM = (
+    0, -1, -2, -3, -4, -5, -6, -7, -8)
+TIME_ERROR = np.iinfo(np.int64).min
+FLAG_PLANE_PARALLEL = 1
+
+
+def build(force=False):
+    """Compile the oracle with gcc (-O2, single thread)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-shared", "-fPIC", SRC, "-o", LIB + ".tmp", "-lm"])
+        os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("channels", ctypes.c_uint32), ("dies_per_channel", ctypes.c_uint32),
+                ("planes_per_die", ctypes.c_uint32), ("page_bytes", ctypes.c_uint32),
+                ("t_read_ns", ctypes.c_int64), ("channel_bytes_per_s", ctypes.c_uint64),
+                ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        # HBF_ORACLE_LIB lets the mutation test load a deliberately broken copy
+        path = os.environ.get("HBF_ORACLE_LIB") or build()
+        lib = ctypes.CDLL(path)
+        vp, i64, u64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int
+        lib.orc_create.argtypes = [ctypes.POINTER(_Params), ctypes.POINTER(vp)]
+        lib.orc_create.restype = i32
+        lib.orc_destroy.argtypes = [vp]
+        lib.orc_destroy.restype = None
+        lib.orc_reset.argtypes = [vp]
+        lib.orc_reset.restype = None
+        lib.orc_xfer_ns.argtypes = [vp]
+        lib.orc_xfer_ns.restype = i64
+        lib.orc_register_range.argtypes = [vp, u64, u64]
+        lib.orc_register_range.restype = i32
+        lib.orc_classify_map.argtypes = [vp, vp, i64, vp]
+        lib.orc_classify_map.restype = i32
+        lib.orc_time_requests.argtypes = [vp, vp, vp, i64, vp]
+        lib.orc_time_requests.restype = i32
+        lib.orc_die_done.argtypes = [vp, vp, vp, i64, vp]
+        lib.orc_die_done.restype = i32
+        lib.orc_get_state.argtypes = [vp, vp, vp]
+        lib.orc_get_state.restype = None
+        lib.orc_set_state.argtypes = [vp, vp, vp]
+        lib.orc_set_state.restype = i32
+        lib.orc_n_die_keys.argtypes = [ctypes.POINTER(_Params)]
+        lib.orc_n_die_keys.restype = ctypes.c_uint32
+        lib.orc_gemv_bf16.argtypes = [vp, i32, i32, i32, vp, i32, vp]
+        lib.orc_gemv_bf16.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p) if a.size else None
+
+
+class OracleModel:
+    """One HBF device model: geometry, timing, ranges and resource clocks."""
+
+    def __init__(self, channels, dies_per_channel, planes_per_die, page_bytes, t_read_ns,
+                 channel_bytes_per_s, flags=0):
+        self._lib = _load()
+        self.params = _Params(channels, dies_per_channel, planes_per_die, page_bytes, t_read_ns,
+                              channel_bytes_per_s, flags)
+        h = ctypes.c_void_p()
+        rc = self._lib.orc_create(ctypes.byref(self.params), ctypes.byref(h))
+        if rc != OK:
+            raise ValueError(f"oracle: invalid parameters (status {rc})")
+        self._h = h
+
+    @classmethod
+    def try_create(cls, **kw):
+        """Return (status, model-or-None) instead of raising."""
+        try:
+            return OK, cls(**kw)
+        except ValueError as e:
+            return int(str(e).split("status ")[1].rstrip(")")), None
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._lib.orc_destroy(h)
+            self._h = None
+
+    @property
+    def xfer_ns(self):
+        return int(self._lib.orc_xfer_ns(self._h))
+
+    @property
+    def n_die_keys(self):
+        return int(self._lib.orc_n_die_keys(ctypes.byref(self.params)))
+
+    def reset(self):
+        self._lib.orc_reset(self._h)
+
+    def register_range(self, base, nbytes):
+        return int(self._lib.orc_register_range(self._h, base, nbytes))
+
+    def classify_map(self, addr):
+        addr = np.ascontiguousarray(addr, dtype=np.uint64)
+        out = np.zeros(addr.size, dtype=np.uint64)
+        rc = self._lib.orc_classify_map(self._h, _ptr(addr), addr.size, _ptr(out))
+        return rc, out
+
+    def time_requests(self, addr, issue):
+        addr = np.ascontiguousarray(addr, dtype=np.uint64)
+        issue = np.ascontiguousarray(issue, dtype=np.int64)
+        assert addr.size == issue.size
+        out = np.zeros(addr.size, dtype=np.int64)
+        rc = self._lib.orc_time_requests(self._h, _ptr(addr), _ptr(issue), addr.size, _ptr(out))
+        return rc, out
+
+    def die_done(self, addr, issue):
+        addr = np.ascontiguousarray(addr, dtype=np.uint64)
+        issue = np.ascontiguousarray(issue, dtype=np.int64)
+        out = np.zeros(addr.size, dtype=np.int64)
+        rc = self._lib.orc_die_done(self._h, _ptr(addr), _ptr(issue), addr.size, _ptr(out))
+        assert rc == OK
+        return out
+
+    def state(self):
+        """(die_free[keys], chan_free[channels]); idle clocks read INT64_MIN."""
+        d = np.zeros(self.n_die_keys, dtype=np.int64)
+        c = np.zeros(self.params.channels, dtype=np.int64)
+        self._lib.orc_get_state(self._h, _ptr(d), _ptr(c))
+        return d, c
+
+
+    def set_state(self, die_free, chan_free):
+        d = np.ascontiguousarray(die_free, dtype=np.int64)
+        c = np.ascontiguousarray(chan_free, dtype=np.int64)
+        assert d.size == self.n_die_keys and c.size == self.params.channels
+        return int(self._lib.orc_set_state(self._h, _ptr(d), _ptr(c)))
+
+
+def gemv_bf16(W, X):
+    """fp64 grouped GEMV over exact bf16 inputs.
+
+    W: uint16 bf16 bits [E, N, K]; X: uint16 bf16 bits [E, B, K] -> float64 [E, B, N].
+    """
+    lib = _load()
+    W = np.ascontiguousarray(W, dtype=np.uint16)
+    X = np.ascontiguousarray(X, dtype=np.uint16)
+    E, N, K = W.shape
+    E2, B, K2 = X.shape
+    assert E == E2 and K == K2
+    Y = np.zeros((E, B, N), dtype=np.float64)
+    rc = lib.orc_gemv_bf16(_ptr(W), E, K, N, _ptr(X), B, _ptr(Y))
+    assert rc == OK
+    return Y
+
+
+def unpack_map(m):
+    """Split the packed classification words into named fields."""
+    m = np.asarray(m, dtype=np.uint64)
+    return {
+        "in_range": (m >> np.uint64(63)).astype(bool),
+        "range": ((m >> np.uint64(56)) & np.uint64(0x7f)).astype(np.int64),
+        "plane": ((m >> np.uint64(50)) & np.uint64(0x3f)).astype(np.int64),
+        "die": ((m >> np.uint64(42)) & np.uint64(0xff)).astype(np.int64),
+        "channel": ((m >> np.uint64(32)) & np.uint64(0x3ff)).astype(np.int64),
+        "page": (m & np.uint64(0xffffffff)).astype(np.int64),
+    }

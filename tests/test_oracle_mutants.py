@@ -1,0 +1,72 @@
+"""Mutation test of the reference model's pins (CPU only).
+
+Each case plants one plausible mistake into a private copy of
+``oracle/hbf_oracle.c`` (a dropped term, a wrong index, a transposed
+operand, a reversed tie-break ...), builds it, and runs the pin suite
+against it.  The pins must fail for every mutant; the unmodified source must
+pass (that is ``test_oracle_pins.py`` itself).
+"""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "hbf_oracle.c")
+
+MUTANTS = {
+    "die-ignores-busy-die": (
+        "int64_t start = db[L.key] ? orc_max(issue[i], df[L.key]) : issue[i];\n    dd[i] = start + tR;",
+        "int64_t start = issue[i];\n    dd[i] = start + tR;"),
+    "channel-tie-reversed": (
+        "if (x->idx != y->idx) return x->idx < y->idx ? -1 : 1;",
+        "if (x->idx != y->idx) return x->idx < y->idx ? 1 : -1;"),
+    "channel-uses-issue": (
+        "int64_t start = cb[c] ? orc_max(dd[i], cf[c]) : dd[i];",
+        "int64_t start = cb[c] ? orc_max(issue[i], cf[c]) : issue[i];"),
+    "map-transposed": (
+        "L.ch = (uint32_t)(dp % p->channels);\n  L.die = (uint32_t)((dp / p->channels) % p->dies_per_channel);",
+        "L.die = (uint32_t)(dp % p->dies_per_channel);\n  L.ch = (uint32_t)((dp / p->dies_per_channel) % p->channels);"),
+    "xfer-floor": (
+        "unsigned __int128 q = (num + p->channel_bytes_per_s - 1) / p->channel_bytes_per_s;",
+        "unsigned __int128 q = num / p->channel_bytes_per_s;"),
+    "native-path-delayed": (
+        "if (!in[i]) complete[i] = issue[i];",
+        "if (!in[i]) complete[i] = issue[i] + tR;"),
+    "range-end-inclusive": (
+        "addr - m->ranges[r].base < m->ranges[r].bytes) return r;",
+        "addr - m->ranges[r].base <= m->ranges[r].bytes) return r;"),
+    "dev-page-base-dropped": (
+        "uint64_t dp = m->ranges[r].dev_page_base + (addr - m->ranges[r].base) / p->page_bytes;",
+        "uint64_t dp = (addr - m->ranges[r].base) / p->page_bytes;"),
+    "plane-flag-ignored": (
+        "if (p->flags & ORC_FLAG_PLANE_PARALLEL) L.key = L.key * p->planes_per_die + L.plane;",
+        "if (p->flags & ORC_FLAG_PLANE_PARALLEL) L.key = L.key * p->planes_per_die;"),
+    "unsorted-not-detected": (
+        "if (i > 0 && issue[i] < issue[i - 1]) bad_order = 1;",
+        "if (i > 1 && issue[i] < issue[i - 2]) bad_order = 1;"),
+    "state-not-committed": (
+        "memcpy(m->chan_free, cf, sizeof(int64_t) * p->channels);",
+        "(void)cf;"),
+    "extra-service-term": (
+        "complete[i] = start + xfer;",
+        "complete[i] = start + xfer + (start > dd[i] ? 1 : 0);"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(tmp_path, name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique/present: {name}"
+    mut = tmp_path / "mutant.c"
+    mut.write_text(src.replace(old, new))
+    lib = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O1", "-std=gnu11", "-shared", "-fPIC", str(mut), "-o", str(lib), "-lm"])
+    env = dict(os.environ, HBF_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
