@@ -1,0 +1,217 @@
+/*
+ * hbf.h -- C ABI of the MI355X (gfx950) HBF service-model hot path.
+ *
+ * HBFSim (arXiv 2609.09800) models High-Bandwidth Flash under real GPU
+ * execution: applications register HBF address ranges, every access is
+ * classified against them, and each in-range access is given a modeled
+ * completion time by an online media model; the running kernel pays that
+ * delay where it first consumes the value.  This library implements that
+ * path as batch calls on device arrays:
+ *
+ *   hbf_register_range   -- explicit ranges (Section "D1: An Explicit and
+ *                           Fail-Closed Boundary")
+ *   hbf_classify_map     -- classification + page-geometry mapping (D1)
+ *   hbf_time_requests    -- modeled completion of every request (Section
+ *                           "Design": each foreground request enters the
+ *                           online media model and its completion returns to
+ *                           that request)
+ *   hbf_gemv_instrumented-- a bf16 grouped GEMV whose weight pages wait for
+ *                           their modeled completion at the point of
+ *                           consumption (Section "D2: Preserving GPU
+ *                           Asynchrony")
+ *
+ * Timing model.  The paper leaves the media model to MQSim and publishes no
+ * HBF timing parameters, so this library fixes one reading and documents
+ * it: each request is a one-page read that first occupies its die for
+ * t_read_ns (FCFS by (issue time, request index)) and then its channel for
+ * xfer_ns = ceil(page_bytes * 1e9 / channel_bytes_per_s) (FCFS by (die-done
+ * time, request index)).  Buffers between the stages are unbounded.  Pages
+ * are striped channel-first: for device page p, ch = p mod C,
+ * die = (p / C) mod D, plane = (p / (C*D)) mod P, page = p / (C*D*P).
+ * Device pages number the registered ranges in registration order.  The die
+ * queue is (ch, die), or (ch, die, plane) with HBF_FLAG_PLANE_PARALLEL.
+ * All times are int64 nanoseconds; results are exact integers.
+ *
+ * Conventions for every call:
+ *  - Pointers named dev_* / device arrays live in GPU memory of the current
+ *    HIP device; host_* pointers are host memory.  The caller owns every
+ *    array it passes; the library never frees caller memory.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls that
+ *    launch work are asynchronous on that stream and return once enqueued.
+ *  - Host-detectable errors return a negative code before any launch and
+ *    leave every output untouched.
+ *  - Device-detected errors (bad issue times, time-domain overflow) are
+ *    fail-closed: every complete_ns[i] of that call is written as
+ *    HBF_TIME_ERROR before the error is recorded, resource clocks keep their
+ *    values from before the call, and hbf_get_status() reports the error.
+ *  - A model handle is not thread-safe; calls on one handle must be ordered
+ *    on one stream (or externally synchronised).
+ */
+#ifndef HBF_H_
+#define HBF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define HBF_OK             0
+#define HBF_EINVAL        -1  /* invalid argument or parameter */
+#define HBF_EALIGN        -2  /* range not page aligned / not a page multiple */
+#define HBF_EOVERLAP      -3  /* range overlaps a registered range */
+#define HBF_ENOWORKSPACE  -4  /* caller workspace smaller than hbf_workspace_bytes */
+#define HBF_EUNSORTED     -5  /* issue_ns decreases somewhere (device-detected) */
+#define HBF_ERANGE_TIME   -6  /* issue_ns outside [0, 2^61) or a modeled time
+                                 reached 2^62 (device-detected) */
+#define HBF_EHIP          -7  /* a HIP runtime call failed */
+#define HBF_ENOMEM        -8  /* host or device allocation failed */
+
+/* complete_ns value written for every request of a failed call. */
+#define HBF_TIME_ERROR    INT64_MIN
+
+/* hbf_params.flags */
+#define HBF_FLAG_PLANE_PARALLEL 1u  /* die queues keyed by (ch, die, plane) */
+
+typedef struct hbf_model *hbf_model_t;  /* opaque, owned by the library */
+
+/* Device geometry and timing.  All integers: there is no floating point on
+ * the timing path. */
+typedef struct {
+  uint32_t channels;          /* C, 1..1024 */
+  uint32_t dies_per_channel;  /* D, 1..256 */
+  uint32_t planes_per_die;    /* P, 1..64 */
+  uint32_t page_bytes;        /* bytes per page (one request reads one page) */
+  int64_t  t_read_ns;         /* tR, die read time, 1..2^29 */
+  uint64_t channel_bytes_per_s; /* channel bandwidth in bytes/s (decimal GB) */
+  uint32_t flags;             /* HBF_FLAG_* */
+} hbf_params;
+
+/* Create a model.  Validates `params` entirely on the host (C*D*P <= 65536,
+ * die queues per channel <= 64, die queues <= 2048, xfer_ns in 1..2^29) and
+ * returns HBF_EINVAL
+ * without touching the GPU if they are invalid.  Resource clocks start
+ * "idle since minus infinity".  Device state is allocated on the current
+ * HIP device at the first call that needs it.  *out receives the handle. */
+int hbf_model_create(const hbf_params *params, hbf_model_t *out);
+
+/* Release the model and everything the library allocated for it.  Waits for
+ * the model's outstanding work. NULL is ignored. */
+void hbf_model_destroy(hbf_model_t model);
+
+/* Derived channel transfer time per page, in ns (host query, no GPU). */
+int hbf_xfer_ns(hbf_model_t model, int64_t *xfer_ns);
+
+/* Number of die queues: C*D, or C*D*P with HBF_FLAG_PLANE_PARALLEL. */
+int hbf_n_die_queues(hbf_model_t model, uint32_t *n);
+
+/* Return every resource clock to "idle since minus infinity" (enqueued on
+ * `stream`). */
+int hbf_model_reset(hbf_model_t model, void *stream);
+
+/* Register the address interval [base, base+bytes) as an HBF range
+ * (Section D1).  base and bytes must be multiples of page_bytes
+ * (HBF_EALIGN), bytes > 0, the interval must not wrap 2^64 (HBF_EINVAL) and
+ * must not overlap a registered range (HBF_EOVERLAP).  At most 64 ranges.
+ * The range's device pages follow those of earlier-registered ranges.
+ * Registration takes effect for calls made after it returns (the device
+ * sees an immutable snapshot per call).  Host only; *range_id (nullable)
+ * receives the registration index. */
+int hbf_register_range(hbf_model_t model, uint64_t base, uint64_t bytes, int32_t *range_id);
+
+/* Device scratch needed by hbf_time_requests for n requests, in bytes. */
+int hbf_workspace_bytes(hbf_model_t model, int64_t n, size_t *bytes);
+
+/* Use caller-owned device memory dev_ptr[0..bytes) as scratch (it must stay
+ * valid while calls that use it run; pass NULL, 0 to go back to
+ * library-owned scratch, which the library allocates and grows itself).
+ * A later hbf_time_requests whose need exceeds `bytes` returns
+ * HBF_ENOWORKSPACE. */
+int hbf_set_workspace(hbf_model_t model, void *dev_ptr, size_t bytes);
+
+/* Classification and page mapping of n addresses (Section D1).
+ * dev_addr: uint64[n] byte addresses (device).  dev_map_out: uint64[n]
+ * (device), one packed word per address:
+ *   bit 63      1 = inside a registered range, 0 = native path (word is 0)
+ *   bits 62..56 range index (registration order)
+ *   bits 55..50 plane, bits 49..42 die, bits 41..32 channel
+ *   bits 31..0  page index within the plane
+ * Requires C <= 1024, D <= 256, P <= 64 and page index < 2^32 (HBF_EINVAL
+ * if a page index overflows: detected on the device, reported by
+ * hbf_get_status, that element's word is 0).  n may be 0. */
+int hbf_classify_map(hbf_model_t model, const uint64_t *dev_addr, int64_t n, uint64_t *dev_map_out,
+                     void *stream);
+
+/* Modeled completion time of n page-read requests.
+ * dev_addr: uint64[n] byte addresses; dev_issue_ns: int64[n] issue times,
+ * nondecreasing in index, each in [0, 2^61); dev_complete_ns: int64[n]
+ * output (all device memory, 0 <= n <= 2^31).  In-range requests get the
+ * completion of the die-read + channel-transfer model above; requests
+ * outside every range get complete = issue (native path, no modeled delay).
+ * Resource clocks persist across calls and a call is a barrier: every
+ * request of a call is served at its die and channel before any request of
+ * a later call.  Device-detected errors: HBF_EUNSORTED, HBF_ERANGE_TIME
+ * (fail-closed, see above).  Returns HBF_OK once enqueued. */
+int hbf_time_requests(hbf_model_t model, const uint64_t *dev_addr, const int64_t *dev_issue_ns,
+                      int64_t n, int64_t *dev_complete_ns, void *stream);
+
+/* Instrumented grouped GEMV with delay injection at consumption
+ * (Section D2: issue is split from consumption; the wait sits at the first
+ * use of the loaded value).
+ *   Y[e][b][nn] = sum_k X[e][b][k] * W[e][nn][k]   (fp32 accumulate)
+ * dev_W: bf16 bits [E][N][K] (each output row's K weights contiguous),
+ *   lying inside one registered range, page aligned;  dev_X: bf16 bits
+ *   [E][B][K] (16-byte aligned);  dev_Y: float [E][B][N].  K must be a
+ *   multiple of 512, at most 4096, with 2*K dividing page_bytes, at most
+ *   16 rows per page, and N a multiple of the rows per page.
+ * dev_page_issue_ns / dev_page_complete_ns: int64 per weight page
+ *   (E*N*K*2 / page_bytes entries, page order of W), e.g. from
+ *   hbf_time_requests.  Page q's consumer waits until
+ *   (complete[q] - issue[q]) ns have elapsed since its loads were issued,
+ *   measured on the GPU's constant-rate wall clock.  Both NULL: no delay.
+ *   A page delay above 1 s is clamped to 1 s and reported as
+ *   HBF_ERANGE_TIME by hbf_get_status (the GPU never spins longer).
+ * dev_measured_delay_ns (nullable): int64 per page, the delay the
+ *   consumer actually waited (wall-clock ticks * tick length), for
+ *   injection-fidelity checks.
+ * 1 <= B <= 64, E >= 1. */
+int hbf_gemv_instrumented(hbf_model_t model, const uint16_t *dev_W, int E, int K, int N,
+                          const uint16_t *dev_X, int B, float *dev_Y,
+                          const int64_t *dev_page_issue_ns, const int64_t *dev_page_complete_ns,
+                          int64_t *dev_measured_delay_ns, void *stream);
+
+/* Wall-clock tick of the delay injection, in picoseconds (10,000 for a
+ * 100 MHz counter).  Needs the GPU. */
+int hbf_wall_clock_tick_ps(hbf_model_t model, int64_t *tick_ps);
+
+/* Synchronise `stream`, then return and clear the sticky device status:
+ * HBF_OK, HBF_ERANGE_TIME, HBF_EUNSORTED or HBF_EINVAL (in that order of
+ * precedence). */
+int hbf_get_status(hbf_model_t model, void *stream);
+
+/* Copy the resource clocks to host memory after synchronising `stream`:
+ * host_die_free[n_die_queues], host_chan_free[channels]; an idle clock
+ * reads INT64_MIN.  Either pointer may be NULL. */
+int hbf_get_state(hbf_model_t model, int64_t *host_die_free, int64_t *host_chan_free, void *stream);
+
+/* Restore clocks saved by hbf_get_state (checkpoint / resume).  Each value
+ * is INT64_MIN (idle) or in [0, 2^62), else HBF_EINVAL.  Synchronous. */
+int hbf_set_state(hbf_model_t model, const int64_t *host_die_free, const int64_t *host_chan_free,
+                  void *stream);
+
+/* Per-kernel timing of hbf_time_requests (diagnostics).  When enabled, each
+ * call records HIP events between its kernels on its stream;
+ * hbf_kernel_times synchronises and returns the durations (ms) of the last
+ * call's kernels in launch order and their names. */
+int hbf_profile(hbf_model_t model, int enable);
+int hbf_kernel_times(hbf_model_t model, float *host_ms, const char **host_names, int max, int *count);
+
+/* Static string for a status code. */
+const char *hbf_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HBF_H_ */

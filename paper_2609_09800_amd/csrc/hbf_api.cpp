@@ -1,0 +1,400 @@
+// C ABI of the HBF hot path: argument validation, range snapshots,
+// workspace management and kernel orchestration.  No torch types; the caller
+// passes device pointers and a hipStream_t.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "hbf.h"
+#include "hbf_internal.h"
+
+namespace hbf {
+hipError_t set_lds_limits(uint32_t K);
+
+static size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
+
+Layout make_layout(const Geo &g, int64_t n) {
+  Layout L{};
+  L.n = n;
+  int64_t te = (n + TARGET_TILES - 1) / TARGET_TILES;
+  te = ((te + CHUNK - 1) / CHUNK) * CHUNK;
+  if (te < CHUNK) te = CHUNK;
+  L.tile_elems = te;
+  L.nt = (uint32_t)((n + te - 1) / te);
+  if (L.nt == 0) L.nt = 1;
+  // cell width 2^s0 <= Ts * tR keeps a cell at <= Ts requests per die queue
+  int64_t Ts = MCAP / (2 * (int64_t)g.Dk);
+  if (Ts < 1) Ts = 1;
+  const int64_t w = Ts * g.tR;
+  uint32_t s0 = 0;
+  while ((int64_t(1) << (s0 + 1)) <= w) s0++;
+  L.s0 = s0;
+  const int64_t per = (int64_t)g.C * g.Dk * Ts;
+  int64_t gm = 4 * ((n + per - 1) / per);
+  if (gm < 64) gm = 64;
+  L.gmax = (uint32_t)gm;
+  const size_t K = g.K, nt = L.nt, C = g.C;
+  size_t o = 0;
+  L.off_ctl = o;      o = up256(o + sizeof(CallCtl));
+  L.off_agg_cnt = o;  o = up256(o + nt * K * 4);
+  L.off_agg_A = o;    o = up256(o + nt * K * 8);
+  L.off_tin_L = o;    o = up256(o + nt * K * 8);
+  L.off_tin_base = o; o = up256(o + nt * K * 4);
+  L.off_totals = o;   o = up256(o + K * 4);
+  L.off_seg = o;      o = up256(o + K * 4);
+  L.off_dfnew = o;    o = up256(o + K * 8);
+  L.off_cfnew = o;    o = up256(o + C * 8);
+  L.off_dd = o;       o = up256(o + (size_t)n * 8);
+  L.off_ix = o;       o = up256(o + (size_t)n * 4);
+  L.off_lb = o;       o = up256(o + C * ((size_t)L.gmax + 1) * g.Dk * 4);
+  L.off_st_agg = o;   o = up256(o + C * (size_t)L.gmax * 8);
+  L.off_st_incl = o;  o = up256(o + C * (size_t)L.gmax * 8);
+  L.total = o;
+  return L;
+}
+}  // namespace hbf
+
+using namespace hbf;
+
+struct hbf_model {
+  hbf_params p;
+  Geo g;
+  std::vector<uint64_t> rbase, rbytes, rpbase;  // registration order
+  uint64_t total_pages = 0;
+  int dev = -1;
+  DevState *st = nullptr;
+  void *ws = nullptr;
+  size_t ws_cap = 0;
+  bool ws_caller = false;
+  bool lib_ws = false;
+  bool prof = false;
+  bool prof_valid = false;
+  hipEvent_t ev[16] = {};
+  int ncu = 0;
+  int64_t tick_ps = 0;
+};
+
+static bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
+static uint32_t lg2(uint64_t x) {
+  uint32_t r = 0;
+  while ((uint64_t(1) << r) < x) r++;
+  return r;
+}
+
+static int ensure_device(hbf_model *m) {
+  if (m->st) return HBF_OK;
+  if (hipGetDevice(&m->dev) != hipSuccess) return HBF_EHIP;
+  void *p = nullptr;
+  if (hipMalloc(&p, sizeof(DevState)) != hipSuccess) return HBF_ENOMEM;
+  m->st = (DevState *)p;
+  std::vector<DevState> host(1);
+  for (int k = 0; k < MAX_KEYS; k++) host[0].die_free[k] = NEG;
+  for (int c = 0; c < MAX_CHANNELS; c++) host[0].chan_free[c] = NEG;
+  host[0].sticky = 0;
+  host[0].pad = 0;
+  if (hipMemcpy(m->st, host.data(), sizeof(DevState), hipMemcpyHostToDevice) != hipSuccess) return HBF_EHIP;
+  if (set_lds_limits(m->g.K) != hipSuccess) return HBF_EHIP;
+  if (hipDeviceGetAttribute(&m->ncu, hipDeviceAttributeMultiprocessorCount, m->dev) != hipSuccess)
+    return HBF_EHIP;
+  int rate_khz = 0;
+  if (hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, m->dev) != hipSuccess ||
+      rate_khz <= 0)
+    return HBF_EHIP;
+  m->tick_ps = 1000000000LL / rate_khz;
+  return HBF_OK;
+}
+
+static RangeTable snapshot(const hbf_model *m) {
+  RangeTable rt;
+  std::memset(&rt, 0, sizeof(rt));
+  const int n = (int)m->rbase.size();
+  std::vector<int> idx(n);
+  for (int i = 0; i < n; i++) idx[i] = i;
+  std::sort(idx.begin(), idx.end(), [&](int a, int b) { return m->rbase[a] < m->rbase[b]; });
+  for (int i = 0; i < n; i++) {
+    rt.base[i] = m->rbase[idx[i]];
+    rt.bytes[i] = m->rbytes[idx[i]];
+    rt.pbase[i] = m->rpbase[idx[i]];
+    rt.rid[i] = (uint32_t)idx[i];
+  }
+  rt.n = n;
+  return rt;
+}
+
+extern "C" {
+
+int hbf_model_create(const hbf_params *params, hbf_model_t *out) {
+  if (!params || !out) return HBF_EINVAL;
+  const hbf_params &p = *params;
+  if (p.channels < 1 || p.channels > 1024) return HBF_EINVAL;
+  if (p.dies_per_channel < 1 || p.dies_per_channel > 256) return HBF_EINVAL;
+  if (p.planes_per_die < 1 || p.planes_per_die > 64) return HBF_EINVAL;
+  if (p.page_bytes == 0) return HBF_EINVAL;
+  if (p.t_read_ns < 1 || p.t_read_ns > SERVICE_LIMIT) return HBF_EINVAL;
+  if (p.channel_bytes_per_s == 0) return HBF_EINVAL;
+  if (p.flags & ~HBF_FLAG_PLANE_PARALLEL) return HBF_EINVAL;
+  const uint64_t cdp = (uint64_t)p.channels * p.dies_per_channel * p.planes_per_die;
+  if (cdp > 65536) return HBF_EINVAL;
+  const bool pp = (p.flags & HBF_FLAG_PLANE_PARALLEL) != 0;
+  const uint64_t Dk = (uint64_t)p.dies_per_channel * (pp ? p.planes_per_die : 1);
+  const uint64_t K = (uint64_t)p.channels * Dk;
+  if (Dk > MAX_RUNS || K > MAX_KEYS) return HBF_EINVAL;
+  const unsigned __int128 num = (unsigned __int128)p.page_bytes * 1000000000u;
+  const unsigned __int128 q = (num + p.channel_bytes_per_s - 1) / p.channel_bytes_per_s;
+  if (q < 1 || q > (unsigned __int128)SERVICE_LIMIT) return HBF_EINVAL;
+  hbf_model *m = new (std::nothrow) hbf_model();
+  if (!m) return HBF_ENOMEM;
+  m->p = p;
+  Geo &g = m->g;
+  g.C = p.channels;
+  g.D = p.dies_per_channel;
+  g.P = p.planes_per_die;
+  g.Dk = (uint32_t)Dk;
+  g.K = (uint32_t)K;
+  g.page_bytes = p.page_bytes;
+  g.plane_parallel = pp;
+  g.pow2 = is_pow2(p.page_bytes) && is_pow2(p.channels) && is_pow2(p.dies_per_channel) &&
+           is_pow2(p.planes_per_die);
+  g.lg_page = lg2(p.page_bytes);
+  g.lg_C = lg2(p.channels);
+  g.lg_D = lg2(p.dies_per_channel);
+  g.lg_P = lg2(p.planes_per_die);
+  g.tR = p.t_read_ns;
+  g.xfer = (int64_t)q;
+  *out = m;
+  return HBF_OK;
+}
+
+void hbf_model_destroy(hbf_model_t m) {
+  if (!m) return;
+  if (m->st) {
+    hipDeviceSynchronize();
+    hipFree(m->st);
+  }
+  if (m->ws && m->lib_ws) hipFree(m->ws);
+  for (auto &e : m->ev)
+    if (e) hipEventDestroy(e);
+  delete m;
+}
+
+int hbf_xfer_ns(hbf_model_t m, int64_t *x) {
+  if (!m || !x) return HBF_EINVAL;
+  *x = m->g.xfer;
+  return HBF_OK;
+}
+
+int hbf_n_die_queues(hbf_model_t m, uint32_t *n) {
+  if (!m || !n) return HBF_EINVAL;
+  *n = m->g.K;
+  return HBF_OK;
+}
+
+int hbf_model_reset(hbf_model_t m, void *stream) {
+  if (!m) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  return launch_reset(m->st, (hipStream_t)stream) == hipSuccess ? HBF_OK : HBF_EHIP;
+}
+
+int hbf_register_range(hbf_model_t m, uint64_t base, uint64_t bytes, int32_t *range_id) {
+  if (!m || bytes == 0) return HBF_EINVAL;
+  if ((int)m->rbase.size() >= MAX_RANGES) return HBF_EINVAL;
+  if (base % m->p.page_bytes || bytes % m->p.page_bytes) return HBF_EALIGN;
+  if (base + bytes < base) return HBF_EINVAL;
+  for (size_t r = 0; r < m->rbase.size(); r++) {
+    const uint64_t b = m->rbase[r], e = b + m->rbytes[r];
+    if (base < e && b < base + bytes) return HBF_EOVERLAP;
+  }
+  if (range_id) *range_id = (int32_t)m->rbase.size();
+  m->rbase.push_back(base);
+  m->rbytes.push_back(bytes);
+  m->rpbase.push_back(m->total_pages);
+  m->total_pages += bytes / m->p.page_bytes;
+  return HBF_OK;
+}
+
+int hbf_workspace_bytes(hbf_model_t m, int64_t n, size_t *bytes) {
+  if (!m || !bytes || n < 0 || n > N_LIMIT) return HBF_EINVAL;
+  *bytes = make_layout(m->g, n).total;
+  return HBF_OK;
+}
+
+int hbf_set_workspace(hbf_model_t m, void *dev_ptr, size_t bytes) {
+  if (!m) return HBF_EINVAL;
+  if ((dev_ptr == nullptr) != (bytes == 0)) return HBF_EINVAL;
+  if ((uintptr_t)dev_ptr % 256) return HBF_EINVAL;
+  if (m->ws && m->lib_ws) {
+    hipDeviceSynchronize();
+    hipFree(m->ws);
+  }
+  m->ws = dev_ptr;
+  m->ws_cap = bytes;
+  m->ws_caller = dev_ptr != nullptr;
+  m->lib_ws = false;
+  return HBF_OK;
+}
+
+int hbf_classify_map(hbf_model_t m, const uint64_t *addr, int64_t n, uint64_t *map, void *stream) {
+  if (!m || n < 0 || n > N_LIMIT || (n > 0 && (!addr || !map))) return HBF_EINVAL;
+  if (m->g.C > 1024 || m->g.D > 256 || m->g.P > 64) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  if (n == 0) return HBF_OK;
+  RangeTable rt = snapshot(m);
+  return launch_classify(m->g, rt, m->st, addr, n, map, (hipStream_t)stream) == hipSuccess ? HBF_OK
+                                                                                         : HBF_EHIP;
+}
+
+int hbf_time_requests(hbf_model_t m, const uint64_t *addr, const int64_t *issue, int64_t n,
+                      int64_t *complete, void *stream) {
+  if (!m || n < 0 || n > N_LIMIT || (n > 0 && (!addr || !issue || !complete))) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  m->prof_valid = false;
+  if (n == 0) return HBF_OK;
+  const Layout L = make_layout(m->g, n);
+  if (m->ws_caller) {
+    if (m->ws_cap < L.total) return HBF_ENOWORKSPACE;
+  } else if (m->ws_cap < L.total) {
+    if (m->ws) {
+      hipDeviceSynchronize();
+      hipFree(m->ws);
+      m->ws = nullptr;
+      m->ws_cap = 0;
+    }
+    void *p = nullptr;
+    if (hipMalloc(&p, L.total) != hipSuccess) return HBF_ENOMEM;
+    m->ws = p;
+    m->ws_cap = L.total;
+    m->lib_ws = true;
+  }
+  RangeTable rt = snapshot(m);
+  hipEvent_t *ev = nullptr;
+  if (m->prof) {
+    for (auto &e : m->ev)
+      if (!e && hipEventCreate(&e) != hipSuccess) return HBF_EHIP;
+    ev = m->ev;
+  }
+  hipError_t e = launch_time_requests(m->g, rt, L, (char *)m->ws, m->st, addr, issue, complete,
+                                      (hipStream_t)stream, ev, kNumTimedKernels + 1);
+  if (e != hipSuccess) return HBF_EHIP;
+  m->prof_valid = m->prof;
+  return HBF_OK;
+}
+
+int hbf_gemv_instrumented(hbf_model_t m, const uint16_t *W, int E, int K, int N, const uint16_t *X,
+                          int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
+                          void *stream) {
+  if (!m || !W || !X || !Y || E < 1 || K < 1 || N < 1 || B < 1 || B > 64) return HBF_EINVAL;
+  if ((pi == nullptr) != (pc == nullptr)) return HBF_EINVAL;
+  const uint64_t pb = m->p.page_bytes;
+  if (K % 512 || K > 4096 || pb % ((uint64_t)K * 2)) return HBF_EINVAL;
+  const uint64_t rows_per_page = pb / ((uint64_t)K * 2);
+  if (rows_per_page > 16 || (uint64_t)N % rows_per_page) return HBF_EINVAL;
+  if (((uintptr_t)W) % pb || ((uintptr_t)X) % 16 || ((uintptr_t)Y) % 4) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  return launch_gemv(W, E, K, N, (int)pb, X, B, Y, pi, pc, meas, m->tick_ps, m->st, (hipStream_t)stream) ==
+                 hipSuccess
+             ? HBF_OK
+             : HBF_EHIP;
+}
+
+int hbf_wall_clock_tick_ps(hbf_model_t m, int64_t *tick_ps) {
+  if (!m || !tick_ps) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  *tick_ps = m->tick_ps;
+  return HBF_OK;
+}
+
+int hbf_get_status(hbf_model_t m, void *stream) {
+  if (!m) return HBF_EINVAL;
+  if (!m->st) return HBF_OK;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return HBF_EHIP;
+  uint32_t s = 0;
+  if (hipMemcpy(&s, &m->st->sticky, 4, hipMemcpyDeviceToHost) != hipSuccess) return HBF_EHIP;
+  const uint32_t z = 0;
+  if (hipMemcpy(&m->st->sticky, &z, 4, hipMemcpyHostToDevice) != hipSuccess) return HBF_EHIP;
+  if (s & (ERR_RANGE_TIME | ERR_OVERFLOW)) return HBF_ERANGE_TIME;
+  if (s & ERR_UNSORTED) return HBF_EUNSORTED;
+  if (s & ERR_MAP) return HBF_EINVAL;
+  return HBF_OK;
+}
+
+int hbf_get_state(hbf_model_t m, int64_t *die_free, int64_t *chan_free, void *stream) {
+  if (!m) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return HBF_EHIP;
+  std::vector<DevState> h(1);
+  if (hipMemcpy(h.data(), m->st, sizeof(DevState), hipMemcpyDeviceToHost) != hipSuccess) return HBF_EHIP;
+  if (die_free)
+    for (uint32_t k = 0; k < m->g.K; k++)
+      die_free[k] = h[0].die_free[k] <= NEG ? INT64_MIN : h[0].die_free[k];
+  if (chan_free)
+    for (uint32_t c = 0; c < m->g.C; c++)
+      chan_free[c] = h[0].chan_free[c] <= NEG ? INT64_MIN : h[0].chan_free[c];
+  return HBF_OK;
+}
+
+int hbf_set_state(hbf_model_t m, const int64_t *die_free, const int64_t *chan_free, void *stream) {
+  if (!m || !die_free || !chan_free) return HBF_EINVAL;
+  for (uint32_t k = 0; k < m->g.K; k++)
+    if (die_free[k] != INT64_MIN && (die_free[k] < 0 || die_free[k] >= TIME_LIMIT)) return HBF_EINVAL;
+  for (uint32_t c = 0; c < m->g.C; c++)
+    if (chan_free[c] != INT64_MIN && (chan_free[c] < 0 || chan_free[c] >= TIME_LIMIT)) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return HBF_EHIP;
+  std::vector<DevState> h(1);
+  if (hipMemcpy(h.data(), m->st, sizeof(DevState), hipMemcpyDeviceToHost) != hipSuccess) return HBF_EHIP;
+  for (uint32_t k = 0; k < m->g.K; k++) h[0].die_free[k] = die_free[k] == INT64_MIN ? NEG : die_free[k];
+  for (uint32_t c = 0; c < m->g.C; c++)
+    h[0].chan_free[c] = chan_free[c] == INT64_MIN ? NEG : chan_free[c];
+  if (hipMemcpy(m->st, h.data(), sizeof(DevState), hipMemcpyHostToDevice) != hipSuccess) return HBF_EHIP;
+  return HBF_OK;
+}
+
+int hbf_profile(hbf_model_t m, int enable) {
+  if (!m) return HBF_EINVAL;
+  m->prof = enable != 0;
+  return HBF_OK;
+}
+
+int hbf_kernel_times(hbf_model_t m, float *ms, const char **names, int max, int *count) {
+  if (!m || !count) return HBF_EINVAL;
+  *count = 0;
+  if (!m->prof_valid) return HBF_OK;
+  if (hipEventSynchronize(m->ev[kNumTimedKernels]) != hipSuccess) return HBF_EHIP;
+  int k = 0;
+  for (; k < kNumTimedKernels && k < max; k++) {
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, m->ev[k], m->ev[k + 1]) != hipSuccess) return HBF_EHIP;
+    if (ms) ms[k] = t;
+    if (names) names[k] = kKernelNames[k];
+  }
+  *count = k;
+  return HBF_OK;
+}
+
+const char *hbf_strerror(int code) {
+  switch (code) {
+    case HBF_OK: return "ok";
+    case HBF_EINVAL: return "invalid argument";
+    case HBF_EALIGN: return "range not page aligned";
+    case HBF_EOVERLAP: return "range overlaps a registered range";
+    case HBF_ENOWORKSPACE: return "workspace too small";
+    case HBF_EUNSORTED: return "issue times decrease";
+    case HBF_ERANGE_TIME: return "time outside the model's domain";
+    case HBF_EHIP: return "HIP runtime error";
+    case HBF_ENOMEM: return "out of memory";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,112 @@
+// Internal declarations shared by the HIP kernels and the C ABI host code.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hbf.h"
+
+namespace hbf {
+
+// "Idle since minus infinity".  Every modeled time of a call lies in
+// [0, 2^62); the prefix maxima of the Lindley form (time - rank * service)
+// stay above -2^60, so -2^61 is below every value that can occur.
+constexpr int64_t NEG = -(int64_t(1) << 61);
+constexpr int64_t ISSUE_LIMIT = int64_t(1) << 61;
+constexpr int64_t TIME_LIMIT = int64_t(1) << 62;
+constexpr int64_t SERVICE_LIMIT = int64_t(1) << 29;
+constexpr int64_t N_LIMIT = int64_t(1) << 31;
+constexpr int MAX_RANGES = 64;
+constexpr int MAX_KEYS = 2048;      // die queues
+constexpr int MAX_CHANNELS = 1024;
+constexpr uint16_t KEY_NONE = 0xFFFF;
+
+// per-call / sticky device error bits
+constexpr uint32_t ERR_RANGE_TIME = 1u;
+constexpr uint32_t ERR_UNSORTED = 2u;
+constexpr uint32_t ERR_OVERFLOW = 4u;
+constexpr uint32_t ERR_MAP = 8u;
+
+// Die stage: 256 threads (4 wave64), 16 items per thread per chunk.
+constexpr int BLK = 256;
+constexpr int WAVES = BLK / 64;
+constexpr int ITEMS = 16;
+constexpr int CHUNK = BLK * ITEMS;  // 4096 requests staged per chunk
+constexpr int TARGET_TILES = 1024;
+
+// Channel stage: a time cell of one channel is merged in LDS if it holds at
+// most MCAP requests, otherwise streamed in MCAP-sized rounds.
+constexpr int MCAP = 2048;
+constexpr int MAX_RUNS = 64;        // die queues per channel (D, or D*P)
+
+// Snapshot of the registered ranges, sorted by base (passed by value).
+struct RangeTable {
+  uint64_t base[MAX_RANGES];
+  uint64_t bytes[MAX_RANGES];
+  uint64_t pbase[MAX_RANGES];     // first device page of the range
+  uint32_t rid[MAX_RANGES];       // registration index
+  int32_t n;
+};
+
+// Geometry and timing (passed by value).
+struct Geo {
+  uint32_t C, D, P;
+  uint32_t Dk;        // die queues per channel (D, or D*P)
+  uint32_t K;         // die queues (C * Dk)
+  uint32_t page_bytes;
+  uint32_t plane_parallel;
+  uint32_t pow2;      // page_bytes, C, D, P all powers of two
+  uint32_t lg_page, lg_C, lg_D, lg_P;
+  int64_t tR, xfer;
+};
+
+// Persistent device state of a model.
+struct DevState {
+  int64_t die_free[MAX_KEYS];     // NEG = idle
+  int64_t chan_free[MAX_CHANNELS];
+  uint32_t sticky;                // sticky error bits
+  uint32_t pad;
+};
+
+// Per-call control block (in the workspace).
+struct CallCtl {
+  uint32_t err;       // per-call error bits
+  uint32_t ticket;    // channel-stage work counter
+  uint32_t n_in;      // in-range requests
+  uint32_t G;         // time cells per channel
+  uint32_t shift;     // log2(cell width in ns)
+  uint32_t pad;
+  int64_t max_dd;     // largest die-done time of the call
+  int64_t cbase;      // origin of the cell grid (= first issue time)
+};
+
+// Workspace layout of one hbf_time_requests call.
+struct Layout {
+  int64_t n;
+  uint32_t nt;            // die-stage tiles
+  int64_t tile_elems;
+  uint32_t gmax;          // cell budget per channel
+  uint32_t s0;            // minimum cell shift
+  size_t off_ctl, off_agg_cnt, off_agg_A, off_tin_L, off_tin_base;
+  size_t off_totals, off_seg, off_dfnew, off_cfnew;
+  size_t off_dd, off_ix, off_lb, off_st_agg, off_st_incl;
+  size_t total;
+};
+
+Layout make_layout(const Geo &g, int64_t n);
+
+// Launchers (hbf_kernels.hip).  All enqueue on `s` and return the first
+// launch error.
+hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout &L, char *ws,
+                                DevState *st, const uint64_t *addr, const int64_t *issue,
+                                int64_t *complete, hipStream_t s, hipEvent_t *ev, int n_ev);
+hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, const uint64_t *addr,
+                           int64_t n, uint64_t *map, hipStream_t s);
+hipError_t launch_reset(DevState *st, hipStream_t s);
+hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
+                       int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
+                       int64_t tick_ps, DevState *st, hipStream_t s);
+extern const char *const kKernelNames[];
+extern const int kNumTimedKernels;
+
+}  // namespace hbf

@@ -1,0 +1,221 @@
+"""Thin ctypes binding of ``libhbf.so`` (the C ABI in ``include/hbf.h``).
+
+Argument marshalling only: every step of the hot path runs in the HIP
+kernels of the library.  PyTorch supplies device memory and streams.  If the
+library has not been built this module raises on use -- there is no CPU
+fallback.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhbf.so")
+
+HBF_OK = 0
+HBF_EINVAL = -1
+HBF_EALIGN = -2
+HBF_EOVERLAP = -3
+HBF_ENOWORKSPACE = -4
+HBF_EUNSORTED = -5
+HBF_ERANGE_TIME = -6
+HBF_EHIP = -7
+HBF_ENOMEM = -8
+HBF_TIME_ERROR = -(1 << 63)
+HBF_FLAG_PLANE_PARALLEL = 1
+
+EXPORTED = [
+    "hbf_model_create", "hbf_model_destroy", "hbf_xfer_ns", "hbf_n_die_queues", "hbf_model_reset",
+    "hbf_register_range", "hbf_workspace_bytes", "hbf_set_workspace", "hbf_classify_map",
+    "hbf_time_requests", "hbf_gemv_instrumented", "hbf_wall_clock_tick_ps", "hbf_get_status",
+    "hbf_get_state", "hbf_set_state", "hbf_profile", "hbf_kernel_times", "hbf_strerror",
+]
+
+
+class hbf_params(ctypes.Structure):
+    _fields_ = [("channels", ctypes.c_uint32), ("dies_per_channel", ctypes.c_uint32),
+                ("planes_per_die", ctypes.c_uint32), ("page_bytes", ctypes.c_uint32),
+                ("t_read_ns", ctypes.c_int64), ("channel_bytes_per_s", ctypes.c_uint64),
+                ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def load_library(path=LIB_PATH):
+    """Load libhbf.so and declare every exported signature."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libhbf.so not built at {path}; run `python -m paper_2609_09800_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i64, u64, i32, u32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int, ctypes.c_uint32
+    sig = {
+        "hbf_model_create": ([ctypes.POINTER(hbf_params), ctypes.POINTER(vp)], i32),
+        "hbf_model_destroy": ([vp], None),
+        "hbf_xfer_ns": ([vp, ctypes.POINTER(i64)], i32),
+        "hbf_n_die_queues": ([vp, ctypes.POINTER(u32)], i32),
+        "hbf_model_reset": ([vp, vp], i32),
+        "hbf_register_range": ([vp, u64, u64, ctypes.POINTER(ctypes.c_int32)], i32),
+        "hbf_workspace_bytes": ([vp, i64, ctypes.POINTER(ctypes.c_size_t)], i32),
+        "hbf_set_workspace": ([vp, vp, ctypes.c_size_t], i32),
+        "hbf_classify_map": ([vp, vp, i64, vp, vp], i32),
+        "hbf_time_requests": ([vp, vp, vp, i64, vp, vp], i32),
+        "hbf_gemv_instrumented": ([vp, vp, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp], i32),
+        "hbf_wall_clock_tick_ps": ([vp, ctypes.POINTER(i64)], i32),
+        "hbf_get_status": ([vp, vp], i32),
+        "hbf_get_state": ([vp, vp, vp, vp], i32),
+        "hbf_set_state": ([vp, vp, vp, vp], i32),
+        "hbf_profile": ([vp, i32], i32),
+        "hbf_kernel_times": ([vp, vp, vp, i32, ctypes.POINTER(i32)], i32),
+        "hbf_strerror": ([i32], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def _dp(t):
+    """Device pointer of a torch tensor (or None)."""
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _sp(stream):
+    """hipStream_t of a torch stream (None -> current stream)."""
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class HbfError(RuntimeError):
+    def __init__(self, code, what):
+        lib = load_library()
+        super().__init__(f"{what}: {lib.hbf_strerror(code).decode()} ({code})")
+        self.code = code
+
+
+def _check(code, what):
+    if code != HBF_OK:
+        raise HbfError(code, what)
+    return code
+
+
+class Model:
+    """An HBF device model on the current GPU (owns one C handle)."""
+
+    def __init__(self, channels, dies_per_channel, planes_per_die, page_bytes, t_read_ns,
+                 channel_bytes_per_s, flags=0):
+        self._lib = load_library()
+        self.params = hbf_params(channels, dies_per_channel, planes_per_die, page_bytes, t_read_ns,
+                                 channel_bytes_per_s, flags)
+        h = ctypes.c_void_p()
+        _check(self._lib.hbf_model_create(ctypes.byref(self.params), ctypes.byref(h)), "hbf_model_create")
+        self._h = h
+
+    @classmethod
+    def from_dict(cls, d):
+        return cls(**d)
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self._lib.hbf_model_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def xfer_ns(self):
+        x = ctypes.c_int64()
+        _check(self._lib.hbf_xfer_ns(self._h, ctypes.byref(x)), "hbf_xfer_ns")
+        return x.value
+
+    @property
+    def n_die_queues(self):
+        x = ctypes.c_uint32()
+        _check(self._lib.hbf_n_die_queues(self._h, ctypes.byref(x)), "hbf_n_die_queues")
+        return x.value
+
+    def register_range(self, base, nbytes):
+        rid = ctypes.c_int32(-1)
+        rc = self._lib.hbf_register_range(self._h, base, nbytes, ctypes.byref(rid))
+        return rc, rid.value
+
+    def reset(self, stream=None):
+        _check(self._lib.hbf_model_reset(self._h, _sp(stream)), "hbf_model_reset")
+
+    def workspace_bytes(self, n):
+        b = ctypes.c_size_t()
+        _check(self._lib.hbf_workspace_bytes(self._h, n, ctypes.byref(b)), "hbf_workspace_bytes")
+        return b.value
+
+    def set_workspace(self, tensor):
+        if tensor is None:
+            return self._lib.hbf_set_workspace(self._h, None, 0)
+        return self._lib.hbf_set_workspace(self._h, _dp(tensor), tensor.numel() * tensor.element_size())
+
+    def classify_map(self, addr, out, stream=None):
+        """addr: uint64-valued int64 tensor [n] (device); out: int64 tensor [n]."""
+        return self._lib.hbf_classify_map(self._h, _dp(addr), addr.numel(), _dp(out), _sp(stream))
+
+    def time_requests(self, addr, issue, complete, stream=None):
+        """addr/issue/complete: int64 device tensors [n] (addr holds uint64 bit patterns)."""
+        n = addr.numel()
+        assert issue.numel() == n and complete.numel() == n
+        return self._lib.hbf_time_requests(self._h, _dp(addr), _dp(issue), n, _dp(complete), _sp(stream))
+
+    def gemv_instrumented(self, W, X, Y, page_issue=None, page_complete=None, measured=None, stream=None):
+        """W: int16 [E,N,K] (bf16 bits); X: int16 [E,B,K]; Y: float32 [E,B,N]."""
+        E, N, K = W.shape
+        B = X.shape[1]
+        return self._lib.hbf_gemv_instrumented(self._h, _dp(W), E, K, N, _dp(X), B, _dp(Y), _dp(page_issue),
+                                               _dp(page_complete), _dp(measured), _sp(stream))
+
+    def wall_clock_tick_ps(self):
+        x = ctypes.c_int64()
+        _check(self._lib.hbf_wall_clock_tick_ps(self._h, ctypes.byref(x)), "hbf_wall_clock_tick_ps")
+        return x.value
+
+    def get_status(self, stream=None):
+        return self._lib.hbf_get_status(self._h, _sp(stream))
+
+    def get_state(self, stream=None):
+        import numpy as np
+        d = np.zeros(self.n_die_queues, dtype=np.int64)
+        c = np.zeros(self.params.channels, dtype=np.int64)
+        _check(self._lib.hbf_get_state(self._h, d.ctypes.data_as(ctypes.c_void_p),
+                                       c.ctypes.data_as(ctypes.c_void_p), _sp(stream)), "hbf_get_state")
+        return d, c
+
+    def set_state(self, die_free, chan_free, stream=None):
+        import numpy as np
+        d = np.ascontiguousarray(die_free, dtype=np.int64)
+        c = np.ascontiguousarray(chan_free, dtype=np.int64)
+        return self._lib.hbf_set_state(self._h, d.ctypes.data_as(ctypes.c_void_p),
+                                       c.ctypes.data_as(ctypes.c_void_p), _sp(stream))
+
+    def profile(self, enable=True):
+        _check(self._lib.hbf_profile(self._h, int(enable)), "hbf_profile")
+
+    def kernel_times(self):
+        """[(kernel name, ms)] of the last hbf_time_requests call (profiling on)."""
+        ms = (ctypes.c_float * 16)()
+        names = (ctypes.c_char_p * 16)()
+        cnt = ctypes.c_int(0)
+        _check(self._lib.hbf_kernel_times(self._h, ms, names, 16, ctypes.byref(cnt)), "hbf_kernel_times")
+        return [(names[i].decode(), ms[i]) for i in range(cnt.value)]
+
+
+def strerror(code):
+    return load_library().hbf_strerror(code).decode()

@@ -1,0 +1,139 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+``include/hbf.h`` declares, and validates arguments on the host (these code
+paths return before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hbf.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hbf_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_09800_amd import hbf
+    if not os.path.exists(hbf.LIB_PATH):
+        from paper_2609_09800_amd import build
+        build.build()
+    return hbf.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    from paper_2609_09800_amd import hbf
+    names = declared_functions()
+    assert len(names) >= 18
+    for n in names:
+        assert hasattr(lib, n), f"libhbf.so does not export {n}"
+    assert sorted(hbf.EXPORTED) == names
+
+
+def test_status_codes_match_header(lib):
+    from paper_2609_09800_amd import hbf
+    src = open(HEADER).read()
+    for name in ["HBF_OK", "HBF_EINVAL", "HBF_EALIGN", "HBF_EOVERLAP", "HBF_ENOWORKSPACE",
+                 "HBF_EUNSORTED", "HBF_ERANGE_TIME", "HBF_EHIP", "HBF_ENOMEM"]:
+        v = int(re.search(rf"#define {name}\s+(-?\d+)", src).group(1))
+        assert getattr(hbf, name) == v
+    assert lib.hbf_strerror(-5) == b"issue times decrease"
+
+
+def P(**kw):
+    from paper_2609_09800_amd import hbf
+    d = dict(channels=16, dies_per_channel=8, planes_per_die=4, page_bytes=16384, t_read_ns=3000,
+             channel_bytes_per_s=8_000_000_000, flags=0)
+    d.update(kw)
+    return hbf.hbf_params(**d)
+
+
+def create(lib, **kw):
+    h = ctypes.c_void_p()
+    rc = lib.hbf_model_create(ctypes.byref(P(**kw)), ctypes.byref(h))
+    return rc, h
+
+
+@pytest.mark.parametrize("kw", [
+    dict(channels=0), dict(channels=1025), dict(dies_per_channel=0), dict(planes_per_die=65),
+    dict(page_bytes=0), dict(t_read_ns=0), dict(t_read_ns=(1 << 29) + 1), dict(channel_bytes_per_s=0),
+    dict(channel_bytes_per_s=1), dict(flags=4), dict(dies_per_channel=128),  # 128 dies > 64 queues per channel
+    dict(channels=64, dies_per_channel=64),                                # 4096 die queues
+    dict(flags=1, dies_per_channel=32),                                    # 32*4 queues per channel
+])
+def test_create_rejects_invalid_params(lib, kw):
+    rc, h = create(lib, **kw)
+    assert rc == -1 and not h.value
+
+
+def test_xfer_and_queue_counts(lib):
+    rc, h = create(lib)
+    assert rc == 0
+    x = ctypes.c_int64()
+    assert lib.hbf_xfer_ns(h, ctypes.byref(x)) == 0 and x.value == 2048
+    q = ctypes.c_uint32()
+    assert lib.hbf_n_die_queues(h, ctypes.byref(q)) == 0 and q.value == 128
+    lib.hbf_model_destroy(h)
+    rc, h = create(lib, flags=1)
+    assert lib.hbf_n_die_queues(h, ctypes.byref(q)) == 0 and q.value == 512
+    lib.hbf_model_destroy(h)
+    rc, h = create(lib, channel_bytes_per_s=4_000_000_000, channels=8, dies_per_channel=4, planes_per_die=1)
+    assert lib.hbf_xfer_ns(h, ctypes.byref(x)) == 0 and x.value == 4096
+    lib.hbf_model_destroy(h)
+
+
+def test_register_range_errors(lib):
+    rc, h = create(lib)
+    page = 16384
+    rid = ctypes.c_int32()
+    reg = lambda b, n: lib.hbf_register_range(h, b, n, ctypes.byref(rid))
+    assert reg(1 << 40, 4 * page) == 0 and rid.value == 0
+    assert reg((1 << 40) + 1, page) == -2
+    assert reg((1 << 40) + 8 * page, page + 1) == -2
+    assert reg((1 << 40) + 3 * page, 2 * page) == -3
+    assert reg((1 << 40) - page, 2 * page) == -3
+    assert reg((1 << 40) + 4 * page, page) == 0 and rid.value == 1
+    assert reg(2**64 - page, 2 * page) == -1
+    assert reg(1 << 41, 0) == -1
+    for i in range(62):
+        assert reg((1 << 42) + i * page, page) == 0
+    assert reg(1 << 43, page) == -1          # 64 ranges at most
+    lib.hbf_model_destroy(h)
+
+
+def test_workspace_and_argument_validation(lib):
+    rc, h = create(lib)
+    b = ctypes.c_size_t()
+    assert lib.hbf_workspace_bytes(h, 1 << 20, ctypes.byref(b)) == 0
+    assert b.value > 12 * (1 << 20)           # die-ordered (time, index) pairs at least
+    assert lib.hbf_workspace_bytes(h, -1, ctypes.byref(b)) == -1
+    assert lib.hbf_workspace_bytes(h, (1 << 31) + 1, ctypes.byref(b)) == -1
+    # null arrays with n > 0, negative n: rejected before any launch
+    assert lib.hbf_time_requests(h, None, None, 5, None, None) == -1
+    assert lib.hbf_time_requests(h, None, None, -1, None, None) == -1
+    assert lib.hbf_classify_map(h, None, 3, None, None) == -1
+    assert lib.hbf_set_workspace(h, ctypes.c_void_p(256), 0) == -1
+    assert lib.hbf_set_workspace(h, ctypes.c_void_p(100), 1024) == -1
+    assert lib.hbf_gemv_instrumented(h, None, 8, 2048, 768, None, 1, None, None, None, None, None) == -1
+    # null handle
+    assert lib.hbf_time_requests(None, None, None, 0, None, None) == -1
+    assert lib.hbf_get_status(None, None) == -1
+    lib.hbf_model_destroy(h)
+    lib.hbf_model_destroy(None)
+
+
+def test_set_state_validation_is_host_side(lib):
+    import numpy as np
+    rc, h = create(lib, channels=2, dies_per_channel=2, planes_per_die=1)
+    d = np.full(4, np.iinfo(np.int64).min, dtype=np.int64)
+    c = np.full(2, np.iinfo(np.int64).min, dtype=np.int64)
+    d[1] = 1 << 62
+    assert lib.hbf_set_state(h, d.ctypes.data_as(ctypes.c_void_p), c.ctypes.data_as(ctypes.c_void_p), None) == -1
+    d[1] = -3
+    assert lib.hbf_set_state(h, d.ctypes.data_as(ctypes.c_void_p), c.ctypes.data_as(ctypes.c_void_p), None) == -1
+    lib.hbf_model_destroy(h)
