@@ -201,10 +201,11 @@ int hbf_get_state(hbf_model_t model, int64_t *host_die_free, int64_t *host_chan_
 int hbf_set_state(hbf_model_t model, const int64_t *host_die_free, const int64_t *host_chan_free,
                   void *stream);
 
-/* Per-kernel timing of hbf_time_requests (diagnostics).  When enabled, each
- * call records HIP events between its kernels on its stream;
- * hbf_kernel_times synchronises and returns the durations (ms) of the last
- * call's kernels in launch order and their names. */
+/* Per-kernel timing of hbf_time_requests (diagnostics).  hbf_profile(m, 1)
+ * starts a new record: every later call records HIP events between its
+ * kernels on its own stream (the last 64 calls are kept).  hbf_kernel_times
+ * synchronises on the last recorded call and returns, in launch order, each
+ * kernel's name and its mean duration (ms) over the recorded calls. */
 int hbf_profile(hbf_model_t model, int enable);
 int hbf_kernel_times(hbf_model_t model, float *host_ms, const char **host_names, int max, int *count);
 

@@ -26,13 +26,13 @@ Layout make_layout(const Geo &g, int64_t n) {
   L.tile_elems = te;
   L.nt = (uint32_t)((n + te - 1) / te);
   if (L.nt == 0) L.nt = 1;
-  // cell width 2^s0 <= Ts * tR keeps a cell at <= Ts requests per die queue
-  int64_t Ts = MCAP / (2 * (int64_t)g.Dk);
-  if (Ts < 1) Ts = 1;
-  const int64_t w = Ts * g.tR;
-  uint32_t s0 = 0;
-  while ((int64_t(1) << (s0 + 1)) <= w) s0++;
-  L.s0 = s0;
+  // cell width 2^s0 = Ts * 2^floor(log2 tR) <= Ts * tR keeps a cell at <= Ts
+  // requests per die queue and at Ts time buckets
+  int64_t Ts = 1;
+  while (Ts * 2 <= MAX_BUCKETS && Ts * 2 * g.Dk <= MCAP) Ts *= 2;
+  uint32_t lt = 0;
+  while (Ts > 1 && (int64_t(1) << (lt + 1)) <= Ts) lt++;
+  L.s0 = g.lg_tR + lt;
   const int64_t per = (int64_t)g.C * g.Dk * Ts;
   int64_t gm = 4 * ((n + per - 1) / per);
   if (gm < 64) gm = 64;
@@ -50,6 +50,7 @@ Layout make_layout(const Geo &g, int64_t n) {
   L.off_cfnew = o;    o = up256(o + C * 8);
   L.off_dd = o;       o = up256(o + (size_t)n * 8);
   L.off_ix = o;       o = up256(o + (size_t)n * 4);
+  L.off_kr = o;       o = up256(o + (size_t)n * 4);
   L.off_lb = o;       o = up256(o + C * ((size_t)L.gmax + 1) * g.Dk * 4);
   L.off_st_agg = o;   o = up256(o + C * (size_t)L.gmax * 8);
   L.off_st_incl = o;  o = up256(o + C * (size_t)L.gmax * 8);
@@ -72,8 +73,9 @@ struct hbf_model {
   bool ws_caller = false;
   bool lib_ws = false;
   bool prof = false;
-  bool prof_valid = false;
-  hipEvent_t ev[16] = {};
+  static constexpr int RING = 64;      // profiled calls kept
+  hipEvent_t ev[RING][16] = {};
+  int prof_calls = 0;                  // calls recorded since hbf_profile(.., 1)
   int ncu = 0;
   int64_t tick_ps = 0;
 };
@@ -164,6 +166,8 @@ int hbf_model_create(const hbf_params *params, hbf_model_t *out) {
   g.lg_D = lg2(p.dies_per_channel);
   g.lg_P = lg2(p.planes_per_die);
   g.tR = p.t_read_ns;
+  g.lg_tR = 0;
+  while ((int64_t(1) << (g.lg_tR + 1)) <= p.t_read_ns) g.lg_tR++;
   g.xfer = (int64_t)q;
   *out = m;
   return HBF_OK;
@@ -176,8 +180,9 @@ void hbf_model_destroy(hbf_model_t m) {
     hipFree(m->st);
   }
   if (m->ws && m->lib_ws) hipFree(m->ws);
-  for (auto &e : m->ev)
-    if (e) hipEventDestroy(e);
+  for (auto &set : m->ev)
+    for (auto &e : set)
+      if (e) hipEventDestroy(e);
   delete m;
 }
 
@@ -254,7 +259,6 @@ int hbf_time_requests(hbf_model_t m, const uint64_t *addr, const int64_t *issue,
   if (!m || n < 0 || n > N_LIMIT || (n > 0 && (!addr || !issue || !complete))) return HBF_EINVAL;
   int rc = ensure_device(m);
   if (rc) return rc;
-  m->prof_valid = false;
   if (n == 0) return HBF_OK;
   const Layout L = make_layout(m->g, n);
   if (m->ws_caller) {
@@ -275,14 +279,15 @@ int hbf_time_requests(hbf_model_t m, const uint64_t *addr, const int64_t *issue,
   RangeTable rt = snapshot(m);
   hipEvent_t *ev = nullptr;
   if (m->prof) {
-    for (auto &e : m->ev)
-      if (!e && hipEventCreate(&e) != hipSuccess) return HBF_EHIP;
-    ev = m->ev;
+    hipEvent_t *set = m->ev[m->prof_calls % hbf_model::RING];
+    for (int k = 0; k <= kNumTimedKernels; k++)
+      if (!set[k] && hipEventCreate(&set[k]) != hipSuccess) return HBF_EHIP;
+    ev = set;
   }
   hipError_t e = launch_time_requests(m->g, rt, L, (char *)m->ws, m->st, addr, issue, complete,
                                       (hipStream_t)stream, ev, kNumTimedKernels + 1);
   if (e != hipSuccess) return HBF_EHIP;
-  m->prof_valid = m->prof;
+  if (m->prof) m->prof_calls++;
   return HBF_OK;
 }
 
@@ -363,19 +368,26 @@ int hbf_set_state(hbf_model_t m, const int64_t *die_free, const int64_t *chan_fr
 int hbf_profile(hbf_model_t m, int enable) {
   if (!m) return HBF_EINVAL;
   m->prof = enable != 0;
+  m->prof_calls = 0;
   return HBF_OK;
 }
 
 int hbf_kernel_times(hbf_model_t m, float *ms, const char **names, int max, int *count) {
   if (!m || !count) return HBF_EINVAL;
   *count = 0;
-  if (!m->prof_valid) return HBF_OK;
-  if (hipEventSynchronize(m->ev[kNumTimedKernels]) != hipSuccess) return HBF_EHIP;
+  const int calls = std::min(m->prof_calls, hbf_model::RING);
+  if (calls == 0) return HBF_OK;
+  const int last = (m->prof_calls - 1) % hbf_model::RING;
+  if (hipEventSynchronize(m->ev[last][kNumTimedKernels]) != hipSuccess) return HBF_EHIP;
   int k = 0;
   for (; k < kNumTimedKernels && k < max; k++) {
-    float t = 0.f;
-    if (hipEventElapsedTime(&t, m->ev[k], m->ev[k + 1]) != hipSuccess) return HBF_EHIP;
-    if (ms) ms[k] = t;
+    double sum = 0.0;
+    for (int c = 0; c < calls; c++) {
+      float t = 0.f;
+      if (hipEventElapsedTime(&t, m->ev[c][k], m->ev[c][k + 1]) != hipSuccess) return HBF_EHIP;
+      sum += t;
+    }
+    if (ms) ms[k] = (float)(sum / calls);
     if (names) names[k] = kKernelNames[k];
   }
   *count = k;

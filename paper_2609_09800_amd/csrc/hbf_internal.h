@@ -36,7 +36,13 @@ constexpr int TARGET_TILES = 1024;
 
 // Channel stage: a time cell of one channel is merged in LDS if it holds at
 // most MCAP requests, otherwise streamed in MCAP-sized rounds.
-constexpr int MCAP = 2048;
+constexpr int MCAP = 1024;
+// Time buckets of width 2^floor(log2 tR) hold at most one request per die;
+// a cell of at most 64 such buckets is ranked with per-die bucket masks.
+constexpr int MAX_BUCKETS = 64;
+// The channel stage hands each XCD (L2 domain) its own time windows, so the
+// requests of one window, from every channel, complete in one L2.
+constexpr int NXCD = 8;
 constexpr int MAX_RUNS = 64;        // die queues per channel (D, or D*P)
 
 // Snapshot of the registered ranges, sorted by base (passed by value).
@@ -57,6 +63,7 @@ struct Geo {
   uint32_t plane_parallel;
   uint32_t pow2;      // page_bytes, C, D, P all powers of two
   uint32_t lg_page, lg_C, lg_D, lg_P;
+  uint32_t lg_tR;     // floor(log2(tR)): bucket width of the channel merge
   int64_t tR, xfer;
 };
 
@@ -71,11 +78,10 @@ struct DevState {
 // Per-call control block (in the workspace).
 struct CallCtl {
   uint32_t err;       // per-call error bits
-  uint32_t ticket;    // channel-stage work counter
+  uint32_t ticket[NXCD];  // channel-stage work counters, one per XCD
   uint32_t n_in;      // in-range requests
   uint32_t G;         // time cells per channel
   uint32_t shift;     // log2(cell width in ns)
-  uint32_t pad;
   int64_t max_dd;     // largest die-done time of the call
   int64_t cbase;      // origin of the cell grid (= first issue time)
 };
@@ -89,7 +95,7 @@ struct Layout {
   uint32_t s0;            // minimum cell shift
   size_t off_ctl, off_agg_cnt, off_agg_A, off_tin_L, off_tin_base;
   size_t off_totals, off_seg, off_dfnew, off_cfnew;
-  size_t off_dd, off_ix, off_lb, off_st_agg, off_st_incl;
+  size_t off_dd, off_ix, off_kr, off_lb, off_st_agg, off_st_incl;
   size_t total;
 };
 

@@ -46,6 +46,13 @@ DEVI int64_t imin(int64_t a, int64_t b) { return a < b ? a : b; }
 
 DEVI uint32_t lane_id() { return __lane_id(); }
 
+// 32 x 32 -> 64-bit product (one v_mad_u64_u32)
+DEVI uint64_t mul32(uint32_t a, uint32_t b) { return (uint64_t)a * (uint64_t)b; }
+
+// LDS index padding: one slot per 16, so blocked per-lane runs of 16
+// consecutive 8-byte entries do not all fall into the same banks
+DEVI uint32_t pad16(uint32_t p) { return p + (p >> 4); }
+
 // number of lanes below this one whose bit is set in `mask`
 DEVI uint32_t mask_below(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -277,7 +284,7 @@ DEVI void cross_wave_offsets(uint16_t *wcnt, uint16_t *tot, uint32_t K) {
 __global__ void k_prologue(CallCtl *ctl, uint64_t *st_agg, uint64_t *st_incl, size_t nst) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ctl->err = 0;
-    ctl->ticket = 0;
+    for (int x = 0; x < NXCD; x++) ctl->ticket[x] = 0;
     ctl->n_in = 0;
     ctl->G = 0;
     ctl->shift = 0;
@@ -300,7 +307,8 @@ __global__ __launch_bounds__(BLK) void k_die_reduce(const uint64_t *__restrict__
                                                     int64_t *__restrict__ complete, Geo g,
                                                     RangeTable rt, int64_t tile_elems,
                                                     uint32_t *__restrict__ agg_cnt,
-                                                    int64_t *__restrict__ agg_A, CallCtl *ctl,
+                                                    int64_t *__restrict__ agg_A,
+                                                    uint32_t *__restrict__ KR, CallCtl *ctl,
                                                     uint32_t kbits) {
   extern __shared__ __align__(16) unsigned char smem[];
   LdsRanges *lr = (LdsRanges *)smem;
@@ -357,9 +365,14 @@ __global__ __launch_bounds__(BLK) void k_die_reduce(const uint64_t *__restrict__
 #pragma unroll
     for (int e = 0; e < ITEMS; e++) {
       const uint32_t k = key[e];
+      const int64_t i = wbase + e * 64 + lane;
       if (k != KEY_NONE) {
-        const int64_t r0 = (int64_t)cnt[k] + mycnt[k] + rank[e];  // 0-based rank in tile
-        atomicMax((long long *)&amax[k], (long long)(iss[e] - r0 * tR));
+        const uint32_t rc = mycnt[k] + rank[e];            // rank among key k in the chunk
+        const uint32_t r0 = cnt[k] + rc;                   // rank among key k in the tile
+        atomicMax((long long *)&amax[k], (long long)(iss[e] - (int64_t)mul32(r0, (uint32_t)tR)));
+        KR[i] = (k << 16) | rc;
+      } else if (i < t1) {
+        KR[i] = (uint32_t)KEY_NONE << 16;
       }
     }
     __syncthreads();
@@ -479,91 +492,95 @@ __global__ __launch_bounds__(BLK) void k_key_scan(const uint32_t *__restrict__ t
 
 // ------------------------------------------------------------------ k_die_scatter
 
-// LDS: ranges | sval[CHUNK] i64 | L[K] i64 | cnt[K] u32 | gbase[K] u32 |
-//      sloc[CHUNK] u16 | skey[CHUNK] u16 | wcnt[WAVES][K] u16 | tot[K] u16 | koff[K] u16
-template <bool POW2>
+// Pass 2 of the die stage.  Per chunk: stage the requests in (die queue,
+// rank) order using the ranks pass 1 stored (LDS histogram + offsets, no
+// re-ranking), compute exact die-done times with a segmented prefix max,
+// and write them in die-queue order, filling the cell table on the way.
+// LDS: sval[CHUNKP] i64 | L[K] i64 | cnt[K] | gbase[K] | segb[K] | totk[K] |
+//      tot[K] | koff[K] (u32) | skey[CHUNKP] u16 | sloc[CHUNKP] u16
+constexpr int CHUNKP = CHUNK + CHUNK / 16;
+
 __global__ __launch_bounds__(BLK) void k_die_scatter(
-    const uint64_t *__restrict__ addr, const int64_t *__restrict__ issue, int64_t n, Geo g,
-    RangeTable rt, int64_t tile_elems, const int64_t *__restrict__ tin_L,
-    const uint32_t *__restrict__ tin_base, const uint32_t *__restrict__ seg_start,
-    const uint32_t *__restrict__ totals, int64_t *__restrict__ DD, uint32_t *__restrict__ IX,
-    uint32_t *__restrict__ LB, uint32_t gmax, CallCtl *ctl, uint32_t kbits) {
+    const int64_t *__restrict__ issue, const uint32_t *__restrict__ KR, int64_t n, Geo g,
+    int64_t tile_elems, const int64_t *__restrict__ tin_L, const uint32_t *__restrict__ tin_base,
+    const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals,
+    int64_t *__restrict__ DD, uint32_t *__restrict__ IX, uint32_t *__restrict__ LB, uint32_t gmax,
+    CallCtl *ctl) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ SegMax shseg[WAVES];
   __shared__ uint32_t shsum[WAVES];
   __shared__ uint32_t s_nvalid;
   if (agent_load32(&ctl->err)) return;
-  LdsRanges *lr = (LdsRanges *)smem;
   const uint32_t K = g.K;
-  int64_t *sval = (int64_t *)(smem + ((sizeof(LdsRanges) + 15) & ~size_t(15)));
-  int64_t *L = sval + CHUNK;
+  int64_t *sval = (int64_t *)smem;
+  int64_t *L = sval + CHUNKP;
   uint32_t *cnt = (uint32_t *)(L + K);
   uint32_t *gbase = cnt + K;
-  uint16_t *sloc = (uint16_t *)(gbase + K);
-  uint16_t *skey = sloc + CHUNK;
-  uint16_t *wcnt = skey + CHUNK;
-  uint16_t *tot = wcnt + WAVES * K;
-  uint16_t *koff = tot + K;
+  uint32_t *segb = gbase + K;
+  uint32_t *totk = segb + K;
+  uint32_t *tot = totk + K;
+  uint32_t *koff = tot + K;
+  uint16_t *skey = (uint16_t *)(koff + K);
+  uint16_t *sloc = skey + CHUNKP;
 
-  load_ranges(lr, rt);
   const size_t row = (size_t)blockIdx.x * K;
   for (uint32_t k = threadIdx.x; k < K; k += BLK) {
     cnt[k] = 0;
     L[k] = tin_L[row + k];
     gbase[k] = tin_base[row + k];  // die rank of the tile's first request of k
+    segb[k] = seg_start[k];
+    totk[k] = totals[k];
   }
   const int64_t cbase = ctl->cbase;
   const uint32_t shift = ctl->shift, G = ctl->G;
-  __syncthreads();
-
-  const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
   const int64_t t0 = (int64_t)blockIdx.x * tile_elems;
   const int64_t t1 = imin(n, t0 + tile_elems);
-  const int64_t tR = g.tR;
-  uint16_t *mycnt = wcnt + w * K;
+  const uint32_t tR = (uint32_t)g.tR;
   const uint32_t Dk = g.Dk;
 
   for (int64_t c0 = t0; c0 < t1; c0 += CHUNK) {
-    for (uint32_t k = lane; k < K; k += 64) mycnt[k] = 0;
-    uint32_t key[ITEMS], rank[ITEMS];
+    for (uint32_t k = threadIdx.x; k < K; k += BLK) tot[k] = 0;
+    __syncthreads();
     int64_t iss[ITEMS];
-    const int64_t wbase = c0 + (int64_t)w * 64 * ITEMS;
+    uint32_t kr[ITEMS];
 #pragma unroll
     for (int e = 0; e < ITEMS; e++) {
-      const int64_t i = wbase + e * 64 + lane;
-      const bool v = i < t1;
-      iss[e] = v ? issue[i] : 0;
-      uint64_t a = v ? addr[i] : 0;
-      key[e] = v ? key_of<POW2>(g, lr, a) : KEY_NONE;
+      const int64_t i = c0 + e * BLK + threadIdx.x;
+      iss[e] = 0;
+      kr[e] = (uint32_t)KEY_NONE << 16;
+      if (i < t1) {
+        iss[e] = issue[i];
+        kr[e] = KR[i];
+      }
     }
-    wave_rank(key, rank, mycnt, kbits);
+#pragma unroll
+    for (int e = 0; e < ITEMS; e++) {
+      const uint32_t k = kr[e] >> 16;
+      if (k != KEY_NONE) atomicAdd(&tot[k], 1u);
+    }
     __syncthreads();
-    cross_wave_offsets(wcnt, tot, K);
-    __syncthreads();
-    // chunk offsets of each key's run: exclusive scan of tot over keys
-    {
+    {  // chunk offsets of each key's run
       const uint32_t per = (K + BLK - 1) / BLK;
-      const uint32_t a = threadIdx.x * per, b = min(K, a + per);
-      uint32_t s = 0;
-      for (uint32_t k = a; k < b; k++) s += tot[k];
+      const uint32_t a0 = threadIdx.x * per, b0 = min(K, a0 + per);
+      uint32_t sum = 0;
+      for (uint32_t k = a0; k < b0; k++) sum += tot[k];
       uint32_t ex;
-      uint32_t all = block_excl_sum(s, &ex, shsum);
-      for (uint32_t k = a; k < b; k++) {
-        koff[k] = (uint16_t)ex;
+      const uint32_t all = block_excl_sum(sum, &ex, shsum);
+      for (uint32_t k = a0; k < b0; k++) {
+        koff[k] = ex;
         ex += tot[k];
       }
       if (threadIdx.x == 0) s_nvalid = all;
     }
     __syncthreads();
-    // stage in (key, rank) order
 #pragma unroll
     for (int e = 0; e < ITEMS; e++) {
-      const uint32_t k = key[e];
+      const uint32_t k = kr[e] >> 16;
       if (k != KEY_NONE) {
-        const uint32_t pos = koff[k] + mycnt[k] + rank[e];
-        sval[pos] = iss[e];
-        skey[pos] = (uint16_t)k;
-        sloc[pos] = (uint16_t)(w * 64 * ITEMS + e * 64 + lane);
+        const uint32_t P = pad16(koff[k] + (kr[e] & 0xFFFFu));
+        sval[P] = iss[e];
+        skey[P] = (uint16_t)k;
+        sloc[P] = (uint16_t)(e * BLK + threadIdx.x);
       }
     }
     __syncthreads();
@@ -577,10 +594,11 @@ __global__ __launch_bounds__(BLK) void k_die_scatter(
 #pragma unroll
       for (int q = 0; q < ITEMS; q++) {
         const uint32_t p = p0 + q;
+        vals[q] = NEG;
         if (p < nv) {
-          const uint32_t k = skey[p];
+          const uint32_t k = skey[pad16(p)];
           const uint32_t j = p - koff[k];
-          const int64_t v = sval[p] - ((int64_t)cnt[k] + j) * tR;
+          const int64_t v = sval[pad16(p)] - (int64_t)mul32(cnt[k] + j, tR);
           vals[q] = v;
           agg = seg_comb(agg, SegMax{j == 0, v});
         }
@@ -591,39 +609,42 @@ __global__ __launch_bounds__(BLK) void k_die_scatter(
       for (int q = 0; q < ITEMS; q++) {
         const uint32_t p = p0 + q;
         if (p < nv) {
-          const uint32_t k = skey[p];
+          const uint32_t k = skey[pad16(p)];
           const uint32_t j = p - koff[k];
           run = (j == 0) ? vals[q] : imax(run, vals[q]);
-          const int64_t r0 = (int64_t)cnt[k] + j;
-          const int64_t M = L[k] - (int64_t)cnt[k] * tR;
-          sval[p] = (r0 + 1) * tR + imax(M, run);
+          const uint32_t r0 = cnt[k] + j;
+          const int64_t M = L[k] - (int64_t)mul32(cnt[k], tR);
+          sval[pad16(p)] = (int64_t)mul32(r0 + 1, tR) + imax(M, run);
         }
       }
     }
     __syncthreads();
     // write die-ordered (die_done, index); fill the cell table
     for (uint32_t p = threadIdx.x; p < nv; p += BLK) {
-      const uint32_t k = skey[p];
+      const uint32_t P = pad16(p);
+      const uint32_t k = skey[P];
       const uint32_t j = p - koff[k];
       const uint32_t r = gbase[k] + cnt[k] + j;  // die rank within this call
-      const int64_t dd = sval[p];
-      const size_t gpos = (size_t)seg_start[k] + r;
-      DD[gpos] = dd;
-      IX[gpos] = (uint32_t)(c0 + sloc[p]);
-      const int64_t prev = (j > 0) ? sval[p - 1] : L[k];
-      const int64_t cell = (dd - cbase) >> shift;
-      const int64_t pcell = (r == 0) ? -1 : ((prev - cbase) >> shift);
+      const int64_t dd = sval[P];
+      const uint32_t gpos = segb[k] + r;
+      if (gpos < n) {
+        DD[gpos] = dd;
+        IX[gpos] = (uint32_t)(c0 + sloc[P]);
+      }
+      const int64_t prev = (j > 0) ? sval[pad16(p - 1)] : L[k];
+      const int64_t cell = imin((dd - cbase) >> shift, (int64_t)G);
+      const int64_t pcell = (r == 0) ? -1 : imin((prev - cbase) >> shift, (int64_t)G);
       const uint32_t ch = k / Dk, dl = k - ch * Dk;
       uint32_t *lbrow = LB + (size_t)ch * (gmax + 1) * Dk + dl;
       for (int64_t c = pcell + 1; c <= cell; c++) lbrow[(size_t)c * Dk] = r;
-      if (r + 1 == totals[k])
+      if (r + 1 == totk[k])
         for (int64_t c = cell + 1; c <= (int64_t)G; c++) lbrow[(size_t)c * Dk] = r + 1;
     }
     __syncthreads();
     for (uint32_t k = threadIdx.x; k < K; k += BLK) {
       const uint32_t t = tot[k];
       if (t) {
-        L[k] = sval[koff[k] + t - 1];
+        L[k] = sval[pad16(koff[k] + t - 1)];
         cnt[k] += t;
       }
     }
@@ -649,334 +670,419 @@ DEVI int run_of(const uint32_t *rb, int R, uint32_t p) {
   return lo;
 }
 
-// Merge R sorted runs (boundaries rb[0..R], R a power of two) of m elements
-// by pairwise merge levels in LDS.  Returns the buffer index holding the
-// sorted result.
-DEVI int lds_merge(int64_t *dd0, uint32_t *ix0, uint8_t *tg0, int64_t *dd1, uint32_t *ix1,
-                   uint8_t *tg1, const uint32_t *rb, int R, uint32_t m, bool tags) {
-  int cur = 0;
-  for (int lvl = 0; (1 << lvl) < R; lvl++) {
-    const int64_t *sd = cur ? dd1 : dd0;
-    const uint32_t *si = cur ? ix1 : ix0;
-    const uint8_t *st = cur ? tg1 : tg0;
-    int64_t *dd = cur ? dd0 : dd1;
-    uint32_t *di = cur ? ix0 : ix1;
-    uint8_t *dt = cur ? tg0 : tg1;
-    for (uint32_t p = threadIdx.x; p < m; p += BLK) {
-      const int d = run_of(rb, R, p);
-      const int gsel = d >> lvl;
-      const uint32_t lo_g = rb[gsel << lvl];
-      const int pg = gsel ^ 1;
-      uint32_t lo = rb[pg << lvl], hi = rb[(pg + 1) << lvl];
-      const int64_t x = sd[p];
-      const uint32_t xi = si[p];
-      // count partner elements less than x
-      uint32_t a = lo, b = hi;
-      while (a < b) {
-        const uint32_t mid = (a + b) >> 1;
-        if (key_less(sd[mid], si[mid], x, xi)) a = mid + 1;
-        else b = mid;
-      }
-      const uint32_t out = rb[(gsel & ~1) << lvl] + (p - lo_g) + (a - lo);
-      dd[out] = x;
-      di[out] = xi;
-      if (tags) dt[out] = st[p];
-    }
-    __syncthreads();
-    cur ^= 1;
+// ---- wave-level helpers (the channel stage runs one wave per block)
+DEVI void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+DEVI uint32_t wave_sum(uint32_t x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+DEVI uint32_t wave_excl_sum(uint32_t v) {
+  const uint32_t lane = lane_id();
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d);
+    if (lane >= (uint32_t)d) x += y;
   }
-  return cur;
+  return x - v;
+}
+DEVI int64_t wave_max(int64_t x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = imax(x, __shfl_xor(x, o));
+  return x;
+}
+DEVI int64_t wave_incl_max(int64_t v) {
+  const uint32_t lane = lane_id();
+  int64_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t y = __shfl_up(x, d);
+    if (lane >= (uint32_t)d) x = imax(x, y);
+  }
+  return x;
 }
 
-struct MergeLds {
-  int64_t dd[2][MCAP];
-  uint32_t ix[2][MCAP];
-  uint8_t tg[2][MCAP];
-  uint32_t rb[MAX_RUNS + 1];
-  uint32_t lo[MAX_RUNS];     // next global position to take, per run
-  uint32_t hi[MAX_RUNS];     // end global position, per run
+constexpr int CAP_S = 512;     // requests per round of a streamed cell
+constexpr int SLOTS_MAX = 16;  // die runs per channel on the bucket path
+
+struct CellLds {
+  union {
+    struct {
+      uint64_t in[MCAP];   // (dd - cell start) << 32 | index, in run order
+      uint64_t out[MCAP + MCAP / 16];  // the same keys in merged order (padded index)
+    } f;
+    struct {
+      int64_t dd[2][CAP_S];
+      uint32_t ix[2][CAP_S];
+      uint8_t tg[2][CAP_S];
+    } s;
+  } u;
+  uint64_t mask[MAX_RUNS];   // per run: occupied time buckets
+  uint32_t rb[MAX_RUNS + 1]; // run offsets in the staging buffer
+  uint32_t lo[MAX_RUNS];     // run bounds: global positions in the die order
+  uint32_t hi[MAX_RUNS];
+  uint32_t cur[MAX_RUNS];
   uint32_t take[MAX_RUNS];
   uint32_t used[MAX_RUNS];
-  int64_t shmax[WAVES];
-  uint32_t shsum[WAVES];
-  uint32_t ticket;
-  uint32_t m;
   uint32_t safe;
-  int64_t gin;
-  int64_t qlast;
-  uint32_t vstar_ok;
-  int64_t vstar_d;
-  uint32_t vstar_i;
 };
 
-// Sizes of cell j of channel c per run, from the cell table; returns total.
-DEVI uint32_t cell_runs(MergeLds &S, const uint32_t *LB, const uint32_t *seg_start,
-                        const uint32_t *totals, uint32_t c, uint32_t j, uint32_t Dk, uint32_t gmax,
-                        int R) {
-  if (threadIdx.x < (uint32_t)R) {
-    const uint32_t d = threadIdx.x;
-    uint32_t lo = 0, hi = 0;
-    if (d < Dk) {
-      const uint32_t k = c * Dk + d;
-      if (totals[k]) {
-        const uint32_t *lbrow = LB + (size_t)c * (gmax + 1) * Dk + d;
-        lo = lbrow[(size_t)j * Dk];
-        hi = lbrow[(size_t)(j + 1) * Dk];
-      }
-      lo += seg_start[k];
-      hi += seg_start[k];
-    }
-    S.lo[d] = lo;
-    S.hi[d] = hi;
-  }
-  __syncthreads();
-  uint32_t tot = 0;
-  if (threadIdx.x == 0) {
-    for (int d = 0; d < R; d++) tot += S.hi[d] - S.lo[d];
-    S.m = tot;
-  }
-  __syncthreads();
-  return S.m;
-}
-
-// Decoupled look-back (wave 0): channel clock entering cell j of channel c.
-DEVI int64_t look_back(const uint64_t *st_agg, const uint64_t *st_incl, const uint32_t *LB,
-                       const uint32_t *totals, const DevState *st, uint32_t c, uint32_t j,
-                       uint32_t Dk, uint32_t gmax, int64_t xfer) {
-  int64_t A = NEG, B = 0;  // composition of the cells between jj and j (identity)
+// Decoupled look-back, 64 predecessors per round: the channel term entering
+// cell j, max(f0, M_j' for j' < j).  Lane l inspects cell base-l; the fold
+// stops at the nearest inclusive prefix and waits only for cells that have
+// published nothing yet.
+DEVI int64_t look_back(const uint64_t *st_agg, const uint64_t *st_incl, int64_t f0, size_t row,
+                       uint32_t j) {
   const uint32_t lane = lane_id();
-  int64_t jj = (int64_t)j - 1;
+  int64_t acc = NEG;
+  int64_t base = (int64_t)j - 1;
   while (true) {
+    const int64_t jj = base - (int64_t)lane;
+    int stt = 0;
+    int64_t v = NEG;
     if (jj < 0) {
-      const int64_t f0 = st->chan_free[c];
-      return imax(A, f0 + B);
-    }
-    const size_t sidx = (size_t)c * gmax + jj;
-    const uint64_t wi = agent_load(&st_incl[sidx]);
-    if (wi) return imax(A, dec_time(wi) + B);
-    const uint64_t wa = agent_load(&st_agg[sidx]);
-    if (wa) {
-      // size of cell jj from the cell table (lanes over dies)
-      uint32_t sz = 0;
-      if (lane < Dk) {
-        const uint32_t k = c * Dk + lane;
-        if (totals[k]) {
-          const uint32_t *lbrow = LB + (size_t)c * (gmax + 1) * Dk + lane;
-          sz = lbrow[(size_t)(jj + 1) * Dk] - lbrow[(size_t)jj * Dk];
+      stt = 2;
+      v = f0;
+    } else {
+      const uint64_t wi = agent_load(&st_incl[row + jj]);
+      if (wi) {
+        stt = 2;
+        v = dec_time(wi);
+      } else {
+        const uint64_t wa = agent_load(&st_agg[row + jj]);
+        if (wa) {
+          stt = 1;
+          v = dec_time(wa);
         }
       }
-#pragma unroll
-      for (int d = 32; d >= 1; d >>= 1) sz += __shfl_xor(sz, d);
-      const int64_t Bj = (int64_t)sz * xfer;
-      A = imax(A, dec_time(wa) + B);
-      B += Bj;
-      jj--;
-      continue;
     }
-    __builtin_amdgcn_s_sleep(2);
+    const uint64_t incl = __ballot(stt == 2);
+    const uint64_t none = __ballot(stt == 0);
+    const uint32_t fi = incl ? (uint32_t)__builtin_ctzll(incl) : 64u;
+    const uint32_t fn = none ? (uint32_t)__builtin_ctzll(none) : 64u;
+    if (fi < fn) return imax(acc, wave_max(lane <= fi ? v : NEG));
+    acc = imax(acc, wave_max(lane < fn ? v : NEG));
+    base -= fn;
+    if (fn == 0) __builtin_amdgcn_s_sleep(1);
   }
 }
 
-// Load runs [lo[d], lo[d]+take[d]) into buffer 0; rb gets the boundaries.
-DEVI uint32_t load_runs(MergeLds &S, const int64_t *DD, const uint32_t *IX, int R, bool tags) {
-  if (threadIdx.x == 0) {
-    uint32_t s = 0;
-    for (int d = 0; d < R; d++) {
-      S.rb[d] = s;
-      s += S.take[d];
-    }
-    S.rb[R] = s;
-  }
-  __syncthreads();
-  const uint32_t m = S.rb[R];
-  for (uint32_t p = threadIdx.x; p < m; p += BLK) {
-    const int d = run_of(S.rb, R, p);
-    const uint32_t src = S.lo[d] + (p - S.rb[d]);
-    S.dd[0][p] = DD[src];
-    S.ix[0][p] = IX[src];
-    if (tags) S.tg[0][p] = (uint8_t)d;
-  }
-  __syncthreads();
-  return m;
-}
-
-// Prefix max of v_p = dd_p - p*xfer over buffer `b`, in place, for p < m.
-// Returns nothing; S.qlast receives the value at m-1.
-DEVI void prefix_q(MergeLds &S, int b, uint32_t m, int64_t xfer) {
-  constexpr int E = MCAP / BLK;
-  const uint32_t p0 = threadIdx.x * E;
-  int64_t loc = NEG;
+// Ascending bitonic sorting network over SL registers (SL a power of two).
+template <int SL>
+DEVI void sort_slots(uint64_t (&a)[SL]) {
 #pragma unroll
-  for (int q = 0; q < E; q++) {
-    const uint32_t p = p0 + q;
-    if (p < m) loc = imax(loc, S.dd[b][p] - (int64_t)p * xfer);
-  }
-  int64_t run = block_excl_max(loc, S.shmax);
+  for (int k = 2; k <= SL; k <<= 1) {
 #pragma unroll
-  for (int q = 0; q < E; q++) {
-    const uint32_t p = p0 + q;
-    if (p < m) {
-      run = imax(run, S.dd[b][p] - (int64_t)p * xfer);
-      S.dd[b][p] = run;
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) S.qlast = m ? S.dd[b][m - 1] : NEG;
-  __syncthreads();
-}
-
-// One pass over an oversized cell in bounded rounds.  Each round loads at
-// most MCAP/R requests per run, merges them, and serves the prefix that no
-// unloaded request can precede.  Returns the channel clock after the cell;
-// writes complete[] when `emit`.
-DEVI int64_t stream_cell(MergeLds &S, const int64_t *DD, const uint32_t *IX, int R, int64_t gstart,
-                         int64_t xfer, bool emit, int64_t *complete, uint32_t *errb,
-                         const uint32_t *lo0, const uint32_t *hi0) {
-  if (threadIdx.x < (uint32_t)R) {
-    S.lo[threadIdx.x] = lo0[threadIdx.x];
-    S.hi[threadIdx.x] = hi0[threadIdx.x];
-  }
-  __syncthreads();
-  int64_t G = gstart;
-  const uint32_t quota = MCAP / R;
-  while (true) {
-    if (threadIdx.x == 0) {
-      uint32_t rem = 0;
-      for (int d = 0; d < R; d++) rem += S.hi[d] - S.lo[d];
-      const bool all = rem <= MCAP;
-      S.vstar_ok = 0;
-      for (int d = 0; d < R; d++) {
-        const uint32_t r = S.hi[d] - S.lo[d];
-        S.take[d] = all ? r : min(r, quota);
-        S.used[d] = 0;
+    for (int j = k >> 1; j > 0; j >>= 1) {
+#pragma unroll
+      for (int i = 0; i < SL; i++) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint64_t x = a[i], y = a[l];
+          const bool sw = ((i & k) == 0) ? (x > y) : (x < y);
+          a[i] = sw ? y : x;
+          a[l] = sw ? x : y;
+        }
       }
-      S.m = rem;
     }
-    __syncthreads();
-    if (S.m == 0) break;
-    const uint32_t m = load_runs(S, DD, IX, R, true);
-    // bound: smallest last-loaded key among runs with requests left behind
-    if (threadIdx.x == 0) {
+  }
+}
+
+// One wave streams a cell through the LDS in rounds of at most CAP_S
+// requests (cells that are too wide or too full for the bucket path).  Each
+// round loads at most CAP_S/R requests per run, ranks them (binary searches
+// in the other runs), and serves the prefix that no unloaded request can
+// precede.  gacc: running channel term; returns it after the cell.
+DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, int R, int64_t gacc,
+                         int64_t rank0, int64_t xfer, bool emit, int64_t *complete, uint32_t n,
+                         uint32_t *errb) {
+  const uint32_t lane = lane_id();
+  if (lane < (uint32_t)R) S.cur[lane] = S.lo[lane];
+  wave_sync();
+  int64_t done = 0;
+  const uint32_t quota = CAP_S / R;
+  while (true) {
+    uint32_t rem = 0, take = 0;
+    if (lane < (uint32_t)R) rem = S.hi[lane] - S.cur[lane];
+    const uint32_t tot = wave_sum(rem);
+    if (tot == 0) break;
+    take = tot <= (uint32_t)CAP_S ? rem : min(rem, quota);
+    const uint32_t rbx = wave_excl_sum(take);
+    const uint32_t m = wave_sum(take);
+    if (lane < (uint32_t)R) {
+      S.rb[lane] = rbx;
+      S.take[lane] = take;
+      S.used[lane] = 0;
+    }
+    if (lane == 0) S.rb[R] = m;
+    wave_sync();
+    for (uint32_t p = lane; p < m; p += 64) {
+      const int d = run_of(S.rb, R, p);
+      const uint32_t src = S.cur[d] + (p - S.rb[d]);
+      S.u.s.dd[0][p] = DD[src];
+      S.u.s.ix[0][p] = IX[src];
+      S.u.s.tg[0][p] = (uint8_t)d;
+    }
+    wave_sync();
+    // merged order: own index + requests of the other runs that precede
+    for (uint32_t p = lane; p < m; p += 64) {
+      const int d = S.u.s.tg[0][p];
+      const int64_t x = S.u.s.dd[0][p];
+      const uint32_t xi = S.u.s.ix[0][p];
+      uint32_t r = p - S.rb[d];
+      for (int d2 = 0; d2 < R; d2++) {
+        if (d2 == d) continue;
+        uint32_t a = S.rb[d2], b = S.rb[d2 + 1];
+        while (a < b) {
+          const uint32_t mid = (a + b) >> 1;
+          if (key_less(S.u.s.dd[0][mid], S.u.s.ix[0][mid], x, xi)) a = mid + 1;
+          else b = mid;
+        }
+        r += a - S.rb[d2];
+      }
+      S.u.s.dd[1][r] = x;
+      S.u.s.ix[1][r] = xi;
+      S.u.s.tg[1][r] = (uint8_t)d;
+    }
+    wave_sync();
+    // safe prefix: everything up to the smallest last-loaded request of a
+    // run that still has requests behind it
+    if (lane == 0) {
       bool ok = false;
       int64_t vd = 0;
       uint32_t vi = 0;
       for (int d = 0; d < R; d++) {
-        if (S.take[d] < S.hi[d] - S.lo[d] && S.take[d] > 0) {
-          const uint32_t q = S.rb[d + 1] - 1;
-          if (!ok || key_less(S.dd[0][q], S.ix[0][q], vd, vi)) {
-            vd = S.dd[0][q];
-            vi = S.ix[0][q];
+        const uint32_t t = S.take[d];
+        if (t > 0 && t < S.hi[d] - S.cur[d]) {
+          const uint32_t q = S.rb[d] + t - 1;
+          if (!ok || key_less(S.u.s.dd[0][q], S.u.s.ix[0][q], vd, vi)) {
+            vd = S.u.s.dd[0][q];
+            vi = S.u.s.ix[0][q];
             ok = true;
           }
         }
       }
-      S.vstar_ok = ok;
-      S.vstar_d = vd;
-      S.vstar_i = vi;
-    }
-    __syncthreads();
-    const int b = lds_merge(S.dd[0], S.ix[0], S.tg[0], S.dd[1], S.ix[1], S.tg[1], S.rb, R, m, true);
-    // safe prefix: elements <= vstar
-    if (threadIdx.x == 0) {
       uint32_t safe = m;
-      if (S.vstar_ok) {
-        uint32_t a = 0, c = m;
-        while (a < c) {
-          const uint32_t mid = (a + c) >> 1;
-          if (!key_less(S.vstar_d, S.vstar_i, S.dd[b][mid], S.ix[b][mid])) a = mid + 1;
-          else c = mid;
+      if (ok) {
+        uint32_t a = 0, b = m;
+        while (a < b) {
+          const uint32_t mid = (a + b) >> 1;
+          if (!key_less(vd, vi, S.u.s.dd[1][mid], S.u.s.ix[1][mid])) a = mid + 1;
+          else b = mid;
         }
         safe = a;
       }
       S.safe = safe;
     }
-    __syncthreads();
+    wave_sync();
     const uint32_t safe = S.safe;
-    for (uint32_t p = threadIdx.x; p < safe; p += BLK) atomicAdd(&S.used[S.tg[b][p]], 1u);
-    prefix_q(S, b, safe, xfer);
-    if (emit) {
-      for (uint32_t p = threadIdx.x; p < safe; p += BLK) {
-        const int64_t cpl = (int64_t)(p + 1) * xfer + imax(G, S.dd[b][p]);
-        if (cpl >= TIME_LIMIT) *errb |= ERR_OVERFLOW;
-        complete[S.ix[b][p]] = cpl;
+    for (uint32_t base = 0; base < safe; base += 64) {
+      const uint32_t p = base + lane;
+      int64_t v = NEG;
+      if (p < safe) {
+        v = S.u.s.dd[1][p] - (rank0 + done + p) * xfer;
+        atomicAdd(&S.used[S.u.s.tg[1][p]], 1u);
       }
+      const int64_t q = imax(gacc, wave_incl_max(v));
+      if (emit && p < safe) {
+        const int64_t cpl = (rank0 + done + p + 1) * xfer + q;
+        if (cpl >= TIME_LIMIT) *errb |= ERR_OVERFLOW;
+        const uint32_t ix = S.u.s.ix[1][p];
+        if (ix < n) complete[ix] = cpl;
+      }
+      gacc = imax(gacc, wave_max(v));
     }
-    G = (int64_t)safe * xfer + imax(G, S.qlast);
-    __syncthreads();
-    if (threadIdx.x < (uint32_t)R) S.lo[threadIdx.x] += S.used[threadIdx.x];
-    __syncthreads();
+    done += safe;
+    wave_sync();
+    if (lane < (uint32_t)R) S.cur[lane] += S.used[lane];
+    wave_sync();
   }
-  return G;
+  return gacc;
 }
 
-__global__ __launch_bounds__(BLK) void k_channel_merge(
+// Channel stage.  With channel ranks k (1-based) and the channel free at f0
+// before the call, complete_k = k*xfer + max(f0, max_{i<=k} (dd_(i) - (i-1)*xfer)).
+// A cell knows its first rank from the cell table (the sum of its row), so
+// its aggregate is one number, M_j = max over its requests of
+// (dd - (rank-1)*xfer), and the carry between cells is a running maximum.
+//
+// One wave per block and per cell.  The bucket path (buckets of width
+// 2^lg_tR <= tR hold at most one request per die): lane q gathers the
+// requests of bucket q -- die d's is at position popcount(mask_d below q) of
+// its run -- sorts them in registers, and writes them at the bucket's
+// exclusive offset, giving the merged order without any search.
+//
+// Persistent blocks, statically assigned: block b serves XCD space
+// b mod NXCD, which owns the time windows j = k*NXCD + (b mod NXCD); within a
+// space, cells go round robin in window order, so a block only ever waits
+// for cells of earlier windows (all blocks are resident).
+template <int SL>
+__global__ __launch_bounds__(64) void k_channel_merge(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals, Geo g,
     CallCtl *ctl, uint64_t *st_agg, uint64_t *st_incl, const DevState *st,
-    int64_t *__restrict__ cfnew, int64_t *__restrict__ complete, uint32_t gmax) {
+    int64_t *__restrict__ cfnew, int64_t *__restrict__ complete, uint32_t gmax, uint32_t n) {
   extern __shared__ __align__(16) unsigned char smem[];
-  MergeLds &S = *(MergeLds *)smem;
+  CellLds &S = *(CellLds *)smem;
   if (agent_load32(&ctl->err)) return;
+  const uint32_t lane = lane_id();
   const uint32_t G = ctl->G, C = g.C, Dk = g.Dk;
-  const uint64_t ncell = (uint64_t)G * C;
-  int R = 1;
-  while (R < (int)Dk) R <<= 1;
+  const uint32_t shift = ctl->shift;
+  const int64_t cbase = ctl->cbase;
+  const uint32_t lgt = g.lg_tR;
+  const bool bucketable = (shift - lgt <= 6) && shift <= 32 && (int)Dk <= SL;
+  const uint32_t xcd = blockIdx.x % NXCD;
+  const uint32_t nbx = gridDim.x / NXCD;
+  const uint32_t wins = G > xcd ? (G - 1 - xcd) / NXCD + 1 : 0;
+  const uint64_t ncx = (uint64_t)wins * C;
+  const int R = (int)Dk;
   const int64_t xfer = g.xfer;
   uint32_t errb = 0;
-  uint32_t lo0[1], hi0[1];
-  (void)lo0;
-  (void)hi0;
-  __shared__ uint32_t slo[MAX_RUNS], shi[MAX_RUNS];
-  while (true) {
-    if (threadIdx.x == 0) S.ticket = atomicAdd(&ctl->ticket, 1u);
-    __syncthreads();
-    const uint32_t tk = S.ticket;
-    __syncthreads();
-    if ((uint64_t)tk >= ncell) break;
-    const uint32_t c = tk % C, j = tk / C;
-    const uint32_t m = cell_runs(S, LB, seg_start, totals, c, j, Dk, gmax, R);
-    const size_t sidx = (size_t)c * gmax + j;
-    int64_t A;
-    bool resident = m <= MCAP;
-    int b = 0;
-    if (resident) {
-      if (threadIdx.x < (uint32_t)R) S.take[threadIdx.x] = S.hi[threadIdx.x] - S.lo[threadIdx.x];
-      __syncthreads();
-      load_runs(S, DD, IX, R, false);
-      b = lds_merge(S.dd[0], S.ix[0], S.tg[0], S.dd[1], S.ix[1], S.tg[1], S.rb, R, m, false);
-      prefix_q(S, b, m, xfer);
-      A = m ? (int64_t)m * xfer + S.qlast : NEG;
+  // cell-table row of a cell for lane d = die run d (prefetched one cell ahead)
+  auto fetch_row = [&](uint64_t t, uint32_t &lo, uint32_t &hi, uint32_t &seg) {
+    lo = hi = seg = 0;
+    if (t < ncx && lane < Dk) {
+      const uint32_t cc = (uint32_t)(t % C);
+      const uint32_t jj = (uint32_t)(t / C) * NXCD + xcd;
+      const uint32_t k = cc * Dk + lane;
+      const uint32_t *lbrow = LB + (size_t)cc * (gmax + 1) * Dk + lane;
+      lo = lbrow[(size_t)jj * Dk];
+      hi = lbrow[(size_t)(jj + 1) * Dk];
+      seg = seg_start[k];
+      if (totals[k] == 0) lo = hi = 0;
+    }
+  };
+  uint32_t nlo, nhi, nseg;
+  fetch_row(blockIdx.x / NXCD, nlo, nhi, nseg);
+  for (uint64_t tk = blockIdx.x / NXCD; tk < ncx; tk += nbx) {
+    const uint32_t c = (uint32_t)(tk % C);
+    const uint32_t j = (uint32_t)(tk / C) * NXCD + xcd;
+    const int64_t cstart = cbase + ((int64_t)j << shift);
+    // runs of the cell: lane d = die run d
+    uint32_t lo = nlo, hi = nhi;
+    const uint32_t r0 = lo;
+    lo += nseg;
+    hi += nseg;
+    fetch_row(tk + nbx, nlo, nhi, nseg);
+    const uint32_t len = hi - lo;
+    const uint32_t rbx = wave_excl_sum(len);
+    const uint32_t m = wave_sum(len);
+    const int64_t rank0 = wave_sum(r0);  // channel rank of the cell's first request
+    if (lane < Dk) {
+      S.lo[lane] = lo;
+      S.hi[lane] = hi;
+      S.rb[lane] = rbx;
+      S.mask[lane] = 0;
+    }
+    if (lane == 0) S.rb[R] = m;
+    wave_sync();
+    const size_t row = (size_t)c * gmax;
+    const bool fast = bucketable && m <= MCAP;
+    int64_t M = NEG;
+    int64_t Q[MCAP / 64];
+    if (fast) {
+      // load keys in run order (all loads in flight at once); mark buckets
+      constexpr int LE = MCAP / 64;
+      int dv[LE];
+      int64_t ddv[LE];
+      uint32_t ixv[LE];
+#pragma unroll
+      for (int e = 0; e < LE; e++) {
+        const uint32_t p = lane + 64 * e;
+        dv[e] = 0;
+        ddv[e] = 0;
+        ixv[e] = 0;
+        if (p < m) {
+          const int d = run_of(S.rb, R, p);
+          const uint32_t src = S.lo[d] + (p - S.rb[d]);
+          dv[e] = d;
+          ddv[e] = DD[src];
+          ixv[e] = IX[src];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < LE; e++) {
+        const uint32_t p = lane + 64 * e;
+        if (p < m) {
+          const uint64_t rel = (uint64_t)(ddv[e] - cstart);
+          S.u.f.in[p] = (rel << 32) | ixv[e];
+          atomicOr((unsigned long long *)&S.mask[dv[e]], 1ull << (rel >> lgt));
+        }
+      }
+      wave_sync();
+      // lane q: gather, sort and place bucket q
+      uint64_t slot[SL];
+      uint32_t cnt = 0;
+      const uint64_t below = (1ull << lane) - 1;
+#pragma unroll
+      for (int d = 0; d < SL; d++) {
+        slot[d] = ~0ull;
+        if (d < R) {
+          const uint64_t mk = S.mask[d];
+          const uint32_t y = S.rb[d] + (uint32_t)__popcll(mk & below);
+          if (((mk >> lane) & 1ull) && y < m) {
+            slot[d] = S.u.f.in[y];
+            cnt++;
+          }
+        }
+      }
+      sort_slots<SL>(slot);
+      const uint32_t boff = wave_excl_sum(cnt);
+#pragma unroll
+      for (int i = 0; i < SL; i++)
+        if ((uint32_t)i < cnt) S.u.f.out[pad16(boff + i)] = slot[i];
+      wave_sync();
+      // Lindley prefix over the merged order: lane l owns positions 16l..16l+15
+      int64_t loc = NEG;
+      const int64_t cst = cstart - rank0 * xfer;
+#pragma unroll
+      for (int e = 0; e < MCAP / 64; e++) {
+        const uint32_t p = lane * (MCAP / 64) + e;
+        Q[e] = NEG;
+        if (p < m) {
+          const uint32_t rel = (uint32_t)(S.u.f.out[pad16(p)] >> 32);
+          Q[e] = cst + (int64_t)rel - (int64_t)mul32(p, (uint32_t)xfer);
+          loc = imax(loc, Q[e]);
+        }
+      }
+      int64_t run = __shfl_up(wave_incl_max(loc), 1);
+      if (lane == 0) run = NEG;
+#pragma unroll
+      for (int e = 0; e < MCAP / 64; e++) {
+        run = imax(run, Q[e]);
+        Q[e] = run;
+      }
+      M = wave_max(loc);
     } else {
-      if (threadIdx.x < (uint32_t)R) {
-        slo[threadIdx.x] = S.lo[threadIdx.x];
-        shi[threadIdx.x] = S.hi[threadIdx.x];
-      }
-      __syncthreads();
-      A = stream_cell(S, DD, IX, R, NEG, xfer, false, complete, &errb, slo, shi);
+      M = stream_cell(S, DD, IX, R, NEG, rank0, xfer, false, complete, n, &errb);
     }
-    // publish the cell aggregate, then find the incoming channel clock
-    if (threadIdx.x == 0) agent_store(&st_agg[sidx], enc_time(A));
-    if (threadIdx.x < 64) {
-      const int64_t gin = look_back(st_agg, st_incl, LB, totals, st, c, j, Dk, gmax, xfer);
-      if (threadIdx.x == 0) {
-        S.gin = gin;
-        const int64_t gout = imax(A, gin + (int64_t)m * xfer);
-        agent_store(&st_incl[sidx], enc_time(gout));
-        if (j + 1 == G) cfnew[c] = gout;
-      }
+    // publish the aggregate, fold the predecessors, publish the prefix
+    if (lane == 0) agent_store(&st_agg[row + j], enc_time(M));
+    const int64_t gin = look_back(st_agg, st_incl, st->chan_free[c], row, j);
+    if (lane == 0) {
+      agent_store(&st_incl[row + j], enc_time(imax(gin, M)));
+      if (j + 1 == G) cfnew[c] = (rank0 + m) * xfer + imax(gin, M);
     }
-    __syncthreads();
-    const int64_t gin = S.gin;
-    if (resident) {
-      for (uint32_t p = threadIdx.x; p < m; p += BLK) {
-        const int64_t cpl = (int64_t)(p + 1) * xfer + imax(gin, S.dd[b][p]);
-        if (cpl >= TIME_LIMIT) errb |= ERR_OVERFLOW;
-        complete[S.ix[b][p]] = cpl;
+    if (fast) {
+      const int64_t r0x = rank0 * xfer;
+#pragma unroll
+      for (int e = 0; e < MCAP / 64; e++) {
+        const uint32_t p = lane * (MCAP / 64) + e;
+        if (p < m) {
+          const int64_t cpl = r0x + (int64_t)mul32(p + 1, (uint32_t)xfer) + imax(gin, Q[e]);
+          if (cpl >= TIME_LIMIT) errb |= ERR_OVERFLOW;
+          const uint32_t ix = (uint32_t)S.u.f.out[pad16(p)];
+          if (ix < n) complete[ix] = cpl;
+        }
       }
     } else {
-      stream_cell(S, DD, IX, R, gin, xfer, true, complete, &errb, slo, shi);
+      stream_cell(S, DD, IX, R, gin, rank0, xfer, true, complete, n, &errb);
     }
-    __syncthreads();
+    wave_sync();
   }
   if (errb) atomicOr(&ctl->err, errb);
 }
@@ -1054,7 +1160,7 @@ size_t lds_die_reduce(uint32_t K) {
   return align16(sizeof(LdsRanges)) + K * (8 + 4) + WAVES * K * 2 + K * 2;
 }
 size_t lds_die_scatter(uint32_t K) {
-  return align16(sizeof(LdsRanges)) + CHUNK * 8 + K * (8 + 4 + 4) + CHUNK * 4 + WAVES * K * 2 + K * 4;
+  return (size_t)CHUNKP * 8 + (size_t)K * (8 + 4 * 6) + (size_t)CHUNKP * 4;
 }
 
 hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout &Lo, char *ws,
@@ -1071,6 +1177,7 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   int64_t *cfnew = (int64_t *)(ws + Lo.off_cfnew);
   int64_t *DD = (int64_t *)(ws + Lo.off_dd);
   uint32_t *IX = (uint32_t *)(ws + Lo.off_ix);
+  uint32_t *KR = (uint32_t *)(ws + Lo.off_kr);
   uint32_t *LB = (uint32_t *)(ws + Lo.off_lb);
   uint64_t *st_agg = (uint64_t *)(ws + Lo.off_st_agg);
   uint64_t *st_incl = (uint64_t *)(ws + Lo.off_st_incl);
@@ -1095,10 +1202,10 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     const size_t lds = lds_die_reduce(g.K);
     if (p2)
       hipLaunchKernelGGL(k_die_reduce<true>, dim3(Lo.nt), dim3(BLK), lds, s, addr, issue, Lo.n, complete,
-                         g, rt, Lo.tile_elems, agg_cnt, agg_A, ctl, kbits);
+                         g, rt, Lo.tile_elems, agg_cnt, agg_A, KR, ctl, kbits);
     else
       hipLaunchKernelGGL(k_die_reduce<false>, dim3(Lo.nt), dim3(BLK), lds, s, addr, issue, Lo.n,
-                         complete, g, rt, Lo.tile_elems, agg_cnt, agg_A, ctl, kbits);
+                         complete, g, rt, Lo.tile_elems, agg_cnt, agg_A, KR, ctl, kbits);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
@@ -1111,22 +1218,36 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   mark();
   {
     const size_t lds = lds_die_scatter(g.K);
-    if (p2)
-      hipLaunchKernelGGL(k_die_scatter<true>, dim3(Lo.nt), dim3(BLK), lds, s, addr, issue, Lo.n, g, rt,
-                         Lo.tile_elems, tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl, kbits);
-    else
-      hipLaunchKernelGGL(k_die_scatter<false>, dim3(Lo.nt), dim3(BLK), lds, s, addr, issue, Lo.n, g, rt,
-                         Lo.tile_elems, tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl, kbits);
+    hipLaunchKernelGGL(k_die_scatter, dim3(Lo.nt), dim3(BLK), lds, s, issue, KR, Lo.n, g, Lo.tile_elems,
+                       tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
   {
-    int dev = 0, ncu = 256;
+    int dev = 0, ncu = 256, per_cu = 0;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
-    const uint32_t blocks = (uint32_t)ncu * 2;
-    hipLaunchKernelGGL(k_channel_merge, dim3(blocks), dim3(BLK), sizeof(MergeLds), s, DD, IX, LB, seg,
-                       totals, g, ctl, st_agg, st_incl, st, cfnew, complete, Lo.gmax);
+    const void *kfn = g.Dk <= 4 ? (const void *)k_channel_merge<4>
+                      : g.Dk <= 8 ? (const void *)k_channel_merge<8> : (const void *)k_channel_merge<16>;
+    hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64, sizeof(CellLds));
+    // every block must be resident: blocks wait (look-back) on cells that
+    // blocks of another XCD's space hold
+    per_cu = per_cu < 1 ? 1 : (per_cu > 16 ? 16 : per_cu);
+    uint32_t blocks = (uint32_t)ncu * (uint32_t)per_cu;
+    blocks = (blocks / NXCD) * NXCD;
+    if (blocks < NXCD) blocks = NXCD;
+    if (g.Dk <= 4)
+      hipLaunchKernelGGL(k_channel_merge<4>, dim3(blocks), dim3(64), sizeof(CellLds), s, DD, IX, LB, seg,
+                         totals, g, ctl, st_agg, st_incl, st, cfnew, complete, Lo.gmax,
+                         (uint32_t)Lo.n);
+    else if (g.Dk <= 8)
+      hipLaunchKernelGGL(k_channel_merge<8>, dim3(blocks), dim3(64), sizeof(CellLds), s, DD, IX, LB, seg,
+                         totals, g, ctl, st_agg, st_incl, st, cfnew, complete, Lo.gmax,
+                         (uint32_t)Lo.n);
+    else
+      hipLaunchKernelGGL(k_channel_merge<16>, dim3(blocks), dim3(64), sizeof(CellLds), s, DD, IX, LB, seg,
+                         totals, g, ctl, st_agg, st_incl, st, cfnew, complete, Lo.gmax,
+                         (uint32_t)Lo.n);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
@@ -1161,21 +1282,17 @@ hipError_t launch_reset(DevState *st, hipStream_t s) {
 
 hipError_t set_lds_limits(uint32_t K) {
   hipError_t e;
-  const int a = (int)lds_die_reduce(K), b = (int)lds_die_scatter(K), c = (int)sizeof(MergeLds);
+  const int a = (int)lds_die_reduce(K), b = (int)lds_die_scatter(K);
   if ((e = hipFuncSetAttribute((const void *)k_die_reduce<true>,
                                hipFuncAttributeMaxDynamicSharedMemorySize, a)) != hipSuccess)
     return e;
   if ((e = hipFuncSetAttribute((const void *)k_die_reduce<false>,
                                hipFuncAttributeMaxDynamicSharedMemorySize, a)) != hipSuccess)
     return e;
-  if ((e = hipFuncSetAttribute((const void *)k_die_scatter<true>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, b)) != hipSuccess)
+  if ((e = hipFuncSetAttribute((const void *)k_die_scatter, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               b)) != hipSuccess)
     return e;
-  if ((e = hipFuncSetAttribute((const void *)k_die_scatter<false>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, b)) != hipSuccess)
-    return e;
-  return hipFuncSetAttribute((const void *)k_channel_merge, hipFuncAttributeMaxDynamicSharedMemorySize,
-                             c);
+  return hipSuccess;
 }
 
 }  // namespace hbf
