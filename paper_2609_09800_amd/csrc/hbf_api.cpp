@@ -328,6 +328,7 @@ int hbf_get_status(hbf_model_t m, void *stream) {
   if (s & (ERR_RANGE_TIME | ERR_OVERFLOW)) return HBF_ERANGE_TIME;
   if (s & ERR_UNSORTED) return HBF_EUNSORTED;
   if (s & ERR_MAP) return HBF_EINVAL;
+  if (s & ERR_INTERNAL) return HBF_EHIP;
   return HBF_OK;
 }
 

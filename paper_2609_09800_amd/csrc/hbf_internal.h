@@ -26,6 +26,7 @@ constexpr uint32_t ERR_RANGE_TIME = 1u;
 constexpr uint32_t ERR_UNSORTED = 2u;
 constexpr uint32_t ERR_OVERFLOW = 4u;
 constexpr uint32_t ERR_MAP = 8u;
+constexpr uint32_t ERR_INTERNAL = 16u;  // a bounded device wait gave up (a bug, never expected)
 
 // Die stage: 256 threads (4 wave64), 16 items per thread per chunk.
 constexpr int BLK = 256;

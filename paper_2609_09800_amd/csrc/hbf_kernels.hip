@@ -675,45 +675,68 @@ DEVI void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
 }
-DEVI uint32_t wave_sum(uint32_t x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+// DPP cross-lane moves (gfx9 row_shr / row_bcast): lanes without a source, or
+// in rows outside ROWMASK, keep `old`.
+template <int CTRL, int ROWMASK>
+DEVI uint32_t dpp32(uint32_t old, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROWMASK, 0xF, false);
+}
+template <int CTRL, int ROWMASK>
+DEVI int64_t dpp64(int64_t old, int64_t x) {
+  const uint32_t lo = dpp32<CTRL, ROWMASK>((uint32_t)old, (uint32_t)x);
+  const uint32_t hi = dpp32<CTRL, ROWMASK>((uint32_t)((uint64_t)old >> 32), (uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114, DPP_ROW_SHR8 = 0x118;
+constexpr int DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
+// Inclusive scans over the 64 lanes: within rows of 16 by shifts of 1, 2,
+// 4, 8, then row 0 -> 1 and 2 -> 3 (bcast15), then rows 0-1 -> 2-3 (bcast31).
+DEVI uint32_t wave_incl_sum(uint32_t x) {
+  x += dpp32<DPP_ROW_SHR1, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_SHR2, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_SHR4, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_SHR8, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_BCAST15, 0xA>(0u, x);
+  x += dpp32<DPP_ROW_BCAST31, 0xC>(0u, x);
   return x;
 }
-DEVI uint32_t wave_excl_sum(uint32_t v) {
-  const uint32_t lane = lane_id();
-  uint32_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t y = __shfl_up(x, d);
-    if (lane >= (uint32_t)d) x += y;
-  }
-  return x - v;
-}
-DEVI int64_t wave_max(int64_t x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = imax(x, __shfl_xor(x, o));
+DEVI uint32_t wave_incl_umax(uint32_t x) {
+  x = max(x, dpp32<DPP_ROW_SHR1, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_SHR2, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_SHR4, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_SHR8, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_BCAST15, 0xA>(0u, x));
+  x = max(x, dpp32<DPP_ROW_BCAST31, 0xC>(0u, x));
   return x;
 }
-DEVI int64_t wave_incl_max(int64_t v) {
-  const uint32_t lane = lane_id();
-  int64_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int64_t y = __shfl_up(x, d);
-    if (lane >= (uint32_t)d) x = imax(x, y);
-  }
+DEVI int64_t wave_incl_max(int64_t x) {
+  x = imax(x, dpp64<DPP_ROW_SHR1, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR2, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR4, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR8, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_BCAST15, 0xA>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_BCAST31, 0xC>(NEG, x));
   return x;
 }
+DEVI uint32_t lane63(uint32_t x) { return (uint32_t)__builtin_amdgcn_readlane((int)x, 63); }
+DEVI int64_t lane63(int64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), 63);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+DEVI uint32_t wave_sum(uint32_t x) { return lane63(wave_incl_sum(x)); }
+DEVI uint32_t wave_excl_sum(uint32_t v) { return wave_incl_sum(v) - v; }
+DEVI int64_t wave_max(int64_t x) { return lane63(wave_incl_max(x)); }
+DEVI uint32_t wave_umax(uint32_t x) { return lane63(wave_incl_umax(x)); }
 
-constexpr int CAP_S = 512;     // requests per round of a streamed cell
+constexpr int CAP_S = 256;     // requests per round of a streamed cell
 constexpr int SLOTS_MAX = 16;  // die runs per channel on the bucket path
 
 struct CellLds {
   union {
     struct {
-      uint64_t in[MCAP];   // (dd - cell start) << 32 | index, in run order
-      uint64_t out[MCAP + MCAP / 16];  // the same keys in merged order (padded index)
+      uint64_t in[MCAP];                 // (dd - cell start) << 32 | index, in run order
+      uint8_t tbl[MAX_BUCKETS][SLOTS_MAX];  // 1 + position in its run of die d's request in bucket q
     } f;
     struct {
       int64_t dd[2][CAP_S];
@@ -721,7 +744,6 @@ struct CellLds {
       uint8_t tg[2][CAP_S];
     } s;
   } u;
-  uint64_t mask[MAX_RUNS];   // per run: occupied time buckets
   uint32_t rb[MAX_RUNS + 1]; // run offsets in the staging buffer
   uint32_t lo[MAX_RUNS];     // run bounds: global positions in the die order
   uint32_t hi[MAX_RUNS];
@@ -735,11 +757,16 @@ struct CellLds {
 // cell j, max(f0, M_j' for j' < j).  Lane l inspects cell base-l; the fold
 // stops at the nearest inclusive prefix and waits only for cells that have
 // published nothing yet.
+// The wait is bounded: after LOOKBACK_SPINS empty rounds (far beyond any
+// real wait) it reports ERR_INTERNAL, which fails the call, and returns.
+constexpr uint32_t LOOKBACK_SPINS = 1u << 20;
+
 DEVI int64_t look_back(const uint64_t *st_agg, const uint64_t *st_incl, int64_t f0, size_t row,
-                       uint32_t j) {
+                       uint32_t j, uint32_t *errb) {
   const uint32_t lane = lane_id();
   int64_t acc = NEG;
   int64_t base = (int64_t)j - 1;
+  uint32_t spins = 0;
   while (true) {
     const int64_t jj = base - (int64_t)lane;
     int stt = 0;
@@ -767,7 +794,13 @@ DEVI int64_t look_back(const uint64_t *st_agg, const uint64_t *st_incl, int64_t 
     if (fi < fn) return imax(acc, wave_max(lane <= fi ? v : NEG));
     acc = imax(acc, wave_max(lane < fn ? v : NEG));
     base -= fn;
-    if (fn == 0) __builtin_amdgcn_s_sleep(1);
+    if (fn == 0) {
+      if (++spins > LOOKBACK_SPINS) {
+        *errb |= ERR_INTERNAL;
+        return acc;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
   }
 }
 
@@ -916,10 +949,11 @@ DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, int 
 // its run -- sorts them in registers, and writes them at the bucket's
 // exclusive offset, giving the merged order without any search.
 //
-// Persistent blocks, statically assigned: block b serves XCD space
-// b mod NXCD, which owns the time windows j = k*NXCD + (b mod NXCD); within a
-// space, cells go round robin in window order, so a block only ever waits
-// for cells of earlier windows (all blocks are resident).
+// Persistent blocks: block b serves XCD space b mod NXCD, which owns the
+// time windows j = k*NXCD + (b mod NXCD) (the same window of every channel
+// completes in one L2).  Within a space, cells are claimed in window order
+// from an atomic counter; a cell only waits for cells of earlier windows,
+// each already claimed by a running block, so every wait ends.
 template <int SL>
 __global__ __launch_bounds__(64) void k_channel_merge(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
@@ -936,13 +970,21 @@ __global__ __launch_bounds__(64) void k_channel_merge(
   const uint32_t lgt = g.lg_tR;
   const bool bucketable = (shift - lgt <= 6) && shift <= 32 && (int)Dk <= SL;
   const uint32_t xcd = blockIdx.x % NXCD;
-  const uint32_t nbx = gridDim.x / NXCD;
   const uint32_t wins = G > xcd ? (G - 1 - xcd) / NXCD + 1 : 0;
   const uint64_t ncx = (uint64_t)wins * C;
   const int R = (int)Dk;
   const int64_t xfer = g.xfer;
   uint32_t errb = 0;
-  // cell-table row of a cell for lane d = die run d (prefetched one cell ahead)
+  // cells are claimed in order from this XCD space's counter, one ahead of
+  // the cell being processed (its table row is fetched early too); a block
+  // owns a cell only once it runs, so progress never depends on residency
+  auto claim = [&]() -> uint64_t {
+    uint32_t t = 0;
+    if (lane == 0)
+      t = __hip_atomic_fetch_add(&ctl->ticket[xcd], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return (uint64_t)__builtin_amdgcn_readfirstlane(t);
+  };
+  // cell-table row of a cell for lane d = die run d
   auto fetch_row = [&](uint64_t t, uint32_t &lo, uint32_t &hi, uint32_t &seg) {
     lo = hi = seg = 0;
     if (t < ncx && lane < Dk) {
@@ -957,8 +999,10 @@ __global__ __launch_bounds__(64) void k_channel_merge(
     }
   };
   uint32_t nlo, nhi, nseg;
-  fetch_row(blockIdx.x / NXCD, nlo, nhi, nseg);
-  for (uint64_t tk = blockIdx.x / NXCD; tk < ncx; tk += nbx) {
+  uint64_t tk = claim();
+  fetch_row(tk, nlo, nhi, nseg);
+  while (tk < ncx) {
+    const uint64_t tnext = claim();
     const uint32_t c = (uint32_t)(tk % C);
     const uint32_t j = (uint32_t)(tk / C) * NXCD + xcd;
     const int64_t cstart = cbase + ((int64_t)j << shift);
@@ -967,7 +1011,7 @@ __global__ __launch_bounds__(64) void k_channel_merge(
     const uint32_t r0 = lo;
     lo += nseg;
     hi += nseg;
-    fetch_row(tk + nbx, nlo, nhi, nseg);
+    fetch_row(tnext, nlo, nhi, nseg);
     const uint32_t len = hi - lo;
     const uint32_t rbx = wave_excl_sum(len);
     const uint32_t m = wave_sum(len);
@@ -976,93 +1020,92 @@ __global__ __launch_bounds__(64) void k_channel_merge(
       S.lo[lane] = lo;
       S.hi[lane] = hi;
       S.rb[lane] = rbx;
-      S.mask[lane] = 0;
+
     }
     if (lane == 0) S.rb[R] = m;
     wave_sync();
     const size_t row = (size_t)c * gmax;
-    const bool fast = bucketable && m <= MCAP;
+    const uint32_t maxlen = wave_umax(lane < Dk ? len : 0u);
+    const bool fast = bucketable && maxlen <= 64;
     int64_t M = NEG;
-    int64_t Q[MCAP / 64];
+    // bucket path state: lane q holds the requests of bucket q, which are
+    // merged positions boff..boff+cnt-1 (lanes are in merged order)
+    uint64_t slot[SL];
+    uint32_t idxv[SL];
+    uint32_t cnt = 0, boff = 0;
     if (fast) {
-      // load keys in run order (all loads in flight at once); mark buckets
-      constexpr int LE = MCAP / 64;
-      int dv[LE];
-      int64_t ddv[LE];
-      uint32_t ixv[LE];
+      // clear the bucket table (1 KB: 16 B per lane)
+      reinterpret_cast<uint4 *>(&S.u.f.tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
+      // load every run (one lane per request; all loads in flight at once)
+      int64_t ddv[SL];
+      uint32_t ixv[SL];
 #pragma unroll
-      for (int e = 0; e < LE; e++) {
-        const uint32_t p = lane + 64 * e;
-        dv[e] = 0;
-        ddv[e] = 0;
-        ixv[e] = 0;
-        if (p < m) {
-          const int d = run_of(S.rb, R, p);
-          const uint32_t src = S.lo[d] + (p - S.rb[d]);
-          dv[e] = d;
-          ddv[e] = DD[src];
-          ixv[e] = IX[src];
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < LE; e++) {
-        const uint32_t p = lane + 64 * e;
-        if (p < m) {
-          const uint64_t rel = (uint64_t)(ddv[e] - cstart);
-          S.u.f.in[p] = (rel << 32) | ixv[e];
-          atomicOr((unsigned long long *)&S.mask[dv[e]], 1ull << (rel >> lgt));
+      for (int d = 0; d < SL; d++) {
+        const uint32_t lod = __builtin_amdgcn_readlane(lo, d);
+        const uint32_t lend = __builtin_amdgcn_readlane(len, d);
+        ddv[d] = 0;
+        ixv[d] = 0;
+        if (d < R && lane < lend) {
+          ddv[d] = DD[lod + lane];
+          ixv[d] = IX[lod + lane];
         }
       }
       wave_sync();
-      // lane q: gather, sort and place bucket q
-      uint64_t slot[SL];
-      uint32_t cnt = 0;
-      const uint64_t below = (1ull << lane) - 1;
 #pragma unroll
       for (int d = 0; d < SL; d++) {
+        const uint32_t lend = __builtin_amdgcn_readlane(len, d);
+        const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
+        if (d < R && lane < lend) {
+          const uint64_t rel = (uint64_t)(ddv[d] - cstart);
+          S.u.f.in[rbd + lane] = (rel << 32) | ixv[d];
+          S.u.f.tbl[rel >> lgt][d] = (uint8_t)(lane + 1);
+        }
+      }
+      wave_sync();
+      // lane q: gather, sort and count bucket q
+      const uint4 row = reinterpret_cast<const uint4 *>(&S.u.f.tbl[0][0])[lane];
+      const uint32_t rw[4] = {row.x, row.y, row.z, row.w};
+#pragma unroll
+      for (int d = 0; d < SL; d++) {
+        const uint32_t y = (rw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
+        const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
         slot[d] = ~0ull;
-        if (d < R) {
-          const uint64_t mk = S.mask[d];
-          const uint32_t y = S.rb[d] + (uint32_t)__popcll(mk & below);
-          if (((mk >> lane) & 1ull) && y < m) {
-            slot[d] = S.u.f.in[y];
-            cnt++;
-          }
+        if (y) {
+          slot[d] = S.u.f.in[rbd + y - 1];
+          cnt++;
         }
       }
       sort_slots<SL>(slot);
-      const uint32_t boff = wave_excl_sum(cnt);
-#pragma unroll
-      for (int i = 0; i < SL; i++)
-        if ((uint32_t)i < cnt) S.u.f.out[pad16(boff + i)] = slot[i];
-      wave_sync();
-      // Lindley prefix over the merged order: lane l owns positions 16l..16l+15
-      int64_t loc = NEG;
+      boff = wave_excl_sum(cnt);
+      // Lindley prefix over the merged order, in registers
       const int64_t cst = cstart - rank0 * xfer;
+      int64_t loc = NEG;
 #pragma unroll
-      for (int e = 0; e < MCAP / 64; e++) {
-        const uint32_t p = lane * (MCAP / 64) + e;
-        Q[e] = NEG;
-        if (p < m) {
-          const uint32_t rel = (uint32_t)(S.u.f.out[pad16(p)] >> 32);
-          Q[e] = cst + (int64_t)rel - (int64_t)mul32(p, (uint32_t)xfer);
-          loc = imax(loc, Q[e]);
+      for (int i = 0; i < SL; i++) {
+        if ((uint32_t)i < cnt) {
+          const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+          loc = imax(loc, v);
         }
       }
-      int64_t run = __shfl_up(wave_incl_max(loc), 1);
-      if (lane == 0) run = NEG;
-#pragma unroll
-      for (int e = 0; e < MCAP / 64; e++) {
-        run = imax(run, Q[e]);
-        Q[e] = run;
-      }
       M = wave_max(loc);
+      int64_t carry = __shfl_up(wave_incl_max(loc), 1);
+      if (lane == 0) carry = NEG;
+      // slot i becomes its prefix value; its request index moves to idxv[i]
+#pragma unroll
+      for (int i = 0; i < SL; i++) {
+        idxv[i] = (uint32_t)slot[i];
+        if ((uint32_t)i < cnt) {
+          const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+          carry = imax(carry, v);
+        }
+        slot[i] = (uint64_t)carry;
+      }
     } else {
       M = stream_cell(S, DD, IX, R, NEG, rank0, xfer, false, complete, n, &errb);
     }
     // publish the aggregate, fold the predecessors, publish the prefix
     if (lane == 0) agent_store(&st_agg[row + j], enc_time(M));
-    const int64_t gin = look_back(st_agg, st_incl, st->chan_free[c], row, j);
+    const int64_t gin = look_back(st_agg, st_incl, st->chan_free[c], row, j, &errb);
     if (lane == 0) {
       agent_store(&st_incl[row + j], enc_time(imax(gin, M)));
       if (j + 1 == G) cfnew[c] = (rank0 + m) * xfer + imax(gin, M);
@@ -1070,19 +1113,18 @@ __global__ __launch_bounds__(64) void k_channel_merge(
     if (fast) {
       const int64_t r0x = rank0 * xfer;
 #pragma unroll
-      for (int e = 0; e < MCAP / 64; e++) {
-        const uint32_t p = lane * (MCAP / 64) + e;
-        if (p < m) {
-          const int64_t cpl = r0x + (int64_t)mul32(p + 1, (uint32_t)xfer) + imax(gin, Q[e]);
+      for (int i = 0; i < SL; i++) {
+        if ((uint32_t)i < cnt) {
+          const int64_t cpl = r0x + (int64_t)mul32(boff + i + 1, (uint32_t)xfer) + imax(gin, (int64_t)slot[i]);
           if (cpl >= TIME_LIMIT) errb |= ERR_OVERFLOW;
-          const uint32_t ix = (uint32_t)S.u.f.out[pad16(p)];
-          if (ix < n) complete[ix] = cpl;
+          if (idxv[i] < n) complete[idxv[i]] = cpl;
         }
       }
     } else {
       stream_cell(S, DD, IX, R, gin, rank0, xfer, true, complete, n, &errb);
     }
     wave_sync();
+    tk = tnext;
   }
   if (errb) atomicOr(&ctl->err, errb);
 }
@@ -1230,8 +1272,6 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     const void *kfn = g.Dk <= 4 ? (const void *)k_channel_merge<4>
                       : g.Dk <= 8 ? (const void *)k_channel_merge<8> : (const void *)k_channel_merge<16>;
     hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64, sizeof(CellLds));
-    // every block must be resident: blocks wait (look-back) on cells that
-    // blocks of another XCD's space hold
     per_cu = per_cu < 1 ? 1 : (per_cu > 16 ? 16 : per_cu);
     uint32_t blocks = (uint32_t)ncu * (uint32_t)per_cu;
     blocks = (blocks / NXCD) * NXCD;
