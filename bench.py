@@ -26,8 +26,8 @@ METRIC = "modeled HBF requests/sec + achieved HBM GB/s (% peak), 1 MI355X; delay
 HBM_PEAK_GBPS = 8000.0
 # Algorithmic HBM bytes per in-range request of each timing kernel (reads +
 # writes the kernel cannot avoid), and of the whole call.
-ALG_BYTES = {"k_die_reduce": 16, "k_die_scatter": 28, "k_channel_merge": 20}
-PATH_ALG_BYTES = 24
+ALG_BYTES = {"k_die_reduce": 20, "k_die_scatter": 24, "k_cell_agg": 12, "k_cell_out": 20}
+PATH_ALG_BYTES = 24  # read addr + issue, write complete
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic_config5.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_09800_amd", "csrc", "hbf_kernels.hip")
 
@@ -59,6 +59,25 @@ def traffic_for(kernel, n):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
+def load_or_generate(wl, n, cache):
+    """The large mixed stream; with a cache directory it is generated once and
+    then read back (the generator is deterministic in its seed and size)."""
+    if cache:
+        pa = os.path.join(cache, f"config5_n{n}_addr.npy")
+        pi = os.path.join(cache, f"config5_n{n}_issue.npy")
+        if os.path.exists(pa) and os.path.exists(pi):
+            w = wl.config5(n=1024)  # geometry and ranges
+            w.addr, w.issue = np.load(pa), np.load(pi)
+            assert w.n == n
+            return w
+    w = wl.config5(n=n)
+    if cache:
+        os.makedirs(cache, exist_ok=True)
+        np.save(pa, w.addr)
+        np.save(pi, w.issue)
+    return w
+
+
 def cpu_baseline(w, n_sample):
     from oracle import oracle
     m = oracle.OracleModel(**w.params)
@@ -81,7 +100,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--n", type=int, default=1 << 28, help="requests in the large stream")
     ap.add_argument("--batch", type=int, default=16, help="GEMV batch")
-    ap.add_argument("--cpu-sample", type=int, default=1 << 28)
+    ap.add_argument("--cpu-sample", type=int, default=1 << 28,
+                    help="requests of the stream the CPU reference model times (whole stream: about 20 s)")
+    ap.add_argument("--inputs-cache", default=None,
+                    help="directory to keep the generated stream in (.npy) for repeated runs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--no-gemv", action="store_true", help="time only hbf_time_requests (diagnostic)")
     ap.add_argument("--copy-calib", action="store_true",
@@ -111,11 +133,8 @@ def main():
 
     # ---------------- inputs
     t = time.time()
-    if args.n == 1 << 28:
-        w = wl.config5()
-    else:
-        w = wl.config5(n=args.n)
-    log(f"generated {w.n} requests in {time.time() - t:.1f} s")
+    w = load_or_generate(wl, args.n, args.inputs_cache)
+    log(f"inputs for {w.n} requests ready in {time.time() - t:.1f} s")
     model = hbf.Model(**w.params)
     for b, nb in w.ranges:
         assert model.register_range(b, nb)[0] == 0

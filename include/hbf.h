@@ -187,9 +187,8 @@ int hbf_gemv_instrumented(hbf_model_t model, const uint16_t *dev_W, int E, int K
 int hbf_wall_clock_tick_ps(hbf_model_t model, int64_t *tick_ps);
 
 /* Synchronise `stream`, then return and clear the sticky device status:
- * HBF_OK, HBF_ERANGE_TIME, HBF_EUNSORTED, HBF_EINVAL or HBF_EHIP (in that
- * order of precedence; HBF_EHIP here means a bounded device-side wait gave
- * up, an internal error that fails the call like the others). */
+ * HBF_OK, HBF_ERANGE_TIME, HBF_EUNSORTED or HBF_EINVAL (in that order of
+ * precedence); HBF_EHIP if synchronising or reading the status fails. */
 int hbf_get_status(hbf_model_t model, void *stream);
 
 /* Copy the resource clocks to host memory after synchronising `stream`:

@@ -52,8 +52,8 @@ Layout make_layout(const Geo &g, int64_t n) {
   L.off_ix = o;       o = up256(o + (size_t)n * 4);
   L.off_kr = o;       o = up256(o + (size_t)n * 4);
   L.off_lb = o;       o = up256(o + C * ((size_t)L.gmax + 1) * g.Dk * 4);
-  L.off_st_agg = o;   o = up256(o + C * (size_t)L.gmax * 8);
-  L.off_st_incl = o;  o = up256(o + C * (size_t)L.gmax * 8);
+  L.off_cagg = o;     o = up256(o + C * (size_t)L.gmax * 8);
+  L.off_cgin = o;     o = up256(o + C * (size_t)L.gmax * 8);
   L.total = o;
   return L;
 }
@@ -328,7 +328,6 @@ int hbf_get_status(hbf_model_t m, void *stream) {
   if (s & (ERR_RANGE_TIME | ERR_OVERFLOW)) return HBF_ERANGE_TIME;
   if (s & ERR_UNSORTED) return HBF_EUNSORTED;
   if (s & ERR_MAP) return HBF_EINVAL;
-  if (s & ERR_INTERNAL) return HBF_EHIP;
   return HBF_OK;
 }
 

@@ -26,7 +26,6 @@ constexpr uint32_t ERR_RANGE_TIME = 1u;
 constexpr uint32_t ERR_UNSORTED = 2u;
 constexpr uint32_t ERR_OVERFLOW = 4u;
 constexpr uint32_t ERR_MAP = 8u;
-constexpr uint32_t ERR_INTERNAL = 16u;  // a bounded device wait gave up (a bug, never expected)
 
 // Die stage: 256 threads (4 wave64), 16 items per thread per chunk.
 constexpr int BLK = 256;
@@ -79,7 +78,6 @@ struct DevState {
 // Per-call control block (in the workspace).
 struct CallCtl {
   uint32_t err;       // per-call error bits
-  uint32_t ticket[NXCD];  // channel-stage work counters, one per XCD
   uint32_t n_in;      // in-range requests
   uint32_t G;         // time cells per channel
   uint32_t shift;     // log2(cell width in ns)
@@ -96,7 +94,8 @@ struct Layout {
   uint32_t s0;            // minimum cell shift
   size_t off_ctl, off_agg_cnt, off_agg_A, off_tin_L, off_tin_base;
   size_t off_totals, off_seg, off_dfnew, off_cfnew;
-  size_t off_dd, off_ix, off_kr, off_lb, off_st_agg, off_st_incl;
+  size_t off_dd, off_ix, off_kr, off_lb;
+  size_t off_cagg, off_cgin;  // per (channel, time cell): aggregate, entering term
   size_t total;
 };
 

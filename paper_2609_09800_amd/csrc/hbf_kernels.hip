@@ -23,15 +23,17 @@
 //   k_die_scatter  pass 2: exact die-done times, written in die-queue order
 //                  (an LDS-staged stable multisplit) plus, per (channel,
 //                  time cell, die), the first die rank in that cell.
-//   k_channel_merge per (channel, time cell): merge the cell's die runs in
-//                  LDS by (die-done, index), prefix-max, chain the channel
-//                  clock across cells with a decoupled look-back, scatter
+//   k_cell_agg     per (channel, time cell): merge the cell's die runs by
+//                  (die-done, index) and reduce them to one channel term.
+//   k_cell_scan    per channel, the running maximum of those terms.
+//   k_cell_out     every cell again, with its entering term: write
 //                  complete[] in request order.
 //   k_finalize     fail-closed error fill, or commit of the new clocks.
 //
 // A die emits at most one request per t_read_ns, so a time cell of width
-// 2^shift <= T * t_read_ns holds at most T requests per die: cells are
-// bounded by construction and need no sort of 64-bit keys.
+// 2^shift <= T * t_read_ns holds at most T requests per die, and a bucket
+// of width 2^floor(log2 t_read_ns) at most one: cells are bounded by
+// construction and merge without searching.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -59,19 +61,10 @@ DEVI uint32_t mask_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-DEVI uint64_t agent_load(const uint64_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-DEVI void agent_store(uint64_t *p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 DEVI uint32_t agent_load32(const uint32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// look-back status words: 0 = not yet published, else value + 2^62
-DEVI uint64_t enc_time(int64_t x) { return (uint64_t)x + (uint64_t(1) << 62); }
-DEVI int64_t dec_time(uint64_t w) { return (int64_t)(w - (uint64_t(1) << 62)); }
 
 // ------------------------------------------------------------------ block scans
 
@@ -281,20 +274,14 @@ DEVI void cross_wave_offsets(uint16_t *wcnt, uint16_t *tot, uint32_t K) {
 
 // ------------------------------------------------------------------ k_prologue
 
-__global__ void k_prologue(CallCtl *ctl, uint64_t *st_agg, uint64_t *st_incl, size_t nst) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+__global__ void k_prologue(CallCtl *ctl) {
+  if (threadIdx.x == 0) {
     ctl->err = 0;
-    for (int x = 0; x < NXCD; x++) ctl->ticket[x] = 0;
     ctl->n_in = 0;
     ctl->G = 0;
     ctl->shift = 0;
     ctl->max_dd = NEG;
     ctl->cbase = 0;
-  }
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < nst;
-       i += (size_t)gridDim.x * blockDim.x) {
-    st_agg[i] = 0;
-    st_incl[i] = 0;
   }
 }
 
@@ -652,7 +639,7 @@ __global__ __launch_bounds__(BLK) void k_die_scatter(
   }
 }
 
-// ------------------------------------------------------------------ k_channel_merge
+// ------------------------------------------------------------------ channel stage
 
 // (dd, idx) lexicographic order; idx is unique.
 DEVI bool key_less(int64_t da, uint32_t ia, int64_t db, uint32_t ib) {
@@ -752,57 +739,6 @@ struct CellLds {
   uint32_t used[MAX_RUNS];
   uint32_t safe;
 };
-
-// Decoupled look-back, 64 predecessors per round: the channel term entering
-// cell j, max(f0, M_j' for j' < j).  Lane l inspects cell base-l; the fold
-// stops at the nearest inclusive prefix and waits only for cells that have
-// published nothing yet.
-// The wait is bounded: after LOOKBACK_SPINS empty rounds (far beyond any
-// real wait) it reports ERR_INTERNAL, which fails the call, and returns.
-constexpr uint32_t LOOKBACK_SPINS = 1u << 20;
-
-DEVI int64_t look_back(const uint64_t *st_agg, const uint64_t *st_incl, int64_t f0, size_t row,
-                       uint32_t j, uint32_t *errb) {
-  const uint32_t lane = lane_id();
-  int64_t acc = NEG;
-  int64_t base = (int64_t)j - 1;
-  uint32_t spins = 0;
-  while (true) {
-    const int64_t jj = base - (int64_t)lane;
-    int stt = 0;
-    int64_t v = NEG;
-    if (jj < 0) {
-      stt = 2;
-      v = f0;
-    } else {
-      const uint64_t wi = agent_load(&st_incl[row + jj]);
-      if (wi) {
-        stt = 2;
-        v = dec_time(wi);
-      } else {
-        const uint64_t wa = agent_load(&st_agg[row + jj]);
-        if (wa) {
-          stt = 1;
-          v = dec_time(wa);
-        }
-      }
-    }
-    const uint64_t incl = __ballot(stt == 2);
-    const uint64_t none = __ballot(stt == 0);
-    const uint32_t fi = incl ? (uint32_t)__builtin_ctzll(incl) : 64u;
-    const uint32_t fn = none ? (uint32_t)__builtin_ctzll(none) : 64u;
-    if (fi < fn) return imax(acc, wave_max(lane <= fi ? v : NEG));
-    acc = imax(acc, wave_max(lane < fn ? v : NEG));
-    base -= fn;
-    if (fn == 0) {
-      if (++spins > LOOKBACK_SPINS) {
-        *errb |= ERR_INTERNAL;
-        return acc;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-}
 
 // Ascending bitonic sorting network over SL registers (SL a power of two).
 template <int SL>
@@ -941,192 +877,240 @@ DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, int 
 // before the call, complete_k = k*xfer + max(f0, max_{i<=k} (dd_(i) - (i-1)*xfer)).
 // A cell knows its first rank from the cell table (the sum of its row), so
 // its aggregate is one number, M_j = max over its requests of
-// (dd - (rank-1)*xfer), and the carry between cells is a running maximum.
+// (dd - (rank-1)*xfer), and the term entering cell j is max(f0, M_j' for
+// j' < j).  The stage runs as reduce, scan, reduce again:
+//   k_cell_agg   M_j of every cell;
+//   k_cell_scan  per channel, the running maximum of M_j seeded with f0;
+//   k_cell_out   every cell again, now writing complete[] with its term.
+// No block ever waits for another.
 //
-// One wave per block and per cell.  The bucket path (buckets of width
-// 2^lg_tR <= tR hold at most one request per die): lane q gathers the
-// requests of bucket q -- die d's is at position popcount(mask_d below q) of
-// its run -- sorts them in registers, and writes them at the bucket's
-// exclusive offset, giving the merged order without any search.
-//
-// Persistent blocks: block b serves XCD space b mod NXCD, which owns the
-// time windows j = k*NXCD + (b mod NXCD) (the same window of every channel
-// completes in one L2).  Within a space, cells are claimed in window order
-// from an atomic counter; a cell only waits for cells of earlier windows,
-// each already claimed by a running block, so every wait ends.
+// One wave per cell.  The bucket path (buckets of width 2^lg_tR <= tR hold
+// at most one request per die): lane q gathers the requests of bucket q --
+// die d's is at 1 + the byte the LDS table holds for (q, d) -- sorts them
+// in registers, and owns merged positions boff..boff+cnt-1 of the cell.
+// Cells that are too wide or too full stream through the LDS instead.
+#ifndef HBF_OUT_WCH
+#define HBF_OUT_WCH 0
+#endif
+constexpr uint32_t OUT_WCH = HBF_OUT_WCH;
+
+// Cell of iteration `it` of this block.  OUT_WCH == 0: (window, channel)
+// order, grid-stride, so all blocks move along one common time front and
+// the scattered complete[] stores of requests that finish close in time
+// (close in request order, as a rule) meet in a bounded span of lines.
+// OUT_WCH > 0: XCD space x = block mod NXCD takes runs of OUT_WCH
+// consecutive windows (all channels), runs dealt round robin, so those
+// stores meet in one L2.
+DEVI bool cell_at(uint32_t it, uint32_t N, uint32_t C, uint32_t G, uint32_t &c, uint32_t &j) {
+  if (OUT_WCH == 0) {
+    const uint64_t cell = (uint64_t)blockIdx.x + (uint64_t)it * gridDim.x;
+    if (cell >= N) return false;
+    j = (uint32_t)cell / C;
+    c = (uint32_t)cell - j * C;
+    return true;
+  }
+  const uint32_t xcd = blockIdx.x % NXCD;
+  const uint32_t nfull = G / OUT_WCH, wrem = G % OUT_WCH;
+  const uint32_t wins = (nfull / NXCD + (xcd < nfull % NXCD ? 1u : 0u)) * OUT_WCH +
+                        (nfull % NXCD == xcd ? wrem : 0u);
+  const uint64_t i = (uint64_t)(blockIdx.x / NXCD) + (uint64_t)it * (gridDim.x / NXCD);
+  if (i >= (uint64_t)wins * C) return false;
+  const uint32_t lw = (uint32_t)i / C;
+  c = (uint32_t)i - lw * C;
+  j = ((lw / OUT_WCH) * NXCD + xcd) * OUT_WCH + lw % OUT_WCH;
+  return true;
+}
+
+// One pass over cell (c, j).  Returns M_j; with EMIT, writes instead the
+// completion of each of its requests given the entering term gin.
+template <int SL, bool EMIT>
+DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX,
+                       const uint32_t *__restrict__ LB, const uint32_t *__restrict__ seg_start,
+                       const uint32_t *__restrict__ totals, const Geo &g, uint32_t gmax, uint32_t shift,
+                       int64_t cbase, uint32_t c, uint32_t j, int64_t gin, int64_t *complete, uint32_t n,
+                       uint32_t *errb) {
+  const uint32_t lane = lane_id();
+  const uint32_t Dk = g.Dk;
+  const uint32_t lgt = g.lg_tR;
+  const bool bucketable = (shift - lgt <= 6) && shift <= 32 && (int)Dk <= SL;
+  const int R = (int)Dk;
+  const int64_t xfer = g.xfer;
+  const int64_t cstart = cbase + ((int64_t)j << shift);
+  // runs of the cell: lane d = die run d
+  uint32_t lo = 0, hi = 0, r0 = 0;
+  if (lane < Dk) {
+    const uint32_t k = c * Dk + lane;
+    if (totals[k] != 0) {
+      const uint32_t *lbrow = LB + (size_t)c * (gmax + 1) * Dk + lane;
+      const uint32_t sg = seg_start[k];
+      r0 = lbrow[(size_t)j * Dk];
+      lo = r0 + sg;
+      hi = lbrow[(size_t)(j + 1) * Dk] + sg;
+    }
+  }
+  const uint32_t len = hi - lo;
+  const uint32_t rbx = wave_excl_sum(len);
+  const uint32_t m = wave_sum(len);
+  const int64_t rank0 = wave_sum(r0);  // channel rank of the cell's first request
+  if (m == 0) return NEG;
+  if (lane < Dk) {
+    S.lo[lane] = lo;
+    S.hi[lane] = hi;
+    S.rb[lane] = rbx;
+  }
+  if (lane == 0) S.rb[R] = m;
+  wave_sync();
+  const uint32_t maxlen = wave_umax(lane < Dk ? len : 0u);
+  if (!(bucketable && maxlen <= 64)) {
+    if (EMIT) {
+      stream_cell(S, DD, IX, R, gin, rank0, xfer, true, complete, n, errb);
+      return NEG;
+    }
+    return stream_cell(S, DD, IX, R, NEG, rank0, xfer, false, complete, n, errb);
+  }
+  uint64_t slot[SL];
+  uint32_t cnt = 0;
+  // clear the bucket table (1 KB: 16 B per lane)
+  reinterpret_cast<uint4 *>(&S.u.f.tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
+  // load every run (one lane per request; all loads in flight at once)
+  int64_t ddv[SL];
+  uint32_t ixv[SL];
+#pragma unroll
+  for (int d = 0; d < SL; d++) {
+    const uint32_t lod = __builtin_amdgcn_readlane(lo, d);
+    const uint32_t lend = __builtin_amdgcn_readlane(len, d);
+    ddv[d] = 0;
+    ixv[d] = 0;
+    if (d < R && lane < lend) {
+      ddv[d] = DD[lod + lane];
+      ixv[d] = IX[lod + lane];
+    }
+  }
+  wave_sync();
+#pragma unroll
+  for (int d = 0; d < SL; d++) {
+    const uint32_t lend = __builtin_amdgcn_readlane(len, d);
+    const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
+    if (d < R && lane < lend) {
+      const uint64_t rel = (uint64_t)(ddv[d] - cstart);
+      S.u.f.in[rbd + lane] = (rel << 32) | ixv[d];
+      S.u.f.tbl[rel >> lgt][d] = (uint8_t)(lane + 1);
+    }
+  }
+  wave_sync();
+  // lane q: gather, sort and count bucket q
+  {
+    const uint4 row = reinterpret_cast<const uint4 *>(&S.u.f.tbl[0][0])[lane];
+    const uint32_t rw[4] = {row.x, row.y, row.z, row.w};
+#pragma unroll
+    for (int d = 0; d < SL; d++) {
+      const uint32_t y = (rw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
+      const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
+      slot[d] = ~0ull;
+      if (y) {
+        slot[d] = S.u.f.in[rbd + y - 1];
+        cnt++;
+      }
+    }
+  }
+  sort_slots<SL>(slot);
+  const uint32_t boff = wave_excl_sum(cnt);
+  // Lindley prefix over the merged order, in registers
+  const int64_t cst = cstart - rank0 * xfer;
+  int64_t loc = NEG;
+#pragma unroll
+  for (int i = 0; i < SL; i++) {
+    if ((uint32_t)i < cnt) {
+      const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+      loc = imax(loc, v);
+    }
+  }
+  if (!EMIT) return wave_max(loc);
+  int64_t carry = __shfl_up(wave_incl_max(loc), 1);
+  if (lane == 0) carry = NEG;
+  carry = imax(carry, gin);
+  const int64_t r0x = rank0 * xfer;
+#pragma unroll
+  for (int i = 0; i < SL; i++) {
+    if ((uint32_t)i < cnt) {
+      const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+      carry = imax(carry, v);
+      const int64_t cpl = r0x + (int64_t)mul32(boff + i + 1, (uint32_t)xfer) + carry;
+      if (cpl >= TIME_LIMIT) *errb |= ERR_OVERFLOW;
+      const uint32_t ix = (uint32_t)slot[i];
+      if (ix < n) complete[ix] = cpl;
+    }
+  }
+  return NEG;
+}
+
 template <int SL>
-__global__ __launch_bounds__(64) void k_channel_merge(
+__global__ __launch_bounds__(64) void k_cell_agg(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals, Geo g,
-    CallCtl *ctl, uint64_t *st_agg, uint64_t *st_incl, const DevState *st,
-    int64_t *__restrict__ cfnew, int64_t *__restrict__ complete, uint32_t gmax, uint32_t n) {
+    const CallCtl *ctl, int64_t *__restrict__ AGG, uint32_t gmax, uint32_t n) {
   extern __shared__ __align__(16) unsigned char smem[];
   CellLds &S = *(CellLds *)smem;
   if (agent_load32(&ctl->err)) return;
-  const uint32_t lane = lane_id();
-  const uint32_t G = ctl->G, C = g.C, Dk = g.Dk;
-  const uint32_t shift = ctl->shift;
+  const uint32_t G = ctl->G, N = G * g.C, shift = ctl->shift;
   const int64_t cbase = ctl->cbase;
-  const uint32_t lgt = g.lg_tR;
-  const bool bucketable = (shift - lgt <= 6) && shift <= 32 && (int)Dk <= SL;
-  const uint32_t xcd = blockIdx.x % NXCD;
-  const uint32_t wins = G > xcd ? (G - 1 - xcd) / NXCD + 1 : 0;
-  const uint64_t ncx = (uint64_t)wins * C;
-  const int R = (int)Dk;
-  const int64_t xfer = g.xfer;
   uint32_t errb = 0;
-  // cells are claimed in order from this XCD space's counter, one ahead of
-  // the cell being processed (its table row is fetched early too); a block
-  // owns a cell only once it runs, so progress never depends on residency
-  auto claim = [&]() -> uint64_t {
-    uint32_t t = 0;
-    if (lane == 0)
-      t = __hip_atomic_fetch_add(&ctl->ticket[xcd], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return (uint64_t)__builtin_amdgcn_readfirstlane(t);
-  };
-  // cell-table row of a cell for lane d = die run d
-  auto fetch_row = [&](uint64_t t, uint32_t &lo, uint32_t &hi, uint32_t &seg) {
-    lo = hi = seg = 0;
-    if (t < ncx && lane < Dk) {
-      const uint32_t cc = (uint32_t)(t % C);
-      const uint32_t jj = (uint32_t)(t / C) * NXCD + xcd;
-      const uint32_t k = cc * Dk + lane;
-      const uint32_t *lbrow = LB + (size_t)cc * (gmax + 1) * Dk + lane;
-      lo = lbrow[(size_t)jj * Dk];
-      hi = lbrow[(size_t)(jj + 1) * Dk];
-      seg = seg_start[k];
-      if (totals[k] == 0) lo = hi = 0;
-    }
-  };
-  uint32_t nlo, nhi, nseg;
-  uint64_t tk = claim();
-  fetch_row(tk, nlo, nhi, nseg);
-  while (tk < ncx) {
-    const uint64_t tnext = claim();
-    const uint32_t c = (uint32_t)(tk % C);
-    const uint32_t j = (uint32_t)(tk / C) * NXCD + xcd;
-    const int64_t cstart = cbase + ((int64_t)j << shift);
-    // runs of the cell: lane d = die run d
-    uint32_t lo = nlo, hi = nhi;
-    const uint32_t r0 = lo;
-    lo += nseg;
-    hi += nseg;
-    fetch_row(tnext, nlo, nhi, nseg);
-    const uint32_t len = hi - lo;
-    const uint32_t rbx = wave_excl_sum(len);
-    const uint32_t m = wave_sum(len);
-    const int64_t rank0 = wave_sum(r0);  // channel rank of the cell's first request
-    if (lane < Dk) {
-      S.lo[lane] = lo;
-      S.hi[lane] = hi;
-      S.rb[lane] = rbx;
-
-    }
-    if (lane == 0) S.rb[R] = m;
+  uint32_t c, j;
+  for (uint32_t it = 0; cell_at(it, N, g.C, G, c, j); it++) {
+    const int64_t M = cell_pass<SL, false>(S, DD, IX, LB, seg_start, totals, g, gmax, shift, cbase, c, j,
+                                           NEG, nullptr, n, &errb);
+    if (lane_id() == 0) AGG[(size_t)c * gmax + j] = M;
     wave_sync();
-    const size_t row = (size_t)c * gmax;
-    const uint32_t maxlen = wave_umax(lane < Dk ? len : 0u);
-    const bool fast = bucketable && maxlen <= 64;
-    int64_t M = NEG;
-    // bucket path state: lane q holds the requests of bucket q, which are
-    // merged positions boff..boff+cnt-1 (lanes are in merged order)
-    uint64_t slot[SL];
-    uint32_t idxv[SL];
-    uint32_t cnt = 0, boff = 0;
-    if (fast) {
-      // clear the bucket table (1 KB: 16 B per lane)
-      reinterpret_cast<uint4 *>(&S.u.f.tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
-      // load every run (one lane per request; all loads in flight at once)
-      int64_t ddv[SL];
-      uint32_t ixv[SL];
-#pragma unroll
-      for (int d = 0; d < SL; d++) {
-        const uint32_t lod = __builtin_amdgcn_readlane(lo, d);
-        const uint32_t lend = __builtin_amdgcn_readlane(len, d);
-        ddv[d] = 0;
-        ixv[d] = 0;
-        if (d < R && lane < lend) {
-          ddv[d] = DD[lod + lane];
-          ixv[d] = IX[lod + lane];
-        }
-      }
-      wave_sync();
-#pragma unroll
-      for (int d = 0; d < SL; d++) {
-        const uint32_t lend = __builtin_amdgcn_readlane(len, d);
-        const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
-        if (d < R && lane < lend) {
-          const uint64_t rel = (uint64_t)(ddv[d] - cstart);
-          S.u.f.in[rbd + lane] = (rel << 32) | ixv[d];
-          S.u.f.tbl[rel >> lgt][d] = (uint8_t)(lane + 1);
-        }
-      }
-      wave_sync();
-      // lane q: gather, sort and count bucket q
-      const uint4 row = reinterpret_cast<const uint4 *>(&S.u.f.tbl[0][0])[lane];
-      const uint32_t rw[4] = {row.x, row.y, row.z, row.w};
-#pragma unroll
-      for (int d = 0; d < SL; d++) {
-        const uint32_t y = (rw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
-        const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
-        slot[d] = ~0ull;
-        if (y) {
-          slot[d] = S.u.f.in[rbd + y - 1];
-          cnt++;
-        }
-      }
-      sort_slots<SL>(slot);
-      boff = wave_excl_sum(cnt);
-      // Lindley prefix over the merged order, in registers
-      const int64_t cst = cstart - rank0 * xfer;
-      int64_t loc = NEG;
-#pragma unroll
-      for (int i = 0; i < SL; i++) {
-        if ((uint32_t)i < cnt) {
-          const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
-          loc = imax(loc, v);
-        }
-      }
-      M = wave_max(loc);
-      int64_t carry = __shfl_up(wave_incl_max(loc), 1);
-      if (lane == 0) carry = NEG;
-      // slot i becomes its prefix value; its request index moves to idxv[i]
-#pragma unroll
-      for (int i = 0; i < SL; i++) {
-        idxv[i] = (uint32_t)slot[i];
-        if ((uint32_t)i < cnt) {
-          const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
-          carry = imax(carry, v);
-        }
-        slot[i] = (uint64_t)carry;
-      }
-    } else {
-      M = stream_cell(S, DD, IX, R, NEG, rank0, xfer, false, complete, n, &errb);
-    }
-    // publish the aggregate, fold the predecessors, publish the prefix
-    if (lane == 0) agent_store(&st_agg[row + j], enc_time(M));
-    const int64_t gin = look_back(st_agg, st_incl, st->chan_free[c], row, j, &errb);
-    if (lane == 0) {
-      agent_store(&st_incl[row + j], enc_time(imax(gin, M)));
-      if (j + 1 == G) cfnew[c] = (rank0 + m) * xfer + imax(gin, M);
-    }
-    if (fast) {
-      const int64_t r0x = rank0 * xfer;
-#pragma unroll
-      for (int i = 0; i < SL; i++) {
-        if ((uint32_t)i < cnt) {
-          const int64_t cpl = r0x + (int64_t)mul32(boff + i + 1, (uint32_t)xfer) + imax(gin, (int64_t)slot[i]);
-          if (cpl >= TIME_LIMIT) errb |= ERR_OVERFLOW;
-          if (idxv[i] < n) complete[idxv[i]] = cpl;
-        }
-      }
-    } else {
-      stream_cell(S, DD, IX, R, gin, rank0, xfer, true, complete, n, &errb);
-    }
-    wave_sync();
-    tk = tnext;
   }
-  if (errb) atomicOr(&ctl->err, errb);
+}
+
+// Per channel: GIN[j] = max(f0, M_j' for j' < j); the channel clock after the
+// call is (its request count) * xfer + max(f0, every M_j).
+__global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ AGG, int64_t *__restrict__ GIN,
+                                                   const uint32_t *__restrict__ totals, Geo g,
+                                                   const CallCtl *ctl, const DevState *st,
+                                                   int64_t *__restrict__ cfnew, uint32_t gmax) {
+  __shared__ int64_t sh[WAVES];
+  __shared__ int64_t s_carry;
+  if (agent_load32(&ctl->err)) return;
+  const uint32_t c = blockIdx.x, G = ctl->G;
+  const size_t row = (size_t)c * gmax;
+  int64_t carry = st->chan_free[c];
+  for (uint32_t base = 0; base < G; base += BLK) {
+    const uint32_t jj = base + threadIdx.x;
+    const int64_t v = jj < G ? AGG[row + jj] : NEG;
+    const int64_t ex = block_excl_max(v, sh);
+    if (jj < G) GIN[row + jj] = imax(carry, ex);
+    if (threadIdx.x == BLK - 1) s_carry = imax(carry, imax(ex, v));
+    __syncthreads();
+    carry = s_carry;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    uint64_t tot = 0;
+    for (uint32_t d = 0; d < g.Dk; d++) tot += totals[c * g.Dk + d];
+    cfnew[c] = (int64_t)tot * g.xfer + carry;
+  }
+}
+
+template <int SL>
+__global__ __launch_bounds__(64) void k_cell_out(
+    const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
+    const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals, Geo g, CallCtl *ctl,
+    const int64_t *__restrict__ GIN, int64_t *__restrict__ complete, uint32_t gmax, uint32_t n) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  CellLds &S = *(CellLds *)smem;
+  if (agent_load32(&ctl->err)) return;
+  const uint32_t G = ctl->G, N = G * g.C, shift = ctl->shift;
+  const int64_t cbase = ctl->cbase;
+  uint32_t errb = 0;
+  uint32_t c, j;
+  for (uint32_t it = 0; cell_at(it, N, g.C, G, c, j); it++) {
+    cell_pass<SL, true>(S, DD, IX, LB, seg_start, totals, g, gmax, shift, cbase, c, j,
+                        GIN[(size_t)c * gmax + j], complete, n, &errb);
+    wave_sync();
+  }
+  if (errb && lane_id() == 0) atomicOr(&ctl->err, errb);
 }
 
 // ------------------------------------------------------------------ k_finalize
@@ -1186,9 +1170,10 @@ __global__ void k_reset(DevState *st) {
 
 // ------------------------------------------------------------------ launchers
 
-const char *const kKernelNames[] = {"k_prologue",    "k_die_reduce",    "k_tile_scan", "k_key_scan",
-                                    "k_die_scatter", "k_channel_merge", "k_finalize"};
-const int kNumTimedKernels = 7;
+const char *const kKernelNames[] = {"k_prologue",  "k_die_reduce", "k_tile_scan",
+                                    "k_key_scan",  "k_die_scatter", "k_cell_agg",
+                                    "k_cell_scan", "k_cell_out",    "k_finalize"};
+const int kNumTimedKernels = 9;
 
 static uint32_t bits_for(uint32_t K) {
   uint32_t b = 0;
@@ -1221,23 +1206,17 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   uint32_t *IX = (uint32_t *)(ws + Lo.off_ix);
   uint32_t *KR = (uint32_t *)(ws + Lo.off_kr);
   uint32_t *LB = (uint32_t *)(ws + Lo.off_lb);
-  uint64_t *st_agg = (uint64_t *)(ws + Lo.off_st_agg);
-  uint64_t *st_incl = (uint64_t *)(ws + Lo.off_st_incl);
+  int64_t *AGG = (int64_t *)(ws + Lo.off_cagg);
+  int64_t *GIN = (int64_t *)(ws + Lo.off_cgin);
   const uint32_t kbits = bits_for(g.K);
   const bool p2 = g.pow2 != 0;
-  const size_t nst = (size_t)g.C * Lo.gmax;
   int evi = 0;
   auto mark = [&]() {
     if (ev && evi < n_ev) hipEventRecord(ev[evi++], s);
   };
   hipError_t e;
   mark();
-  {
-    size_t blocks = (nst + BLK - 1) / BLK;
-    if (blocks > 2048) blocks = 2048;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(k_prologue, dim3((uint32_t)blocks), dim3(BLK), 0, s, ctl, st_agg, st_incl, nst);
-  }
+  hipLaunchKernelGGL(k_prologue, dim3(1), dim3(64), 0, s, ctl);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
   {
@@ -1266,28 +1245,45 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
   {
+    // channel stage: enough one-wave blocks to fill the chip, a multiple of
+    // the XCD count, and no more than there can be cells
     int dev = 0, ncu = 256, per_cu = 0;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
-    const void *kfn = g.Dk <= 4 ? (const void *)k_channel_merge<4>
-                      : g.Dk <= 8 ? (const void *)k_channel_merge<8> : (const void *)k_channel_merge<16>;
+    const int sl = g.Dk <= 4 ? 4 : g.Dk <= 8 ? 8 : 16;
+    const void *kfn = sl == 4 ? (const void *)k_cell_out<4>
+                      : sl == 8 ? (const void *)k_cell_out<8> : (const void *)k_cell_out<16>;
     hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64, sizeof(CellLds));
-    per_cu = per_cu < 1 ? 1 : (per_cu > 16 ? 16 : per_cu);
-    uint32_t blocks = (uint32_t)ncu * (uint32_t)per_cu;
+    per_cu = per_cu < 1 ? 1 : (per_cu > 32 ? 32 : per_cu);
+    uint64_t blocks = (uint64_t)ncu * (uint64_t)per_cu;
+    const uint64_t cells = (uint64_t)g.C * Lo.gmax;
+    const uint64_t need = ((cells + NXCD - 1) / NXCD) * NXCD;
+    if (blocks > need) blocks = need;
     blocks = (blocks / NXCD) * NXCD;
     if (blocks < NXCD) blocks = NXCD;
-    if (g.Dk <= 4)
-      hipLaunchKernelGGL(k_channel_merge<4>, dim3(blocks), dim3(64), sizeof(CellLds), s, DD, IX, LB, seg,
-                         totals, g, ctl, st_agg, st_incl, st, cfnew, complete, Lo.gmax,
-                         (uint32_t)Lo.n);
-    else if (g.Dk <= 8)
-      hipLaunchKernelGGL(k_channel_merge<8>, dim3(blocks), dim3(64), sizeof(CellLds), s, DD, IX, LB, seg,
-                         totals, g, ctl, st_agg, st_incl, st, cfnew, complete, Lo.gmax,
-                         (uint32_t)Lo.n);
+    const dim3 gr((uint32_t)blocks), bl(64);
+    const size_t lds = sizeof(CellLds);
+    const uint32_t nn = (uint32_t)Lo.n;
+    if (sl == 4)
+      hipLaunchKernelGGL(k_cell_agg<4>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, Lo.gmax, nn);
+    else if (sl == 8)
+      hipLaunchKernelGGL(k_cell_agg<8>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, Lo.gmax, nn);
     else
-      hipLaunchKernelGGL(k_channel_merge<16>, dim3(blocks), dim3(64), sizeof(CellLds), s, DD, IX, LB, seg,
-                         totals, g, ctl, st_agg, st_incl, st, cfnew, complete, Lo.gmax,
-                         (uint32_t)Lo.n);
+      hipLaunchKernelGGL(k_cell_agg<16>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, Lo.gmax, nn);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    mark();
+    hipLaunchKernelGGL(k_cell_scan, dim3(g.C), dim3(BLK), 0, s, AGG, GIN, totals, g, ctl, st, cfnew, Lo.gmax);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    mark();
+    if (sl == 4)
+      hipLaunchKernelGGL(k_cell_out<4>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
+                         Lo.gmax, nn);
+    else if (sl == 8)
+      hipLaunchKernelGGL(k_cell_out<8>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
+                         Lo.gmax, nn);
+    else
+      hipLaunchKernelGGL(k_cell_out<16>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
+                         Lo.gmax, nn);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
