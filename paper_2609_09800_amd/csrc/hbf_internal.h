@@ -28,11 +28,13 @@ constexpr uint32_t ERR_OVERFLOW = 4u;
 constexpr uint32_t ERR_MAP = 8u;
 
 // Die stage: 256 threads (4 wave64), 16 items per thread per chunk.
-constexpr int BLK = 256;
+constexpr int BLK = 256;            // threads per block of the small kernels
 constexpr int WAVES = BLK / 64;
-constexpr int ITEMS = 16;
-constexpr int CHUNK = BLK * ITEMS;  // 4096 requests staged per chunk
-constexpr int TARGET_TILES = 1024;
+constexpr int DBLK = 512;           // threads per block of the two die-stage passes
+constexpr int DWAVES = DBLK / 64;
+constexpr int DITEMS = 8;           // requests per thread per chunk
+constexpr int CHUNK = DBLK * DITEMS;  // 4096 requests staged per chunk
+constexpr int TARGET_TILES = 512;   // die-stage tiles: two 512-thread blocks per CU
 
 // Channel stage: a time cell of one channel is merged in LDS if it holds at
 // most MCAP requests, otherwise streamed in MCAP-sized rounds.

@@ -51,8 +51,8 @@ DEVI uint32_t lane_id() { return __lane_id(); }
 // 32 x 32 -> 64-bit product (one v_mad_u64_u32)
 DEVI uint64_t mul32(uint32_t a, uint32_t b) { return (uint64_t)a * (uint64_t)b; }
 
-// LDS index padding: one slot per 16, so blocked per-lane runs of 16
-// consecutive 8-byte entries do not all fall into the same banks
+// LDS index padding of the die-order staging arrays: one slot per 16
+// (measured: fewer bank conflicts than one per 8 for the blocked scan).
 DEVI uint32_t pad16(uint32_t p) { return p + (p >> 4); }
 
 // number of lanes below this one whose bit is set in `mask`
@@ -68,8 +68,9 @@ DEVI uint32_t agent_load32(const uint32_t *p) {
 
 // ------------------------------------------------------------------ block scans
 
-// Exclusive prefix sum over the block (256 threads); returns the block total.
-DEVI uint32_t block_excl_sum(uint32_t v, uint32_t *excl, uint32_t *sh /*[WAVES]*/) {
+// Exclusive prefix sum over a block of NW waves; returns the block total.
+template <int NW>
+DEVI uint32_t block_excl_sum(uint32_t v, uint32_t *excl, uint32_t *sh /*[NW]*/) {
   const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
   uint32_t x = v;
 #pragma unroll
@@ -81,7 +82,7 @@ DEVI uint32_t block_excl_sum(uint32_t v, uint32_t *excl, uint32_t *sh /*[WAVES]*
   __syncthreads();
   uint32_t base = 0, tot = 0;
 #pragma unroll
-  for (int i = 0; i < WAVES; i++) {
+  for (int i = 0; i < NW; i++) {
     uint32_t t = sh[i];
     base += (i < (int)w) ? t : 0u;
     tot += t;
@@ -91,8 +92,9 @@ DEVI uint32_t block_excl_sum(uint32_t v, uint32_t *excl, uint32_t *sh /*[WAVES]*
   return tot;
 }
 
-// Exclusive prefix max over the block; identity NEG.
-DEVI int64_t block_excl_max(int64_t v, int64_t *sh /*[WAVES]*/) {
+// Exclusive prefix max over a block of NW waves; identity NEG.
+template <int NW>
+DEVI int64_t block_excl_max(int64_t v, int64_t *sh /*[NW]*/) {
   const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
   int64_t x = v;
 #pragma unroll
@@ -106,7 +108,7 @@ DEVI int64_t block_excl_max(int64_t v, int64_t *sh /*[WAVES]*/) {
   __syncthreads();
   int64_t pre = NEG;
 #pragma unroll
-  for (int i = 0; i < WAVES; i++)
+  for (int i = 0; i < NW; i++)
     if (i < (int)w) pre = imax(pre, sh[i]);
   __syncthreads();
   return imax(pre, ex);
@@ -123,7 +125,8 @@ DEVI SegMax seg_comb(SegMax a, SegMax b) {
   r.v = b.f ? b.v : imax(a.v, b.v);
   return r;
 }
-DEVI SegMax block_excl_segmax(SegMax v, SegMax *sh /*[WAVES]*/) {
+template <int NW>
+DEVI SegMax block_excl_segmax(SegMax v, SegMax *sh /*[NW]*/) {
   const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
   SegMax x = v;
 #pragma unroll
@@ -144,7 +147,7 @@ DEVI SegMax block_excl_segmax(SegMax v, SegMax *sh /*[WAVES]*/) {
   __syncthreads();
   SegMax pre = {0, NEG};
 #pragma unroll
-  for (int i = 0; i < WAVES; i++)
+  for (int i = 0; i < NW; i++)
     if (i < (int)w) pre = seg_comb(pre, sh[i]);
   __syncthreads();
   return seg_comb(pre, ex);
@@ -235,7 +238,7 @@ DEVI uint32_t key_of(const Geo &g, const LdsRanges *lr, uint64_t a) {
 // Match-any over the key bits: lanes whose keys agree on every bit are peers.
 DEVI void wave_rank(const uint32_t *key, uint32_t *rank, uint16_t *wcnt, uint32_t kbits) {
 #pragma unroll
-  for (int e = 0; e < ITEMS; e++) {
+  for (int e = 0; e < DITEMS; e++) {
     const uint32_t k = key[e];
     const bool valid = k != KEY_NONE;
     uint64_t peers = __ballot(valid);
@@ -260,10 +263,10 @@ DEVI void wave_rank(const uint32_t *key, uint32_t *rank, uint16_t *wcnt, uint32_
 // After wave_rank: turn wcnt[w][k] into the wave's exclusive offset among
 // the block's waves and write the chunk total of key k to tot[k].
 DEVI void cross_wave_offsets(uint16_t *wcnt, uint16_t *tot, uint32_t K) {
-  for (uint32_t k = threadIdx.x; k < K; k += BLK) {
+  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
     uint32_t run = 0;
 #pragma unroll
-    for (int w = 0; w < WAVES; w++) {
+    for (int w = 0; w < DWAVES; w++) {
       uint32_t c = wcnt[w * K + k];
       wcnt[w * K + k] = (uint16_t)run;
       run += c;
@@ -287,9 +290,10 @@ __global__ void k_prologue(CallCtl *ctl) {
 
 // ------------------------------------------------------------------ k_die_reduce
 
-// LDS: ranges | wcnt[WAVES][K] u16 | tot[K] u16 | cnt[K] u32 | amax[K] i64
+
+// LDS: ranges | wcnt[DWAVES][K] u16 | tot[K] u16 | cnt[K] u32 | amax[K] i64
 template <bool POW2>
-__global__ __launch_bounds__(BLK) void k_die_reduce(const uint64_t *__restrict__ addr,
+__global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict__ addr,
                                                     const int64_t *__restrict__ issue, int64_t n,
                                                     int64_t *__restrict__ complete, Geo g,
                                                     RangeTable rt, int64_t tile_elems,
@@ -303,10 +307,10 @@ __global__ __launch_bounds__(BLK) void k_die_reduce(const uint64_t *__restrict__
   int64_t *amax = (int64_t *)(smem + ((sizeof(LdsRanges) + 15) & ~size_t(15)));
   uint32_t *cnt = (uint32_t *)(amax + K);
   uint16_t *wcnt = (uint16_t *)(cnt + K);
-  uint16_t *tot = wcnt + WAVES * K;
+  uint16_t *tot = wcnt + DWAVES * K;
 
   load_ranges(lr, rt);
-  for (uint32_t k = threadIdx.x; k < K; k += BLK) {
+  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
     cnt[k] = 0;
     amax[k] = NEG;
   }
@@ -319,23 +323,47 @@ __global__ __launch_bounds__(BLK) void k_die_reduce(const uint64_t *__restrict__
   uint32_t errb = 0;
   uint16_t *mycnt = wcnt + w * K;
 
+  // the next chunk's requests are loaded while this one is ranked
+  int64_t nx[DITEMS], nb = 0;
+  uint64_t na[DITEMS];
+  auto fetch = [&](int64_t cc) {
+    const int64_t wb = cc + (int64_t)w * 64 * DITEMS;
+#pragma unroll
+    for (int e = 0; e < DITEMS; e++) {
+      const int64_t i = wb + e * 64 + lane;
+      const bool v = i < t1;
+      nx[e] = v ? issue[i] : 0;
+      na[e] = v ? addr[i] : 0;
+    }
+    nb = (lane == 0 && wb > 0 && wb < t1) ? issue[wb - 1] : 0;
+  };
+  if (t0 < t1) fetch(t0);
   for (int64_t c0 = t0; c0 < t1; c0 += CHUNK) {
     for (uint32_t k = lane; k < K; k += 64) mycnt[k] = 0;
-    uint32_t key[ITEMS], rank[ITEMS];
-    int64_t iss[ITEMS];
-    int64_t carry_prev = 0;
-    const int64_t wbase = c0 + (int64_t)w * 64 * ITEMS;
+    uint32_t key[DITEMS], rank[DITEMS];
+    int64_t iss[DITEMS];
+    int64_t cx[DITEMS];
+    uint64_t ca[DITEMS];
 #pragma unroll
-    for (int e = 0; e < ITEMS; e++) {
+    for (int e = 0; e < DITEMS; e++) {
+      cx[e] = nx[e];
+      ca[e] = na[e];
+    }
+    const int64_t before = nb;  // issue time preceding this wave's first request
+    if (c0 + CHUNK < t1) fetch(c0 + CHUNK);
+    int64_t carry_prev = 0;
+    const int64_t wbase = c0 + (int64_t)w * 64 * DITEMS;
+#pragma unroll
+    for (int e = 0; e < DITEMS; e++) {
       const int64_t i = wbase + e * 64 + lane;
       const bool v = i < t1;
-      int64_t x = v ? issue[i] : 0;
-      uint64_t a = v ? addr[i] : 0;
+      const int64_t x = cx[e];
+      const uint64_t a = ca[e];
       // previous request's issue time, for the order check
       int64_t prev = __shfl_up(x, 1);
       int64_t last_of_prev_item = carry_prev;
       carry_prev = __shfl(x, 63);
-      if (lane == 0) prev = (e > 0) ? last_of_prev_item : ((i > 0 && v) ? issue[i - 1] : x);
+      if (lane == 0) prev = (e > 0) ? last_of_prev_item : ((i > 0 && v) ? before : x);
       if (v) {
         if (x < 0 || x >= ISSUE_LIMIT) errb |= ERR_RANGE_TIME;
         if (i > 0 && x < prev) errb |= ERR_UNSORTED;
@@ -350,7 +378,7 @@ __global__ __launch_bounds__(BLK) void k_die_reduce(const uint64_t *__restrict__
     cross_wave_offsets(wcnt, tot, K);
     __syncthreads();
 #pragma unroll
-    for (int e = 0; e < ITEMS; e++) {
+    for (int e = 0; e < DITEMS; e++) {
       const uint32_t k = key[e];
       const int64_t i = wbase + e * 64 + lane;
       if (k != KEY_NONE) {
@@ -363,12 +391,12 @@ __global__ __launch_bounds__(BLK) void k_die_reduce(const uint64_t *__restrict__
       }
     }
     __syncthreads();
-    for (uint32_t k = threadIdx.x; k < K; k += BLK) cnt[k] += tot[k];
+    for (uint32_t k = threadIdx.x; k < K; k += DBLK) cnt[k] += tot[k];
     __syncthreads();
   }
   // tile aggregate per die queue: departure of the last request from an idle die
   const size_t row = (size_t)blockIdx.x * K;
-  for (uint32_t k = threadIdx.x; k < K; k += BLK) {
+  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
     const uint32_t c = cnt[k];
     agg_cnt[row + k] = c;
     agg_A[row + k] = c ? (int64_t)c * tR + amax[k] : NEG;
@@ -454,7 +482,7 @@ __global__ __launch_bounds__(BLK) void k_key_scan(const uint32_t *__restrict__ t
   uint32_t s = 0;
   for (uint32_t k = a; k < b; k++) s += totals[k];
   uint32_t ex;
-  uint32_t tot = block_excl_sum(s, &ex, sh);
+  uint32_t tot = block_excl_sum<WAVES>(s, &ex, sh);
   for (uint32_t k = a; k < b; k++) {
     seg_start[k] = ex;
     ex += totals[k];
@@ -483,56 +511,71 @@ __global__ __launch_bounds__(BLK) void k_key_scan(const uint32_t *__restrict__ t
 // rank) order using the ranks pass 1 stored (LDS histogram + offsets, no
 // re-ranking), compute exact die-done times with a segmented prefix max,
 // and write them in die-queue order, filling the cell table on the way.
-// LDS: sval[CHUNKP] i64 | L[K] i64 | cnt[K] | gbase[K] | segb[K] | totk[K] |
-//      tot[K] | koff[K] (u32) | skey[CHUNKP] u16 | sloc[CHUNKP] u16
+//
+// Per die queue k the chunk needs a handful of numbers; they sit in two
+// 16-byte records so that each phase reads one record per request (random
+// k: one bank-conflicted access instead of several):
+//   KA[k] = {koff: offset of k's run in the chunk, cnt: k's requests in the
+//            tile before this chunk, L: die clock entering the chunk}
+//   KW[k] = {rbase: die rank (within the call) of k's first request in the
+//            chunk, pbase: its die-order position, lbo: k's column in the
+//            cell table, tot: k's requests in the call}
+// LDS: sval[CHUNKP] i64 | KA[K] | KW[K] | hist[K] u32 | skey, srank,
+//      sloc [CHUNKP] u16
 constexpr int CHUNKP = CHUNK + CHUNK / 16;
 
-__global__ __launch_bounds__(BLK) void k_die_scatter(
+struct KeyA {
+  uint32_t koff, cnt;
+  int64_t L;
+};
+struct KeyW {
+  uint32_t rbase, pbase, lbo, tot;
+};
+
+__global__ __launch_bounds__(DBLK) void k_die_scatter(
     const int64_t *__restrict__ issue, const uint32_t *__restrict__ KR, int64_t n, Geo g,
     int64_t tile_elems, const int64_t *__restrict__ tin_L, const uint32_t *__restrict__ tin_base,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals,
     int64_t *__restrict__ DD, uint32_t *__restrict__ IX, uint32_t *__restrict__ LB, uint32_t gmax,
     CallCtl *ctl) {
   extern __shared__ __align__(16) unsigned char smem[];
-  __shared__ SegMax shseg[WAVES];
-  __shared__ uint32_t shsum[WAVES];
+  __shared__ SegMax shseg[DWAVES];
+  __shared__ uint32_t shsum[DWAVES];
   __shared__ uint32_t s_nvalid;
   if (agent_load32(&ctl->err)) return;
   const uint32_t K = g.K;
   int64_t *sval = (int64_t *)smem;
-  int64_t *L = sval + CHUNKP;
-  uint32_t *cnt = (uint32_t *)(L + K);
-  uint32_t *gbase = cnt + K;
-  uint32_t *segb = gbase + K;
-  uint32_t *totk = segb + K;
-  uint32_t *tot = totk + K;
-  uint32_t *koff = tot + K;
-  uint16_t *skey = (uint16_t *)(koff + K);
-  uint16_t *sloc = skey + CHUNKP;
+  KeyA *KA = (KeyA *)(sval + CHUNKP);
+  KeyW *KW = (KeyW *)(KA + K);
+  uint32_t *hist = (uint32_t *)(KW + K);
+  uint16_t *skey = (uint16_t *)(hist + K);
+  uint16_t *srank = skey + CHUNKP;
+  uint16_t *sloc = srank + CHUNKP;
 
+  const uint32_t Dk = g.Dk;
   const size_t row = (size_t)blockIdx.x * K;
-  for (uint32_t k = threadIdx.x; k < K; k += BLK) {
-    cnt[k] = 0;
-    L[k] = tin_L[row + k];
-    gbase[k] = tin_base[row + k];  // die rank of the tile's first request of k
-    segb[k] = seg_start[k];
-    totk[k] = totals[k];
+  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+    const uint32_t base = tin_base[row + k];  // die rank of the tile's first request of k
+    KA[k] = KeyA{0u, 0u, tin_L[row + k]};
+    const uint32_t ch = k / Dk;
+    KW[k] = KeyW{base, seg_start[k] + base, ch * (gmax + 1) * Dk + (k - ch * Dk), totals[k]};
   }
   const int64_t cbase = ctl->cbase;
   const uint32_t shift = ctl->shift, G = ctl->G;
+  const bool narrow = shift <= 32;
+  const uint64_t relmask = narrow ? (uint64_t(1) << shift) - 1 : 0;
   const int64_t t0 = (int64_t)blockIdx.x * tile_elems;
   const int64_t t1 = imin(n, t0 + tile_elems);
   const uint32_t tR = (uint32_t)g.tR;
-  const uint32_t Dk = g.Dk;
 
-  for (int64_t c0 = t0; c0 < t1; c0 += CHUNK) {
-    for (uint32_t k = threadIdx.x; k < K; k += BLK) tot[k] = 0;
-    __syncthreads();
-    int64_t iss[ITEMS];
-    uint32_t kr[ITEMS];
+  // a chunk's requests are loaded while the previous one is scanned and
+  // written (they are only needed up to the staging step)
+  int64_t iss[DITEMS];
+  uint32_t kr[DITEMS];
+  auto fetch = [&](int64_t cc) {
 #pragma unroll
-    for (int e = 0; e < ITEMS; e++) {
-      const int64_t i = c0 + e * BLK + threadIdx.x;
+    for (int e = 0; e < DITEMS; e++) {
+      const int64_t i = cc + e * DBLK + threadIdx.x;
       iss[e] = 0;
       kr[e] = (uint32_t)KEY_NONE << 16;
       if (i < t1) {
@@ -540,99 +583,115 @@ __global__ __launch_bounds__(BLK) void k_die_scatter(
         kr[e] = KR[i];
       }
     }
+  };
+  if (t0 < t1) fetch(t0);
+  for (int64_t c0 = t0; c0 < t1; c0 += CHUNK) {
+    for (uint32_t k = threadIdx.x; k < K; k += DBLK) hist[k] = 0;
+    __syncthreads();
 #pragma unroll
-    for (int e = 0; e < ITEMS; e++) {
+    for (int e = 0; e < DITEMS; e++) {
       const uint32_t k = kr[e] >> 16;
-      if (k != KEY_NONE) atomicAdd(&tot[k], 1u);
+      if (k != KEY_NONE) atomicAdd(&hist[k], 1u);
     }
     __syncthreads();
     {  // chunk offsets of each key's run
-      const uint32_t per = (K + BLK - 1) / BLK;
+      const uint32_t per = (K + DBLK - 1) / DBLK;
       const uint32_t a0 = threadIdx.x * per, b0 = min(K, a0 + per);
       uint32_t sum = 0;
-      for (uint32_t k = a0; k < b0; k++) sum += tot[k];
+      for (uint32_t k = a0; k < b0; k++) sum += hist[k];
       uint32_t ex;
-      const uint32_t all = block_excl_sum(sum, &ex, shsum);
+      const uint32_t all = block_excl_sum<DWAVES>(sum, &ex, shsum);
       for (uint32_t k = a0; k < b0; k++) {
-        koff[k] = ex;
-        ex += tot[k];
+        KA[k].koff = ex;
+        ex += hist[k];
       }
       if (threadIdx.x == 0) s_nvalid = all;
     }
     __syncthreads();
+    // stage v = issue - r0*tR in die order (r0 = rank of the request among
+    // k's in the tile); a run's head also folds in the entering clock,
+    // M_k = L_k - cnt_k*tR, so the segmented prefix max below is the whole
+    // Lindley term: die_done = (r0+1)*tR + max(M_k, max of v over the run)
 #pragma unroll
-    for (int e = 0; e < ITEMS; e++) {
+    for (int e = 0; e < DITEMS; e++) {
       const uint32_t k = kr[e] >> 16;
       if (k != KEY_NONE) {
-        const uint32_t P = pad16(koff[k] + (kr[e] & 0xFFFFu));
-        sval[P] = iss[e];
+        const KeyA ka = KA[k];
+        const uint32_t rc = kr[e] & 0xFFFFu;
+        const uint32_t P = pad16(ka.koff + rc);
+        int64_t v = iss[e] - (int64_t)mul32(ka.cnt + rc, tR);
+        if (rc == 0) v = imax(v, ka.L - (int64_t)mul32(ka.cnt, tR));
+        sval[P] = v;
         skey[P] = (uint16_t)k;
-        sloc[P] = (uint16_t)(e * BLK + threadIdx.x);
+        srank[P] = (uint16_t)rc;
+        sloc[P] = (uint16_t)(e * DBLK + threadIdx.x);
       }
     }
     __syncthreads();
+    if (c0 + CHUNK < t1) fetch(c0 + CHUNK);
     const uint32_t nv = s_nvalid;
-    // segmented prefix max of v = issue - r0*tR over each key's run, then
-    // die_done = (r0+1)*tR + max(M_k, prefix), M_k = L_k - cnt_k*tR
     {
-      const uint32_t p0 = threadIdx.x * ITEMS;
-      int64_t vals[ITEMS];
+      const uint32_t p0 = threadIdx.x * DITEMS;
+      int64_t vals[DITEMS];
       SegMax agg = {0, NEG};
 #pragma unroll
-      for (int q = 0; q < ITEMS; q++) {
+      for (int q = 0; q < DITEMS; q++) {
         const uint32_t p = p0 + q;
         vals[q] = NEG;
         if (p < nv) {
-          const uint32_t k = skey[pad16(p)];
-          const uint32_t j = p - koff[k];
-          const int64_t v = sval[pad16(p)] - (int64_t)mul32(cnt[k] + j, tR);
+          const int64_t v = sval[pad16(p)];
           vals[q] = v;
-          agg = seg_comb(agg, SegMax{j == 0, v});
+          agg = seg_comb(agg, SegMax{srank[pad16(p)] == 0, v});
         }
       }
-      SegMax ex = block_excl_segmax(agg, shseg);
+      SegMax ex = block_excl_segmax<DWAVES>(agg, shseg);
       int64_t run = ex.v;  // prefix of the segment continuing into this thread
 #pragma unroll
-      for (int q = 0; q < ITEMS; q++) {
+      for (int q = 0; q < DITEMS; q++) {
         const uint32_t p = p0 + q;
         if (p < nv) {
-          const uint32_t k = skey[pad16(p)];
-          const uint32_t j = p - koff[k];
-          run = (j == 0) ? vals[q] : imax(run, vals[q]);
-          const uint32_t r0 = cnt[k] + j;
-          const int64_t M = L[k] - (int64_t)mul32(cnt[k], tR);
-          sval[pad16(p)] = (int64_t)mul32(r0 + 1, tR) + imax(M, run);
+          const uint32_t rc = srank[pad16(p)];
+          run = (rc == 0) ? vals[q] : imax(run, vals[q]);
+          const uint32_t r0 = KA[skey[pad16(p)]].cnt + rc;
+          sval[pad16(p)] = (int64_t)mul32(r0 + 1, tR) + run;
         }
       }
     }
     __syncthreads();
     // write die-ordered (die_done, index); fill the cell table
-    for (uint32_t p = threadIdx.x; p < nv; p += BLK) {
+    for (uint32_t p = threadIdx.x; p < nv; p += DBLK) {
       const uint32_t P = pad16(p);
       const uint32_t k = skey[P];
-      const uint32_t j = p - koff[k];
-      const uint32_t r = gbase[k] + cnt[k] + j;  // die rank within this call
+      const uint32_t rc = srank[P];
+      const KeyW kw = KW[k];
+      const uint32_t r = kw.rbase + rc;  // die rank within this call
       const int64_t dd = sval[P];
-      const uint32_t gpos = segb[k] + r;
+      const uint32_t gpos = kw.pbase + rc;
       if (gpos < n) {
-        DD[gpos] = dd;
-        IX[gpos] = (uint32_t)(c0 + sloc[P]);
+        const uint32_t ix = (uint32_t)(c0 + sloc[P]);
+        if (narrow)  // one word: offset of die-done in its cell, request index
+          reinterpret_cast<uint64_t *>(DD)[gpos] = ((uint64_t)(dd - cbase) & relmask) << 32 | ix;
+        else {
+          DD[gpos] = dd;
+          IX[gpos] = ix;
+        }
       }
-      const int64_t prev = (j > 0) ? sval[pad16(p - 1)] : L[k];
+      const int64_t prev = (rc > 0) ? sval[pad16(p - 1)] : KA[k].L;
       const int64_t cell = imin((dd - cbase) >> shift, (int64_t)G);
       const int64_t pcell = (r == 0) ? -1 : imin((prev - cbase) >> shift, (int64_t)G);
-      const uint32_t ch = k / Dk, dl = k - ch * Dk;
-      uint32_t *lbrow = LB + (size_t)ch * (gmax + 1) * Dk + dl;
+      uint32_t *lbrow = LB + kw.lbo;
       for (int64_t c = pcell + 1; c <= cell; c++) lbrow[(size_t)c * Dk] = r;
-      if (r + 1 == totk[k])
+      if (r + 1 == kw.tot)
         for (int64_t c = cell + 1; c <= (int64_t)G; c++) lbrow[(size_t)c * Dk] = r + 1;
     }
     __syncthreads();
-    for (uint32_t k = threadIdx.x; k < K; k += BLK) {
-      const uint32_t t = tot[k];
+    for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+      const uint32_t t = hist[k];
       if (t) {
-        L[k] = sval[pad16(koff[k] + t - 1)];
-        cnt[k] += t;
+        KA[k].L = sval[pad16(KA[k].koff + t - 1)];
+        KA[k].cnt += t;
+        KW[k].rbase += t;
+        KW[k].pbase += t;
       }
     }
     __syncthreads();
@@ -766,9 +825,9 @@ DEVI void sort_slots(uint64_t (&a)[SL]) {
 // round loads at most CAP_S/R requests per run, ranks them (binary searches
 // in the other runs), and serves the prefix that no unloaded request can
 // precede.  gacc: running channel term; returns it after the cell.
-DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, int R, int64_t gacc,
-                         int64_t rank0, int64_t xfer, bool emit, int64_t *complete, uint32_t n,
-                         uint32_t *errb) {
+DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, bool narrow, int64_t cstart,
+                         int R, int64_t gacc, int64_t rank0, int64_t xfer, bool emit, int64_t *complete,
+                         uint32_t n, uint32_t *errb) {
   const uint32_t lane = lane_id();
   if (lane < (uint32_t)R) S.cur[lane] = S.lo[lane];
   wave_sync();
@@ -792,8 +851,14 @@ DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, int 
     for (uint32_t p = lane; p < m; p += 64) {
       const int d = run_of(S.rb, R, p);
       const uint32_t src = S.cur[d] + (p - S.rb[d]);
-      S.u.s.dd[0][p] = DD[src];
-      S.u.s.ix[0][p] = IX[src];
+      if (narrow) {
+        const uint64_t x = reinterpret_cast<const uint64_t *>(DD)[src];
+        S.u.s.dd[0][p] = cstart + (int64_t)(x >> 32);
+        S.u.s.ix[0][p] = (uint32_t)x;
+      } else {
+        S.u.s.dd[0][p] = DD[src];
+        S.u.s.ix[0][p] = IX[src];
+      }
       S.u.s.tg[0][p] = (uint8_t)d;
     }
     wave_sync();
@@ -963,28 +1028,26 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   const uint32_t maxlen = wave_umax(lane < Dk ? len : 0u);
   if (!(bucketable && maxlen <= 64)) {
     if (EMIT) {
-      stream_cell(S, DD, IX, R, gin, rank0, xfer, true, complete, n, errb);
+      stream_cell(S, DD, IX, shift <= 32, cstart, R, gin, rank0, xfer, true, complete, n, errb);
       return NEG;
     }
-    return stream_cell(S, DD, IX, R, NEG, rank0, xfer, false, complete, n, errb);
+    return stream_cell(S, DD, IX, shift <= 32, cstart, R, NEG, rank0, xfer, false, complete, n, errb);
   }
   uint64_t slot[SL];
   uint32_t cnt = 0;
   // clear the bucket table (1 KB: 16 B per lane)
   reinterpret_cast<uint4 *>(&S.u.f.tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
-  // load every run (one lane per request; all loads in flight at once)
-  int64_t ddv[SL];
-  uint32_t ixv[SL];
+  // load every run (one lane per request; all loads in flight at once).
+  // Bucketable cells are at most 2^32 ns wide, so their entries are packed
+  // words (offset in the cell << 32 | index): already the merge's sort key.
+  const uint64_t *DX = reinterpret_cast<const uint64_t *>(DD);
+  uint64_t xv[SL];
 #pragma unroll
   for (int d = 0; d < SL; d++) {
     const uint32_t lod = __builtin_amdgcn_readlane(lo, d);
     const uint32_t lend = __builtin_amdgcn_readlane(len, d);
-    ddv[d] = 0;
-    ixv[d] = 0;
-    if (d < R && lane < lend) {
-      ddv[d] = DD[lod + lane];
-      ixv[d] = IX[lod + lane];
-    }
+    xv[d] = 0;
+    if (d < R && lane < lend) xv[d] = DX[lod + lane];
   }
   wave_sync();
 #pragma unroll
@@ -992,9 +1055,8 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
     const uint32_t lend = __builtin_amdgcn_readlane(len, d);
     const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
     if (d < R && lane < lend) {
-      const uint64_t rel = (uint64_t)(ddv[d] - cstart);
-      S.u.f.in[rbd + lane] = (rel << 32) | ixv[d];
-      S.u.f.tbl[rel >> lgt][d] = (uint8_t)(lane + 1);
+      S.u.f.in[rbd + lane] = xv[d];
+      S.u.f.tbl[(xv[d] >> 32) >> lgt][d] = (uint8_t)(lane + 1);
     }
   }
   wave_sync();
@@ -1079,7 +1141,7 @@ __global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ A
   for (uint32_t base = 0; base < G; base += BLK) {
     const uint32_t jj = base + threadIdx.x;
     const int64_t v = jj < G ? AGG[row + jj] : NEG;
-    const int64_t ex = block_excl_max(v, sh);
+    const int64_t ex = block_excl_max<WAVES>(v, sh);
     if (jj < G) GIN[row + jj] = imax(carry, ex);
     if (threadIdx.x == BLK - 1) s_carry = imax(carry, imax(ex, v));
     __syncthreads();
@@ -1183,11 +1245,12 @@ static uint32_t bits_for(uint32_t K) {
 
 static size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
 
+// LDS of pass 1: range table | amax[K] i64 | cnt[K] | wcnt[DWAVES][K] u16 | tot[K] u16
 size_t lds_die_reduce(uint32_t K) {
-  return align16(sizeof(LdsRanges)) + K * (8 + 4) + WAVES * K * 2 + K * 2;
+  return align16(sizeof(LdsRanges)) + K * (8 + 4) + DWAVES * K * 2 + K * 2;
 }
 size_t lds_die_scatter(uint32_t K) {
-  return (size_t)CHUNKP * 8 + (size_t)K * (8 + 4 * 6) + (size_t)CHUNKP * 4;
+  return (size_t)CHUNKP * 8 + (size_t)K * (sizeof(KeyA) + sizeof(KeyW) + 4) + (size_t)CHUNKP * 6;
 }
 
 hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout &Lo, char *ws,
@@ -1222,10 +1285,10 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   {
     const size_t lds = lds_die_reduce(g.K);
     if (p2)
-      hipLaunchKernelGGL(k_die_reduce<true>, dim3(Lo.nt), dim3(BLK), lds, s, addr, issue, Lo.n, complete,
+      hipLaunchKernelGGL(k_die_reduce<true>, dim3(Lo.nt), dim3(DBLK), lds, s, addr, issue, Lo.n, complete,
                          g, rt, Lo.tile_elems, agg_cnt, agg_A, KR, ctl, kbits);
     else
-      hipLaunchKernelGGL(k_die_reduce<false>, dim3(Lo.nt), dim3(BLK), lds, s, addr, issue, Lo.n,
+      hipLaunchKernelGGL(k_die_reduce<false>, dim3(Lo.nt), dim3(DBLK), lds, s, addr, issue, Lo.n,
                          complete, g, rt, Lo.tile_elems, agg_cnt, agg_A, KR, ctl, kbits);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1239,7 +1302,7 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   mark();
   {
     const size_t lds = lds_die_scatter(g.K);
-    hipLaunchKernelGGL(k_die_scatter, dim3(Lo.nt), dim3(BLK), lds, s, issue, KR, Lo.n, g, Lo.tile_elems,
+    hipLaunchKernelGGL(k_die_scatter, dim3(Lo.nt), dim3(DBLK), lds, s, issue, KR, Lo.n, g, Lo.tile_elems,
                        tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
