@@ -80,6 +80,38 @@ def load_or_generate(wl, n, cache):
     return w
 
 
+def closed_loop(torch, hbf, wl, steps=2, reps=3):
+    """The next row of the path: config 3's decode as a closed loop
+    (hbf_time_layers), each layer issued 2 us after the previous layer's
+    last modeled completion.  Reports the GPU time per call and the modeled
+    decode-step times; not part of the headline value."""
+    w, ls = wl.config3_layers(steps=steps)
+    m = hbf.Model(**w.params)
+    for b, nb in w.ranges:
+        assert m.register_range(b, nb)[0] == 0
+    a = torch.from_numpy(w.addr.view(np.int64)).cuda()
+    iss = torch.empty_like(a)
+    cpl = torch.empty_like(a)
+    L = len(ls) - 1
+    done = torch.empty(L, dtype=torch.int64, device="cuda")
+    m.reset()
+    assert m.time_layers(a, ls, 0, 2000, iss, cpl, done) == 0
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(reps):
+        m.reset()
+        assert m.time_layers(a, ls, 0, 2000, iss, cpl, done) == 0
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t) * 1e3 / reps
+    assert m.get_status() == 0
+    d = done.cpu().numpy()
+    per_step = L // steps
+    step_ns = [int(d[(k + 1) * per_step - 1] - (d[k * per_step - 1] + 2000 if k else 0)) for k in range(steps)]
+    return dict(workload=f"config-3 MoE decode, {steps} steps x {per_step} layers, closed loop, 2 us compute/layer",
+                requests=int(w.n), layers=L, ms_per_call=ms, requests_per_s=w.n / (ms / 1e3),
+                modeled_decode_step_ns=step_ns)
+
+
 def cpu_baseline(w, n_sample):
     from oracle import oracle
     m = oracle.OracleModel(**w.params)
@@ -108,6 +140,7 @@ def main():
                     help="directory to keep the generated stream in (.npy) for repeated runs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--no-gemv", action="store_true", help="time only hbf_time_requests (diagnostic)")
+    ap.add_argument("--no-closed-loop", action="store_true", help="skip the closed-loop decode report")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -238,6 +271,9 @@ def main():
         "parity_vs_reference_digest": parity,
         "delay": delay,
     }
+    if not args.no_closed_loop:
+        log("closed-loop decode timing")
+        out["closed_loop"] = closed_loop(torch, hbf, wl)
     if not args.no_cpu:
         log("timing the reference model on the CPU sample")
         out["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, n))

@@ -157,6 +157,27 @@ int hbf_classify_map(hbf_model_t model, const uint64_t *dev_addr, int64_t n, uin
 int hbf_time_requests(hbf_model_t model, const uint64_t *dev_addr, const int64_t *dev_issue_ns,
                       int64_t n, int64_t *dev_complete_ns, void *stream);
 
+/* Closed-loop timing of a layered decode: the running program pays each
+ * layer's modeled delays before it issues the next layer's reads (Section
+ * "Introduction": delays are paid by the running program; Section D2: the
+ * wait sits where the loaded values are first used, here the next layer).
+ * The n requests form L consecutive layers: layer l is
+ * [host_layer_start[l], host_layer_start[l+1]) (host array of L+1 entries,
+ * nondecreasing, first 0, last n; empty layers allowed).  Every request of
+ * layer l is issued at
+ *     t_0 = t_start_ns,   t_(l+1) = done_l + compute_ns,
+ *     done_l = max(t_l, max over layer l of complete_ns)
+ * and is timed on the persistent model exactly as one hbf_time_requests call
+ * holding that layer would time it.  All on `stream`; no host round trip.
+ * Outputs (device): dev_issue_ns[n] (the issue times assigned),
+ * dev_complete_ns[n], dev_layer_done_ns[L].  t_start_ns and compute_ns in
+ * [0, 2^61).  Device-detected errors fail the layer as in hbf_time_requests;
+ * its done time becomes HBF_TIME_ERROR and every later layer fails too. */
+int hbf_time_layers(hbf_model_t model, const uint64_t *dev_addr, int64_t n,
+                    const int64_t *host_layer_start, int L, int64_t t_start_ns, int64_t compute_ns,
+                    int64_t *dev_issue_ns, int64_t *dev_complete_ns, int64_t *dev_layer_done_ns,
+                    void *stream);
+
 /* Instrumented grouped GEMV with delay injection at consumption
  * (Section D2: issue is split from consumption; the wait sits at the first
  * use of the loaded value).

@@ -10,6 +10,9 @@ the address mapping is pinned separately):
   request at t and a page finishing its die read at t can start its channel
   transfer at t.  Dies serve their queue first come first served by
   (issue, index); channels by (arrival at the channel, index).
+* :func:`closed_loop_stepped` runs the same 1 ns clock over a layered
+  program: the requests of layer l+1 appear compute ticks after the tick
+  at which the last request of layer l completed.
 * :func:`enumerate_orders` lists every service order of a single server with
   identical service times and keeps the work-conserving ones: with identical
   services they all share one multiset of departure epochs, and the
@@ -109,3 +112,59 @@ def enumerate_orders(arrival, service, free=None):
         if work_conserving(order, arrival, s, f, free):
             out.append((order, f))
     return out
+
+
+def closed_loop_stepped(layer_of, die_key, chan, t_read, xfer, t_start, compute, n_layers):
+    """Layered program of ``n_layers`` layers on one 1 ns clock.
+    ``layer_of[i]`` is request i's layer (nondecreasing); all of a layer's
+    requests appear together, at t_start for layer 0 and ``compute`` ticks
+    after the previous layer's last completion (or after its own start, if it
+    has no requests).  Same service rules as :func:`time_stepped`; every
+    request must be in range (die_key >= 0).  Returns (issue, complete,
+    layer_done) lists."""
+    n = len(layer_of)
+    assert all(k >= 0 for k in die_key)
+    L = n_layers
+    members = [[] for _ in range(L)]
+    for i in range(n):
+        members[layer_of[i]].append(i)
+    issue = [None] * n
+    complete = [None] * n
+    done = []
+    die_q, chan_q, die_job, chan_job = {}, {}, {}, {}
+    t = t_start
+    limit = t_start + (n + L + 2) * (t_read + xfer + compute + 2) * 4
+    for l in range(L):
+        start = t
+        for i in members[l]:
+            issue[i] = start
+            die_q.setdefault(die_key[i], deque()).append(i)
+        left = len(members[l])
+        last = start
+        while left:
+            if t > limit:
+                raise RuntimeError("closed-loop simulation did not drain")
+            for d, (i, fin) in list(die_job.items()):
+                if fin == t:
+                    del die_job[d]
+                    chan_q.setdefault(chan[i], []).append((t, i))
+            for c, (i, fin) in list(chan_job.items()):
+                if fin == t:
+                    del chan_job[c]
+                    complete[i] = t
+                    last = t
+                    left -= 1
+            if not left:
+                break
+            for d, q in die_q.items():
+                if q and d not in die_job:
+                    die_job[d] = (q.popleft(), t + t_read)
+            for c, q in chan_q.items():
+                if q and c not in chan_job:
+                    q.sort()
+                    _, i = q.pop(0)
+                    chan_job[c] = (i, t + xfer)
+            t += 1
+        done.append(last)
+        t = last + compute
+    return issue, complete, done

@@ -139,6 +139,38 @@ class OracleModel:
         rc = self._lib.orc_time_requests(self._h, _ptr(addr), _ptr(issue), addr.size, _ptr(out))
         return rc, out
 
+    def time_layers(self, addr, layer_start, t_start, compute_ns):
+        """Closed-loop layered decode: the running program pays each layer's
+        modeled delays before it issues the next layer (paper, Section
+        "Introduction" and Section D2).  Every request of layer l is issued at
+        t_l; t_0 = t_start and t_(l+1) = max(t_l, latest completion in layer l)
+        + compute_ns.  Each layer is one call of the model.  A failed layer
+        (its completions are TIME_ERROR) makes its done time TIME_ERROR, and
+        every later layer is issued at a negative time and fails as well.
+        Returns (rc of the first failure or OK, issue, complete, done)."""
+        addr = np.ascontiguousarray(addr, dtype=np.uint64)
+        ls = [int(x) for x in layer_start]
+        issue = np.zeros(addr.size, dtype=np.int64)
+        complete = np.zeros(addr.size, dtype=np.int64)
+        done = np.zeros(len(ls) - 1, dtype=np.int64)
+        rc_first = OK
+        t = int(t_start)
+        for l in range(len(ls) - 1):
+            a, b = ls[l], ls[l + 1]
+            issue[a:b] = t
+            failed = t < 0
+            if b > a:
+                rc, c = self.time_requests(addr[a:b], issue[a:b])
+                complete[a:b] = c
+                if rc != OK:
+                    failed = True
+                    if rc_first == OK:
+                        rc_first = rc
+            d = TIME_ERROR if failed else max([t] + [int(x) for x in complete[a:b]])
+            done[l] = d
+            t = d + int(compute_ns)
+        return rc_first, issue, complete, done
+
     def die_done(self, addr, issue):
         addr = np.ascontiguousarray(addr, dtype=np.uint64)
         issue = np.ascontiguousarray(issue, dtype=np.int64)

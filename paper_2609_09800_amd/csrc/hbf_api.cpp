@@ -254,29 +254,29 @@ int hbf_classify_map(hbf_model_t m, const uint64_t *addr, int64_t n, uint64_t *m
                                                                                          : HBF_EHIP;
 }
 
-int hbf_time_requests(hbf_model_t m, const uint64_t *addr, const int64_t *issue, int64_t n,
-                      int64_t *complete, void *stream) {
-  if (!m || n < 0 || n > N_LIMIT || (n > 0 && (!addr || !issue || !complete))) return HBF_EINVAL;
-  int rc = ensure_device(m);
-  if (rc) return rc;
-  if (n == 0) return HBF_OK;
+// Workspace for calls of up to n requests (grows library-owned scratch).
+static int ensure_ws(hbf_model_t m, int64_t n) {
   const Layout L = make_layout(m->g, n);
-  if (m->ws_caller) {
-    if (m->ws_cap < L.total) return HBF_ENOWORKSPACE;
-  } else if (m->ws_cap < L.total) {
-    if (m->ws) {
-      hipDeviceSynchronize();
-      hipFree(m->ws);
-      m->ws = nullptr;
-      m->ws_cap = 0;
-    }
-    void *p = nullptr;
-    if (hipMalloc(&p, L.total) != hipSuccess) return HBF_ENOMEM;
-    m->ws = p;
-    m->ws_cap = L.total;
-    m->lib_ws = true;
+  if (m->ws_caller) return m->ws_cap < L.total ? HBF_ENOWORKSPACE : HBF_OK;
+  if (m->ws_cap >= L.total) return HBF_OK;
+  if (m->ws) {
+    hipDeviceSynchronize();
+    hipFree(m->ws);
+    m->ws = nullptr;
+    m->ws_cap = 0;
   }
-  RangeTable rt = snapshot(m);
+  void *p = nullptr;
+  if (hipMalloc(&p, L.total) != hipSuccess) return HBF_ENOMEM;
+  m->ws = p;
+  m->ws_cap = L.total;
+  m->lib_ws = true;
+  return HBF_OK;
+}
+
+// Enqueue one timing call (workspace already sized for n > 0).
+static int time_call(hbf_model_t m, const RangeTable &rt, const uint64_t *addr, const int64_t *issue,
+                     int64_t n, int64_t *complete, void *stream) {
+  const Layout L = make_layout(m->g, n);
   hipEvent_t *ev = nullptr;
   if (m->prof) {
     hipEvent_t *set = m->ev[m->prof_calls % hbf_model::RING];
@@ -288,6 +288,46 @@ int hbf_time_requests(hbf_model_t m, const uint64_t *addr, const int64_t *issue,
                                       (hipStream_t)stream, ev, kNumTimedKernels + 1);
   if (e != hipSuccess) return HBF_EHIP;
   if (m->prof) m->prof_calls++;
+  return HBF_OK;
+}
+
+int hbf_time_requests(hbf_model_t m, const uint64_t *addr, const int64_t *issue, int64_t n,
+                      int64_t *complete, void *stream) {
+  if (!m || n < 0 || n > N_LIMIT || (n > 0 && (!addr || !issue || !complete))) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  if (n == 0) return HBF_OK;
+  if ((rc = ensure_ws(m, n))) return rc;
+  return time_call(m, snapshot(m), addr, issue, n, complete, stream);
+}
+
+int hbf_time_layers(hbf_model_t m, const uint64_t *addr, int64_t n, const int64_t *ls, int L,
+                    int64_t t_start, int64_t compute_ns, int64_t *issue, int64_t *complete, int64_t *done,
+                    void *stream) {
+  if (!m || n < 0 || n > N_LIMIT || L < 0 || !ls) return HBF_EINVAL;
+  if (t_start < 0 || t_start >= ISSUE_LIMIT || compute_ns < 0 || compute_ns >= ISSUE_LIMIT) return HBF_EINVAL;
+  if (ls[0] != 0 || ls[L] != n) return HBF_EINVAL;
+  int64_t most = 0;
+  for (int l = 0; l < L; l++) {
+    if (ls[l + 1] < ls[l]) return HBF_EINVAL;
+    most = std::max(most, ls[l + 1] - ls[l]);
+  }
+  if (L > 0 && !done) return HBF_EINVAL;
+  if (n > 0 && (!addr || !issue || !complete)) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  if (L == 0) return HBF_OK;
+  if (most > 0 && (rc = ensure_ws(m, most))) return rc;
+  const RangeTable rt = snapshot(m);
+  const hipStream_t s = (hipStream_t)stream;
+  for (int l = 0; l < L; l++) {
+    const int64_t a = ls[l], cnt = ls[l + 1] - ls[l];
+    const int64_t *prev = l > 0 ? done + (l - 1) : nullptr;
+    if (launch_layer_issue(issue + a, cnt, prev, t_start, compute_ns, s) != hipSuccess) return HBF_EHIP;
+    if (cnt > 0 && (rc = time_call(m, rt, addr + a, issue + a, cnt, complete + a, stream))) return rc;
+    if (launch_layer_done(complete + a, cnt, prev, t_start, compute_ns, done + l, s) != hipSuccess)
+      return HBF_EHIP;
+  }
   return HBF_OK;
 }
 

@@ -111,6 +111,11 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
 hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, const uint64_t *addr,
                            int64_t n, uint64_t *map, hipStream_t s);
 hipError_t launch_reset(DevState *st, hipStream_t s);
+// Closed-loop layers: write the issue times of one layer / reduce its done time.
+hipError_t launch_layer_issue(int64_t *issue, int64_t count, const int64_t *prev_done, int64_t t_start,
+                              int64_t compute_ns, hipStream_t s);
+hipError_t launch_layer_done(const int64_t *complete, int64_t count, const int64_t *prev_done,
+                             int64_t t_start, int64_t compute_ns, int64_t *done, hipStream_t s);
 hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
                        int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
                        int64_t tick_ps, DevState *st, hipStream_t s);

@@ -959,6 +959,11 @@ DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, bool
 #endif
 constexpr uint32_t OUT_WCH = HBF_OUT_WCH;
 
+#ifndef HBF_OUT_WAVES_PER_CU
+#define HBF_OUT_WAVES_PER_CU 8
+#endif
+constexpr int OUT_WAVES_PER_CU = HBF_OUT_WAVES_PER_CU;
+
 // Cell of iteration `it` of this block.  OUT_WCH == 0: (window, channel)
 // order, grid-stride, so all blocks move along one common time front and
 // the scattered complete[] stores of requests that finish close in time
@@ -1318,13 +1323,20 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
                       : sl == 8 ? (const void *)k_cell_out<8> : (const void *)k_cell_out<16>;
     hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64, sizeof(CellLds));
     per_cu = per_cu < 1 ? 1 : (per_cu > 32 ? 32 : per_cu);
-    uint64_t blocks = (uint64_t)ncu * (uint64_t)per_cu;
     const uint64_t cells = (uint64_t)g.C * Lo.gmax;
-    const uint64_t need = ((cells + NXCD - 1) / NXCD) * NXCD;
-    if (blocks > need) blocks = need;
-    blocks = (blocks / NXCD) * NXCD;
-    if (blocks < NXCD) blocks = NXCD;
-    const dim3 gr((uint32_t)blocks), bl(64);
+    auto grid_of = [&](int waves_per_cu) {
+      uint64_t blocks = (uint64_t)ncu * (uint64_t)waves_per_cu;
+      const uint64_t need = ((cells + NXCD - 1) / NXCD) * NXCD;
+      if (blocks > need) blocks = need;
+      blocks = (blocks / NXCD) * NXCD;
+      if (blocks < NXCD) blocks = NXCD;
+      return dim3((uint32_t)blocks);
+    };
+    // the aggregate pass runs at full occupancy; the output pass keeps fewer
+    // cells in flight, which narrows the time front its scattered stores
+    // cover (measured: 8 waves per CU beat 4 and 15-24)
+    const dim3 gr = grid_of(per_cu), gro = grid_of(per_cu < OUT_WAVES_PER_CU ? per_cu : OUT_WAVES_PER_CU);
+    const dim3 bl(64);
     const size_t lds = sizeof(CellLds);
     const uint32_t nn = (uint32_t)Lo.n;
     if (sl == 4)
@@ -1339,13 +1351,13 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     if ((e = hipGetLastError()) != hipSuccess) return e;
     mark();
     if (sl == 4)
-      hipLaunchKernelGGL(k_cell_out<4>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
+      hipLaunchKernelGGL(k_cell_out<4>, gro, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
                          Lo.gmax, nn);
     else if (sl == 8)
-      hipLaunchKernelGGL(k_cell_out<8>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
+      hipLaunchKernelGGL(k_cell_out<8>, gro, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
                          Lo.gmax, nn);
     else
-      hipLaunchKernelGGL(k_cell_out<16>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
+      hipLaunchKernelGGL(k_cell_out<16>, gro, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
                          Lo.gmax, nn);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1376,6 +1388,71 @@ hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, con
 
 hipError_t launch_reset(DevState *st, hipStream_t s) {
   hipLaunchKernelGGL(k_reset, dim3(1), dim3(BLK), 0, s, st);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ closed-loop layers
+
+// Issue time of a layer: t_start for the first, else the previous layer's
+// done time + compute_ns (an error value stays negative and fails the layer).
+DEVI int64_t layer_time(const int64_t *prev_done, int64_t t_start, int64_t compute_ns) {
+  return prev_done ? *prev_done + compute_ns : t_start;
+}
+
+__global__ __launch_bounds__(BLK) void k_layer_issue(int64_t *__restrict__ issue, int64_t count,
+                                                     const int64_t *prev_done, int64_t t_start,
+                                                     int64_t compute_ns) {
+  const int64_t t = layer_time(prev_done, t_start, compute_ns);
+  for (int64_t i = (int64_t)blockIdx.x * BLK + threadIdx.x; i < count; i += (int64_t)gridDim.x * BLK)
+    issue[i] = t;
+}
+
+// done = max(t, every completion of the layer), or HBF_TIME_ERROR if the
+// layer failed (its completions hold that value).  One block.
+__global__ __launch_bounds__(1024) void k_layer_done(const int64_t *__restrict__ complete, int64_t count,
+                                                     const int64_t *prev_done, int64_t t_start,
+                                                     int64_t compute_ns, int64_t *done) {
+  __shared__ int64_t smax[16];
+  __shared__ int sbad[16];
+  const int64_t t = layer_time(prev_done, t_start, compute_ns);
+  int64_t mx = t;
+  int bad = t < 0;
+  for (int64_t i = threadIdx.x; i < count; i += 1024) {
+    const int64_t c = complete[i];
+    bad |= c == HBF_TIME_ERROR;
+    mx = imax(mx, c);
+  }
+  mx = wave_max(mx);
+  bad = __ballot(bad) != 0;
+  const uint32_t w = threadIdx.x >> 6;
+  if (lane_id() == 0) {
+    smax[w] = mx;
+    sbad[w] = bad;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int q = 1; q < 16; q++) {
+      mx = imax(mx, smax[q]);
+      bad |= sbad[q];
+    }
+    *done = bad ? HBF_TIME_ERROR : mx;
+  }
+}
+
+hipError_t launch_layer_issue(int64_t *issue, int64_t count, const int64_t *prev_done, int64_t t_start,
+                              int64_t compute_ns, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  int64_t blocks = (count + BLK - 1) / BLK;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_layer_issue, dim3((uint32_t)blocks), dim3(BLK), 0, s, issue, count, prev_done, t_start,
+                     compute_ns);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_done(const int64_t *complete, int64_t count, const int64_t *prev_done,
+                             int64_t t_start, int64_t compute_ns, int64_t *done, hipStream_t s) {
+  hipLaunchKernelGGL(k_layer_done, dim3(1), dim3(1024), 0, s, complete, count, prev_done, t_start, compute_ns,
+                     done);
   return hipGetLastError();
 }
 

@@ -26,7 +26,7 @@ HBF_FLAG_PLANE_PARALLEL = 1
 EXPORTED = [
     "hbf_model_create", "hbf_model_destroy", "hbf_xfer_ns", "hbf_n_die_queues", "hbf_model_reset",
     "hbf_register_range", "hbf_workspace_bytes", "hbf_set_workspace", "hbf_classify_map",
-    "hbf_time_requests", "hbf_gemv_instrumented", "hbf_wall_clock_tick_ps", "hbf_get_status",
+    "hbf_time_requests", "hbf_time_layers", "hbf_gemv_instrumented", "hbf_wall_clock_tick_ps", "hbf_get_status",
     "hbf_get_state", "hbf_set_state", "hbf_profile", "hbf_kernel_times", "hbf_strerror",
 ]
 
@@ -68,6 +68,7 @@ def load_library(path=LIB_PATH):
         "hbf_set_state": ([vp, vp, vp, vp], i32),
         "hbf_profile": ([vp, i32], i32),
         "hbf_kernel_times": ([vp, vp, vp, i32, ctypes.POINTER(i32)], i32),
+        "hbf_time_layers": ([vp, vp, i64, vp, i32, i64, i64, vp, vp, vp, vp], i32),
         "hbf_strerror": ([i32], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -174,6 +175,18 @@ class Model:
         n = addr.numel()
         assert issue.numel() == n and complete.numel() == n
         return self._lib.hbf_time_requests(self._h, _dp(addr), _dp(issue), n, _dp(complete), _sp(stream))
+
+    def time_layers(self, addr, layer_start, t_start_ns, compute_ns, issue, complete, layer_done, stream=None):
+        """Closed-loop layers.  addr/issue/complete: int64 device tensors [n];
+        layer_start: host int64 array [L+1]; layer_done: int64 device tensor [L]."""
+        import numpy as np
+        ls = np.ascontiguousarray(layer_start, dtype=np.int64)
+        L = ls.size - 1
+        n = addr.numel()
+        assert issue.numel() == n and complete.numel() == n and layer_done.numel() >= L
+        return self._lib.hbf_time_layers(self._h, _dp(addr), n, ls.ctypes.data_as(ctypes.c_void_p), L,
+                                         t_start_ns, compute_ns, _dp(issue), _dp(complete), _dp(layer_done),
+                                         _sp(stream))
 
     def gemv_instrumented(self, W, X, Y, page_issue=None, page_complete=None, measured=None, stream=None):
         """W: int16 [E,N,K] (bf16 bits); X: int16 [E,B,K]; Y: float32 [E,B,N]."""

@@ -197,6 +197,27 @@ def config3(seed=0, steps=16, tokens=64):
                     meta=dict(active_per_layer=np.array(per_layer)))
 
 
+def config3_layers(seed=0, steps=2, tokens=64):
+    """The config-3 decode as a closed loop: the same pages, grouped per
+    (step, layer) in program order, for issue times that follow the modeled
+    completions.  Returns (workload with issue times zero, layer_start[L+1])."""
+    rng = _rng(seed)
+    router = MoeRouter(rng)
+    pages, sizes = [], []
+    for s in range(steps):
+        act = router.active(tokens)
+        pg, lay = moe_step_pages(act)
+        pages.append(pg)
+        sizes.extend(np.bincount(lay, minlength=MOE_LAYERS).tolist())
+    pg = np.concatenate(pages)
+    addr = np.uint64(RANGE_BASE) + pg.astype(np.uint64) * np.uint64(PAGE)
+    rbytes = MOE_LAYERS * MOE_EXPERTS * EXPERT_BYTES
+    ls = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    w = Workload("config3-moe-decode-closed-loop", geometry(16, 8, 4), [(RANGE_BASE, rbytes)], addr,
+                 np.zeros(addr.size, dtype=np.int64))
+    return w, ls
+
+
 def dedup_demand(seed=0, batches=(1, 8, 16), steps=16):
     """Mean deduplicated active experts per layer at several batch sizes
     (the quantity of the paper's MoE-demand figure, EQ3)."""

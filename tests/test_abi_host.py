@@ -127,6 +127,27 @@ def test_workspace_and_argument_validation(lib):
     lib.hbf_model_destroy(None)
 
 
+def test_time_layers_validation_is_host_side(lib):
+    import numpy as np
+    rc, h = create(lib)
+    fake = ctypes.c_void_p(4096)  # never dereferenced: every case fails validation first
+
+    def call(ls, n, t0=0, comp=0, L=None):
+        a = np.ascontiguousarray(ls, dtype=np.int64)
+        L = a.size - 1 if L is None else L
+        return lib.hbf_time_layers(h, fake, n, a.ctypes.data_as(ctypes.c_void_p), L, t0, comp, fake, fake,
+                                   fake, None)
+    assert call([0, 5, 3, 9], 9) == -1          # decreasing layer starts
+    assert call([0, 5, 9], 10) == -1            # last start != n
+    assert call([1, 5, 9], 9) == -1             # first start != 0
+    assert call([0, 9], 9, t0=-1) == -1
+    assert call([0, 9], 9, t0=1 << 61) == -1
+    assert call([0, 9], 9, comp=-5) == -1
+    assert call([0, 9], 9, L=-1) == -1
+    assert lib.hbf_time_layers(h, fake, 9, None, 1, 0, 0, fake, fake, fake, None) == -1
+    lib.hbf_model_destroy(h)
+
+
 def test_set_state_validation_is_host_side(lib):
     import numpy as np
     rc, h = create(lib, channels=2, dies_per_channel=2, planes_per_die=1)
