@@ -993,11 +993,49 @@ DEVI bool cell_at(uint32_t it, uint32_t N, uint32_t C, uint32_t G, uint32_t &c, 
 
 // One pass over cell (c, j).  Returns M_j; with EMIT, writes instead the
 // completion of each of its requests given the entering term gin.
+// A cell's runs, lane d = die run d: die-order bounds [lo, hi) and the die
+// rank r0 of the first one.
+struct CellRuns {
+  uint32_t lo, hi, r0;
+};
+DEVI CellRuns cell_runs(const uint32_t *__restrict__ LB, const uint32_t *__restrict__ seg_start,
+                        const uint32_t *__restrict__ totals, uint32_t Dk, uint32_t gmax, uint32_t c,
+                        uint32_t j) {
+  CellRuns r = {0, 0, 0};
+  const uint32_t lane = lane_id();
+  if (lane < Dk) {
+    const uint32_t k = c * Dk + lane;
+    if (totals[k] != 0) {
+      const uint32_t *lbrow = LB + (size_t)c * (gmax + 1) * Dk + lane;
+      const uint32_t sg = seg_start[k];
+      r.r0 = lbrow[(size_t)j * Dk];
+      r.lo = r.r0 + sg;
+      r.hi = lbrow[(size_t)(j + 1) * Dk] + sg;
+    }
+  }
+  return r;
+}
+
+// The bucket path's loads: lane q < 64 reads entry q of every run (runs of
+// bucketable cells hold at most 64), all in flight at once.
+template <int SL>
+DEVI void load_runs(const int64_t *__restrict__ DD, const CellRuns &cr, int R, uint64_t (&xv)[SL]) {
+  const uint32_t lane = lane_id();
+  const uint64_t *DX = reinterpret_cast<const uint64_t *>(DD);
+  const uint32_t len = cr.hi - cr.lo;
+#pragma unroll
+  for (int d = 0; d < SL; d++) {
+    const uint32_t lod = __builtin_amdgcn_readlane(cr.lo, d);
+    const uint32_t lend = __builtin_amdgcn_readlane(len, d);
+    xv[d] = 0;
+    if (d < R && lane < lend) xv[d] = DX[lod + lane];
+  }
+}
+
 template <int SL, bool EMIT>
 DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX,
-                       const uint32_t *__restrict__ LB, const uint32_t *__restrict__ seg_start,
-                       const uint32_t *__restrict__ totals, const Geo &g, uint32_t gmax, uint32_t shift,
-                       int64_t cbase, uint32_t c, uint32_t j, int64_t gin, int64_t *complete, uint32_t n,
+                       const CellRuns &cr, const uint64_t (&xv)[SL], const Geo &g, uint32_t shift,
+                       int64_t cbase, uint32_t j, int64_t gin, int64_t *complete, uint32_t n,
                        uint32_t *errb) {
   const uint32_t lane = lane_id();
   const uint32_t Dk = g.Dk;
@@ -1006,18 +1044,7 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   const int R = (int)Dk;
   const int64_t xfer = g.xfer;
   const int64_t cstart = cbase + ((int64_t)j << shift);
-  // runs of the cell: lane d = die run d
-  uint32_t lo = 0, hi = 0, r0 = 0;
-  if (lane < Dk) {
-    const uint32_t k = c * Dk + lane;
-    if (totals[k] != 0) {
-      const uint32_t *lbrow = LB + (size_t)c * (gmax + 1) * Dk + lane;
-      const uint32_t sg = seg_start[k];
-      r0 = lbrow[(size_t)j * Dk];
-      lo = r0 + sg;
-      hi = lbrow[(size_t)(j + 1) * Dk] + sg;
-    }
-  }
+  const uint32_t lo = cr.lo, hi = cr.hi, r0 = cr.r0;
   const uint32_t len = hi - lo;
   const uint32_t rbx = wave_excl_sum(len);
   const uint32_t m = wave_sum(len);
@@ -1042,18 +1069,9 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   uint32_t cnt = 0;
   // clear the bucket table (1 KB: 16 B per lane)
   reinterpret_cast<uint4 *>(&S.u.f.tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
-  // load every run (one lane per request; all loads in flight at once).
-  // Bucketable cells are at most 2^32 ns wide, so their entries are packed
-  // words (offset in the cell << 32 | index): already the merge's sort key.
-  const uint64_t *DX = reinterpret_cast<const uint64_t *>(DD);
-  uint64_t xv[SL];
-#pragma unroll
-  for (int d = 0; d < SL; d++) {
-    const uint32_t lod = __builtin_amdgcn_readlane(lo, d);
-    const uint32_t lend = __builtin_amdgcn_readlane(len, d);
-    xv[d] = 0;
-    if (d < R && lane < lend) xv[d] = DX[lod + lane];
-  }
+  // the runs were loaded by load_runs.  Bucketable cells are at most 2^32 ns
+  // wide, so their entries are packed words (offset in the cell << 32 |
+  // index): already the merge's sort key.
   wave_sync();
 #pragma unroll
   for (int d = 0; d < SL; d++) {
@@ -1111,6 +1129,23 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   return NEG;
 }
 
+// The cell loop of both passes.  (Loading the next cell's runs while the
+// current one merges needs a second set of run registers: it halved the
+// occupancy of the aggregate pass and measured slower in the output pass.)
+template <int SL, typename Body>
+DEVI void cell_loop(const int64_t *__restrict__ DD, const uint32_t *__restrict__ LB,
+                    const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals, const Geo &g,
+                    uint32_t gmax, uint32_t N, uint32_t G, Body body) {
+  uint32_t c, j;
+  for (uint32_t it = 0; cell_at(it, N, g.C, G, c, j); it++) {
+    const CellRuns cr = cell_runs(LB, seg_start, totals, g.Dk, gmax, c, j);
+    uint64_t xv[SL];
+    load_runs<SL>(DD, cr, (int)g.Dk, xv);
+    body(c, j, cr, xv);
+    wave_sync();
+  }
+}
+
 template <int SL>
 __global__ __launch_bounds__(64) void k_cell_agg(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
@@ -1122,13 +1157,12 @@ __global__ __launch_bounds__(64) void k_cell_agg(
   const uint32_t G = ctl->G, N = G * g.C, shift = ctl->shift;
   const int64_t cbase = ctl->cbase;
   uint32_t errb = 0;
-  uint32_t c, j;
-  for (uint32_t it = 0; cell_at(it, N, g.C, G, c, j); it++) {
-    const int64_t M = cell_pass<SL, false>(S, DD, IX, LB, seg_start, totals, g, gmax, shift, cbase, c, j,
-                                           NEG, nullptr, n, &errb);
-    if (lane_id() == 0) AGG[(size_t)c * gmax + j] = M;
-    wave_sync();
-  }
+  cell_loop<SL>(DD, LB, seg_start, totals, g, gmax, N, G,
+                [&](uint32_t c, uint32_t j, const CellRuns &cr, const uint64_t (&xv)[SL]) {
+                  const int64_t M = cell_pass<SL, false>(S, DD, IX, cr, xv, g, shift, cbase, j, NEG,
+                                                         nullptr, n, &errb);
+                  if (lane_id() == 0) AGG[(size_t)c * gmax + j] = M;
+                });
 }
 
 // Per channel: GIN[j] = max(f0, M_j' for j' < j); the channel clock after the
@@ -1171,12 +1205,11 @@ __global__ __launch_bounds__(64) void k_cell_out(
   const uint32_t G = ctl->G, N = G * g.C, shift = ctl->shift;
   const int64_t cbase = ctl->cbase;
   uint32_t errb = 0;
-  uint32_t c, j;
-  for (uint32_t it = 0; cell_at(it, N, g.C, G, c, j); it++) {
-    cell_pass<SL, true>(S, DD, IX, LB, seg_start, totals, g, gmax, shift, cbase, c, j,
-                        GIN[(size_t)c * gmax + j], complete, n, &errb);
-    wave_sync();
-  }
+  cell_loop<SL>(DD, LB, seg_start, totals, g, gmax, N, G,
+                [&](uint32_t c, uint32_t j, const CellRuns &cr, const uint64_t (&xv)[SL]) {
+                  cell_pass<SL, true>(S, DD, IX, cr, xv, g, shift, cbase, j, GIN[(size_t)c * gmax + j],
+                                      complete, n, &errb);
+                });
   if (errb && lane_id() == 0) atomicOr(&ctl->err, errb);
 }
 
@@ -1319,8 +1352,8 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
     const int sl = g.Dk <= 4 ? 4 : g.Dk <= 8 ? 8 : 16;
-    const void *kfn = sl == 4 ? (const void *)k_cell_out<4>
-                      : sl == 8 ? (const void *)k_cell_out<8> : (const void *)k_cell_out<16>;
+    const void *kfn = sl == 4 ? (const void *)k_cell_agg<4>
+                      : sl == 8 ? (const void *)k_cell_agg<8> : (const void *)k_cell_agg<16>;
     hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64, sizeof(CellLds));
     per_cu = per_cu < 1 ? 1 : (per_cu > 32 ? 32 : per_cu);
     const uint64_t cells = (uint64_t)g.C * Lo.gmax;
