@@ -799,21 +799,34 @@ struct CellLds {
   uint32_t safe;
 };
 
-// Ascending bitonic sorting network over SL registers (SL a power of two).
+// Sort keys of the bucket path are integers below 2^51 held in the mantissa
+// of a double in [1, 2) (exponent bits 0x3FF): there IEEE order is integer
+// order, so one exact v_min_f64 / v_max_f64 pair is a whole compare-exchange.
+constexpr uint64_t KEY_ONE = uint64_t(0x3FF) << 52;
+constexpr uint64_t KEY_EMPTY = KEY_ONE | ((uint64_t(1) << 52) - 1);  // above every key
+
+DEVI void cx_key(uint64_t &lo, uint64_t &hi) {
+  const double a = __builtin_bit_cast(double, lo), b = __builtin_bit_cast(double, hi);
+  double mn, mx;
+  asm("v_min_f64 %0, %1, %2" : "=v"(mn) : "v"(a), "v"(b));
+  asm("v_max_f64 %0, %1, %2" : "=v"(mx) : "v"(a), "v"(b));
+  lo = __builtin_bit_cast(uint64_t, mn);
+  hi = __builtin_bit_cast(uint64_t, mx);
+}
+
+// Batcher's odd-even merge sort over SL registers (SL a power of two; 63
+// compare-exchanges for 16), ascending.
 template <int SL>
 DEVI void sort_slots(uint64_t (&a)[SL]) {
 #pragma unroll
-  for (int k = 2; k <= SL; k <<= 1) {
+  for (int p = 1; p < SL; p <<= 1) {
 #pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
+    for (int k = p; k >= 1; k >>= 1) {
 #pragma unroll
-      for (int i = 0; i < SL; i++) {
-        const int l = i ^ j;
-        if (l > i) {
-          const uint64_t x = a[i], y = a[l];
-          const bool sw = ((i & k) == 0) ? (x > y) : (x < y);
-          a[i] = sw ? y : x;
-          a[l] = sw ? x : y;
+      for (int j = k % p; j + k < SL; j += 2 * k) {
+#pragma unroll
+        for (int i = 0; i < k; i++) {
+          if (i + j + k < SL && (i + j) / (2 * p) == (i + j + k) / (2 * p)) cx_key(a[i + j], a[i + j + k]);
         }
       }
     }
@@ -1040,7 +1053,7 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   const uint32_t lane = lane_id();
   const uint32_t Dk = g.Dk;
   const uint32_t lgt = g.lg_tR;
-  const bool bucketable = (shift - lgt <= 6) && shift <= 32 && (int)Dk <= SL;
+  const bool bucketable = (shift - lgt <= 6) && shift <= 32 && lgt <= 20 && (int)Dk <= SL;
   const int R = (int)Dk;
   const int64_t xfer = g.xfer;
   const int64_t cstart = cbase + ((int64_t)j << shift);
@@ -1071,15 +1084,18 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   reinterpret_cast<uint4 *>(&S.u.f.tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
   // the runs were loaded by load_runs.  Bucketable cells are at most 2^32 ns
   // wide, so their entries are packed words (offset in the cell << 32 |
-  // index): already the merge's sort key.
+  // index); staged as the bucket's sort key: offset in the bucket (< 2^20)
+  // << 31 | index.
   wave_sync();
+  const uint64_t offmask = (uint64_t(1) << lgt) - 1;
 #pragma unroll
   for (int d = 0; d < SL; d++) {
     const uint32_t lend = __builtin_amdgcn_readlane(len, d);
     const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
     if (d < R && lane < lend) {
-      S.u.f.in[rbd + lane] = xv[d];
-      S.u.f.tbl[(xv[d] >> 32) >> lgt][d] = (uint8_t)(lane + 1);
+      const uint64_t rel = xv[d] >> 32;
+      S.u.f.in[rbd + lane] = KEY_ONE | (rel & offmask) << 31 | (xv[d] & 0xFFFFFFFFull);
+      S.u.f.tbl[rel >> lgt][d] = (uint8_t)(lane + 1);
     }
   }
   wave_sync();
@@ -1091,7 +1107,7 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
     for (int d = 0; d < SL; d++) {
       const uint32_t y = (rw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
       const uint32_t rbd = __builtin_amdgcn_readlane(rbx, d);
-      slot[d] = ~0ull;
+      slot[d] = KEY_EMPTY;
       if (y) {
         slot[d] = S.u.f.in[rbd + y - 1];
         cnt++;
@@ -1100,13 +1116,14 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   }
   sort_slots<SL>(slot);
   const uint32_t boff = wave_excl_sum(cnt);
-  // Lindley prefix over the merged order, in registers
-  const int64_t cst = cstart - rank0 * xfer;
+  // Lindley prefix over the merged order, in registers: merged position p
+  // has value dd - (rank0 + p) * xfer, dd = cell start + bucket start + offset
+  const int64_t cst = cstart + ((int64_t)lane << lgt) - rank0 * xfer;
   int64_t loc = NEG;
 #pragma unroll
   for (int i = 0; i < SL; i++) {
     if ((uint32_t)i < cnt) {
-      const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+      const int64_t v = cst + (int64_t)((slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(boff + i, (uint32_t)xfer);
       loc = imax(loc, v);
     }
   }
@@ -1118,11 +1135,11 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
 #pragma unroll
   for (int i = 0; i < SL; i++) {
     if ((uint32_t)i < cnt) {
-      const int64_t v = cst + (int64_t)(slot[i] >> 32) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+      const int64_t v = cst + (int64_t)((slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(boff + i, (uint32_t)xfer);
       carry = imax(carry, v);
       const int64_t cpl = r0x + (int64_t)mul32(boff + i + 1, (uint32_t)xfer) + carry;
       if (cpl >= TIME_LIMIT) *errb |= ERR_OVERFLOW;
-      const uint32_t ix = (uint32_t)slot[i];
+      const uint32_t ix = (uint32_t)slot[i] & 0x7FFFFFFFu;
       if (ix < n) complete[ix] = cpl;
     }
   }

@@ -119,6 +119,9 @@ GEOMS = [
     ("3x5x2-nonpow2", wl.geometry(3, 5, 2, t_read_ns=700, bw=5_000_000_000, page=12288)),
     ("1x1x1", wl.geometry(1, 1, 1, t_read_ns=50, bw=16384 * 10_000_000)),
     ("16x8x4-pp64", wl.geometry(16, 16, 4, t_read_ns=3000, bw=8_000_000_000, flags=1)),
+    # the limits: 2,048 die queues (32 ch x 64 per channel), 1,024 channels
+    ("32x16x4-pp-maxK", wl.geometry(32, 16, 4, t_read_ns=3000, bw=8_000_000_000, flags=1)),
+    ("1024x2x1-maxC", wl.geometry(1024, 2, 1, t_read_ns=20_000, bw=24_000_000_000)),
 ]
 
 STREAMS = [
