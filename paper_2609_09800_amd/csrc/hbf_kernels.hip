@@ -305,7 +305,8 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
   LdsRanges *lr = (LdsRanges *)smem;
   const uint32_t K = g.K;
   int64_t *amax = (int64_t *)(smem + ((sizeof(LdsRanges) + 15) & ~size_t(15)));
-  uint32_t *cnt = (uint32_t *)(amax + K);
+  int64_t *cmax = amax + K;  // this chunk's max of issue - (rank in chunk)*tR, per key
+  uint32_t *cnt = (uint32_t *)(cmax + K);
   uint16_t *wcnt = (uint16_t *)(cnt + K);
   uint16_t *tot = wcnt + DWAVES * K;
 
@@ -313,6 +314,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
   for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
     cnt[k] = 0;
     amax[k] = NEG;
+    cmax[k] = NEG;
   }
   __syncthreads();
 
@@ -382,16 +384,23 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
       const uint32_t k = key[e];
       const int64_t i = wbase + e * 64 + lane;
       if (k != KEY_NONE) {
-        const uint32_t rc = mycnt[k] + rank[e];            // rank among key k in the chunk
-        const uint32_t r0 = cnt[k] + rc;                   // rank among key k in the tile
-        atomicMax((long long *)&amax[k], (long long)(iss[e] - (int64_t)mul32(r0, (uint32_t)tR)));
+        const uint32_t rc = mycnt[k] + rank[e];  // rank among key k in the chunk
+        atomicMax((long long *)&cmax[k], (long long)(iss[e] - (int64_t)mul32(rc, (uint32_t)tR)));
         KR[i] = (k << 16) | rc;
       } else if (i < t1) {
         KR[i] = (uint32_t)KEY_NONE << 16;
       }
     }
     __syncthreads();
-    for (uint32_t k = threadIdx.x; k < K; k += DBLK) cnt[k] += tot[k];
+    // fold the chunk into the tile: ranks in the tile are cnt[k] + rank in chunk
+    for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+      const uint32_t t = tot[k];
+      if (t) {
+        amax[k] = imax(amax[k], cmax[k] - (int64_t)mul32(cnt[k], (uint32_t)tR));
+        cmax[k] = NEG;
+        cnt[k] += t;
+      }
+    }
     __syncthreads();
   }
   // tile aggregate per die queue: departure of the last request from an idle die
@@ -404,9 +413,12 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
   if (errb) atomicOr(&ctl->err, errb);
 }
 
-// ------------------------------------------------------------------ k_tile_scan
-
-// Per die queue, compose the tiles in order.  Block = 16 keys x 16 tile groups.
+// Per die queue, compose the tiles in order.  One wave per die queue, lane g
+// holding a contiguous group of tiles: each lane folds its group, a wave
+// scan composes the groups, and each lane walks its group again writing the
+// clock and rank entering every tile.  Composition of (A, count) segments in
+// order: (A1, c1) then (A2, c2) = (max(A2, A1 + c2*tR), c1 + c2), A = NEG
+// when empty; a clock L entering a segment leaves as max(A, L + c*tR).
 __global__ __launch_bounds__(BLK) void k_tile_scan(const uint32_t *__restrict__ agg_cnt,
                                                    const int64_t *__restrict__ agg_A, uint32_t nt,
                                                    uint32_t K, int64_t tR, const DevState *st,
@@ -414,57 +426,57 @@ __global__ __launch_bounds__(BLK) void k_tile_scan(const uint32_t *__restrict__ 
                                                    uint32_t *__restrict__ tin_base,
                                                    uint32_t *__restrict__ totals,
                                                    int64_t *__restrict__ dfnew, CallCtl *ctl) {
-  __shared__ int64_t gA[16][16];
-  __shared__ uint32_t gC[16][16];
-  __shared__ int64_t inL[16][16];
-  __shared__ uint32_t inB[16][16];
   if (agent_load32(&ctl->err)) return;
-  const uint32_t kk = threadIdx.x & 15, tg = threadIdx.x >> 4;
-  const uint32_t k = blockIdx.x * 16 + kk;
-  const uint32_t per = (nt + 15) / 16;
-  const uint32_t ta = tg * per, tb = min(nt, ta + per);
-  // group aggregate: (A, count), A = NEG when empty
+  const uint32_t lane = lane_id();
+  const uint32_t k = blockIdx.x * WAVES + (threadIdx.x >> 6);
+  if (k >= K) return;  // whole wave
+  const uint32_t per = (nt + 63) / 64;
+  const uint32_t ta = min(nt, lane * per), tb = min(nt, ta + per);
   int64_t A = NEG;
   uint32_t C = 0;
-  if (k < K) {
-    for (uint32_t t = ta; t < tb; t++) {
-      const uint32_t c = agg_cnt[(size_t)t * K + k];
-      if (c) {
-        A = imax(agg_A[(size_t)t * K + k], A + (int64_t)c * tR);
-        C += c;
-      }
+  for (uint32_t t = ta; t < tb; t++) {
+    const uint32_t c = agg_cnt[(size_t)t * K + k];
+    if (c) {
+      A = imax(agg_A[(size_t)t * K + k], A + (int64_t)c * tR);
+      C += c;
     }
   }
-  gA[tg][kk] = A;
-  gC[tg][kk] = C;
-  __syncthreads();
-  if (tg == 0 && k < K) {
-    int64_t L = st->die_free[k];
-    uint32_t base = 0;
-    for (int q = 0; q < 16; q++) {
-      inL[q][kk] = L;
-      inB[q][kk] = base;
-      if (gC[q][kk]) L = imax(gA[q][kk], L + (int64_t)gC[q][kk] * tR);
-      base += gC[q][kk];
-    }
-    totals[k] = base;
-    dfnew[k] = L;
-    if (base) {
-      atomicMax((long long *)&ctl->max_dd, (long long)L);
-      if (L >= TIME_LIMIT) atomicOr(&ctl->err, ERR_OVERFLOW);
+  // inclusive scan over the lanes' groups
+  int64_t iA = A;
+  uint32_t iC = C;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int64_t pA = __shfl_up(iA, d);
+    const uint32_t pC = __shfl_up(iC, d);
+    if (lane >= (uint32_t)d) {
+      iA = imax(iA, pA + (int64_t)iC * tR);
+      iC += pC;
     }
   }
-  __syncthreads();
-  if (k < K) {
-    int64_t L = inL[tg][kk];
-    uint32_t base = inB[tg][kk];
-    for (uint32_t t = ta; t < tb; t++) {
-      tin_L[(size_t)t * K + k] = L;
-      tin_base[(size_t)t * K + k] = base;
-      const uint32_t c = agg_cnt[(size_t)t * K + k];
-      if (c) L = imax(agg_A[(size_t)t * K + k], L + (int64_t)c * tR);
-      base += c;
+  int64_t xA = __shfl_up(iA, 1);
+  uint32_t xC = __shfl_up(iC, 1);
+  if (lane == 0) {
+    xA = NEG;
+    xC = 0;
+  }
+  const int64_t f0 = st->die_free[k];
+  int64_t L = imax(xA, f0 + (int64_t)xC * tR);  // clock entering the lane's group
+  uint32_t base = xC;
+  if (lane == 63) {
+    const int64_t Lend = imax(iA, f0 + (int64_t)iC * tR);
+    totals[k] = iC;
+    dfnew[k] = Lend;
+    if (iC) {
+      atomicMax((long long *)&ctl->max_dd, (long long)Lend);
+      if (Lend >= TIME_LIMIT) atomicOr(&ctl->err, ERR_OVERFLOW);
     }
+  }
+  for (uint32_t t = ta; t < tb; t++) {
+    tin_L[(size_t)t * K + k] = L;
+    tin_base[(size_t)t * K + k] = base;
+    const uint32_t c = agg_cnt[(size_t)t * K + k];
+    if (c) L = imax(agg_A[(size_t)t * K + k], L + (int64_t)c * tR);
+    base += c;
   }
 }
 
@@ -1183,31 +1195,31 @@ __global__ __launch_bounds__(64) void k_cell_agg(
 }
 
 // Per channel: GIN[j] = max(f0, M_j' for j' < j); the channel clock after the
-// call is (its request count) * xfer + max(f0, every M_j).
+// call is (its request count) * xfer + max(f0, every M_j).  One block per
+// channel, each thread a contiguous range of windows: fold, block scan, walk.
 __global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ AGG, int64_t *__restrict__ GIN,
                                                    const uint32_t *__restrict__ totals, Geo g,
                                                    const CallCtl *ctl, const DevState *st,
                                                    int64_t *__restrict__ cfnew, uint32_t gmax) {
   __shared__ int64_t sh[WAVES];
-  __shared__ int64_t s_carry;
   if (agent_load32(&ctl->err)) return;
   const uint32_t c = blockIdx.x, G = ctl->G;
   const size_t row = (size_t)c * gmax;
-  int64_t carry = st->chan_free[c];
-  for (uint32_t base = 0; base < G; base += BLK) {
-    const uint32_t jj = base + threadIdx.x;
-    const int64_t v = jj < G ? AGG[row + jj] : NEG;
-    const int64_t ex = block_excl_max<WAVES>(v, sh);
-    if (jj < G) GIN[row + jj] = imax(carry, ex);
-    if (threadIdx.x == BLK - 1) s_carry = imax(carry, imax(ex, v));
-    __syncthreads();
-    carry = s_carry;
-    __syncthreads();
+  const uint32_t per = (G + BLK - 1) / BLK;
+  const uint32_t ja = min(G, threadIdx.x * per), jb = min(G, ja + per);
+  int64_t m = NEG;
+  for (uint32_t j = ja; j < jb; j++) m = imax(m, AGG[row + j]);
+  const int64_t ex = block_excl_max<WAVES>(m, sh);
+  const int64_t f0 = st->chan_free[c];
+  int64_t carry = imax(f0, ex);
+  for (uint32_t j = ja; j < jb; j++) {
+    GIN[row + j] = carry;
+    carry = imax(carry, AGG[row + j]);
   }
-  if (threadIdx.x == 0) {
+  if (threadIdx.x == BLK - 1) {
     uint64_t tot = 0;
     for (uint32_t d = 0; d < g.Dk; d++) tot += totals[c * g.Dk + d];
-    cfnew[c] = (int64_t)tot * g.xfer + carry;
+    cfnew[c] = (int64_t)tot * g.xfer + imax(f0, imax(ex, m));
   }
 }
 
@@ -1300,9 +1312,9 @@ static uint32_t bits_for(uint32_t K) {
 
 static size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
 
-// LDS of pass 1: range table | amax[K] i64 | cnt[K] | wcnt[DWAVES][K] u16 | tot[K] u16
+// LDS of pass 1: range table | amax[K], cmax[K] i64 | cnt[K] | wcnt[DWAVES][K] u16 | tot[K] u16
 size_t lds_die_reduce(uint32_t K) {
-  return align16(sizeof(LdsRanges)) + K * (8 + 4) + DWAVES * K * 2 + K * 2;
+  return align16(sizeof(LdsRanges)) + K * (8 + 8 + 4) + DWAVES * K * 2 + K * 2;
 }
 size_t lds_die_scatter(uint32_t K) {
   return (size_t)CHUNKP * 8 + (size_t)K * (sizeof(KeyA) + sizeof(KeyW) + 4) + (size_t)CHUNKP * 6;
@@ -1348,7 +1360,7 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
-  hipLaunchKernelGGL(k_tile_scan, dim3((g.K + 15) / 16), dim3(BLK), 0, s, agg_cnt, agg_A, Lo.nt, g.K,
+  hipLaunchKernelGGL(k_tile_scan, dim3((g.K + WAVES - 1) / WAVES), dim3(BLK), 0, s, agg_cnt, agg_A, Lo.nt, g.K,
                      g.tR, st, tin_L, tin_base, totals, dfnew, ctl);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
