@@ -535,6 +535,9 @@ __global__ __launch_bounds__(BLK) void k_key_scan(const uint32_t *__restrict__ t
 // LDS: sval[CHUNKP] i64 | KA[K] | KW[K] | hist[K] u32 | skey, srank,
 //      sloc [CHUNKP] u16
 constexpr int CHUNKP = CHUNK + CHUNK / 16;
+// Runs up to this length are scanned by one thread each; a chunk with a
+// longer run (a hot die) takes the block-wide segmented scan.
+constexpr uint32_t RUN_WALK_MAX = 64;
 
 struct KeyA {
   uint32_t koff, cnt;
@@ -553,7 +556,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ SegMax shseg[DWAVES];
   __shared__ uint32_t shsum[DWAVES];
-  __shared__ uint32_t s_nvalid;
+  __shared__ uint32_t s_nvalid, s_longrun;
   if (agent_load32(&ctl->err)) return;
   const uint32_t K = g.K;
   int64_t *sval = (int64_t *)smem;
@@ -599,6 +602,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
   if (t0 < t1) fetch(t0);
   for (int64_t c0 = t0; c0 < t1; c0 += CHUNK) {
     for (uint32_t k = threadIdx.x; k < K; k += DBLK) hist[k] = 0;
+    if (threadIdx.x == 0) s_longrun = 0;
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < DITEMS; e++) {
@@ -613,11 +617,14 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
       for (uint32_t k = a0; k < b0; k++) sum += hist[k];
       uint32_t ex;
       const uint32_t all = block_excl_sum<DWAVES>(sum, &ex, shsum);
+      uint32_t longest = 0;
       for (uint32_t k = a0; k < b0; k++) {
         KA[k].koff = ex;
         ex += hist[k];
+        longest = max(longest, hist[k]);
       }
       if (threadIdx.x == 0) s_nvalid = all;
+      if (longest > RUN_WALK_MAX) s_longrun = 1u;
     }
     __syncthreads();
     // stage v = issue - r0*tR in die order (r0 = rank of the request among
@@ -642,7 +649,21 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
     __syncthreads();
     if (c0 + CHUNK < t1) fetch(c0 + CHUNK);
     const uint32_t nv = s_nvalid;
-    {
+    if (!s_longrun) {
+      // one thread per die queue walks its run with a running maximum (the
+      // run's head already holds the entering clock)
+      for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+        const uint32_t t = hist[k];
+        if (!t) continue;
+        const KeyA ka = KA[k];
+        int64_t run = NEG;
+        for (uint32_t q = 0; q < t; q++) {
+          const uint32_t P = pad16(ka.koff + q);
+          run = imax(run, sval[P]);
+          sval[P] = (int64_t)mul32(ka.cnt + q + 1, tR) + run;
+        }
+      }
+    } else {  // a long run: segmented scan over the whole block
       const uint32_t p0 = threadIdx.x * DITEMS;
       int64_t vals[DITEMS];
       SegMax agg = {0, NEG};
