@@ -13,11 +13,16 @@ the address mapping is pinned separately):
 * :func:`closed_loop_stepped` runs the same 1 ns clock over a layered
   program: the requests of layer l+1 appear compute ticks after the tick
   at which the last request of layer l completed.
+* :func:`event_driven` and :func:`closed_loop_events` follow the same
+  rules with a discrete-event calendar (a heap of timed events) instead of
+  a 1 ns clock, so they reach the nanosecond timings of real geometries
+  (microsecond reads, thousands of requests) that the clock cannot.
 * :func:`enumerate_orders` lists every service order of a single server with
   identical service times and keeps the work-conserving ones: with identical
   services they all share one multiset of departure epochs, and the
   first-come-first-served order minimises the largest flow time.
 """
+import heapq
 import itertools
 from collections import deque
 
@@ -168,3 +173,131 @@ def closed_loop_stepped(layer_of, die_key, chan, t_read, xfer, t_start, compute,
         done.append(last)
         t = last + compute
     return issue, complete, done
+
+
+# ---------------------------------------------------------------- event calendar
+
+_DIE_END, _CHAN_END, _ARRIVE, _WAKE_DIE, _WAKE_CHAN, _RELEASE = range(6)
+
+
+class _Calendar:
+    """Two-station system on a heap of (time, kind, item) events.  All
+    events of one instant are applied before any service starts, matching
+    the completions-then-arrivals-then-starts order of the 1 ns clock."""
+
+    def __init__(self, die_key, chan, t_read, xfer, die_free, chan_free):
+        self.die_key, self.chan = die_key, chan
+        self.t_read, self.xfer = t_read, xfer
+        self.die_free = dict(die_free or {})    # busy-until of a die before its first start
+        self.chan_free = dict(chan_free or {})
+        self.die_q, self.chan_q = {}, {}        # resource -> heap of (priority, request)
+        self.die_busy, self.chan_busy = set(), set()
+        self.ev = []
+        n = len(die_key)
+        self.die_done = [None] * n
+        self.complete = [None] * n
+
+    def push(self, t, kind, x):
+        heapq.heappush(self.ev, (t, kind, x))
+
+    def run(self, on_complete=None):
+        while self.ev:
+            t = self.ev[0][0]
+            dies, chans = set(), set()
+            while self.ev and self.ev[0][0] == t:
+                _, kind, x = heapq.heappop(self.ev)
+                if kind == _DIE_END:
+                    d, c = self.die_key[x], self.chan[x]
+                    self.die_busy.discard(d)
+                    self.die_done[x] = t
+                    heapq.heappush(self.chan_q.setdefault(c, []), (t, x))
+                    dies.add(d)
+                    chans.add(c)
+                elif kind == _CHAN_END:
+                    c = self.chan[x]
+                    self.chan_busy.discard(c)
+                    self.complete[x] = t
+                    chans.add(c)
+                    if on_complete is not None:
+                        on_complete(t, x)
+                elif kind == _ARRIVE:
+                    i, prio = x
+                    d = self.die_key[i]
+                    heapq.heappush(self.die_q.setdefault(d, []), (prio, i))
+                    dies.add(d)
+                elif kind == _WAKE_DIE:
+                    dies.add(x)
+                elif kind == _WAKE_CHAN:
+                    chans.add(x)
+                else:  # _RELEASE: a callback that schedules more arrivals
+                    x(t)
+            for d in dies:
+                self._start(t, d, self.die_q, self.die_busy, self.die_free, self.t_read, _DIE_END, _WAKE_DIE)
+            for c in chans:
+                self._start(t, c, self.chan_q, self.chan_busy, self.chan_free, self.xfer, _CHAN_END, _WAKE_CHAN)
+
+    def _start(self, t, r, queues, busy, free, service, end_kind, wake_kind):
+        q = queues.get(r)
+        if not q or r in busy:
+            return
+        if free.get(r, t) > t:
+            self.push(free[r], wake_kind, r)
+            return
+        free.pop(r, None)
+        _, i = heapq.heappop(q)
+        busy.add(r)
+        self.push(t + service, end_kind, i)
+
+
+def event_driven(issue, die_key, chan, t_read, xfer, die_free=None, chan_free=None):
+    """Same contract as :func:`time_stepped`, on an event calendar."""
+    cal = _Calendar(die_key, chan, t_read, xfer, die_free, chan_free)
+    for i in range(len(issue)):
+        if die_key[i] >= 0:
+            cal.push(issue[i], _ARRIVE, (i, (issue[i], i)))
+    cal.run()
+    return cal.die_done, cal.complete
+
+
+def closed_loop_events(layer_of, die_key, chan, t_read, xfer, t_start, compute, n_layers,
+                       die_free=None, chan_free=None):
+    """Same contract as :func:`closed_loop_stepped` on an event calendar:
+    layer l+1's requests arrive ``compute`` ns after layer l's last
+    completion (after its start if it is empty).  Requests with die_key < 0
+    complete at their issue time."""
+    n = len(layer_of)
+    members = [[] for _ in range(n_layers)]
+    for i in range(n):
+        members[layer_of[i]].append(i)
+    issue = [None] * n
+    done = [None] * n_layers
+    cal = _Calendar(die_key, chan, t_read, xfer, die_free, chan_free)
+    state = {"layer": -1, "left": 0, "last": None}
+
+    def release(t):
+        # layer state["layer"] + 1 starts at t
+        l = state["layer"] + 1
+        if l >= n_layers:
+            return
+        state["layer"], state["last"], state["left"] = l, t, 0
+        for i in members[l]:
+            issue[i] = t
+            if die_key[i] >= 0:
+                state["left"] += 1
+                cal.push(t, _ARRIVE, (i, (t, i)))
+            else:
+                cal.complete[i] = t
+        if state["left"] == 0:
+            done[l] = t
+            cal.push(t + compute, _RELEASE, release)
+
+    def on_complete(t, i):
+        state["left"] -= 1
+        state["last"] = max(state["last"], t)
+        if state["left"] == 0:
+            done[state["layer"]] = state["last"]
+            cal.push(state["last"] + compute, _RELEASE, release)
+
+    cal.push(t_start, _RELEASE, release)
+    cal.run(on_complete)
+    return issue, cal.complete, done

@@ -67,6 +67,7 @@ def test_pins_catch_mutant(tmp_path, name):
     subprocess.check_call(["gcc", "-O1", "-std=gnu11", "-shared", "-fPIC", str(mut), "-o", str(lib), "-lm"])
     env = dict(os.environ, HBF_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_events.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
