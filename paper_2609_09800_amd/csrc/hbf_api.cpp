@@ -325,8 +325,10 @@ int hbf_time_layers(hbf_model_t m, const uint64_t *addr, int64_t n, const int64_
     const int64_t *prev = l > 0 ? done + (l - 1) : nullptr;
     if (launch_layer_issue(issue + a, cnt, prev, t_start, compute_ns, s) != hipSuccess) return HBF_EHIP;
     if (cnt > 0 && (rc = time_call(m, rt, addr + a, issue + a, cnt, complete + a, stream))) return rc;
-    if (launch_layer_done(complete + a, cnt, prev, t_start, compute_ns, done + l, s) != hipSuccess)
-      return HBF_EHIP;
+    // the control block of the call just enqueued; read only when cnt > 0
+    const CallCtl *ctl = cnt > 0 ? reinterpret_cast<const CallCtl *>((char *)m->ws + make_layout(m->g, cnt).off_ctl)
+                                 : nullptr;
+    if (launch_layer_done(ctl, cnt, prev, t_start, compute_ns, done + l, s) != hipSuccess) return HBF_EHIP;
   }
   return HBF_OK;
 }

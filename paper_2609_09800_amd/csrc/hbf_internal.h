@@ -84,6 +84,7 @@ struct CallCtl {
   uint32_t G;         // time cells per channel
   uint32_t shift;     // log2(cell width in ns)
   int64_t max_dd;     // largest die-done time of the call
+  int64_t max_cpl;    // largest in-range completion of the call (NEG if none)
   int64_t cbase;      // origin of the cell grid (= first issue time)
 };
 
@@ -114,8 +115,8 @@ hipError_t launch_reset(DevState *st, hipStream_t s);
 // Closed-loop layers: write the issue times of one layer / reduce its done time.
 hipError_t launch_layer_issue(int64_t *issue, int64_t count, const int64_t *prev_done, int64_t t_start,
                               int64_t compute_ns, hipStream_t s);
-hipError_t launch_layer_done(const int64_t *complete, int64_t count, const int64_t *prev_done,
-                             int64_t t_start, int64_t compute_ns, int64_t *done, hipStream_t s);
+hipError_t launch_layer_done(const CallCtl *ctl, int64_t count, const int64_t *prev_done, int64_t t_start,
+                             int64_t compute_ns, int64_t *done, hipStream_t s);
 hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
                        int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
                        int64_t tick_ps, DevState *st, hipStream_t s);

@@ -284,6 +284,7 @@ __global__ void k_prologue(CallCtl *ctl) {
     ctl->G = 0;
     ctl->shift = 0;
     ctl->max_dd = NEG;
+    ctl->max_cpl = NEG;
     ctl->cbase = 0;
   }
 }
@@ -1220,7 +1221,7 @@ __global__ __launch_bounds__(64) void k_cell_agg(
 // channel, each thread a contiguous range of windows: fold, block scan, walk.
 __global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ AGG, int64_t *__restrict__ GIN,
                                                    const uint32_t *__restrict__ totals, Geo g,
-                                                   const CallCtl *ctl, const DevState *st,
+                                                   CallCtl *ctl, const DevState *st,
                                                    int64_t *__restrict__ cfnew, uint32_t gmax) {
   __shared__ int64_t sh[WAVES];
   if (agent_load32(&ctl->err)) return;
@@ -1240,7 +1241,10 @@ __global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ A
   if (threadIdx.x == BLK - 1) {
     uint64_t tot = 0;
     for (uint32_t d = 0; d < g.Dk; d++) tot += totals[c * g.Dk + d];
-    cfnew[c] = (int64_t)tot * g.xfer + imax(f0, imax(ex, m));
+    const int64_t last = (int64_t)tot * g.xfer + imax(f0, imax(ex, m));
+    cfnew[c] = last;
+    // the channel's last completion of this call
+    if (tot) atomicMax((long long *)&ctl->max_cpl, (long long)last);
   }
 }
 
@@ -1491,35 +1495,23 @@ __global__ __launch_bounds__(BLK) void k_layer_issue(int64_t *__restrict__ issue
 }
 
 // done = max(t, every completion of the layer), or HBF_TIME_ERROR if the
-// layer failed (its completions hold that value).  One block.
-__global__ __launch_bounds__(1024) void k_layer_done(const int64_t *__restrict__ complete, int64_t count,
-                                                     const int64_t *prev_done, int64_t t_start,
-                                                     int64_t compute_ns, int64_t *done) {
-  __shared__ int64_t smax[16];
-  __shared__ int sbad[16];
+// layer failed.  Its in-range completions end no later than the last one
+// of each channel, which the channel scan recorded in the call's control
+// block; native requests complete at t.
+__global__ void k_layer_done(const CallCtl *ctl, int64_t count, const int64_t *prev_done, int64_t t_start,
+                             int64_t compute_ns, int64_t *done) {
+  if (threadIdx.x != 0) return;
   const int64_t t = layer_time(prev_done, t_start, compute_ns);
-  int64_t mx = t;
-  int bad = t < 0;
-  for (int64_t i = threadIdx.x; i < count; i += 1024) {
-    const int64_t c = complete[i];
-    bad |= c == HBF_TIME_ERROR;
-    mx = imax(mx, c);
-  }
-  mx = wave_max(mx);
-  bad = __ballot(bad) != 0;
-  const uint32_t w = threadIdx.x >> 6;
-  if (lane_id() == 0) {
-    smax[w] = mx;
-    sbad[w] = bad;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int q = 1; q < 16; q++) {
-      mx = imax(mx, smax[q]);
-      bad |= sbad[q];
-    }
-    *done = bad ? HBF_TIME_ERROR : mx;
-  }
+  int64_t d;
+  if (t < 0)
+    d = HBF_TIME_ERROR;
+  else if (count == 0)
+    d = t;
+  else if (agent_load32(&ctl->err))
+    d = HBF_TIME_ERROR;
+  else
+    d = imax(t, ctl->max_cpl);
+  *done = d;
 }
 
 hipError_t launch_layer_issue(int64_t *issue, int64_t count, const int64_t *prev_done, int64_t t_start,
@@ -1532,10 +1524,9 @@ hipError_t launch_layer_issue(int64_t *issue, int64_t count, const int64_t *prev
   return hipGetLastError();
 }
 
-hipError_t launch_layer_done(const int64_t *complete, int64_t count, const int64_t *prev_done,
-                             int64_t t_start, int64_t compute_ns, int64_t *done, hipStream_t s) {
-  hipLaunchKernelGGL(k_layer_done, dim3(1), dim3(1024), 0, s, complete, count, prev_done, t_start, compute_ns,
-                     done);
+hipError_t launch_layer_done(const CallCtl *ctl, int64_t count, const int64_t *prev_done, int64_t t_start,
+                             int64_t compute_ns, int64_t *done, hipStream_t s) {
+  hipLaunchKernelGGL(k_layer_done, dim3(1), dim3(64), 0, s, ctl, count, prev_done, t_start, compute_ns, done);
   return hipGetLastError();
 }
 
