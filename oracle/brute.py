@@ -13,6 +13,9 @@ the address mapping is pinned separately):
 * :func:`closed_loop_stepped` runs the same 1 ns clock over a layered
   program: the requests of layer l+1 appear compute ticks after the tick
   at which the last request of layer l completed.
+* :func:`event_driven_refresh` adds pending refresh quanta (Section D4) to
+  the calendar: a die that starts a read with a quantum pending runs the
+  quantum first.
 * :func:`event_driven` and :func:`closed_loop_events` follow the same
   rules with a discrete-event calendar (a heap of timed events) instead of
   a 1 ns clock, so they reach the nanosecond timings of real geometries
@@ -185,9 +188,14 @@ class _Calendar:
     events of one instant are applied before any service starts, matching
     the completions-then-arrivals-then-starts order of the 1 ns clock."""
 
-    def __init__(self, die_key, chan, t_read, xfer, die_free, chan_free):
+    def __init__(self, die_key, chan, t_read, xfer, die_free, chan_free, t_quantum=0, quanta=None):
         self.die_key, self.chan = die_key, chan
         self.t_read, self.xfer = t_read, xfer
+        # refresh: per die, the ids of its pending quanta (oldest first); a
+        # die that starts a read with one pending runs the quantum first
+        self.t_quantum = t_quantum
+        self.quanta = {d: deque(q) for d, q in (quanta or {}).items()}
+        self.quantum_done = {}
         self.die_free = dict(die_free or {})    # busy-until of a die before its first start
         self.chan_free = dict(chan_free or {})
         self.die_q, self.chan_q = {}, {}        # resource -> heap of (priority, request)
@@ -232,7 +240,13 @@ class _Calendar:
                 else:  # _RELEASE: a callback that schedules more arrivals
                     x(t)
             for d in dies:
-                self._start(t, d, self.die_q, self.die_busy, self.die_free, self.t_read, _DIE_END, _WAKE_DIE)
+                q = self.quanta.get(d)
+                claim = bool(q) and bool(self.die_q.get(d)) and d not in self.die_busy \
+                    and self.die_free.get(d, t) <= t
+                if claim:
+                    self.quantum_done[q.popleft()] = t + self.t_quantum
+                self._start(t, d, self.die_q, self.die_busy, self.die_free,
+                            self.t_read + (self.t_quantum if claim else 0), _DIE_END, _WAKE_DIE)
             for c in chans:
                 self._start(t, c, self.chan_q, self.chan_busy, self.chan_free, self.xfer, _CHAN_END, _WAKE_CHAN)
 
@@ -259,45 +273,17 @@ def event_driven(issue, die_key, chan, t_read, xfer, die_free=None, chan_free=No
     return cal.die_done, cal.complete
 
 
-def closed_loop_events(layer_of, die_key, chan, t_read, xfer, t_start, compute, n_layers,
-                       die_free=None, chan_free=None):
-    """Same contract as :func:`closed_loop_stepped` on an event calendar:
-    layer l+1's requests arrive ``compute`` ns after layer l's last
-    completion (after its start if it is empty).  Requests with die_key < 0
-    complete at their issue time."""
-    n = len(layer_of)
-    members = [[] for _ in range(n_layers)]
-    for i in range(n):
-        members[layer_of[i]].append(i)
-    issue = [None] * n
-    done = [None] * n_layers
-    cal = _Calendar(die_key, chan, t_read, xfer, die_free, chan_free)
-    state = {"layer": -1, "left": 0, "last": None}
+def event_driven_refresh(issue, die_key, chan, t_read, xfer, t_quantum, quanta, die_free=None, chan_free=None):
+    """:func:`event_driven` with refresh quanta pending at the dies:
+    ``quanta`` maps a die to the ids of its pending quanta, oldest first.  A
+    die that starts serving a read while it has one pending runs that quantum
+    first, for ``t_quantum``.  Returns (die_done, complete, {id: quantum
+    completion}, {die: ids still pending})."""
+    cal = _Calendar(die_key, chan, t_read, xfer, die_free, chan_free, t_quantum, quanta)
+    for i in range(len(issue)):
+        if die_key[i] >= 0:
+            cal.push(issue[i], _ARRIVE, (i, (issue[i], i)))
+    cal.run()
+    left = {d: list(q) for d, q in cal.quanta.items() if q}
+    return cal.die_done, cal.complete, cal.quantum_done, left
 
-    def release(t):
-        # layer state["layer"] + 1 starts at t
-        l = state["layer"] + 1
-        if l >= n_layers:
-            return
-        state["layer"], state["last"], state["left"] = l, t, 0
-        for i in members[l]:
-            issue[i] = t
-            if die_key[i] >= 0:
-                state["left"] += 1
-                cal.push(t, _ARRIVE, (i, (t, i)))
-            else:
-                cal.complete[i] = t
-        if state["left"] == 0:
-            done[l] = t
-            cal.push(t + compute, _RELEASE, release)
-
-    def on_complete(t, i):
-        state["left"] -= 1
-        state["last"] = max(state["last"], t)
-        if state["left"] == 0:
-            done[state["layer"]] = state["last"]
-            cal.push(state["last"] + compute, _RELEASE, release)
-
-    cal.push(t_start, _RELEASE, release)
-    cal.run(on_complete)
-    return issue, cal.complete, done

@@ -87,7 +87,16 @@ typedef struct {
   int64_t *chan_free;
   uint8_t *chan_busy;
   uint32_t n_die_keys;
+  /* refresh (Section D4): per die queue, the ids of its pending quanta in
+   * plan order; the completion time of every quantum ever submitted */
+  int64_t t_prog_ns;
+  struct orc_fifo *fifo;
+  int64_t *qdone;
+  int64_t nq, qcap;
 } orc_model;
+
+typedef struct orc_fifo { int64_t *id; int64_t head, len, cap; } orc_fifo;
+#define ORC_REFRESH_PENDING ((int64_t)-1)
 
 uint32_t orc_n_die_keys(const orc_params *p) {
   uint64_t k = (uint64_t)p->channels * p->dies_per_channel;
@@ -126,6 +135,9 @@ int orc_create(const orc_params *p, orc_model **out) {
 
 void orc_destroy(orc_model *m) {
   if (!m) return;
+  if (m->fifo)
+    for (uint32_t k = 0; k < m->n_die_keys; k++) free(m->fifo[k].id);
+  free(m->fifo); free(m->qdone);
   free(m->die_free); free(m->die_busy); free(m->chan_free); free(m->chan_busy);
   free(m);
 }
@@ -134,6 +146,9 @@ int64_t orc_xfer_ns(const orc_model *m) { return m->xfer_ns; }
 
 /* Return every resource to "idle since minus infinity". */
 void orc_reset(orc_model *m) {
+  /* pending refresh quanta are dropped; their completion stays pending */
+  if (m->fifo)
+    for (uint32_t k = 0; k < m->n_die_keys; k++) m->fifo[k].head = m->fifo[k].len = 0;
   memset(m->die_busy, 0, m->n_die_keys);
   memset(m->chan_busy, 0, m->p.channels);
   memset(m->die_free, 0, sizeof(int64_t) * m->n_die_keys);
@@ -169,10 +184,9 @@ static int orc_classify(const orc_model *m, uint64_t addr) {
 
 typedef struct { uint32_t ch, die, plane; uint64_t page; uint32_t key; } orc_loc;
 
-/* Device page and its (channel, die, plane, page) by channel-first striping. */
-static orc_loc orc_map(const orc_model *m, int r, uint64_t addr) {
+/* (channel, die, plane, page) of device page dp by channel-first striping. */
+static orc_loc orc_locate(const orc_model *m, uint64_t dp) {
   const orc_params *p = &m->p;
-  uint64_t dp = m->ranges[r].dev_page_base + (addr - m->ranges[r].base) / p->page_bytes;
   orc_loc L;
   L.ch = (uint32_t)(dp % p->channels);
   L.die = (uint32_t)((dp / p->channels) % p->dies_per_channel);
@@ -181,6 +195,11 @@ static orc_loc orc_map(const orc_model *m, int r, uint64_t addr) {
   L.key = L.ch * p->dies_per_channel + L.die;
   if (p->flags & ORC_FLAG_PLANE_PARALLEL) L.key = L.key * p->planes_per_die + L.plane;
   return L;
+}
+
+/* Device page of addr in range r, and its location. */
+static orc_loc orc_map(const orc_model *m, int r, uint64_t addr) {
+  return orc_locate(m, m->ranges[r].dev_page_base + (addr - m->ranges[r].base) / m->p.page_bytes);
 }
 
 /* Packed classification word (documented format of hbf_classify_map):
@@ -265,15 +284,30 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
   memcpy(cf, m->chan_free, sizeof(int64_t) * p->channels);
   memcpy(cb, m->chan_busy, p->channels);
 
+  /* refresh claims of this call per die queue (committed with the clocks) */
+  int64_t *claimed = (int64_t *)calloc(m->n_die_keys, sizeof(int64_t));
+  if (!claimed) {
+    free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord);
+    return ORC_ENOMEM;
+  }
+  const int64_t tQ = tR + m->t_prog_ns;
+
   int overflow = 0;
   int64_t n_in = 0;
-  /* 2.+3. classify, map and serve each request at its die, in index order */
+  /* 2.+3. classify, map and serve each request at its die, in index order;
+   * an admission to a die with pending refresh quanta first has the die
+   * serve the oldest of them (Section D4) */
   for (int64_t i = 0; i < n; i++) {
     int r = orc_classify(m, addr[i]);
     if (r < 0) { in[i] = 0; continue; }
     in[i] = 1;
     orc_loc L = orc_map(m, r, addr[i]);
     int64_t start = db[L.key] ? orc_max(issue[i], df[L.key]) : issue[i];
+    if (m->fifo && claimed[L.key] < m->fifo[L.key].len - m->fifo[L.key].head) {
+      claimed[L.key]++;
+      in[i] = 2;  /* in range, claims a quantum */
+      start += tQ;
+    }
     dd[i] = start + tR;
     if (dd[i] >= ORC_TIME_LIMIT) overflow = 1;
     df[L.key] = dd[i];
@@ -308,9 +342,103 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
     memcpy(m->die_busy, db, m->n_die_keys);
     memcpy(m->chan_free, cf, sizeof(int64_t) * p->channels);
     memcpy(m->chan_busy, cb, p->channels);
+    /* each claimed quantum, oldest first per die, completes tR before the
+     * die-done time of the admission that claimed it */
+    for (int64_t i = 0; i < n; i++)
+      if (in[i] == 2) {
+        orc_fifo *f = &m->fifo[orc_map(m, orc_classify(m, addr[i]), addr[i]).key];
+        m->qdone[f->id[f->head++]] = dd[i] - tR;
+      }
   }
+  free(claimed);
   free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord);
   return rc;
+}
+
+/* ---------------------------------------------------------------- refresh
+ * Section D4: refresh read-rewrite pairs enter the same die queues as the
+ * application's reads, under ids of their own, and the running program pays
+ * for them.  Readings (the paper gives no timing for them):
+ *  - one quantum = the read and the rewrite of one device page; it occupies
+ *    that page's die queue for tQ = tR + tPROG and no channel time (the
+ *    page is rewritten inside its die); tPROG is a model parameter;
+ *  - each die queue keeps its pending quanta in submission order; a
+ *    quantum's id is its position in the sequence of all submitted quanta;
+ *  - an application admission to a die queue with pending quanta claims the
+ *    oldest one and the die serves it just before the admission's own read
+ *    (die service tQ + tR; the quantum completes tR before the read does);
+ *  - pending quanta drain while a die is idle only over a window the caller
+ *    names (no application read is issued inside it);
+ *  - a failed timing call claims nothing; reset drops pending quanta. */
+
+int orc_refresh_configure(orc_model *m, int64_t t_prog_ns) {
+  if (!m || t_prog_ns < 0) return ORC_EINVAL;
+  /* the longest die service, tQ + tR, stays within the service bound */
+  if (2 * m->p.t_read_ns + t_prog_ns > ORC_SERVICE_LIMIT) return ORC_EINVAL;
+  m->t_prog_ns = t_prog_ns;
+  return ORC_OK;
+}
+
+/* Queue quanta for device pages pages[0..nq) in plan order; their ids are
+ * *first_id .. *first_id + nq - 1. */
+int orc_refresh_submit(orc_model *m, const uint64_t *pages, int64_t nq, int64_t *first_id) {
+  if (!m || nq < 0 || (nq > 0 && !pages)) return ORC_EINVAL;
+  if (!m->fifo) {
+    m->fifo = (orc_fifo *)calloc(m->n_die_keys, sizeof(orc_fifo));
+    if (!m->fifo) return ORC_ENOMEM;
+  }
+  if (m->nq + nq > m->qcap) {
+    int64_t cap = m->qcap ? m->qcap : 64;
+    while (cap < m->nq + nq) cap *= 2;
+    int64_t *q = (int64_t *)realloc(m->qdone, sizeof(int64_t) * cap);
+    if (!q) return ORC_ENOMEM;
+    m->qdone = q;
+    m->qcap = cap;
+  }
+  if (first_id) *first_id = m->nq;
+  for (int64_t j = 0; j < nq; j++) {
+    orc_fifo *f = &m->fifo[orc_locate(m, pages[j]).key];
+    if (f->len == f->cap) {
+      int64_t cap = f->cap ? 2 * f->cap : 16;
+      int64_t *id = (int64_t *)realloc(f->id, sizeof(int64_t) * cap);
+      if (!id) return ORC_ENOMEM;
+      f->id = id;
+      f->cap = cap;
+    }
+    f->id[f->len++] = m->nq;
+    m->qdone[m->nq++] = ORC_REFRESH_PENDING;
+  }
+  return ORC_OK;
+}
+
+/* Serve pending quanta in idle die time inside [t_from, t_to): each die, in
+ * its queue order, starts the next quantum at max(its clock, t_from) (t_from
+ * if idle since minus infinity) while that quantum ends by t_to. */
+int orc_refresh_drain(orc_model *m, int64_t t_from, int64_t t_to) {
+  if (!m || t_from < 0 || t_to < t_from || t_to >= ORC_ISSUE_LIMIT) return ORC_EINVAL;
+  if (!m->fifo) return ORC_OK;
+  const int64_t tQ = m->p.t_read_ns + m->t_prog_ns;
+  for (uint32_t k = 0; k < m->n_die_keys; k++) {
+    orc_fifo *f = &m->fifo[k];
+    while (f->head < f->len) {
+      int64_t start = m->die_busy[k] ? orc_max(m->die_free[k], t_from) : t_from;
+      if (start + tQ > t_to) break;
+      m->qdone[f->id[f->head++]] = start + tQ;
+      m->die_free[k] = start + tQ;
+      m->die_busy[k] = 1;
+    }
+  }
+  return ORC_OK;
+}
+
+/* Pending quanta per die queue, and completion times of quanta 0..nq-1
+ * (ORC_REFRESH_PENDING while not served). */
+void orc_refresh_pending(const orc_model *m, int64_t *pend) {
+  for (uint32_t k = 0; k < m->n_die_keys; k++) pend[k] = m->fifo ? m->fifo[k].len - m->fifo[k].head : 0;
+}
+int64_t orc_refresh_count(const orc_model *m) { return m->nq; }
+void orc_refresh_done(const orc_model *m, int64_t *done) {
+  if (m->nq) memcpy(done, m->qdone, sizeof(int64_t) * m->nq);
 }
 
 /* Die-stage completion times alone (a diagnostic used by the tests): the

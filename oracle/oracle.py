@@ -75,6 +75,18 @@ def _load():
         lib.orc_n_die_keys.restype = ctypes.c_uint32
         lib.orc_gemv_bf16.argtypes = [vp, i32, i32, i32, vp, i32, vp]
         lib.orc_gemv_bf16.restype = i32
+        lib.orc_refresh_configure.argtypes = [vp, i64]
+        lib.orc_refresh_configure.restype = i32
+        lib.orc_refresh_submit.argtypes = [vp, vp, i64, ctypes.POINTER(i64)]
+        lib.orc_refresh_submit.restype = i32
+        lib.orc_refresh_drain.argtypes = [vp, i64, i64]
+        lib.orc_refresh_drain.restype = i32
+        lib.orc_refresh_pending.argtypes = [vp, vp]
+        lib.orc_refresh_pending.restype = None
+        lib.orc_refresh_count.argtypes = [vp]
+        lib.orc_refresh_count.restype = i64
+        lib.orc_refresh_done.argtypes = [vp, vp]
+        lib.orc_refresh_done.restype = None
         _lib = lib
     return _lib
 
@@ -192,6 +204,79 @@ class OracleModel:
         c = np.ascontiguousarray(chan_free, dtype=np.int64)
         assert d.size == self.n_die_keys and c.size == self.params.channels
         return int(self._lib.orc_set_state(self._h, _ptr(d), _ptr(c)))
+
+    # -- refresh (Section D4; readings in hbf_oracle.c)
+
+    def refresh_configure(self, t_prog_ns):
+        return int(self._lib.orc_refresh_configure(self._h, int(t_prog_ns)))
+
+    def refresh_submit(self, dev_pages):
+        """Queue one quantum per device page, in the given (plan) order.
+        Returns (rc, id of the first quantum)."""
+        pg = np.ascontiguousarray(dev_pages, dtype=np.uint64)
+        first = ctypes.c_int64(0)
+        rc = self._lib.orc_refresh_submit(self._h, _ptr(pg), pg.size, ctypes.byref(first))
+        return int(rc), int(first.value)
+
+    def refresh_drain(self, t_from, t_to):
+        return int(self._lib.orc_refresh_drain(self._h, int(t_from), int(t_to)))
+
+    def refresh_pending(self):
+        out = np.zeros(self.n_die_keys, dtype=np.int64)
+        self._lib.orc_refresh_pending(self._h, _ptr(out))
+        return out
+
+    def refresh_done(self):
+        """Completion time of every quantum submitted so far (REFRESH_PENDING
+        while not served)."""
+        out = np.zeros(int(self._lib.orc_refresh_count(self._h)), dtype=np.int64)
+        self._lib.orc_refresh_done(self._h, _ptr(out))
+        return out
+
+
+REFRESH_PENDING = -1
+
+
+def refresh_plan(params, blocks, pages_per_block):
+    """Device pages of a refresh plan in the scheduler's order (Section D4):
+    eligibility epoch, then channel round robin, then die round robin, then
+    zone, block and page.
+
+    ``blocks``: (epoch, zone, channel, die, plane, block) per eligible block.
+    Block b of plane (channel, die, plane) holds that plane's pages
+    b*pages_per_block .. (b+1)*pages_per_block - 1; plane page pg is device
+    page ((pg*P + plane)*D + die)*C + channel (channel-first striping).
+
+    Reading of the round robin: within an epoch, rounds visit the channels
+    that still have pages in ascending order; each visit takes one page from
+    the channel's next die (cyclically after the die it served last, lowest
+    first) that still has pages.  Within a die, pages follow (zone, block,
+    plane, page)."""
+    C, D, P = params.channels, params.dies_per_channel, params.planes_per_die
+    out = []
+    for epoch in sorted({b[0] for b in blocks}):
+        per_die = {}
+        for (e, zone, ch, die, plane, blk) in blocks:
+            if e != epoch:
+                continue
+            assert 0 <= ch < C and 0 <= die < D and 0 <= plane < P
+            for j in range(pages_per_block):
+                per_die.setdefault((ch, die), []).append((zone, blk, plane, j))
+        for key in per_die:
+            per_die[key].sort()
+        last_die = {}
+        while per_die:
+            for ch in sorted({c for (c, _) in per_die}):
+                dies = sorted(d for (c, d) in per_die if c == ch)
+                prev = last_die.get(ch, -1)
+                die = next((d for d in dies if d > prev), dies[0])
+                zone, blk, plane, j = per_die[(ch, die)].pop(0)
+                if not per_die[(ch, die)]:
+                    del per_die[(ch, die)]
+                last_die[ch] = die
+                pg = blk * pages_per_block + j
+                out.append(((pg * P + plane) * D + die) * C + ch)
+    return out
 
 
 def gemv_bf16(W, X):

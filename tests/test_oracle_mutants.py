@@ -50,6 +50,18 @@ MUTANTS = {
     "state-not-committed": (
         "memcpy(m->chan_free, cf, sizeof(int64_t) * p->channels);",
         "(void)cf;"),
+    "refresh-quantum-free": (
+        "      in[i] = 2;  /* in range, claims a quantum */\n      start += tQ;",
+        "      in[i] = 2;  /* in range, claims a quantum */"),
+    "refresh-done-at-read-end": (
+        "m->qdone[f->id[f->head++]] = dd[i] - tR;",
+        "m->qdone[f->id[f->head++]] = dd[i];"),
+    "refresh-quantum-without-read": (
+        "const int64_t tQ = tR + m->t_prog_ns;\n\n  int overflow",
+        "const int64_t tQ = m->t_prog_ns;\n\n  int overflow"),
+    "refresh-drain-ignores-clock": (
+        "int64_t start = m->die_busy[k] ? orc_max(m->die_free[k], t_from) : t_from;",
+        "int64_t start = t_from;"),
     "extra-service-term": (
         "complete[i] = start + xfer;",
         "complete[i] = start + xfer + (start > dd[i] ? 1 : 0);"),
@@ -68,6 +80,7 @@ def test_pins_catch_mutant(tmp_path, name):
     env = dict(os.environ, HBF_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_events.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_events.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_refresh.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
