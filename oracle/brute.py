@@ -287,3 +287,46 @@ def event_driven_refresh(issue, die_key, chan, t_read, xfer, t_quantum, quanta, 
     left = {d: list(q) for d, q in cal.quanta.items() if q}
     return cal.die_done, cal.complete, cal.quantum_done, left
 
+
+def closed_loop_events(layer_of, die_key, chan, t_read, xfer, t_start, compute, n_layers,
+                       die_free=None, chan_free=None):
+    """Same contract as :func:`closed_loop_stepped` on an event calendar:
+    layer l+1's requests arrive ``compute`` ns after layer l's last
+    completion (after its start if it is empty).  Requests with die_key < 0
+    complete at their issue time."""
+    n = len(layer_of)
+    members = [[] for _ in range(n_layers)]
+    for i in range(n):
+        members[layer_of[i]].append(i)
+    issue = [None] * n
+    done = [None] * n_layers
+    cal = _Calendar(die_key, chan, t_read, xfer, die_free, chan_free)
+    state = {"layer": -1, "left": 0, "last": None}
+
+    def release(t):
+        # layer state["layer"] + 1 starts at t
+        l = state["layer"] + 1
+        if l >= n_layers:
+            return
+        state["layer"], state["last"], state["left"] = l, t, 0
+        for i in members[l]:
+            issue[i] = t
+            if die_key[i] >= 0:
+                state["left"] += 1
+                cal.push(t, _ARRIVE, (i, (t, i)))
+            else:
+                cal.complete[i] = t
+        if state["left"] == 0:
+            done[l] = t
+            cal.push(t + compute, _RELEASE, release)
+
+    def on_complete(t, i):
+        state["left"] -= 1
+        state["last"] = max(state["last"], t)
+        if state["left"] == 0:
+            done[state["layer"]] = state["last"]
+            cal.push(state["last"] + compute, _RELEASE, release)
+
+    cal.push(t_start, _RELEASE, release)
+    cal.run(on_complete)
+    return issue, cal.complete, done

@@ -18,8 +18,8 @@ SRC = os.path.join(ROOT, "oracle", "hbf_oracle.c")
 
 MUTANTS = {
     "die-ignores-busy-die": (
-        "int64_t start = db[L.key] ? orc_max(issue[i], df[L.key]) : issue[i];\n    dd[i] = start + tR;",
-        "int64_t start = issue[i];\n    dd[i] = start + tR;"),
+        "int64_t start = db[L.key] ? orc_max(issue[i], df[L.key]) : issue[i];\n    if (m->fifo",
+        "int64_t start = issue[i];\n    if (m->fifo"),
     "channel-tie-reversed": (
         "if (x->idx != y->idx) return x->idx < y->idx ? -1 : 1;",
         "if (x->idx != y->idx) return x->idx < y->idx ? 1 : -1;"),
@@ -39,8 +39,8 @@ MUTANTS = {
         "addr - m->ranges[r].base < m->ranges[r].bytes) return r;",
         "addr - m->ranges[r].base <= m->ranges[r].bytes) return r;"),
     "dev-page-base-dropped": (
-        "uint64_t dp = m->ranges[r].dev_page_base + (addr - m->ranges[r].base) / p->page_bytes;",
-        "uint64_t dp = (addr - m->ranges[r].base) / p->page_bytes;"),
+        "return orc_locate(m, m->ranges[r].dev_page_base + (addr - m->ranges[r].base) / m->p.page_bytes);",
+        "return orc_locate(m, (addr - m->ranges[r].base) / m->p.page_bytes);"),
     "plane-flag-ignored": (
         "if (p->flags & ORC_FLAG_PLANE_PARALLEL) L.key = L.key * p->planes_per_die + L.plane;",
         "if (p->flags & ORC_FLAG_PLANE_PARALLEL) L.key = L.key * p->planes_per_die;"),
