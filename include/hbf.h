@@ -203,6 +203,75 @@ int hbf_gemv_instrumented(hbf_model_t model, const uint16_t *dev_W, int E, int K
                           const int64_t *dev_page_issue_ns, const int64_t *dev_page_complete_ns,
                           int64_t *dev_measured_delay_ns, void *stream);
 
+/* ---- Refresh traffic in the same queues (Section "D4: Retention, Refresh,
+ * and Wear as Injected Latency": refresh read-rewrite pairs get ids of their
+ * own, enter the same queues as the application's reads, and an admission
+ * claims at most one refresh quantum, served before its own service).
+ * Reading used here (the paper gives no refresh timing):
+ *  - one quantum = the read and the rewrite of one device page; it occupies
+ *    that page's die queue for tQ = t_read_ns + t_prog_ns and no channel
+ *    time (the page is rewritten inside its die);
+ *  - each die queue holds its pending quanta in submission order; every
+ *    in-range admission to a die queue with quanta pending claims the
+ *    oldest one: the die serves it right before the admission's read, so
+ *    that read's die service is tQ + t_read_ns and the quantum completes
+ *    t_read_ns before the read leaves the die;
+ *  - pending quanta drain in idle die time only over a window the caller
+ *    names (hbf_refresh_drain);
+ *  - a call that fails (device-detected error) claims nothing; reset drops
+ *    every pending quantum.
+ * With quanta pending, hbf_time_requests / hbf_time_layers run one extra
+ * counting pass over the addresses. */
+
+/* One eligible erase block of a refresh plan. */
+typedef struct {
+  uint32_t epoch;    /* eligibility epoch */
+  uint32_t zone;
+  uint32_t channel, die, plane;
+  uint32_t block;    /* block index within its plane */
+} hbf_refresh_block;
+
+/* Device pages of a refresh plan in the scheduler's deterministic order
+ * (Section D4: eligibility epoch, then channel round robin, then die round
+ * robin, then zone, block and page).  Host-only, no model needed.
+ * Block b of plane (channel, die, plane) holds that plane's pages
+ * b*pages_per_block .. (b+1)*pages_per_block - 1; plane page pg is device
+ * page ((pg*P + plane)*D + die)*C + channel.  Within an epoch, rounds visit
+ * the channels that still have pages in ascending order, and each visit
+ * takes one page from the channel's next die (cyclically after the die it
+ * served last, lowest first) that still has pages; a die's pages go in
+ * (zone, block, plane, page) order.  host_pages_out receives
+ * n_blocks * pages_per_block entries (capacity `cap`, else HBF_EINVAL).
+ * Block fields out of the geometry: HBF_EINVAL. */
+int hbf_refresh_plan(const hbf_params *params, const hbf_refresh_block *host_blocks, int64_t n_blocks,
+                     uint32_t pages_per_block, uint64_t *host_pages_out, int64_t cap);
+
+/* Set tPROG, the page program time of a refresh rewrite (>= 0, with
+ * 2 * t_read_ns + t_prog_ns <= 2^29).  Required before hbf_refresh_submit;
+ * applies to quanta served from the next call on. */
+int hbf_refresh_configure(hbf_model_t model, int64_t t_prog_ns);
+
+/* Queue one quantum per device page host_pages[0..nq), in that (plan)
+ * order.  dev_done_ns: int64[nq] device array that receives quantum j's
+ * completion time when it is served (claimed by an admission or drained);
+ * the library fills it with -1 (pending) now.  The caller keeps it alive
+ * while any of its quanta is pending (until reset, or until
+ * hbf_refresh_pending reports none).  Synchronises `stream` (the host
+ * rebuilds the pending lists).  0 <= nq <= 2^31. */
+int hbf_refresh_submit(hbf_model_t model, const uint64_t *host_pages, int64_t nq, int64_t *dev_done_ns,
+                       void *stream);
+
+/* Serve pending quanta in idle die time inside [t_from_ns, t_to_ns): each
+ * die queue, oldest quantum first, starts the next one at max(its clock,
+ * t_from_ns) while it ends by t_to_ns, and its clock advances.  The caller
+ * promises no admission is issued inside the window.
+ * 0 <= t_from_ns <= t_to_ns < 2^61.  Asynchronous on `stream`. */
+int hbf_refresh_drain(hbf_model_t model, int64_t t_from_ns, int64_t t_to_ns, void *stream);
+
+/* Pending quanta per die queue (host_pending[n_die_queues]), after
+ * synchronising `stream`. */
+int hbf_refresh_pending(hbf_model_t model, uint32_t *host_pending, void *stream);
+
 /* Wall-clock tick of the delay injection, in picoseconds (10,000 for a
  * 100 MHz counter).  Needs the GPU. */
 int hbf_wall_clock_tick_ps(hbf_model_t model, int64_t *tick_ps);

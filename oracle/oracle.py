@@ -251,17 +251,18 @@ def refresh_plan(params, blocks, pages_per_block):
     that still have pages in ascending order; each visit takes one page from
     the channel's next die (cyclically after the die it served last, lowest
     first) that still has pages.  Within a die, pages follow (zone, block,
-    plane, page)."""
+    plane, page); a block listed twice is refreshed twice, entries in list
+    order."""
     C, D, P = params.channels, params.dies_per_channel, params.planes_per_die
     out = []
     for epoch in sorted({b[0] for b in blocks}):
         per_die = {}
-        for (e, zone, ch, die, plane, blk) in blocks:
+        for bi, (e, zone, ch, die, plane, blk) in enumerate(blocks):
             if e != epoch:
                 continue
             assert 0 <= ch < C and 0 <= die < D and 0 <= plane < P
             for j in range(pages_per_block):
-                per_die.setdefault((ch, die), []).append((zone, blk, plane, j))
+                per_die.setdefault((ch, die), []).append((zone, blk, plane, bi, j))
         for key in per_die:
             per_die[key].sort()
         last_die = {}
@@ -270,7 +271,7 @@ def refresh_plan(params, blocks, pages_per_block):
                 dies = sorted(d for (c, d) in per_die if c == ch)
                 prev = last_die.get(ch, -1)
                 die = next((d for d in dies if d > prev), dies[0])
-                zone, blk, plane, j = per_die[(ch, die)].pop(0)
+                zone, blk, plane, _, j = per_die[(ch, die)].pop(0)
                 if not per_die[(ch, die)]:
                     del per_die[(ch, die)]
                 last_die[ch] = die

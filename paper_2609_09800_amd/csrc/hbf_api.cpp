@@ -78,6 +78,14 @@ struct hbf_model {
   int prof_calls = 0;                  // calls recorded since hbf_profile(.., 1)
   int ncu = 0;
   int64_t tick_ps = 0;
+  // refresh: tPROG (-1 = not configured); per die queue, the completion
+  // cells of the quanta uploaded last (the device consumes a prefix of each
+  // list); whether quanta may still be pending on the device
+  int64_t t_prog = -1;
+  std::vector<std::vector<int64_t *>> ref_q;
+  bool ref_maybe = false;
+  int64_t **ref_slot = nullptr;
+  size_t ref_slot_cap = 0;
 };
 
 static bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
@@ -180,6 +188,7 @@ void hbf_model_destroy(hbf_model_t m) {
     hipFree(m->st);
   }
   if (m->ws && m->lib_ws) hipFree(m->ws);
+  if (m->ref_slot) hipFree(m->ref_slot);
   for (auto &set : m->ev)
     for (auto &e : set)
       if (e) hipEventDestroy(e);
@@ -202,6 +211,8 @@ int hbf_model_reset(hbf_model_t m, void *stream) {
   if (!m) return HBF_EINVAL;
   int rc = ensure_device(m);
   if (rc) return rc;
+  for (auto &q : m->ref_q) q.clear();
+  m->ref_maybe = false;
   return launch_reset(m->st, (hipStream_t)stream) == hipSuccess ? HBF_OK : HBF_EHIP;
 }
 
@@ -285,7 +296,7 @@ static int time_call(hbf_model_t m, const RangeTable &rt, const uint64_t *addr, 
     ev = set;
   }
   hipError_t e = launch_time_requests(m->g, rt, L, (char *)m->ws, m->st, addr, issue, complete,
-                                      (hipStream_t)stream, ev, kNumTimedKernels + 1);
+                                      (hipStream_t)stream, ev, kNumTimedKernels + 1, m->ref_maybe);
   if (e != hipSuccess) return HBF_EHIP;
   if (m->prof) m->prof_calls++;
   return HBF_OK;
@@ -330,6 +341,157 @@ int hbf_time_layers(hbf_model_t m, const uint64_t *addr, int64_t n, const int64_
                                  : nullptr;
     if (launch_layer_done(ctl, cnt, prev, t_start, compute_ns, done + l, s) != hipSuccess) return HBF_EHIP;
   }
+  return HBF_OK;
+}
+
+// ---- refresh (Section D4)
+
+// Die queue of device page p (channel-first striping).
+static uint32_t key_of_page(const Geo &g, uint64_t p) {
+  const uint32_t ch = (uint32_t)(p % g.C), die = (uint32_t)((p / g.C) % g.D);
+  const uint32_t plane = (uint32_t)((p / ((uint64_t)g.C * g.D)) % g.P);
+  const uint32_t k = ch * g.D + die;
+  return g.plane_parallel ? k * g.P + plane : k;
+}
+
+int hbf_refresh_plan(const hbf_params *params, const hbf_refresh_block *blocks, int64_t n_blocks,
+                     uint32_t ppb, uint64_t *out, int64_t cap) {
+  if (!params || n_blocks < 0 || (n_blocks > 0 && (!blocks || !out)) || ppb < 1) return HBF_EINVAL;
+  const uint64_t C = params->channels, D = params->dies_per_channel, P = params->planes_per_die;
+  if (C < 1 || D < 1 || P < 1) return HBF_EINVAL;
+  if ((unsigned __int128)n_blocks * ppb > (unsigned __int128)cap) return HBF_EINVAL;
+  for (int64_t b = 0; b < n_blocks; b++)
+    if (blocks[b].channel >= C || blocks[b].die >= D || blocks[b].plane >= P) return HBF_EINVAL;
+  // per epoch: each die's pages in (zone, block, plane, page) order
+  std::vector<int64_t> idx(n_blocks);
+  for (int64_t b = 0; b < n_blocks; b++) idx[b] = b;
+  std::sort(idx.begin(), idx.end(), [&](int64_t x, int64_t y) {
+    const hbf_refresh_block &a = blocks[x], &c = blocks[y];
+    if (a.epoch != c.epoch) return a.epoch < c.epoch;
+    if (a.zone != c.zone) return a.zone < c.zone;
+    if (a.block != c.block) return a.block < c.block;
+    if (a.plane != c.plane) return a.plane < c.plane;
+    return x < y;
+  });
+  int64_t w = 0;
+  for (int64_t e0 = 0; e0 < n_blocks;) {
+    int64_t e1 = e0;
+    while (e1 < n_blocks && blocks[idx[e1]].epoch == blocks[idx[e0]].epoch) e1++;
+    // die (c, d) -> its blocks of this epoch in order; cursor in pages
+    std::vector<std::vector<int64_t>> die_blocks(C * D);
+    for (int64_t i = e0; i < e1; i++) {
+      const hbf_refresh_block &b = blocks[idx[i]];
+      die_blocks[(uint64_t)b.channel * D + b.die].push_back(idx[i]);
+    }
+    std::vector<uint64_t> cur(C * D, 0), left(C * D, 0);
+    std::vector<uint64_t> chan_left(C, 0);
+    for (uint64_t cd = 0; cd < C * D; cd++) {
+      left[cd] = (uint64_t)die_blocks[cd].size() * ppb;
+      chan_left[cd / D] += left[cd];
+    }
+    std::vector<int64_t> last(C, -1);
+    uint64_t total = (uint64_t)(e1 - e0) * ppb;
+    while (total) {
+      for (uint64_t c = 0; c < C; c++) {
+        if (!chan_left[c]) continue;
+        // next die after the last served one, cyclically, with pages left
+        uint64_t d = (uint64_t)(last[c] + 1) % D;
+        while (!left[c * D + d]) d = (d + 1) % D;
+        const uint64_t cd = c * D + d;
+        const hbf_refresh_block &b = blocks[die_blocks[cd][cur[cd] / ppb]];
+        const uint64_t pg = (uint64_t)b.block * ppb + cur[cd] % ppb;
+        out[w++] = ((pg * P + b.plane) * D + d) * C + c;
+        cur[cd]++;
+        left[cd]--;
+        chan_left[c]--;
+        total--;
+        last[c] = (int64_t)d;
+      }
+    }
+    e0 = e1;
+  }
+  return HBF_OK;
+}
+
+int hbf_refresh_configure(hbf_model_t m, int64_t t_prog_ns) {
+  if (!m || t_prog_ns < 0 || 2 * m->g.tR + t_prog_ns > SERVICE_LIMIT) return HBF_EINVAL;
+  m->t_prog = t_prog_ns;
+  m->g.tQ = m->g.tR + t_prog_ns;
+  return HBF_OK;
+}
+
+int hbf_refresh_submit(hbf_model_t m, const uint64_t *pages, int64_t nq, int64_t *done, void *stream) {
+  if (!m || m->t_prog < 0 || nq < 0 || nq > N_LIMIT || (nq > 0 && (!pages || !done))) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  const uint32_t K = m->g.K;
+  const hipStream_t s = (hipStream_t)stream;
+  if (m->ref_q.size() != K) m->ref_q.assign(K, {});
+  // what the device consumed of the lists uploaded last
+  std::vector<uint32_t> head(K), pend(K);
+  if (hipStreamSynchronize(s) != hipSuccess ||
+      hipMemcpy(head.data(), m->st->ref_head, K * 4, hipMemcpyDeviceToHost) != hipSuccess ||
+      hipMemcpy(pend.data(), m->st->ref_pend, K * 4, hipMemcpyDeviceToHost) != hipSuccess)
+    return HBF_EHIP;
+  uint64_t total = nq;
+  for (uint32_t k = 0; k < K; k++) {
+    std::vector<int64_t *> &q = m->ref_q[k];
+    if ((uint64_t)head[k] + pend[k] > q.size()) return HBF_EHIP;  // device state out of step
+    q.erase(q.begin(), q.begin() + head[k]);
+    q.resize(pend[k]);
+    total += q.size();
+  }
+  if (total > (uint64_t)UINT32_MAX) return HBF_EINVAL;
+  for (int64_t j = 0; j < nq; j++) m->ref_q[key_of_page(m->g, pages[j])].push_back(done + j);
+  // flatten: die queue k's pending cells at [off[k], off[k] + pend[k])
+  std::vector<int64_t *> flat;
+  flat.reserve(total);
+  std::vector<uint32_t> off(K);
+  for (uint32_t k = 0; k < K; k++) {
+    off[k] = (uint32_t)flat.size();
+    pend[k] = (uint32_t)m->ref_q[k].size();
+    head[k] = 0;
+    flat.insert(flat.end(), m->ref_q[k].begin(), m->ref_q[k].end());
+  }
+  if (flat.size() > m->ref_slot_cap) {
+    if (m->ref_slot) hipFree(m->ref_slot);
+    m->ref_slot = nullptr;
+    m->ref_slot_cap = 0;
+    void *p = nullptr;
+    if (hipMalloc(&p, flat.size() * sizeof(int64_t *)) != hipSuccess) return HBF_ENOMEM;
+    m->ref_slot = (int64_t **)p;
+    m->ref_slot_cap = flat.size();
+  }
+  if ((!flat.empty() &&
+       hipMemcpy(m->ref_slot, flat.data(), flat.size() * sizeof(int64_t *), hipMemcpyHostToDevice) != hipSuccess) ||
+      hipMemcpy(&m->st->ref_slot, &m->ref_slot, sizeof(int64_t **), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(m->st->ref_off, off.data(), K * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(m->st->ref_head, head.data(), K * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(m->st->ref_pend, pend.data(), K * 4, hipMemcpyHostToDevice) != hipSuccess)
+    return HBF_EHIP;
+  if (launch_fill(done, nq, REFRESH_PENDING, s) != hipSuccess) return HBF_EHIP;
+  m->ref_maybe = !flat.empty();
+  return HBF_OK;
+}
+
+int hbf_refresh_drain(hbf_model_t m, int64_t t_from, int64_t t_to, void *stream) {
+  if (!m || t_from < 0 || t_to < t_from || t_to >= ISSUE_LIMIT) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  if (!m->ref_maybe) return HBF_OK;
+  return launch_refresh_drain(m->g, m->st, t_from, t_to, (hipStream_t)stream) == hipSuccess ? HBF_OK : HBF_EHIP;
+}
+
+int hbf_refresh_pending(hbf_model_t m, uint32_t *host_pending, void *stream) {
+  if (!m || !host_pending) return HBF_EINVAL;
+  int rc = ensure_device(m);
+  if (rc) return rc;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess ||
+      hipMemcpy(host_pending, m->st->ref_pend, m->g.K * 4, hipMemcpyDeviceToHost) != hipSuccess)
+    return HBF_EHIP;
+  bool any = false;
+  for (uint32_t k = 0; k < m->g.K; k++) any |= host_pending[k] != 0;
+  m->ref_maybe = any;
   return HBF_OK;
 }
 

@@ -67,15 +67,26 @@ struct Geo {
   uint32_t lg_page, lg_C, lg_D, lg_P;
   uint32_t lg_tR;     // floor(log2(tR)): bucket width of the channel merge
   int64_t tR, xfer;
+  int64_t tQ;         // die time of one refresh quantum (tR + tPROG), 0 if unset
 };
 
-// Persistent device state of a model.
+// Persistent device state of a model.  Refresh quanta pending at die queue
+// k are entries ref_off[k] + ref_head[k] .. + ref_pend[k] - 1 of ref_slot,
+// oldest first; each entry points at the caller's cell that receives the
+// quantum's completion time.
 struct DevState {
   int64_t die_free[MAX_KEYS];     // NEG = idle
   int64_t chan_free[MAX_CHANNELS];
   uint32_t sticky;                // sticky error bits
   uint32_t pad;
+  uint32_t ref_pend[MAX_KEYS];
+  uint32_t ref_head[MAX_KEYS];
+  uint32_t ref_off[MAX_KEYS];
+  int64_t **ref_slot;
 };
+
+// Completion cell of a refresh quantum that has not been served.
+constexpr int64_t REFRESH_PENDING = -1;
 
 // Per-call control block (in the workspace).
 struct CallCtl {
@@ -106,9 +117,14 @@ Layout make_layout(const Geo &g, int64_t n);
 
 // Launchers (hbf_kernels.hip).  All enqueue on `s` and return the first
 // launch error.
+// refresh: quanta may be pending (the die stage then charges them to the
+// admissions that claim them; a count pass comes first)
 hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout &L, char *ws,
                                 DevState *st, const uint64_t *addr, const int64_t *issue,
-                                int64_t *complete, hipStream_t s, hipEvent_t *ev, int n_ev);
+                                int64_t *complete, hipStream_t s, hipEvent_t *ev, int n_ev,
+                                bool refresh);
+hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s);
+hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
 hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, const uint64_t *addr,
                            int64_t n, uint64_t *map, hipStream_t s);
 hipError_t launch_reset(DevState *st, hipStream_t s);

@@ -153,6 +153,66 @@ DEVI SegMax block_excl_segmax(SegMax v, SegMax *sh /*[NW]*/) {
   return seg_comb(pre, ex);
 }
 
+// ------------------------------------------------------------------ wave-level helpers
+
+DEVI void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+// DPP cross-lane moves (gfx9 row_shr / row_bcast): lanes without a source, or
+// in rows outside ROWMASK, keep `old`.
+template <int CTRL, int ROWMASK>
+DEVI uint32_t dpp32(uint32_t old, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROWMASK, 0xF, false);
+}
+template <int CTRL, int ROWMASK>
+DEVI int64_t dpp64(int64_t old, int64_t x) {
+  const uint32_t lo = dpp32<CTRL, ROWMASK>((uint32_t)old, (uint32_t)x);
+  const uint32_t hi = dpp32<CTRL, ROWMASK>((uint32_t)((uint64_t)old >> 32), (uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114, DPP_ROW_SHR8 = 0x118;
+constexpr int DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
+// Inclusive scans over the 64 lanes: within rows of 16 by shifts of 1, 2,
+// 4, 8, then row 0 -> 1 and 2 -> 3 (bcast15), then rows 0-1 -> 2-3 (bcast31).
+DEVI uint32_t wave_incl_sum(uint32_t x) {
+  x += dpp32<DPP_ROW_SHR1, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_SHR2, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_SHR4, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_SHR8, 0xF>(0u, x);
+  x += dpp32<DPP_ROW_BCAST15, 0xA>(0u, x);
+  x += dpp32<DPP_ROW_BCAST31, 0xC>(0u, x);
+  return x;
+}
+DEVI uint32_t wave_incl_umax(uint32_t x) {
+  x = max(x, dpp32<DPP_ROW_SHR1, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_SHR2, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_SHR4, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_SHR8, 0xF>(0u, x));
+  x = max(x, dpp32<DPP_ROW_BCAST15, 0xA>(0u, x));
+  x = max(x, dpp32<DPP_ROW_BCAST31, 0xC>(0u, x));
+  return x;
+}
+DEVI int64_t wave_incl_max(int64_t x) {
+  x = imax(x, dpp64<DPP_ROW_SHR1, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR2, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR4, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR8, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_BCAST15, 0xA>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_BCAST31, 0xC>(NEG, x));
+  return x;
+}
+DEVI uint32_t lane63(uint32_t x) { return (uint32_t)__builtin_amdgcn_readlane((int)x, 63); }
+DEVI int64_t lane63(int64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), 63);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+DEVI uint32_t wave_sum(uint32_t x) { return lane63(wave_incl_sum(x)); }
+DEVI uint32_t wave_excl_sum(uint32_t v) { return wave_incl_sum(v) - v; }
+DEVI int64_t wave_max(int64_t x) { return lane63(wave_incl_max(x)); }
+DEVI uint32_t wave_umax(uint32_t x) { return lane63(wave_incl_umax(x)); }
+
 // ------------------------------------------------------------------ classification
 
 // Copy the range table into LDS (dynamic indexing then stays in LDS).
@@ -292,8 +352,19 @@ __global__ void k_prologue(CallCtl *ctl) {
 // ------------------------------------------------------------------ k_die_reduce
 
 
+// Die time of the first g admissions of a die queue in one call when the
+// first R of them each also carry a refresh quantum (Section D4): the sum of
+// their services, g*tR + min(g, R)*tQ.  With R = 0 it is the plain g*tR.
+DEVI int64_t svc_sum(uint32_t g, uint32_t R, int64_t tR, int64_t tQ) {
+  return (int64_t)g * tR + (int64_t)min(g, R) * tQ;
+}
+
+// With refresh quanta pending (REF) the service of a die queue's request
+// depends on its rank in the call, so the tile aggregate is kept in global
+// form, max over the tile of issue - svc_sum(global rank), with the global
+// ranks of the tile's first requests taken from a count pass (tin_base).
 // LDS: ranges | wcnt[DWAVES][K] u16 | tot[K] u16 | cnt[K] u32 | amax[K] i64
-template <bool POW2>
+template <bool POW2, bool REF>
 __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict__ addr,
                                                     const int64_t *__restrict__ issue, int64_t n,
                                                     int64_t *__restrict__ complete, Geo g,
@@ -301,7 +372,8 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
                                                     uint32_t *__restrict__ agg_cnt,
                                                     int64_t *__restrict__ agg_A,
                                                     uint32_t *__restrict__ KR, CallCtl *ctl,
-                                                    uint32_t kbits) {
+                                                    uint32_t kbits, const uint32_t *__restrict__ tin_base,
+                                                    const DevState *st) {
   extern __shared__ __align__(16) unsigned char smem[];
   LdsRanges *lr = (LdsRanges *)smem;
   const uint32_t K = g.K;
@@ -313,7 +385,8 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
 
   load_ranges(lr, rt);
   for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
-    cnt[k] = 0;
+    // REF: cnt holds the call-wide rank of the tile's next request of k
+    cnt[k] = REF ? tin_base[(size_t)blockIdx.x * K + k] : 0;
     amax[k] = NEG;
     cmax[k] = NEG;
   }
@@ -386,7 +459,11 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
       const int64_t i = wbase + e * 64 + lane;
       if (k != KEY_NONE) {
         const uint32_t rc = mycnt[k] + rank[e];  // rank among key k in the chunk
-        atomicMax((long long *)&cmax[k], (long long)(iss[e] - (int64_t)mul32(rc, (uint32_t)tR)));
+        if (REF)
+          atomicMax((long long *)&amax[k],
+                    (long long)(iss[e] - svc_sum(cnt[k] + rc, st->ref_pend[k], tR, g.tQ)));
+        else
+          atomicMax((long long *)&cmax[k], (long long)(iss[e] - (int64_t)mul32(rc, (uint32_t)tR)));
         KR[i] = (k << 16) | rc;
       } else if (i < t1) {
         KR[i] = (uint32_t)KEY_NONE << 16;
@@ -397,21 +474,105 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
     for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
       const uint32_t t = tot[k];
       if (t) {
-        amax[k] = imax(amax[k], cmax[k] - (int64_t)mul32(cnt[k], (uint32_t)tR));
-        cmax[k] = NEG;
+        if (!REF) {
+          amax[k] = imax(amax[k], cmax[k] - (int64_t)mul32(cnt[k], (uint32_t)tR));
+          cmax[k] = NEG;
+        }
         cnt[k] += t;
       }
     }
     __syncthreads();
   }
-  // tile aggregate per die queue: departure of the last request from an idle die
   const size_t row = (size_t)blockIdx.x * K;
   for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
-    const uint32_t c = cnt[k];
-    agg_cnt[row + k] = c;
-    agg_A[row + k] = c ? (int64_t)c * tR + amax[k] : NEG;
+    if (REF) {  // global form; the counts came from the count pass
+      agg_A[row + k] = amax[k];
+    } else {    // departure of the tile's last request of k from an idle die
+      const uint32_t c = cnt[k];
+      agg_cnt[row + k] = c;
+      agg_A[row + k] = c ? (int64_t)c * tR + amax[k] : NEG;
+    }
   }
   if (errb) atomicOr(&ctl->err, errb);
+}
+
+// Count pass of the refresh path: per tile, the in-range requests of each
+// die queue (no ranks, no times).
+template <bool POW2>
+__global__ __launch_bounds__(DBLK) void k_die_count(const uint64_t *__restrict__ addr, int64_t n, Geo g,
+                                                   RangeTable rt, int64_t tile_elems,
+                                                   uint32_t *__restrict__ agg_cnt) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  LdsRanges *lr = (LdsRanges *)smem;
+  uint32_t *cnt = (uint32_t *)(smem + ((sizeof(LdsRanges) + 15) & ~size_t(15)));
+  const uint32_t K = g.K;
+  load_ranges(lr, rt);
+  for (uint32_t k = threadIdx.x; k < K; k += DBLK) cnt[k] = 0;
+  __syncthreads();
+  const int64_t t0 = (int64_t)blockIdx.x * tile_elems;
+  const int64_t t1 = imin(n, t0 + tile_elems);
+  for (int64_t i = t0 + threadIdx.x; i < t1; i += DBLK) {
+    const uint32_t k = key_of<POW2>(g, lr, addr[i]);
+    if (k != KEY_NONE) atomicAdd(&cnt[k], 1u);
+  }
+  __syncthreads();
+  for (uint32_t k = threadIdx.x; k < K; k += DBLK) agg_cnt[(size_t)blockIdx.x * K + k] = cnt[k];
+}
+
+// Refresh path: per die queue, the call-wide rank of each tile's first
+// request (exclusive prefix over tiles) and the queue's total.  One wave
+// per die queue, lane = contiguous group of tiles.
+__global__ __launch_bounds__(BLK) void k_tile_count(const uint32_t *__restrict__ agg_cnt, uint32_t nt, uint32_t K,
+                                                    uint32_t *__restrict__ tin_base,
+                                                    uint32_t *__restrict__ totals) {
+  const uint32_t lane = lane_id();
+  const uint32_t k = blockIdx.x * WAVES + (threadIdx.x >> 6);
+  if (k >= K) return;  // whole wave
+  const uint32_t per = (nt + 63) / 64;
+  const uint32_t ta = min(nt, lane * per), tb = min(nt, ta + per);
+  uint32_t C = 0;
+  for (uint32_t t = ta; t < tb; t++) C += agg_cnt[(size_t)t * K + k];
+  uint32_t base = wave_excl_sum(C);
+  if (lane == 63) totals[k] = base + C;
+  for (uint32_t t = ta; t < tb; t++) {
+    tin_base[(size_t)t * K + k] = base;
+    base += agg_cnt[(size_t)t * K + k];
+  }
+}
+
+// Refresh path: per die queue, the clock entering each tile from the
+// global-form tile maxima M_t:  L = svc_sum(base) + max(f0, max of M before).
+__global__ __launch_bounds__(BLK) void k_tile_scan_ref(const int64_t *__restrict__ agg_A, uint32_t nt, Geo g,
+                                                       const DevState *st, const uint32_t *__restrict__ tin_base,
+                                                       const uint32_t *__restrict__ totals,
+                                                       int64_t *__restrict__ tin_L,
+                                                       int64_t *__restrict__ dfnew, CallCtl *ctl) {
+  if (agent_load32(&ctl->err)) return;
+  const uint32_t lane = lane_id(), K = g.K;
+  const uint32_t k = blockIdx.x * WAVES + (threadIdx.x >> 6);
+  if (k >= K) return;  // whole wave
+  const uint32_t per = (nt + 63) / 64;
+  const uint32_t ta = min(nt, lane * per), tb = min(nt, ta + per);
+  int64_t M = NEG;
+  for (uint32_t t = ta; t < tb; t++) M = imax(M, agg_A[(size_t)t * K + k]);
+  const int64_t inc = wave_incl_max(M);
+  int64_t run = __shfl_up(inc, 1);
+  if (lane == 0) run = NEG;
+  const int64_t f0 = st->die_free[k];
+  const uint32_t R = st->ref_pend[k];
+  if (lane == 63) {
+    const uint32_t tot = totals[k];
+    if (tot) {
+      const int64_t Lend = svc_sum(tot, R, g.tR, g.tQ) + imax(f0, inc);
+      dfnew[k] = Lend;
+      atomicMax((long long *)&ctl->max_dd, (long long)Lend);
+      if (Lend >= TIME_LIMIT) atomicOr(&ctl->err, ERR_OVERFLOW);
+    }
+  }
+  for (uint32_t t = ta; t < tb; t++) {
+    tin_L[(size_t)t * K + k] = svc_sum(tin_base[(size_t)t * K + k], R, g.tR, g.tQ) + imax(f0, run);
+    run = imax(run, agg_A[(size_t)t * K + k]);
+  }
 }
 
 // Per die queue, compose the tiles in order.  One wave per die queue, lane g
@@ -548,12 +709,17 @@ struct KeyW {
   uint32_t rbase, pbase, lbo, tot;
 };
 
+// REF (refresh quanta pending): the services depend on the call-wide rank,
+// so the staged terms are issue - svc_sum(rank) and die_done =
+// svc_sum(rank + 1) + prefix max; each admission that claims a quantum
+// writes the quantum's completion (tR before its own read ends).
+template <bool REF>
 __global__ __launch_bounds__(DBLK) void k_die_scatter(
     const int64_t *__restrict__ issue, const uint32_t *__restrict__ KR, int64_t n, Geo g,
     int64_t tile_elems, const int64_t *__restrict__ tin_L, const uint32_t *__restrict__ tin_base,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals,
     int64_t *__restrict__ DD, uint32_t *__restrict__ IX, uint32_t *__restrict__ LB, uint32_t gmax,
-    CallCtl *ctl) {
+    CallCtl *ctl, const DevState *st) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ SegMax shseg[DWAVES];
   __shared__ uint32_t shsum[DWAVES];
@@ -639,8 +805,15 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
         const KeyA ka = KA[k];
         const uint32_t rc = kr[e] & 0xFFFFu;
         const uint32_t P = pad16(ka.koff + rc);
-        int64_t v = iss[e] - (int64_t)mul32(ka.cnt + rc, tR);
-        if (rc == 0) v = imax(v, ka.L - (int64_t)mul32(ka.cnt, tR));
+        int64_t v;
+        if (REF) {
+          const uint32_t R = st->ref_pend[k], g0 = KW[k].rbase;
+          v = iss[e] - svc_sum(g0 + rc, R, g.tR, g.tQ);
+          if (rc == 0) v = imax(v, ka.L - svc_sum(g0, R, g.tR, g.tQ));
+        } else {
+          v = iss[e] - (int64_t)mul32(ka.cnt + rc, tR);
+          if (rc == 0) v = imax(v, ka.L - (int64_t)mul32(ka.cnt, tR));
+        }
         sval[P] = v;
         skey[P] = (uint16_t)k;
         srank[P] = (uint16_t)rc;
@@ -658,6 +831,15 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
         if (!t) continue;
         const KeyA ka = KA[k];
         int64_t run = NEG;
+        if (REF) {
+          const uint32_t R = st->ref_pend[k], g0 = KW[k].rbase;
+          for (uint32_t q = 0; q < t; q++) {
+            const uint32_t P = pad16(ka.koff + q);
+            run = imax(run, sval[P]);
+            sval[P] = svc_sum(g0 + q + 1, R, g.tR, g.tQ) + run;
+          }
+          continue;
+        }
         for (uint32_t q = 0; q < t; q++) {
           const uint32_t P = pad16(ka.koff + q);
           run = imax(run, sval[P]);
@@ -686,8 +868,11 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
         if (p < nv) {
           const uint32_t rc = srank[pad16(p)];
           run = (rc == 0) ? vals[q] : imax(run, vals[q]);
-          const uint32_t r0 = KA[skey[pad16(p)]].cnt + rc;
-          sval[pad16(p)] = (int64_t)mul32(r0 + 1, tR) + run;
+          const uint32_t kk = skey[pad16(p)];
+          if (REF)
+            sval[pad16(p)] = svc_sum(KW[kk].rbase + rc + 1, st->ref_pend[kk], g.tR, g.tQ) + run;
+          else
+            sval[pad16(p)] = (int64_t)mul32(KA[kk].cnt + rc + 1, tR) + run;
         }
       }
     }
@@ -710,6 +895,8 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
           IX[gpos] = ix;
         }
       }
+      if (REF && r < st->ref_pend[k])  // this admission claimed quantum r of k's pending ones
+        *st->ref_slot[st->ref_off[k] + st->ref_head[k] + r] = dd - g.tR;
       const int64_t prev = (rc > 0) ? sval[pad16(p - 1)] : KA[k].L;
       const int64_t cell = imin((dd - cbase) >> shift, (int64_t)G);
       const int64_t pcell = (r == 0) ? -1 : imin((prev - cbase) >> shift, (int64_t)G);
@@ -750,64 +937,6 @@ DEVI int run_of(const uint32_t *rb, int R, uint32_t p) {
   return lo;
 }
 
-// ---- wave-level helpers (the channel stage runs one wave per block)
-DEVI void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-}
-// DPP cross-lane moves (gfx9 row_shr / row_bcast): lanes without a source, or
-// in rows outside ROWMASK, keep `old`.
-template <int CTRL, int ROWMASK>
-DEVI uint32_t dpp32(uint32_t old, uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROWMASK, 0xF, false);
-}
-template <int CTRL, int ROWMASK>
-DEVI int64_t dpp64(int64_t old, int64_t x) {
-  const uint32_t lo = dpp32<CTRL, ROWMASK>((uint32_t)old, (uint32_t)x);
-  const uint32_t hi = dpp32<CTRL, ROWMASK>((uint32_t)((uint64_t)old >> 32), (uint32_t)((uint64_t)x >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114, DPP_ROW_SHR8 = 0x118;
-constexpr int DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
-// Inclusive scans over the 64 lanes: within rows of 16 by shifts of 1, 2,
-// 4, 8, then row 0 -> 1 and 2 -> 3 (bcast15), then rows 0-1 -> 2-3 (bcast31).
-DEVI uint32_t wave_incl_sum(uint32_t x) {
-  x += dpp32<DPP_ROW_SHR1, 0xF>(0u, x);
-  x += dpp32<DPP_ROW_SHR2, 0xF>(0u, x);
-  x += dpp32<DPP_ROW_SHR4, 0xF>(0u, x);
-  x += dpp32<DPP_ROW_SHR8, 0xF>(0u, x);
-  x += dpp32<DPP_ROW_BCAST15, 0xA>(0u, x);
-  x += dpp32<DPP_ROW_BCAST31, 0xC>(0u, x);
-  return x;
-}
-DEVI uint32_t wave_incl_umax(uint32_t x) {
-  x = max(x, dpp32<DPP_ROW_SHR1, 0xF>(0u, x));
-  x = max(x, dpp32<DPP_ROW_SHR2, 0xF>(0u, x));
-  x = max(x, dpp32<DPP_ROW_SHR4, 0xF>(0u, x));
-  x = max(x, dpp32<DPP_ROW_SHR8, 0xF>(0u, x));
-  x = max(x, dpp32<DPP_ROW_BCAST15, 0xA>(0u, x));
-  x = max(x, dpp32<DPP_ROW_BCAST31, 0xC>(0u, x));
-  return x;
-}
-DEVI int64_t wave_incl_max(int64_t x) {
-  x = imax(x, dpp64<DPP_ROW_SHR1, 0xF>(NEG, x));
-  x = imax(x, dpp64<DPP_ROW_SHR2, 0xF>(NEG, x));
-  x = imax(x, dpp64<DPP_ROW_SHR4, 0xF>(NEG, x));
-  x = imax(x, dpp64<DPP_ROW_SHR8, 0xF>(NEG, x));
-  x = imax(x, dpp64<DPP_ROW_BCAST15, 0xA>(NEG, x));
-  x = imax(x, dpp64<DPP_ROW_BCAST31, 0xC>(NEG, x));
-  return x;
-}
-DEVI uint32_t lane63(uint32_t x) { return (uint32_t)__builtin_amdgcn_readlane((int)x, 63); }
-DEVI int64_t lane63(int64_t x) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), 63);
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-DEVI uint32_t wave_sum(uint32_t x) { return lane63(wave_incl_sum(x)); }
-DEVI uint32_t wave_excl_sum(uint32_t v) { return wave_incl_sum(v) - v; }
-DEVI int64_t wave_max(int64_t x) { return lane63(wave_incl_max(x)); }
-DEVI uint32_t wave_umax(uint32_t x) { return lane63(wave_incl_umax(x)); }
 
 constexpr int CAP_S = 256;     // requests per round of a streamed cell
 constexpr int SLOTS_MAX = 16;  // die runs per channel on the bucket path
@@ -1318,8 +1447,60 @@ __global__ __launch_bounds__(BLK) void k_classify(const uint64_t *__restrict__ a
 }
 
 __global__ void k_reset(DevState *st) {
-  for (uint32_t k = threadIdx.x; k < MAX_KEYS; k += blockDim.x) st->die_free[k] = NEG;
+  for (uint32_t k = threadIdx.x; k < MAX_KEYS; k += blockDim.x) {
+    st->die_free[k] = NEG;
+    st->ref_pend[k] = 0;  // pending refresh quanta are dropped
+    st->ref_head[k] = 0;
+  }
   for (uint32_t c = threadIdx.x; c < MAX_CHANNELS; c += blockDim.x) st->chan_free[c] = NEG;
+}
+
+// ------------------------------------------------------------------ refresh bookkeeping
+
+// After a call on the refresh path: die queue k's first min(pending, its
+// admissions) quanta were claimed.  Success retires them; a failed call
+// claims nothing, so their completion cells go back to pending.
+__global__ __launch_bounds__(BLK) void k_refresh_commit(const CallCtl *ctl, DevState *st,
+                                                        const uint32_t *__restrict__ totals, uint32_t K) {
+  const uint32_t err = agent_load32(&ctl->err);
+  for (uint32_t k = blockIdx.x * BLK + threadIdx.x; k < K; k += gridDim.x * BLK) {
+    const uint32_t R = st->ref_pend[k], used = min(R, totals[k]);
+    if (!used) continue;
+    if (err) {
+      int64_t *const *q = st->ref_slot + st->ref_off[k] + st->ref_head[k];
+      for (uint32_t r = 0; r < used; r++) *q[r] = REFRESH_PENDING;
+    } else {
+      st->ref_head[k] += used;
+      st->ref_pend[k] = R - used;
+    }
+  }
+}
+
+// Idle-window drain: each die queue, oldest quantum first, starts the next
+// one at max(its clock, t_from) while it ends by t_to.
+__global__ __launch_bounds__(BLK) void k_refresh_drain(DevState *st, uint32_t K, int64_t tQ, int64_t t_from,
+                                                       int64_t t_to) {
+  const uint32_t k = blockIdx.x * BLK + threadIdx.x;
+  if (k >= K) return;
+  uint32_t R = st->ref_pend[k], h = st->ref_head[k];
+  if (!R) return;
+  int64_t t = imax(st->die_free[k], t_from);  // NEG (idle since -inf) -> t_from
+  int64_t *const *q = st->ref_slot + st->ref_off[k];
+  const uint32_t R0 = R;
+  while (R && t + tQ <= t_to) {
+    t += tQ;
+    *q[h++] = t;
+    R--;
+  }
+  if (R != R0) {
+    st->die_free[k] = t;
+    st->ref_head[k] = h;
+    st->ref_pend[k] = R;
+  }
+}
+
+__global__ __launch_bounds__(BLK) void k_fill(int64_t *__restrict__ p, int64_t n, int64_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * BLK + threadIdx.x; i < n; i += (int64_t)gridDim.x * BLK) p[i] = v;
 }
 
 // ------------------------------------------------------------------ launchers
@@ -1341,13 +1522,15 @@ static size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
 size_t lds_die_reduce(uint32_t K) {
   return align16(sizeof(LdsRanges)) + K * (8 + 8 + 4) + DWAVES * K * 2 + K * 2;
 }
+size_t lds_die_count(uint32_t K) { return align16(sizeof(LdsRanges)) + K * 4; }
 size_t lds_die_scatter(uint32_t K) {
   return (size_t)CHUNKP * 8 + (size_t)K * (sizeof(KeyA) + sizeof(KeyW) + 4) + (size_t)CHUNKP * 6;
 }
 
 hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout &Lo, char *ws,
                                 DevState *st, const uint64_t *addr, const int64_t *issue,
-                                int64_t *complete, hipStream_t s, hipEvent_t *ev, int n_ev) {
+                                int64_t *complete, hipStream_t s, hipEvent_t *ev, int n_ev,
+                                bool refresh) {
   CallCtl *ctl = (CallCtl *)(ws + Lo.off_ctl);
   uint32_t *agg_cnt = (uint32_t *)(ws + Lo.off_agg_cnt);
   int64_t *agg_A = (int64_t *)(ws + Lo.off_agg_A);
@@ -1374,19 +1557,35 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   hipLaunchKernelGGL(k_prologue, dim3(1), dim3(64), 0, s, ctl);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
+  const dim3 key_waves((g.K + WAVES - 1) / WAVES);
+  if (refresh) {
+    // count pass and per-tile rank bases first (timed with pass 1)
+    const size_t lds = lds_die_count(g.K);
+    if (p2)
+      hipLaunchKernelGGL(k_die_count<true>, dim3(Lo.nt), dim3(DBLK), lds, s, addr, Lo.n, g, rt, Lo.tile_elems,
+                         agg_cnt);
+    else
+      hipLaunchKernelGGL(k_die_count<false>, dim3(Lo.nt), dim3(DBLK), lds, s, addr, Lo.n, g, rt,
+                         Lo.tile_elems, agg_cnt);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_tile_count, key_waves, dim3(BLK), 0, s, agg_cnt, Lo.nt, g.K, tin_base, totals);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   {
     const size_t lds = lds_die_reduce(g.K);
-    if (p2)
-      hipLaunchKernelGGL(k_die_reduce<true>, dim3(Lo.nt), dim3(DBLK), lds, s, addr, issue, Lo.n, complete,
-                         g, rt, Lo.tile_elems, agg_cnt, agg_A, KR, ctl, kbits);
-    else
-      hipLaunchKernelGGL(k_die_reduce<false>, dim3(Lo.nt), dim3(DBLK), lds, s, addr, issue, Lo.n,
-                         complete, g, rt, Lo.tile_elems, agg_cnt, agg_A, KR, ctl, kbits);
+    auto kfn = p2 ? (refresh ? k_die_reduce<true, true> : k_die_reduce<true, false>)
+                  : (refresh ? k_die_reduce<false, true> : k_die_reduce<false, false>);
+    hipLaunchKernelGGL(kfn, dim3(Lo.nt), dim3(DBLK), lds, s, addr, issue, Lo.n, complete, g, rt, Lo.tile_elems,
+                       agg_cnt, agg_A, KR, ctl, kbits, tin_base, st);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
-  hipLaunchKernelGGL(k_tile_scan, dim3((g.K + WAVES - 1) / WAVES), dim3(BLK), 0, s, agg_cnt, agg_A, Lo.nt, g.K,
-                     g.tR, st, tin_L, tin_base, totals, dfnew, ctl);
+  if (refresh)
+    hipLaunchKernelGGL(k_tile_scan_ref, key_waves, dim3(BLK), 0, s, agg_A, Lo.nt, g, st, tin_base, totals, tin_L,
+                       dfnew, ctl);
+  else
+    hipLaunchKernelGGL(k_tile_scan, key_waves, dim3(BLK), 0, s, agg_cnt, agg_A, Lo.nt, g.K, g.tR, st, tin_L,
+                       tin_base, totals, dfnew, ctl);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
   hipLaunchKernelGGL(k_key_scan, dim3(1), dim3(BLK), 0, s, totals, g.K, seg, issue, Lo.gmax, Lo.s0, ctl);
@@ -1394,8 +1593,9 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   mark();
   {
     const size_t lds = lds_die_scatter(g.K);
-    hipLaunchKernelGGL(k_die_scatter, dim3(Lo.nt), dim3(DBLK), lds, s, issue, KR, Lo.n, g, Lo.tile_elems,
-                       tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl);
+    hipLaunchKernelGGL(refresh ? k_die_scatter<true> : k_die_scatter<false>, dim3(Lo.nt), dim3(DBLK), lds, s,
+                       issue, KR, Lo.n, g, Lo.tile_elems, tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl,
+                       st);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
@@ -1457,6 +1657,10 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
                        totals, cfnew, g.K, g.C);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (refresh) {
+    hipLaunchKernelGGL(k_refresh_commit, dim3((g.K + BLK - 1) / BLK), dim3(BLK), 0, s, ctl, st, totals, g.K);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   mark();
   return hipSuccess;
 }
@@ -1532,17 +1736,31 @@ hipError_t launch_layer_done(const CallCtl *ctl, int64_t count, const int64_t *p
 
 hipError_t set_lds_limits(uint32_t K) {
   hipError_t e;
-  const int a = (int)lds_die_reduce(K), b = (int)lds_die_scatter(K);
-  if ((e = hipFuncSetAttribute((const void *)k_die_reduce<true>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, a)) != hipSuccess)
-    return e;
-  if ((e = hipFuncSetAttribute((const void *)k_die_reduce<false>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, a)) != hipSuccess)
-    return e;
-  if ((e = hipFuncSetAttribute((const void *)k_die_scatter, hipFuncAttributeMaxDynamicSharedMemorySize,
-                               b)) != hipSuccess)
-    return e;
+  const int a = (int)lds_die_reduce(K), b = (int)lds_die_scatter(K), c = (int)lds_die_count(K);
+  const void *fa[] = {(const void *)k_die_reduce<true, false>, (const void *)k_die_reduce<false, false>,
+                      (const void *)k_die_reduce<true, true>, (const void *)k_die_reduce<false, true>};
+  for (const void *f : fa)
+    if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, a)) != hipSuccess) return e;
+  const void *fb[] = {(const void *)k_die_scatter<false>, (const void *)k_die_scatter<true>};
+  for (const void *f : fb)
+    if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, b)) != hipSuccess) return e;
+  const void *fc[] = {(const void *)k_die_count<true>, (const void *)k_die_count<false>};
+  for (const void *f : fc)
+    if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, c)) != hipSuccess) return e;
   return hipSuccess;
+}
+
+hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s) {
+  hipLaunchKernelGGL(k_refresh_drain, dim3((g.K + BLK - 1) / BLK), dim3(BLK), 0, s, st, g.K, g.tQ, t_from, t_to);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + BLK - 1) / BLK;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_fill, dim3((uint32_t)blocks), dim3(BLK), 0, s, p, n, v);
+  return hipGetLastError();
 }
 
 }  // namespace hbf

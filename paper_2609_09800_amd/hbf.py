@@ -28,7 +28,9 @@ EXPORTED = [
     "hbf_register_range", "hbf_workspace_bytes", "hbf_set_workspace", "hbf_classify_map",
     "hbf_time_requests", "hbf_time_layers", "hbf_gemv_instrumented", "hbf_wall_clock_tick_ps", "hbf_get_status",
     "hbf_get_state", "hbf_set_state", "hbf_profile", "hbf_kernel_times", "hbf_strerror",
+    "hbf_refresh_plan", "hbf_refresh_configure", "hbf_refresh_submit", "hbf_refresh_drain", "hbf_refresh_pending",
 ]
+REFRESH_PENDING = -1
 
 
 class hbf_params(ctypes.Structure):
@@ -36,6 +38,11 @@ class hbf_params(ctypes.Structure):
                 ("planes_per_die", ctypes.c_uint32), ("page_bytes", ctypes.c_uint32),
                 ("t_read_ns", ctypes.c_int64), ("channel_bytes_per_s", ctypes.c_uint64),
                 ("flags", ctypes.c_uint32)]
+
+
+class hbf_refresh_block(ctypes.Structure):
+    _fields_ = [("epoch", ctypes.c_uint32), ("zone", ctypes.c_uint32), ("channel", ctypes.c_uint32),
+                ("die", ctypes.c_uint32), ("plane", ctypes.c_uint32), ("block", ctypes.c_uint32)]
 
 
 _lib = None
@@ -70,6 +77,11 @@ def load_library(path=LIB_PATH):
         "hbf_kernel_times": ([vp, vp, vp, i32, ctypes.POINTER(i32)], i32),
         "hbf_time_layers": ([vp, vp, i64, vp, i32, i64, i64, vp, vp, vp, vp], i32),
         "hbf_strerror": ([i32], ctypes.c_char_p),
+        "hbf_refresh_plan": ([ctypes.POINTER(hbf_params), vp, i64, u32, vp, i64], i32),
+        "hbf_refresh_configure": ([vp, i64], i32),
+        "hbf_refresh_submit": ([vp, vp, i64, vp, vp], i32),
+        "hbf_refresh_drain": ([vp, i64, i64, vp], i32),
+        "hbf_refresh_pending": ([vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -218,6 +230,30 @@ class Model:
         return self._lib.hbf_set_state(self._h, d.ctypes.data_as(ctypes.c_void_p),
                                        c.ctypes.data_as(ctypes.c_void_p), _sp(stream))
 
+    # -- refresh traffic (Section D4; reading in include/hbf.h)
+
+    def refresh_configure(self, t_prog_ns):
+        return self._lib.hbf_refresh_configure(self._h, int(t_prog_ns))
+
+    def refresh_submit(self, pages, done, stream=None):
+        """pages: host uint64 array of device pages in plan order; done: int64
+        device tensor [len(pages)] receiving each quantum's completion."""
+        import numpy as np
+        pg = np.ascontiguousarray(pages, dtype=np.uint64)
+        assert done is None or done.numel() >= pg.size
+        return self._lib.hbf_refresh_submit(self._h, pg.ctypes.data_as(ctypes.c_void_p) if pg.size else None,
+                                            pg.size, _dp(done), _sp(stream))
+
+    def refresh_drain(self, t_from_ns, t_to_ns, stream=None):
+        return self._lib.hbf_refresh_drain(self._h, int(t_from_ns), int(t_to_ns), _sp(stream))
+
+    def refresh_pending(self, stream=None):
+        import numpy as np
+        out = np.zeros(self.n_die_queues, dtype=np.uint32)
+        _check(self._lib.hbf_refresh_pending(self._h, out.ctypes.data_as(ctypes.c_void_p), _sp(stream)),
+               "hbf_refresh_pending")
+        return out
+
     def profile(self, enable=True):
         _check(self._lib.hbf_profile(self._h, int(enable)), "hbf_profile")
 
@@ -228,6 +264,22 @@ class Model:
         cnt = ctypes.c_int(0)
         _check(self._lib.hbf_kernel_times(self._h, ms, names, 16, ctypes.byref(cnt)), "hbf_kernel_times")
         return [(names[i].decode(), ms[i]) for i in range(cnt.value)]
+
+
+def refresh_plan(params, blocks, pages_per_block):
+    """Device pages of a refresh plan in the scheduler's order (host-only).
+    params: dict of model parameters; blocks: (epoch, zone, channel, die,
+    plane, block) tuples.  Returns (status, uint64 array)."""
+    import numpy as np
+    lib = load_library()
+    p = hbf_params(params["channels"], params["dies_per_channel"], params["planes_per_die"],
+                   params["page_bytes"], params["t_read_ns"], params["channel_bytes_per_s"],
+                   params.get("flags", 0))
+    arr = (hbf_refresh_block * max(1, len(blocks)))(*[hbf_refresh_block(*b) for b in blocks])
+    out = np.zeros(max(1, len(blocks) * pages_per_block), dtype=np.uint64)
+    rc = lib.hbf_refresh_plan(ctypes.byref(p), ctypes.cast(arr, ctypes.c_void_p), len(blocks), pages_per_block,
+                              out.ctypes.data_as(ctypes.c_void_p), len(blocks) * pages_per_block)
+    return rc, out[:len(blocks) * pages_per_block]
 
 
 def strerror(code):

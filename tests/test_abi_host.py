@@ -158,3 +158,55 @@ def test_set_state_validation_is_host_side(lib):
     d[1] = -3
     assert lib.hbf_set_state(h, d.ctypes.data_as(ctypes.c_void_p), c.ctypes.data_as(ctypes.c_void_p), None) == -1
     lib.hbf_model_destroy(h)
+
+
+def test_refresh_validation_is_host_side(lib):
+    rc, h = create(lib)   # tR = 3000 ns
+    fake = ctypes.c_void_p(4096)  # never dereferenced
+    assert lib.hbf_refresh_configure(h, -1) == -1
+    assert lib.hbf_refresh_configure(h, (1 << 29) - 6000 + 1) == -1
+    # submit before configure, negative count, null arrays
+    assert lib.hbf_refresh_submit(h, fake, 1, fake, None) == -1
+    assert lib.hbf_refresh_configure(h, (1 << 29) - 6000) == 0
+    assert lib.hbf_refresh_submit(h, fake, -1, fake, None) == -1
+    assert lib.hbf_refresh_submit(h, None, 3, fake, None) == -1
+    assert lib.hbf_refresh_submit(h, fake, 3, None, None) == -1
+    assert lib.hbf_refresh_drain(h, -1, 5, None) == -1
+    assert lib.hbf_refresh_drain(h, 6, 5, None) == -1
+    assert lib.hbf_refresh_drain(h, 0, 1 << 61, None) == -1
+    assert lib.hbf_refresh_pending(h, None, None) == -1
+    lib.hbf_model_destroy(h)
+
+
+def _plan_params(C, D, P):
+    return dict(channels=C, dies_per_channel=D, planes_per_die=P, page_bytes=16384, t_read_ns=3000,
+                channel_bytes_per_s=8_000_000_000)
+
+
+def test_refresh_plan_hand_example(lib):
+    from paper_2609_09800_amd import hbf
+    blocks = [(1, 0, 0, 0, 0, 0), (0, 0, 0, 0, 0, 1), (0, 0, 0, 1, 0, 0), (0, 0, 1, 0, 0, 3)]
+    rc, out = hbf.refresh_plan(_plan_params(2, 2, 1), blocks, 2)
+    assert rc == 0 and list(out) == [8, 25, 2, 29, 12, 6, 0, 4]
+    rc, out = hbf.refresh_plan(_plan_params(2, 2, 1), [(0, 0, 2, 0, 0, 0)], 1)   # channel out of range
+    assert rc == -1
+    rc, out = hbf.refresh_plan(_plan_params(2, 2, 1), [], 4)
+    assert rc == 0 and out.size == 0
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_refresh_plan_matches_reference(lib, oracle_mod, seed):
+    import numpy as np
+    from paper_2609_09800_amd import hbf
+    rng = np.random.default_rng(50 + seed)
+    C, D, P = [(4, 3, 2), (1, 1, 4), (8, 4, 1), (3, 5, 2), (2, 8, 4), (16, 2, 1)][seed]
+    ppb = int(rng.integers(1, 5))
+    nb = int(rng.integers(0, 60))
+    blocks = [(int(rng.integers(0, 3)), int(rng.integers(0, 3)), int(rng.integers(0, C)), int(rng.integers(0, D)),
+               int(rng.integers(0, P)), int(rng.integers(0, 6))) for _ in range(nb)]
+    rc, out = hbf.refresh_plan(_plan_params(C, D, P), blocks, ppb)
+    assert rc == 0
+
+    class Prm:
+        channels, dies_per_channel, planes_per_die = C, D, P
+    assert [int(x) for x in out] == oracle_mod.refresh_plan(Prm, blocks, ppb)
