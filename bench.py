@@ -61,6 +61,17 @@ def traffic_for(kernel, n):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
+def path_traffic(n):
+    """HBM bytes of one hbf_time_requests call (all its kernels) from the
+    committed counters, if taken on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC_JSON):
+        return None
+    t = json.load(open(TRAFFIC_JSON))
+    if t.get("kernel_src_sha256") != file_sha(KERNEL_SRC) or t.get("n") != n:
+        return None
+    return sum(k.get("hbm_bytes_per_launch", 0) for k in t.get("kernels", {}).values())
+
+
 def load_or_generate(wl, n, cache):
     """The large mixed stream; with a cache directory it is generated once and
     then read back (the generator is deterministic in its seed and size)."""
@@ -112,6 +123,44 @@ def closed_loop(torch, hbf, wl, steps=2, reps=3):
                 modeled_decode_step_ns=step_ns)
 
 
+def refresh_leg(torch, hbf, wl, w, model, addr, issue, complete, reps=3):
+    """The refresh row: the same stream timed with a refresh plan pending
+    (Section D4), which adds a counting pass and rank-dependent die service.
+    Each rep resets the model and resubmits the plan outside the timed
+    region; the call is timed with events on the stream it runs on."""
+    blocks, ppb, t_prog = wl.config5_refresh_blocks()
+    rc, pages = hbf.refresh_plan(w.params, blocks, ppb)
+    assert rc == 0
+    assert model.refresh_configure(t_prog) == 0
+    done = torch.empty(pages.size, dtype=torch.int64, device="cuda")
+    s = torch.cuda.current_stream()
+    times = []
+    for r in range(reps + 1):
+        model.reset(s)
+        assert model.refresh_submit(pages, done, s) == 0
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        assert model.time_requests(addr, issue, complete, s) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+        if r:  # the first is a warm-up
+            times.append(e0.elapsed_time(e1))
+    assert model.get_status() == 0
+    parity = None
+    gold_p = os.path.join(ROOT, "tests", "golden", "oracle_digests.json")
+    if w.n == 1 << 28 and os.path.exists(gold_p):
+        gold = json.load(open(gold_p)).get("config5_refresh")
+        if gold:
+            parity = (sha(complete.cpu().numpy()) == gold["complete_sha256"]
+                      and sha(done.cpu().numpy()) == gold["quantum_done_sha256"])
+    pending = int(model.refresh_pending().sum())
+    model.reset(s)
+    ms = float(np.median(times))
+    return dict(workload=f"the same {w.n} requests with a {pages.size}-quantum refresh plan pending "
+                         f"(tPROG {t_prog} ns)", quanta=int(pages.size), quanta_left_pending=pending,
+                ms_per_call=ms, requests_per_s=w.n / (ms / 1e3), parity_vs_reference_digest=parity)
+
+
 def cpu_baseline(w, n_sample):
     from oracle import oracle
     m = oracle.OracleModel(**w.params)
@@ -141,6 +190,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--no-gemv", action="store_true", help="time only hbf_time_requests (diagnostic)")
     ap.add_argument("--no-closed-loop", action="store_true", help="skip the closed-loop decode report")
+    ap.add_argument("--no-refresh", action="store_true", help="skip the refresh-plan report")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -267,13 +317,22 @@ def main():
         "time_requests_req_per_s": n / (tr_ms / 1e3),
         "path_algorithmic_GBps": PATH_ALG_BYTES * n / (tr_ms / 1e3) / 1e9,
         "path_algorithmic_frac": PATH_ALG_BYTES * n / (tr_ms / 1e3) / 1e9 / HBM_PEAK_GBPS,
+        "path_counter_GBps": None,
+        "path_counter_frac": None,
         "kernel_ms": per_kernel,
         "parity_vs_reference_digest": parity,
         "delay": delay,
     }
+    pt = path_traffic(n)
+    if pt:  # counter-measured HBM bytes of the whole call / its kernels' time
+        out["path_counter_GBps"] = pt / (tr_ms / 1e3) / 1e9
+        out["path_counter_frac"] = out["path_counter_GBps"] / HBM_PEAK_GBPS
     if not args.no_closed_loop:
         log("closed-loop decode timing")
         out["closed_loop"] = closed_loop(torch, hbf, wl)
+    if not args.no_refresh:
+        log("refresh-plan timing")
+        out["refresh"] = refresh_leg(torch, hbf, wl, w, model, addr, issue, complete)
     if not args.no_cpu:
         log("timing the reference model on the CPU sample")
         out["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, n))

@@ -300,6 +300,27 @@ def config5(seed=0, n=1 << 28):
                     meta=dict(n_kv=n_kv, steps=steps))
 
 
+def config5_refresh_blocks(seed=0):
+    """A refresh plan for the large mixed stream's device (32 ch x 16 die x
+    4 plane), Section D4: epoch 0 makes one block of every plane eligible
+    (zone = plane mod 2), epoch 1 one more plane-0 block of a random half of
+    the dies; 32 pages per block, block indices uniform in [0, 1024).  The
+    paper gives no program time; tPROG = 30,000 ns (10 tR) is assumed.
+    Returns (blocks, pages_per_block, t_prog_ns)."""
+    rng = _rng(seed + 5)
+    blocks = []
+    for ch in range(32):
+        for die in range(16):
+            for plane in range(4):
+                blocks.append((0, plane % 2, ch, die, plane, int(rng.integers(0, 1024))))
+    again = rng.random((32, 16)) < 0.5
+    for ch in range(32):
+        for die in range(16):
+            if again[ch, die]:
+                blocks.append((1, 0, ch, die, 0, int(rng.integers(0, 1024))))
+    return blocks, 32, 30_000
+
+
 def random_stream(seed, n, params, range_pages, mean_gap, out_frac=0.0, run_frac=0.0,
                   hot_dies=None, base=RANGE_BASE, burst=None):
     """Generic seeded stream for the parity suite.

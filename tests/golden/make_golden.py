@@ -1,5 +1,6 @@
 """Write tests/golden/oracle_digests.json: SHA-256 digests of the reference
-model's outputs on the seeded workloads (configs 1, 2, 3 and 5).
+model's outputs on the seeded workloads (configs 1, 2, 3 and 5, and config
+5 with a refresh plan pending: argument "5r").
 
 Calls only ``oracle/`` and the input generators; nothing here comes from
 the HIP path.  Usage:  python tests/golden/make_golden.py [config ...]
@@ -50,14 +51,41 @@ def digest(cfg):
     return rec
 
 
+def digest_refresh():
+    """The large mixed stream timed with a refresh plan pending (Section D4)."""
+    w = wl.config5()
+    blocks, ppb, t_prog = wl.config5_refresh_blocks()
+    m = oracle.OracleModel(**w.params)
+    for b, n in w.ranges:
+        assert m.register_range(b, n) == 0
+    pages = np.array(oracle.refresh_plan(m.params, blocks, ppb), dtype=np.uint64)
+    assert m.refresh_configure(t_prog) == 0
+    assert m.refresh_submit(pages)[0] == 0
+    t = time.time()
+    rc, c = m.time_requests(w.addr, w.issue)
+    to = time.time() - t
+    assert rc == 0
+    d, ch = m.state()
+    q = m.refresh_done()
+    rec = dict(n=w.n, quanta=int(pages.size), plan_sha256=sha(pages), complete_sha256=sha(c),
+               quantum_done_sha256=sha(q), pending_sum=int(m.refresh_pending().sum()),
+               die_free_sha256=sha(d), chan_free_sha256=sha(ch), max_complete=int(c.max()),
+               oracle_s=round(to, 1))
+    print("config5_refresh", rec, flush=True)
+    return rec
+
+
 def main(cfgs):
     data = json.load(open(OUT)) if os.path.exists(OUT) else {}
     data["_comment"] = ("SHA-256 of the reference model's outputs (int64 little endian) on the "
                         "seeded workloads; written by tests/golden/make_golden.py (oracle only)")
     for c in cfgs:
-        data[f"config{c}"] = digest(c)
+        if c == "5r":
+            data["config5_refresh"] = digest_refresh()
+        else:
+            data[f"config{c}"] = digest(int(c))
         json.dump(data, open(OUT, "w"), indent=1, sort_keys=True)
 
 
 if __name__ == "__main__":
-    main([int(a) for a in sys.argv[1:]] or [1, 2, 3, 5])
+    main(sys.argv[1:] or ["1", "2", "3", "5", "5r"])

@@ -182,3 +182,48 @@ def test_closed_loop_with_refresh(torch):
     assert np.array_equal(iss.cpu().numpy(), wi) and np.array_equal(c.cpu().numpy(), wc)
     assert np.array_equal(d.cpu().numpy(), wd)
     p.check("closed loop")
+
+
+def test_large_mixed_stream_with_refresh_digest(torch):
+    """2^28 requests of the large mixed stream with a 73,696-quantum plan
+    pending, against digests the reference model wrote
+    (tests/golden/make_golden.py 5r)."""
+    import hashlib
+    import json
+    import os
+    from paper_2609_09800_amd import hbf
+
+    def sha(*arrays):
+        h = hashlib.sha256()
+        for a in arrays:
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()
+
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "oracle_digests.json")))["config5_refresh"]
+    say(f"config5 + refresh: generating {gold['n']} requests")
+    w = wl.config5()
+    blocks, ppb, t_prog = wl.config5_refresh_blocks()
+    rc, pages = hbf.refresh_plan(w.params, blocks, ppb)
+    assert rc == 0 and pages.size == gold["quanta"] and sha(pages) == gold["plan_sha256"]
+    g = hbf.Model(**w.params)
+    for b, nb in w.ranges:
+        assert g.register_range(b, nb)[0] == 0
+    assert g.refresh_configure(t_prog) == 0
+    done = torch.empty(pages.size, dtype=torch.int64, device="cuda")
+    assert g.refresh_submit(pages, done) == 0
+    a = dev(torch, w.addr)
+    i = dev(torch, w.issue)
+    del w
+    c = torch.empty_like(i)
+    say("config5 + refresh: timing on the GPU")
+    assert g.time_requests(a, i, c) == 0
+    assert g.get_status() == 0
+    del a, i
+    got = c.cpu().numpy()
+    assert int(got.max()) == gold["max_complete"]
+    assert sha(got) == gold["complete_sha256"]
+    assert sha(done.cpu().numpy()) == gold["quantum_done_sha256"]
+    assert int(g.refresh_pending().sum()) == gold["pending_sum"]
+    d, ch = g.get_state()
+    assert sha(d) == gold["die_free_sha256"] and sha(ch) == gold["chan_free_sha256"]
+    g.close()
