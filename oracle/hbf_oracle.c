@@ -441,6 +441,113 @@ void orc_refresh_done(const orc_model *m, int64_t *done) {
   if (m->nq) memcpy(done, m->qdone, sizeof(int64_t) * m->nq);
 }
 
+/* ---------------------------------------------------------------- capacity
+ * Sections D5 and D6: a capacity range is served from a bounded frame cache
+ * in HBM; an access whose page is not resident faults and reads it from the
+ * media; the speculative prefetcher then fetches the pages that follow the
+ * faulting page.  Prefetch reads never enter the timing path (D6), so the
+ * cache only decides which accesses become media reads.  Readings (the paper
+ * names no replacement policy and no prefetch depth):
+ *  - pages are numbered within the capacity range, [0, range_pages);
+ *  - F frames with FIFO replacement: every insertion takes the frame that
+ *    was filled longest ago; a hit changes nothing;
+ *  - a fault on page p inserts p, then, for k = 1 .. d in that order while
+ *    p + k < range_pages, inserts p + k if it is not resident at that moment
+ *    (one prefetch read each);
+ *  - a prefetched page counts as used at its first hit and as unused if it
+ *    is evicted before one.
+ */
+typedef struct {
+  int64_t frames, degree, range_pages;
+  int64_t *frame_page;   /* page held by each frame, -1 = empty */
+  uint8_t *frame_pf;     /* 1 = prefetched and not hit since */
+  int64_t *slot;         /* frame holding each page, -1 = not resident */
+  int64_t head;          /* next frame to fill (the oldest) */
+  int64_t hits, misses, pf_reads, pf_used, pf_unused;
+} orc_cache;
+
+void orc_cache_destroy(orc_cache *c) {
+  if (!c) return;
+  free(c->frame_page); free(c->frame_pf); free(c->slot); free(c);
+}
+
+void orc_cache_reset(orc_cache *c) {
+  for (int64_t f = 0; f < c->frames; f++) { c->frame_page[f] = -1; c->frame_pf[f] = 0; }
+  for (int64_t q = 0; q < c->range_pages; q++) c->slot[q] = -1;
+  c->head = c->hits = c->misses = c->pf_reads = c->pf_used = c->pf_unused = 0;
+}
+
+int orc_cache_create(int64_t frames, int64_t degree, int64_t range_pages, orc_cache **out) {
+  if (!out || frames < 1 || degree < 0 || degree >= frames || range_pages < 1) return ORC_EINVAL;
+  orc_cache *c = (orc_cache *)calloc(1, sizeof(orc_cache));
+  if (!c) return ORC_ENOMEM;
+  c->frames = frames; c->degree = degree; c->range_pages = range_pages;
+  c->frame_page = (int64_t *)malloc(sizeof(int64_t) * frames);
+  c->frame_pf = (uint8_t *)malloc(frames);
+  c->slot = (int64_t *)malloc(sizeof(int64_t) * range_pages);
+  if (!c->frame_page || !c->frame_pf || !c->slot) { orc_cache_destroy(c); return ORC_ENOMEM; }
+  orc_cache_reset(c);
+  *out = c;
+  return ORC_OK;
+}
+
+/* Put page q into the oldest frame; returns nothing, updates the counters. */
+static void orc_cache_insert(orc_cache *c, int64_t q, int prefetched) {
+  int64_t f = c->head;
+  int64_t old = c->frame_page[f];
+  if (old >= 0) {
+    c->slot[old] = -1;
+    if (c->frame_pf[f]) c->pf_unused++;
+  }
+  c->frame_page[f] = q;
+  c->frame_pf[f] = (uint8_t)prefetched;
+  c->slot[q] = f;
+  c->head = (f + 1) % c->frames;
+}
+
+/* Serve pages[0..n) in order.  hit[i] = 1 if access i found its page
+ * resident, 0 if it faulted.  The first pf_cap prefetch reads issued, in
+ * order, go to pf_page / pf_src (the faulting access); *n_pf = the number
+ * issued.  Pages outside the range: EINVAL before anything changes. */
+int orc_cache_access(orc_cache *c, const uint64_t *pages, int64_t n, uint8_t *hit, uint64_t *pf_page,
+                     int64_t *pf_src, int64_t pf_cap, int64_t *n_pf) {
+  if (!c || n < 0 || (n > 0 && (!pages || !hit)) || pf_cap < 0) return ORC_EINVAL;
+  for (int64_t i = 0; i < n; i++)
+    if (pages[i] >= (uint64_t)c->range_pages) return ORC_EINVAL;
+  int64_t npf = 0;
+  for (int64_t i = 0; i < n; i++) {
+    const int64_t p = (int64_t)pages[i];
+    if (c->slot[p] >= 0) {
+      hit[i] = 1;
+      c->hits++;
+      if (c->frame_pf[c->slot[p]]) { c->frame_pf[c->slot[p]] = 0; c->pf_used++; }
+      continue;
+    }
+    hit[i] = 0;
+    c->misses++;
+    orc_cache_insert(c, p, 0);
+    for (int64_t k = 1; k <= c->degree && p + k < c->range_pages; k++) {
+      if (c->slot[p + k] >= 0) continue;
+      orc_cache_insert(c, p + k, 1);
+      c->pf_reads++;
+      if (npf < pf_cap && pf_page) { pf_page[npf] = (uint64_t)(p + k); pf_src[npf] = i; }
+      npf++;
+    }
+  }
+  if (n_pf) *n_pf = npf;
+  return ORC_OK;
+}
+
+/* hits, faults, prefetch reads, prefetched pages used, evicted unused. */
+void orc_cache_counts(const orc_cache *c, int64_t *out) {
+  out[0] = c->hits; out[1] = c->misses; out[2] = c->pf_reads; out[3] = c->pf_used; out[4] = c->pf_unused;
+}
+
+void orc_cache_frames(const orc_cache *c, int64_t *frame_page, int64_t *head) {
+  memcpy(frame_page, c->frame_page, sizeof(int64_t) * c->frames);
+  *head = c->head;
+}
+
 /* Die-stage completion times alone (a diagnostic used by the tests): the
  * same step 3 as above, without touching the model's clocks.  Out-of-range
  * requests get ORC_TIME_ERROR. */

@@ -87,6 +87,18 @@ def _load():
         lib.orc_refresh_count.restype = i64
         lib.orc_refresh_done.argtypes = [vp, vp]
         lib.orc_refresh_done.restype = None
+        lib.orc_cache_create.argtypes = [i64, i64, i64, ctypes.POINTER(vp)]
+        lib.orc_cache_create.restype = i32
+        lib.orc_cache_destroy.argtypes = [vp]
+        lib.orc_cache_destroy.restype = None
+        lib.orc_cache_reset.argtypes = [vp]
+        lib.orc_cache_reset.restype = None
+        lib.orc_cache_access.argtypes = [vp, vp, i64, vp, vp, vp, i64, ctypes.POINTER(i64)]
+        lib.orc_cache_access.restype = i32
+        lib.orc_cache_counts.argtypes = [vp, vp]
+        lib.orc_cache_counts.restype = None
+        lib.orc_cache_frames.argtypes = [vp, vp, ctypes.POINTER(i64)]
+        lib.orc_cache_frames.restype = None
         _lib = lib
     return _lib
 
@@ -235,6 +247,55 @@ class OracleModel:
 
 
 REFRESH_PENDING = -1
+
+
+class OracleCache:
+    """Capacity-mode frame cache with the next-page prefetcher (Sections D5,
+    D6; readings in hbf_oracle.c): F frames, FIFO replacement, a fault on
+    page p also fetches the non-resident pages among p+1 .. p+degree."""
+
+    def __init__(self, frames, degree, range_pages):
+        self._lib = _load()
+        h = ctypes.c_void_p()
+        rc = self._lib.orc_cache_create(frames, degree, range_pages, ctypes.byref(h))
+        if rc != OK:
+            raise ValueError(f"oracle cache: invalid parameters (status {rc})")
+        self._h = h
+        self.frames = frames
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._lib.orc_cache_destroy(h)
+            self._h = None
+
+    def reset(self):
+        self._lib.orc_cache_reset(self._h)
+
+    def access(self, pages, pf_cap=None):
+        """Returns (rc, hit[n] uint8, prefetch pages, prefetch source access)."""
+        pg = np.ascontiguousarray(pages, dtype=np.uint64)
+        hit = np.zeros(pg.size, dtype=np.uint8)
+        cap = pg.size * 64 if pf_cap is None else pf_cap
+        pp = np.zeros(max(cap, 1), dtype=np.uint64)
+        ps = np.zeros(max(cap, 1), dtype=np.int64)
+        npf = ctypes.c_int64(0)
+        rc = self._lib.orc_cache_access(self._h, _ptr(pg), pg.size, _ptr(hit), _ptr(pp), _ptr(ps), cap,
+                                        ctypes.byref(npf))
+        k = min(npf.value, cap)
+        return int(rc), hit, pp[:k], ps[:k]
+
+    def counts(self):
+        """(hits, faults, prefetch reads, prefetched pages used, evicted unused)."""
+        out = np.zeros(5, dtype=np.int64)
+        self._lib.orc_cache_counts(self._h, _ptr(out))
+        return out
+
+    def frames_state(self):
+        fp = np.zeros(self.frames, dtype=np.int64)
+        head = ctypes.c_int64(0)
+        self._lib.orc_cache_frames(self._h, _ptr(fp), ctypes.byref(head))
+        return fp, head.value
 
 
 def refresh_plan(params, blocks, pages_per_block):

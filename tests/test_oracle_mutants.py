@@ -62,6 +62,18 @@ MUTANTS = {
     "refresh-drain-ignores-clock": (
         "int64_t start = m->die_busy[k] ? orc_max(m->die_free[k], t_from) : t_from;",
         "int64_t start = t_from;"),
+    "cache-prefetch-ignores-residency": (
+        "      if (c->slot[p + k] >= 0) continue;\n",
+        ""),
+    "cache-prefetch-depth-short": (
+        "for (int64_t k = 1; k <= c->degree && p + k < c->range_pages; k++) {",
+        "for (int64_t k = 1; k < c->degree && p + k < c->range_pages; k++) {"),
+    "cache-eviction-keeps-page": (
+        "    c->slot[old] = -1;\n",
+        ""),
+    "cache-hit-not-counted-used": (
+        "if (c->frame_pf[c->slot[p]]) { c->frame_pf[c->slot[p]] = 0; c->pf_used++; }",
+        "if (c->frame_pf[c->slot[p]]) { c->frame_pf[c->slot[p]] = 0; }"),
     "extra-service-term": (
         "complete[i] = start + xfer;",
         "complete[i] = start + xfer + (start > dd[i] ? 1 : 0);"),
@@ -81,6 +93,7 @@ def test_pins_catch_mutant(tmp_path, name):
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_events.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_refresh.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_refresh.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_cache.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
