@@ -272,6 +272,57 @@ int hbf_refresh_drain(hbf_model_t model, int64_t t_from_ns, int64_t t_to_ns, voi
  * synchronising `stream`. */
 int hbf_refresh_pending(hbf_model_t model, uint32_t *host_pending, void *stream);
 
+/* ---- Capacity mode: frame cache and next-page prefetcher (Section "D5:
+ * Capacity": a capacity range is served from a bounded frame cache in HBM,
+ * a miss reads the page from the media; Section "D6: Speculative
+ * Prefetcher": the pages that follow a served fault are fetched too, and
+ * prefetch reads never enter the timing path).  This step decides which
+ * accesses become media reads; a faulting access is then timed like any
+ * other read (e.g. by hbf_time_requests on the faulting accesses).
+ * Reading used here (the paper names no replacement policy or depth):
+ *  - pages are numbered within the capacity range, [0, range_pages);
+ *  - `frames` frames, FIFO replacement: every insertion takes the frame
+ *    filled longest ago, a hit changes nothing;
+ *  - a fault on page p inserts p, then for k = 1 .. prefetch_pages in that
+ *    order while p + k < range_pages, inserts p + k if it is not resident
+ *    at that moment (one prefetch read each);
+ *  - a prefetched page counts as used at its first hit and as unused if it
+ *    is evicted before one.
+ * 1 <= frames < 2^31, prefetch_pages < frames and <= 63,
+ * 1 <= range_pages <= 2^31.  The cache state lives on the current HIP
+ * device and persists across calls until reset. */
+typedef struct hbf_cache *hbf_cache_t;  /* opaque, owned by the library */
+
+/* Create an empty cache (allocates frames*12 + range_pages*4 bytes of device
+ * memory; synchronous). */
+int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pages, hbf_cache_t *out);
+void hbf_cache_destroy(hbf_cache_t cache);
+/* Empty every frame and zero the counters (asynchronous on `stream`). */
+int hbf_cache_reset(hbf_cache_t cache, void *stream);
+
+/* Serve dev_pages[0..n) (uint64 page numbers within the range) in order.
+ * dev_hit[n] (uint8): 1 = the page was resident, 0 = the access faulted.
+ * dev_pf_page / dev_pf_src (both NULL or both set): the first pf_cap
+ * prefetch reads issued by this call, in order: page, and the index of the
+ * faulting access that issued it.  dev_counts (int64[8], device): [0..4]
+ * hits, faults, prefetch reads, prefetched pages used, prefetched pages
+ * evicted unused, all since the last reset; [5] prefetch reads issued by
+ * this call; [6] 0, or HBF_EINVAL if some page was >= range_pages (then
+ * nothing changed and dev_hit is not written); [7] 0.  Asynchronous. */
+int hbf_cache_access(hbf_cache_t cache, const uint64_t *dev_pages, int64_t n, uint8_t *dev_hit,
+                     uint64_t *dev_pf_page, int64_t *dev_pf_src, int64_t pf_cap, int64_t *dev_counts,
+                     void *stream);
+
+/* Many caches over one stream at once (a sweep of frame budgets and
+ * prefetch depths): configuration b has host_frames[b] frames and
+ * host_prefetch[b] prefetch pages, starts empty, and serves all of
+ * dev_pages[0..n).  dev_counts: int64[n_cfg][5], the five counters of
+ * each.  1 <= n_cfg <= 65535.  Allocates the caches' state for the call
+ * and synchronises `stream` before returning; returns HBF_EINVAL if some
+ * page was >= range_pages (counts then all zero). */
+int hbf_cache_sweep(const uint32_t *host_frames, const uint32_t *host_prefetch, int n_cfg, uint64_t range_pages,
+                    const uint64_t *dev_pages, int64_t n, int64_t *dev_counts, void *stream);
+
 /* Wall-clock tick of the delay injection, in picoseconds (10,000 for a
  * 100 MHz counter).  Needs the GPU. */
 int hbf_wall_clock_tick_ps(hbf_model_t model, int64_t *tick_ps);

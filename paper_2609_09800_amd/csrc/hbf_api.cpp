@@ -495,6 +495,141 @@ int hbf_refresh_pending(hbf_model_t m, uint32_t *host_pending, void *stream) {
   return HBF_OK;
 }
 
+// ---- capacity-mode frame cache (Sections D5, D6)
+
+}  // extern "C"
+
+struct hbf_cache {
+  uint32_t F = 0, d = 0;
+  uint64_t R = 0;
+  void *mem = nullptr;         // frames | flags | slots | ctl | cfg | status, n_pf
+  CacheCfg *dcfg = nullptr;
+  int64_t *status = nullptr;   // [0] status, [1] prefetch reads of the call
+};
+
+static bool cache_params_ok(uint32_t F, uint32_t d, uint64_t R) {
+  return F >= 1 && F < (1u << 31) && d < F && d <= CACHE_MAX_PREFETCH && R >= 1 && R <= (uint64_t)N_LIMIT;
+}
+
+// Device state of n caches in one allocation; returns the config array.
+static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, void **mem, CacheCfg **dcfg,
+                       int64_t **status) {
+  size_t o = 0;
+  std::vector<size_t> off(n);
+  for (int b = 0; b < n; b++) {
+    off[b] = o;
+    o = up256(o + (size_t)F[b] * 8);
+    o = up256(o + (size_t)F[b] * 4);
+    o = up256(o + (size_t)R * 4);
+    o = up256(o + sizeof(CacheCtl));
+  }
+  const size_t ocfg = o;
+  o = up256(o + sizeof(CacheCfg) * n);
+  const size_t ost = o;
+  o = up256(o + 16);
+  void *p = nullptr;
+  if (hipMalloc(&p, o) != hipSuccess) return HBF_ENOMEM;
+  char *base = (char *)p;
+  std::vector<CacheCfg> cfg(n);
+  for (int b = 0; b < n; b++) {
+    size_t q = off[b];
+    cfg[b].frame_page = (int64_t *)(base + q);
+    q = up256(q + (size_t)F[b] * 8);
+    cfg[b].frame_pf = (uint32_t *)(base + q);
+    q = up256(q + (size_t)F[b] * 4);
+    cfg[b].slot = (int32_t *)(base + q);
+    q = up256(q + (size_t)R * 4);
+    cfg[b].ctl = (CacheCtl *)(base + q);
+    cfg[b].F = F[b];
+    cfg[b].d = d[b];
+  }
+  if (hipMemcpy(base + ocfg, cfg.data(), sizeof(CacheCfg) * n, hipMemcpyHostToDevice) != hipSuccess) {
+    hipFree(p);
+    return HBF_EHIP;
+  }
+  *mem = p;
+  *dcfg = (CacheCfg *)(base + ocfg);
+  *status = (int64_t *)(base + ost);
+  return HBF_OK;
+}
+
+extern "C" {
+
+int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pages, hbf_cache_t *out) {
+  if (!out || !cache_params_ok(frames, prefetch_pages, range_pages)) return HBF_EINVAL;
+  hbf_cache *c = new (std::nothrow) hbf_cache();
+  if (!c) return HBF_ENOMEM;
+  c->F = frames;
+  c->d = prefetch_pages;
+  c->R = range_pages;
+  int rc = cache_alloc(&c->F, &c->d, 1, c->R, &c->mem, &c->dcfg, &c->status);
+  if (rc) {
+    delete c;
+    return rc;
+  }
+  if (launch_cache_clear(c->dcfg, 1, c->R, c->F, nullptr) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+    hipFree(c->mem);
+    delete c;
+    return HBF_EHIP;
+  }
+  *out = c;
+  return HBF_OK;
+}
+
+void hbf_cache_destroy(hbf_cache_t c) {
+  if (!c) return;
+  hipDeviceSynchronize();
+  hipFree(c->mem);
+  delete c;
+}
+
+int hbf_cache_reset(hbf_cache_t c, void *stream) {
+  if (!c) return HBF_EINVAL;
+  return launch_cache_clear(c->dcfg, 1, c->R, c->F, (hipStream_t)stream) == hipSuccess ? HBF_OK : HBF_EHIP;
+}
+
+int hbf_cache_access(hbf_cache_t c, const uint64_t *pages, int64_t n, uint8_t *hit, uint64_t *pf_page,
+                     int64_t *pf_src, int64_t pf_cap, int64_t *counts, void *stream) {
+  if (!c || !counts || n < 0 || n > N_LIMIT || (n > 0 && (!pages || !hit))) return HBF_EINVAL;
+  if ((pf_page == nullptr) != (pf_src == nullptr) || pf_cap < 0) return HBF_EINVAL;
+  const hipStream_t s = (hipStream_t)stream;
+  if (launch_fill(c->status, 2, 0, s) != hipSuccess) return HBF_EHIP;
+  if (n > 0 && launch_cache_run(c->dcfg, 1, c->R, pages, n, hit, pf_page, pf_src, pf_page ? pf_cap : 0, c->status,
+                                c->status + 1, s) != hipSuccess)
+    return HBF_EHIP;
+  return launch_cache_report(c->dcfg, 1, c->status + 1, c->status, counts, 8, s) == hipSuccess ? HBF_OK
+                                                                                              : HBF_EHIP;
+}
+
+int hbf_cache_sweep(const uint32_t *frames, const uint32_t *prefetch, int n_cfg, uint64_t range_pages,
+                    const uint64_t *pages, int64_t n, int64_t *counts, void *stream) {
+  if (!frames || !prefetch || n_cfg < 1 || n_cfg > 65535 || !counts || n < 0 || n > N_LIMIT || (n > 0 && !pages))
+    return HBF_EINVAL;
+  uint32_t max_f = 0;
+  for (int b = 0; b < n_cfg; b++) {
+    if (!cache_params_ok(frames[b], prefetch[b], range_pages)) return HBF_EINVAL;
+    max_f = std::max(max_f, frames[b]);
+  }
+  void *mem = nullptr;
+  CacheCfg *dcfg = nullptr;
+  int64_t *status = nullptr;
+  int rc = cache_alloc(frames, prefetch, n_cfg, range_pages, &mem, &dcfg, &status);
+  if (rc) return rc;
+  const hipStream_t s = (hipStream_t)stream;
+  bool ok = launch_fill(status, 2, 0, s) == hipSuccess &&
+            launch_cache_clear(dcfg, n_cfg, range_pages, max_f, s) == hipSuccess &&
+            (n == 0 || launch_cache_run(dcfg, n_cfg, range_pages, pages, n, nullptr, nullptr, nullptr, 0, status,
+                                        nullptr, s) == hipSuccess) &&
+            launch_cache_report(dcfg, n_cfg, nullptr, status, counts, 5, s) == hipSuccess;
+  // the temporary state is freed once the sweep has run
+  ok = hipStreamSynchronize(s) == hipSuccess && ok;
+  int64_t st = 0;
+  ok = ok && hipMemcpy(&st, status, 8, hipMemcpyDeviceToHost) == hipSuccess;
+  hipFree(mem);
+  if (!ok) return HBF_EHIP;
+  return st ? (int)st : HBF_OK;
+}
+
 int hbf_gemv_instrumented(hbf_model_t m, const uint16_t *W, int E, int K, int N, const uint16_t *X,
                           int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
                           void *stream) {

@@ -136,6 +136,31 @@ hipError_t launch_layer_done(const CallCtl *ctl, int64_t count, const int64_t *p
 hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
                        int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
                        int64_t tick_ps, DevState *st, hipStream_t s);
+// Capacity-mode frame cache (hbf_cache.hip): per cache, the page held by
+// each frame (-1 empty), a prefetched-and-not-yet-hit flag per frame, the
+// frame holding each page of the range (-1 not resident), the FIFO head and
+// the counters (hits, faults, prefetch reads, prefetched used, evicted
+// unused).
+struct CacheCtl {
+  uint32_t head;
+  uint32_t pad;
+  int64_t count[5];
+};
+struct CacheCfg {
+  int64_t *frame_page;
+  uint32_t *frame_pf;
+  int32_t *slot;
+  CacheCtl *ctl;
+  uint32_t F, d;
+};
+constexpr uint32_t CACHE_MAX_PREFETCH = 63;  // one fault's candidates fit one wave
+hipError_t launch_cache_clear(CacheCfg *dev_cfgs, int n_cfg, uint64_t R, uint32_t max_f, hipStream_t s);
+hipError_t launch_cache_run(const CacheCfg *dev_cfgs, int n_cfg, uint64_t R, const uint64_t *pages, int64_t n,
+                            uint8_t *hit, uint64_t *pf_page, int64_t *pf_src, int64_t pf_cap, int64_t *status,
+                            int64_t *n_pf_out, hipStream_t s);
+hipError_t launch_cache_report(const CacheCfg *dev_cfgs, int n_cfg, const int64_t *n_pf, const int64_t *status,
+                               int64_t *out, int per_cfg, hipStream_t s);
+
 extern const char *const kKernelNames[];
 extern const int kNumTimedKernels;
 

@@ -29,6 +29,7 @@ EXPORTED = [
     "hbf_time_requests", "hbf_time_layers", "hbf_gemv_instrumented", "hbf_wall_clock_tick_ps", "hbf_get_status",
     "hbf_get_state", "hbf_set_state", "hbf_profile", "hbf_kernel_times", "hbf_strerror",
     "hbf_refresh_plan", "hbf_refresh_configure", "hbf_refresh_submit", "hbf_refresh_drain", "hbf_refresh_pending",
+    "hbf_cache_create", "hbf_cache_destroy", "hbf_cache_reset", "hbf_cache_access", "hbf_cache_sweep",
 ]
 REFRESH_PENDING = -1
 
@@ -82,6 +83,11 @@ def load_library(path=LIB_PATH):
         "hbf_refresh_submit": ([vp, vp, i64, vp, vp], i32),
         "hbf_refresh_drain": ([vp, i64, i64, vp], i32),
         "hbf_refresh_pending": ([vp, vp, vp], i32),
+        "hbf_cache_create": ([u32, u32, u64, ctypes.POINTER(vp)], i32),
+        "hbf_cache_destroy": ([vp], None),
+        "hbf_cache_reset": ([vp, vp], i32),
+        "hbf_cache_access": ([vp, vp, i64, vp, vp, vp, i64, vp, vp], i32),
+        "hbf_cache_sweep": ([vp, vp, i32, u64, vp, i64, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -264,6 +270,50 @@ class Model:
         cnt = ctypes.c_int(0)
         _check(self._lib.hbf_kernel_times(self._h, ms, names, 16, ctypes.byref(cnt)), "hbf_kernel_times")
         return [(names[i].decode(), ms[i]) for i in range(cnt.value)]
+
+
+class Cache:
+    """Capacity-mode frame cache with the next-page prefetcher on the current
+    GPU (one C handle; reading in include/hbf.h)."""
+
+    def __init__(self, frames, prefetch_pages, range_pages):
+        self._lib = load_library()
+        h = ctypes.c_void_p()
+        _check(self._lib.hbf_cache_create(frames, prefetch_pages, range_pages, ctypes.byref(h)), "hbf_cache_create")
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self._lib.hbf_cache_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def reset(self, stream=None):
+        return self._lib.hbf_cache_reset(self._h, _sp(stream))
+
+    def access(self, pages, hit, counts, pf_page=None, pf_src=None, stream=None):
+        """pages: int64 device tensor [n] (page numbers); hit: uint8 [n];
+        counts: int64 [8]; pf_page / pf_src: int64 [cap] or None."""
+        cap = 0 if pf_page is None else pf_page.numel()
+        return self._lib.hbf_cache_access(self._h, _dp(pages), pages.numel(), _dp(hit), _dp(pf_page), _dp(pf_src),
+                                          cap, _dp(counts), _sp(stream))
+
+
+def cache_sweep(frames, prefetch, range_pages, pages, counts, stream=None):
+    """Many fresh caches over one stream: frames / prefetch host int lists,
+    pages int64 device tensor, counts int64 device tensor [len(frames), 5]."""
+    import numpy as np
+    lib = load_library()
+    f = np.ascontiguousarray(frames, dtype=np.uint32)
+    d = np.ascontiguousarray(prefetch, dtype=np.uint32)
+    assert f.size == d.size and counts.numel() >= 5 * f.size
+    return lib.hbf_cache_sweep(f.ctypes.data_as(ctypes.c_void_p), d.ctypes.data_as(ctypes.c_void_p), f.size,
+                               range_pages, _dp(pages), pages.numel(), _dp(counts), _sp(stream))
 
 
 def refresh_plan(params, blocks, pages_per_block):

@@ -210,3 +210,19 @@ def test_refresh_plan_matches_reference(lib, oracle_mod, seed):
     class Prm:
         channels, dies_per_channel, planes_per_die = C, D, P
     assert [int(x) for x in out] == oracle_mod.refresh_plan(Prm, blocks, ppb)
+
+
+def test_cache_validation_is_host_side(lib):
+    h = ctypes.c_void_p()
+    for F, d, R in [(0, 0, 8), (4, 4, 8), (100, 64, 8), (1 << 31, 1, 8), (8, 1, 0), (8, 1, (1 << 31) + 1)]:
+        assert lib.hbf_cache_create(F, d, R, ctypes.byref(h)) == -1
+    assert lib.hbf_cache_create(8, 1, 8, None) == -1
+    fake = ctypes.c_void_p(4096)
+    assert lib.hbf_cache_access(None, fake, 1, fake, None, None, 0, fake, None) == -1
+    import numpy as np
+    f = np.array([8, 8], dtype=np.uint32)
+    d = np.array([1, 8], dtype=np.uint32)   # second: prefetch >= frames
+    assert lib.hbf_cache_sweep(f.ctypes.data_as(ctypes.c_void_p), d.ctypes.data_as(ctypes.c_void_p), 2, 64, fake,
+                               10, fake, None) == -1
+    assert lib.hbf_cache_sweep(f.ctypes.data_as(ctypes.c_void_p), d.ctypes.data_as(ctypes.c_void_p), 0, 64, fake,
+                               10, fake, None) == -1

@@ -1,0 +1,146 @@
+"""Capacity-mode frame cache and next-page prefetcher (Sections D5, D6), HIP
+path against the reference model through the C ABI: every hit flag, every
+prefetch read (page and faulting access), the counters, and the sweep of
+many caches over one stream.  Parameters include tight caches (frames =
+prefetch depth + 1) where a fault often evicts one of its own later
+candidates (the in-order replay), the widest prefetch (63 pages), long
+streams spanning many 64-access batches, calls that continue one cache, and
+an out-of-range page.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_09800_amd import hbf
+    hbf.load_library()
+    return t
+
+
+def run_both(torch, F, d, R, calls, what):
+    from oracle import oracle
+    from paper_2609_09800_amd import hbf
+    g = hbf.Cache(F, d, R)
+    o = oracle.OracleCache(F, d, R)
+    for ci, pages in enumerate(calls):
+        pages = np.asarray(pages, dtype=np.int64)
+        n = pages.size
+        say(f"cache {what} F={F} d={d} R={R} call {ci} n={n}")
+        pd = torch.from_numpy(pages).cuda()
+        hit = torch.full((max(n, 1),), 7, dtype=torch.uint8, device="cuda")
+        cap = max(1, n * d)
+        pp = torch.full((cap,), -5, dtype=torch.int64, device="cuda")
+        ps = torch.full((cap,), -5, dtype=torch.int64, device="cuda")
+        cnt = torch.zeros(8, dtype=torch.int64, device="cuda")
+        assert g.access(pd, hit, cnt, pp, ps) == 0
+        c = cnt.cpu().numpy()
+        rc, wh, wp, ws = o.access(pages, pf_cap=cap)
+        assert rc == 0 and c[6] == 0
+        assert np.array_equal(hit.cpu().numpy()[:n], wh), what
+        k = int(c[5])
+        assert k == wp.size, (what, k, wp.size)
+        assert np.array_equal(pp.cpu().numpy()[:k].view(np.uint64), wp), what
+        assert np.array_equal(ps.cpu().numpy()[:k], ws), what
+        assert np.array_equal(c[:5], o.counts()), (what, c[:5], o.counts())
+    g.close()
+
+
+def runs_stream(rng, n, R, max_run=6):
+    pages = []
+    while len(pages) < n:
+        s = int(rng.integers(0, R))
+        pages += [min(s + k, R - 1) for k in range(int(rng.integers(1, max_run)))]
+    return pages[:n]
+
+
+def test_belady_anomaly(torch):
+    from paper_2609_09800_amd import hbf
+    ref = torch.tensor([1, 2, 3, 4, 1, 2, 5, 1, 2, 3, 4, 5], dtype=torch.int64, device="cuda")
+    faults = {}
+    for F in (3, 4):
+        c = hbf.Cache(F, 0, 8)
+        hit = torch.empty(12, dtype=torch.uint8, device="cuda")
+        cnt = torch.zeros(8, dtype=torch.int64, device="cuda")
+        assert c.access(ref, hit, cnt) == 0
+        faults[F] = int(cnt[1])
+        assert int((hit == 0).sum()) == faults[F]
+    assert faults == {3: 9, 4: 10}
+
+
+CASES = [(8, 7, 40), (9, 7, 30), (4, 3, 12), (64, 63, 200), (16, 8, 64), (256, 7, 1033), (1000, 0, 5000),
+         (4096, 31, 1 << 20)]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_random_streams_match_reference(torch, case):
+    F, d, R = CASES[case]
+    rng = np.random.default_rng(60 + case)
+    n = 20000 if R < 10000 else 200000
+    run_both(torch, F, d, R, [runs_stream(rng, n, R, 12)], f"case{case}")
+
+
+def test_calls_continue_one_cache(torch):
+    rng = np.random.default_rng(7)
+    s = runs_stream(rng, 9000, 300, 9)
+    run_both(torch, 32, 7, 300, [s[:100], s[100:101], [], s[101:5000], s[5000:]], "multi-call")
+
+
+def test_moe_expert_stream(torch):
+    """Expert weight pages in layer order (8 pages per expert, 64 experts per
+    layer, a few active per step), 256 frames, prefetch 7: the shape of the
+    paper's prefetcher example."""
+    rng = np.random.default_rng(8)
+    pages = []
+    for step in range(40):
+        for layer in range(4):
+            for e in np.sort(rng.choice(64, 6, replace=False)):
+                base = (layer * 64 + int(e)) * 8
+                pages += list(range(base, base + 8))
+    run_both(torch, 256, 7, 4 * 64 * 8, [pages], "moe")
+
+
+def test_out_of_range_page_changes_nothing(torch):
+    from oracle import oracle
+    from paper_2609_09800_amd import hbf
+    g = hbf.Cache(8, 3, 100)
+    pd = torch.tensor([1, 2, 100, 3], dtype=torch.int64, device="cuda")
+    hit = torch.full((4,), 7, dtype=torch.uint8, device="cuda")
+    cnt = torch.zeros(8, dtype=torch.int64, device="cuda")
+    assert g.access(pd, hit, cnt) == 0
+    c = cnt.cpu().numpy()
+    assert c[6] == -1 and c[:5].sum() == 0 and (hit.cpu().numpy() == 7).all()
+    ok = torch.tensor([1, 2, 3], dtype=torch.int64, device="cuda")
+    assert g.access(ok, hit, cnt) == 0
+    o = oracle.OracleCache(8, 3, 100)
+    o.access([1, 2, 3])
+    assert np.array_equal(cnt.cpu().numpy()[:5], o.counts())
+
+
+def test_sweep_matches_reference(torch):
+    from oracle import oracle
+    from paper_2609_09800_amd import hbf
+    rng = np.random.default_rng(9)
+    R = 3000
+    pages = np.array(runs_stream(rng, 30000, R, 16), dtype=np.int64)
+    frames = [16, 64, 256, 257, 1024, 2999, 3000, 8]
+    pref = [0, 7, 7, 15, 63, 1, 0, 7]
+    say(f"cache sweep: {len(frames)} caches over {pages.size} accesses")
+    cnt = torch.full((len(frames), 5), -9, dtype=torch.int64, device="cuda")
+    assert hbf.cache_sweep(frames, pref, R, torch.from_numpy(pages).cuda(), cnt) == 0
+    got = cnt.cpu().numpy()
+    for b, (F, d) in enumerate(zip(frames, pref)):
+        o = oracle.OracleCache(F, d, R)
+        o.access(pages)
+        assert np.array_equal(got[b], o.counts()), (F, d, got[b], o.counts())
