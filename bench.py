@@ -161,6 +161,62 @@ def refresh_leg(torch, hbf, wl, w, model, addr, issue, complete, reps=3):
                 ms_per_call=ms, requests_per_s=w.n / (ms / 1e3), parity_vs_reference_digest=parity)
 
 
+def capacity_leg(torch, hbf, wl, reps=2):
+    """The capacity row (Sections D5, D6): two config-3 decode steps at batch
+    8 as a capacity-mode stream through one frame cache holding half of the
+    expert set (a step's working set fits, so the second step reuses the
+    first), prefetching 7 pages per fault; then a sweep of 42 caches (frame
+    budgets x prefetch depths) over the same stream, one wave each.  The
+    reference model serves the same stream on the host for parity and for
+    comparison."""
+    from oracle import oracle
+    pages, R = wl.capacity_stream(steps=2, tokens=8)
+    n = int(pages.size)
+    F, d = R // 2, 7
+    pd = torch.from_numpy(pages).cuda()
+    hit = torch.empty(n, dtype=torch.uint8, device="cuda")
+    cnt = torch.zeros(8, dtype=torch.int64, device="cuda")
+    c = hbf.Cache(F, d, R)
+    s = torch.cuda.current_stream()
+    times = []
+    for r in range(reps + 1):
+        c.reset(s)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        assert c.access(pd, hit, cnt, stream=s) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+        if r:
+            times.append(e0.elapsed_time(e1))
+    got = cnt.cpu().numpy()
+    ms = float(np.median(times))
+    oc = oracle.OracleCache(F, d, R)
+    t = time.perf_counter()
+    _, oh, _, _ = oc.access(pages, pf_cap=0)
+    cpu_s = time.perf_counter() - t
+    parity = bool(np.array_equal(got[:5], oc.counts()) and np.array_equal(hit.cpu().numpy(), oh))
+    c.close()
+    fr = [R // 8, R // 4, 3 * R // 8, R // 2, 5 * R // 8, 3 * R // 4]
+    pf = [0, 1, 3, 7, 15, 31, 63]
+    frames = [f for f in fr for _ in pf]
+    pref = [p for _ in fr for p in pf]
+    sc = torch.zeros((len(frames), 5), dtype=torch.int64, device="cuda")
+    t = time.perf_counter()
+    assert hbf.cache_sweep(frames, pref, R, pd, sc, s) == 0
+    sweep_s = time.perf_counter() - t
+    sv = sc.cpu().numpy()
+    h, m, pr, used, unused = (int(x) for x in got[:5])
+    return dict(workload=f"two config-3 decode steps at batch 8 as a capacity stream: {n} accesses over {R} "
+                         f"expert pages, {F} frames (half), prefetch {d} pages per fault",
+                accesses=n, ms_per_call=ms, accesses_per_s=n / (ms / 1e3), hit_share=h / n, faults=m,
+                prefetch_reads=pr, prefetch_used=used, prefetch_evicted_unused=unused,
+                parity_vs_reference=parity, reference_cpu_s=cpu_s, reference_cores=1,
+                sweep=dict(caches=len(frames), seconds=sweep_s,
+                           cache_accesses_per_s=len(frames) * n / sweep_s,
+                           hit_share={f"{f}f/{p}p": float(sv[b, 0] / n) for b, (f, p) in
+                                      enumerate(zip(frames, pref)) if p in (0, 7, 63)}))
+
+
 def cpu_baseline(w, n_sample):
     from oracle import oracle
     m = oracle.OracleModel(**w.params)
@@ -191,6 +247,7 @@ def main():
     ap.add_argument("--no-gemv", action="store_true", help="time only hbf_time_requests (diagnostic)")
     ap.add_argument("--no-closed-loop", action="store_true", help="skip the closed-loop decode report")
     ap.add_argument("--no-refresh", action="store_true", help="skip the refresh-plan report")
+    ap.add_argument("--no-capacity", action="store_true", help="skip the capacity-mode frame cache report")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -333,6 +390,9 @@ def main():
     if not args.no_refresh:
         log("refresh-plan timing")
         out["refresh"] = refresh_leg(torch, hbf, wl, w, model, addr, issue, complete)
+    if not args.no_capacity:
+        log("capacity-mode frame cache timing")
+        out["capacity"] = capacity_leg(torch, hbf, wl)
     if not args.no_cpu:
         log("timing the reference model on the CPU sample")
         out["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, n))

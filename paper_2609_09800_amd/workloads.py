@@ -300,6 +300,20 @@ def config5(seed=0, n=1 << 28):
                     meta=dict(n_kv=n_kv, steps=steps))
 
 
+def capacity_stream(seed=0, steps=1, tokens=64):
+    """Config 3's decode as a capacity-mode stream (Section D5): the expert
+    set (48 x 128 experts x 576 pages) is one capacity range and every
+    access is a page number within it, in program order.  Returns (pages
+    int64, range_pages)."""
+    rng = _rng(seed)
+    router = MoeRouter(rng)
+    out = []
+    for _ in range(steps):
+        pg, _lay = moe_step_pages(router.active(tokens))
+        out.append(pg)
+    return np.concatenate(out).astype(np.int64), MOE_LAYERS * MOE_EXPERTS * PAGES_PER_EXPERT
+
+
 def config5_refresh_blocks(seed=0):
     """A refresh plan for the large mixed stream's device (32 ch x 16 die x
     4 plane), Section D4: epoch 0 makes one block of every plane eligible
