@@ -5,11 +5,13 @@ and are used to pin it (they take the request->resource assignment as given;
 the address mapping is pinned separately):
 
 * :func:`time_stepped` advances a clock 1 ns at a time over the two-station
-  system (die read, then channel transfer).  Within a tick, completions are
-  processed before starts, so a resource freed at t can start a waiting
-  request at t and a page finishing its die read at t can start its channel
-  transfer at t.  Dies serve their queue first come first served by
-  (issue, index); channels by (arrival at the channel, index).
+  system (die read, then channel transfer), optionally with die page-register
+  blocking (a die reads again only once its last page left over the
+  channel).  Within a tick, completions are processed before starts, so a
+  resource freed at t can start a waiting request at t and a page finishing
+  its die read at t can start its channel transfer at t.  Dies serve their
+  queue first come first served by (issue, index); channels by (arrival at
+  the channel, index).
 * :func:`closed_loop_stepped` runs the same 1 ns clock over a layered
   program: the requests of layer l+1 appear compute ticks after the tick
   at which the last request of layer l completed.
@@ -30,11 +32,13 @@ import itertools
 from collections import deque
 
 
-def time_stepped(issue, die_key, chan, t_read, xfer, die_free=None, chan_free=None):
+def time_stepped(issue, die_key, chan, t_read, xfer, die_free=None, chan_free=None, register_blocking=False):
     """Return (die_done, complete) lists; ``None`` entries for die_key < 0.
 
     ``die_free`` / ``chan_free``: dict resource -> time it is busy until
-    (missing = idle since minus infinity).
+    (missing = idle since minus infinity).  ``register_blocking``: a die
+    holds the page it read until the page's channel transfer completes and
+    starts no read meanwhile.
     """
     n = len(issue)
     die_free = dict(die_free or {})
@@ -46,6 +50,7 @@ def time_stepped(issue, die_key, chan, t_read, xfer, die_free=None, chan_free=No
         return die_done, complete
     die_q, chan_q = {}, {}
     die_job, chan_job = {}, {}      # resource -> (request, finish time)
+    held = set()                    # dies whose page register is full
     pending = deque(sorted(live, key=lambda i: (issue[i], i)))
     t = min(issue[i] for i in live)
     left = len(live)
@@ -60,19 +65,22 @@ def time_stepped(issue, die_key, chan, t_read, xfer, die_free=None, chan_free=No
                 del die_job[d]
                 die_done[i] = t
                 chan_q.setdefault(chan[i], []).append((t, i))
+                if register_blocking:
+                    held.add(d)
         # 2. channel completions
         for c, (i, fin) in list(chan_job.items()):
             if fin == t:
                 del chan_job[c]
                 complete[i] = t
                 left -= 1
+                held.discard(die_key[i])
         # 3. arrivals
         while pending and issue[pending[0]] == t:
             i = pending.popleft()
             die_q.setdefault(die_key[i], deque()).append(i)
         # 4. die starts (FCFS by (issue, index): queue order)
         for d, q in die_q.items():
-            if q and d not in die_job and die_free.get(d, t) <= t:
+            if q and d not in die_job and d not in held and die_free.get(d, t) <= t:
                 i = q.popleft()
                 die_job[d] = (i, t + t_read)
         # 5. channel starts (FCFS by (arrival, index))

@@ -31,6 +31,8 @@
  *    ch = p mod C, die = (p / C) mod D, plane = (p / (C*D)) mod P,
  *    pg = p / (C*D*P).
  *  - die queue key = (ch, die); with the plane-parallel flag (ch, die, plane).
+ *  - media variant (flag): die page-register blocking, see
+ *    orc_blocking_stage.
  *  - xfer = ceil(page_bytes * 1e9 / channel_bytes_per_s) in integer ns.
  *  - times are int64 ns; "idle since minus infinity" at create/reset.
  *
@@ -56,6 +58,7 @@
 
 #define ORC_TIME_ERROR    INT64_MIN
 #define ORC_FLAG_PLANE_PARALLEL 1u
+#define ORC_FLAG_REGISTER_BLOCKING 2u
 #define ORC_MAX_RANGES    64
 
 /* Issue times must lie in [0, 2^61); any modeled time reaching 2^62 is an
@@ -110,7 +113,7 @@ int orc_create(const orc_params *p, orc_model **out) {
   if (p->page_bytes == 0) return ORC_EINVAL;
   if (p->t_read_ns < 1 || p->t_read_ns > ORC_SERVICE_LIMIT) return ORC_EINVAL;
   if (p->channel_bytes_per_s == 0) return ORC_EINVAL;
-  if (p->flags & ~ORC_FLAG_PLANE_PARALLEL) return ORC_EINVAL;
+  if (p->flags & ~(ORC_FLAG_PLANE_PARALLEL | ORC_FLAG_REGISTER_BLOCKING)) return ORC_EINVAL;
   if ((uint64_t)p->channels * p->dies_per_channel * p->planes_per_die > 65536u) return ORC_EINVAL;
   /* transfer time: ceil(page_bytes * 1e9 / bytes_per_s), exact integers */
   unsigned __int128 num = (unsigned __int128)p->page_bytes * 1000000000u;
@@ -236,6 +239,81 @@ static int orc_cmp_pair(const void *a, const void *b) {
 static int64_t orc_max(int64_t a, int64_t b) { return a > b ? a : b; }
 
 /*
+ * Media variant: die page-register blocking.  A die queue holds one page
+ * register: a read leaves its page there, and the die's next read may start
+ * only once that page has left the register, i.e. once its channel transfer
+ * has completed.  The channel still serves pages FCFS by (die-done, index).
+ * Each channel and its die queues are simulated in service order: at every
+ * step the pending page with the smallest (die-done, index) among the
+ * channel's die queues is transferred, which frees its die for the next
+ * read (each die queue has at most one page pending).  Refresh claims follow
+ * the same rule as without blocking (a claim adds tQ before the read).
+ * Returns 1 on a time-domain overflow.
+ */
+static int orc_blocking_stage(orc_model *m, const int64_t *issue, int64_t n, int8_t *in, const uint32_t *key,
+                              const uint32_t *chan, int64_t *dd, int64_t *complete, int64_t *df, uint8_t *db,
+                              int64_t *cf, uint8_t *cb, int64_t *claimed, int64_t tQ, int *nomem) {
+  const uint32_t K = m->n_die_keys, C = m->p.channels, Dk = K / C;
+  const int64_t tR = m->p.t_read_ns, xfer = m->xfer_ns;
+  int64_t *start = (int64_t *)calloc((size_t)K + 1, sizeof(int64_t));
+  int64_t *head = (int64_t *)calloc((size_t)K, sizeof(int64_t));
+  int64_t *list = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n ? n : 1));
+  if (!start || !head || !list) { free(start); free(head); free(list); *nomem = 1; return 0; }
+  (void)chan;
+  /* each die queue's requests in index order (= FCFS) */
+  for (int64_t i = 0; i < n; i++)
+    if (in[i]) start[key[i] + 1]++;
+  for (uint32_t k = 0; k < K; k++) start[k + 1] += start[k];
+  for (uint32_t k = 0; k < K; k++) head[k] = start[k];
+  for (int64_t i = 0; i < n; i++)
+    if (in[i]) list[head[key[i]]++] = i;
+  for (uint32_t k = 0; k < K; k++) head[k] = start[k];
+  int overflow = 0;
+  for (uint32_t c = 0; c < C; c++) {
+    /* admit the first request of every die queue of the channel */
+    for (uint32_t k = c * Dk; k < (c + 1) * Dk; k++) {
+      if (head[k] == start[k + 1]) continue;
+      const int64_t i = list[head[k]];
+      int64_t s0 = db[k] ? orc_max(issue[i], df[k]) : issue[i];
+      if (m->fifo && claimed[k] < m->fifo[k].len - m->fifo[k].head) { claimed[k]++; in[i] = 2; s0 += tQ; }
+      dd[i] = s0 + tR;
+      if (dd[i] >= ORC_TIME_LIMIT) overflow = 1;
+    }
+    for (;;) {
+      /* the pending page that reached the channel first: smallest (dd, index) */
+      int64_t best = -1;
+      uint32_t bk = 0;
+      for (uint32_t k = c * Dk; k < (c + 1) * Dk; k++) {
+        if (head[k] == start[k + 1]) continue;
+        const int64_t i = list[head[k]];
+        if (best < 0 || dd[i] < dd[best] || (dd[i] == dd[best] && i < best)) { best = i; bk = k; }
+      }
+      if (best < 0) break;
+      const int64_t s1 = cb[c] ? orc_max(dd[best], cf[c]) : dd[best];
+      complete[best] = s1 + xfer;
+      if (complete[best] >= ORC_TIME_LIMIT) overflow = 1;
+      cf[c] = complete[best];
+      cb[c] = 1;
+      /* the page has left the register: the die may read again */
+      df[bk] = complete[best];
+      db[bk] = 1;
+      head[bk]++;
+      if (head[bk] < start[bk + 1]) {
+        const int64_t i = list[head[bk]];
+        int64_t s0 = orc_max(issue[i], complete[best]);
+        if (m->fifo && claimed[bk] < m->fifo[bk].len - m->fifo[bk].head) { claimed[bk]++; in[i] = 2; s0 += tQ; }
+        dd[i] = s0 + tR;
+        if (dd[i] >= ORC_TIME_LIMIT) overflow = 1;
+      }
+      if (overflow) break;   /* the call fails; the rest does not matter */
+    }
+    if (overflow) break;
+  }
+  free(start); free(head); free(list);
+  return overflow;
+}
+
+/*
  * The timing call.  Steps, in the model's order:
  *  1. validate every issue time (0 <= t < 2^61, nondecreasing in index);
  *  2. classify + map every request;
@@ -275,8 +353,10 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
   uint32_t *chan = (uint32_t *)malloc(sizeof(uint32_t) * n);
   int8_t *in = (int8_t *)malloc(n);
   orc_pair *ord = (orc_pair *)malloc(sizeof(orc_pair) * n);
-  if (!df || !db || !cf || !cb || !dd || !chan || !in || !ord) {
-    free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord);
+  const int blocking = (p->flags & ORC_FLAG_REGISTER_BLOCKING) != 0;
+  uint32_t *key = blocking ? (uint32_t *)malloc(sizeof(uint32_t) * n) : NULL;
+  if (!df || !db || !cf || !cb || !dd || !chan || !in || !ord || (blocking && !key)) {
+    free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord); free(key);
     return ORC_ENOMEM;
   }
   memcpy(df, m->die_free, sizeof(int64_t) * m->n_die_keys);
@@ -287,7 +367,7 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
   /* refresh claims of this call per die queue (committed with the clocks) */
   int64_t *claimed = (int64_t *)calloc(m->n_die_keys, sizeof(int64_t));
   if (!claimed) {
-    free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord);
+    free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord); free(key);
     return ORC_ENOMEM;
   }
   const int64_t tQ = tR + m->t_prog_ns;
@@ -302,6 +382,12 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
     if (r < 0) { in[i] = 0; continue; }
     in[i] = 1;
     orc_loc L = orc_map(m, r, addr[i]);
+    if (blocking) {  /* both stages below, per channel */
+      key[i] = L.key;
+      chan[i] = L.ch;
+      n_in++;
+      continue;
+    }
     int64_t start = db[L.key] ? orc_max(issue[i], df[L.key]) : issue[i];
     if (m->fifo && claimed[L.key] < m->fifo[L.key].len - m->fifo[L.key].head) {
       claimed[L.key]++;
@@ -317,10 +403,17 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
     ord[n_in].idx = i;
     n_in++;
   }
+  int nomem = 0;
+  if (blocking)
+    overflow |= orc_blocking_stage(m, issue, n, in, key, chan, dd, complete, df, db, cf, cb, claimed, tQ, &nomem);
+  if (nomem) {
+    free(claimed); free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord); free(key);
+    return ORC_ENOMEM;
+  }
   /* 4. channel service order: by (die_done, index) */
-  qsort(ord, (size_t)n_in, sizeof(orc_pair), orc_cmp_pair);
+  if (!blocking) qsort(ord, (size_t)n_in, sizeof(orc_pair), orc_cmp_pair);
   /* 5. channel stage */
-  for (int64_t k = 0; k < n_in; k++) {
+  for (int64_t k = 0; !blocking && k < n_in; k++) {
     int64_t i = ord[k].idx;
     uint32_t c = chan[i];
     int64_t start = cb[c] ? orc_max(dd[i], cf[c]) : dd[i];
@@ -351,7 +444,7 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
       }
   }
   free(claimed);
-  free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord);
+  free(df); free(db); free(cf); free(cb); free(dd); free(chan); free(in); free(ord); free(key);
   return rc;
 }
 

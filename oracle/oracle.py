@@ -24,6 +24,7 @@ OK, EINVAL, EALIGN, EOVERLAP, ENOWORKSPACE, EUNSORTED, ERANGE_TIME, EHIP, ENOMEM
     0, -1, -2, -3, -4, -5, -6, -7, -8)
 TIME_ERROR = np.iinfo(np.int64).min
 FLAG_PLANE_PARALLEL = 1
+FLAG_REGISTER_BLOCKING = 2
 
 
 def build(force=False):

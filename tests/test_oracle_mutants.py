@@ -74,6 +74,12 @@ MUTANTS = {
     "cache-hit-not-counted-used": (
         "if (c->frame_pf[c->slot[p]]) { c->frame_pf[c->slot[p]] = 0; c->pf_used++; }",
         "if (c->frame_pf[c->slot[p]]) { c->frame_pf[c->slot[p]] = 0; }"),
+    "blocking-register-freed-at-read-end": (
+        "int64_t s0 = orc_max(issue[i], complete[best]);",
+        "int64_t s0 = orc_max(issue[i], dd[best]);"),
+    "blocking-channel-tie-reversed": (
+        "(dd[i] == dd[best] && i < best)",
+        "(dd[i] == dd[best] && i > best)"),
     "extra-service-term": (
         "complete[i] = start + xfer;",
         "complete[i] = start + xfer + (start > dd[i] ? 1 : 0);"),
@@ -94,6 +100,7 @@ def test_pins_catch_mutant(tmp_path, name):
                         os.path.join(ROOT, "tests", "test_oracle_pins.py"),
                         os.path.join(ROOT, "tests", "test_oracle_events.py"),
                         os.path.join(ROOT, "tests", "test_oracle_refresh.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_cache.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_cache.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_blocking.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
