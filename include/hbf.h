@@ -74,6 +74,14 @@ extern "C" {
 
 /* hbf_params.flags */
 #define HBF_FLAG_PLANE_PARALLEL 1u  /* die queues keyed by (ch, die, plane) */
+/* Media variant: die page-register blocking.  Each die queue holds one page
+ * register: a read leaves its page there, and the die starts no other read
+ * until that page's channel transfer has completed (the page has left the
+ * register).  Channels still serve pages FCFS by (die-done, index).  The
+ * die's clock after a call is its last transfer's completion.  Timed per
+ * channel in service order (one wave per channel): slower than the default
+ * unblocked model, which needs no such order. */
+#define HBF_FLAG_REGISTER_BLOCKING 2u
 
 typedef struct hbf_model *hbf_model_t;  /* opaque, owned by the library */
 

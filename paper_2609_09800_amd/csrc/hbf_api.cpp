@@ -146,7 +146,7 @@ int hbf_model_create(const hbf_params *params, hbf_model_t *out) {
   if (p.page_bytes == 0) return HBF_EINVAL;
   if (p.t_read_ns < 1 || p.t_read_ns > SERVICE_LIMIT) return HBF_EINVAL;
   if (p.channel_bytes_per_s == 0) return HBF_EINVAL;
-  if (p.flags & ~HBF_FLAG_PLANE_PARALLEL) return HBF_EINVAL;
+  if (p.flags & ~(HBF_FLAG_PLANE_PARALLEL | HBF_FLAG_REGISTER_BLOCKING)) return HBF_EINVAL;
   const uint64_t cdp = (uint64_t)p.channels * p.dies_per_channel * p.planes_per_die;
   if (cdp > 65536) return HBF_EINVAL;
   const bool pp = (p.flags & HBF_FLAG_PLANE_PARALLEL) != 0;
@@ -167,6 +167,7 @@ int hbf_model_create(const hbf_params *params, hbf_model_t *out) {
   g.K = (uint32_t)K;
   g.page_bytes = p.page_bytes;
   g.plane_parallel = pp;
+  g.reg_block = (p.flags & HBF_FLAG_REGISTER_BLOCKING) != 0;
   g.pow2 = is_pow2(p.page_bytes) && is_pow2(p.channels) && is_pow2(p.dies_per_channel) &&
            is_pow2(p.planes_per_die);
   g.lg_page = lg2(p.page_bytes);

@@ -1,0 +1,253 @@
+// Media variant: die page-register blocking (the die-read + channel-transfer
+// path of HBFSim, arXiv 2609.09800, Section "Design", with one page register
+// per die queue).  A read leaves its page in the die's register; the die
+// starts no other read until that page's channel transfer has completed.
+// The channel still serves pages first come first served by (die-done,
+// request index).
+//
+// The die and channel stages are now coupled: a die's next read waits on the
+// channel, whose order depends on every die's reads.  A channel and its die
+// queues form an independent system, so one wave runs each channel, one lane
+// per die queue.  Every die queue has at most one page pending at a time;
+// each step transfers the pending page with the smallest (die-done, index)
+// (a wave-wide minimum) and lets its die read its next request.  The
+// die-order request lists come from the unblocked path's die stage (same
+// ranks, same segments).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hbf_internal.h"
+
+namespace hbf {
+
+namespace {
+
+__device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+__device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
+
+// Wave-wide minima with DPP row shifts (within rows of 16 by 1, 2, 4, 8,
+// then row 0 -> 1, 2 -> 3 and rows 0-1 -> 2-3): lane 63 ends with the
+// minimum of all 64 lanes, which readlane broadcasts.  Lanes without a
+// source keep the identity.
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROWMASK, 0xF, false);
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ int64_t dpp_i64(int64_t old, int64_t x) {
+  const uint32_t lo = dpp_u32<CTRL, ROWMASK>((uint32_t)old, (uint32_t)x);
+  const uint32_t hi = dpp_u32<CTRL, ROWMASK>((uint32_t)((uint64_t)old >> 32), (uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+constexpr int SHR1 = 0x111, SHR2 = 0x112, SHR4 = 0x114, SHR8 = 0x118, BC15 = 0x142, BC31 = 0x143;
+
+__device__ __forceinline__ int64_t wave_min64(int64_t x) {
+  x = min64(x, dpp_i64<SHR1, 0xF>(INT64_MAX, x));
+  x = min64(x, dpp_i64<SHR2, 0xF>(INT64_MAX, x));
+  x = min64(x, dpp_i64<SHR4, 0xF>(INT64_MAX, x));
+  x = min64(x, dpp_i64<SHR8, 0xF>(INT64_MAX, x));
+  x = min64(x, dpp_i64<BC15, 0xA>(INT64_MAX, x));
+  x = min64(x, dpp_i64<BC31, 0xC>(INT64_MAX, x));
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), 63);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ uint32_t wave_min32(uint32_t x) {
+  x = min(x, dpp_u32<SHR1, 0xF>(UINT32_MAX, x));
+  x = min(x, dpp_u32<SHR2, 0xF>(UINT32_MAX, x));
+  x = min(x, dpp_u32<SHR4, 0xF>(UINT32_MAX, x));
+  x = min(x, dpp_u32<SHR8, 0xF>(UINT32_MAX, x));
+  x = min(x, dpp_u32<BC15, 0xA>(UINT32_MAX, x));
+  x = min(x, dpp_u32<BC31, 0xC>(UINT32_MAX, x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+}  // namespace
+
+// Per lane, the die queue's upcoming requests (index, issue time) wait in an
+// LDS ring of RING entries, refilled CHUNK_R at a time for every lane at once
+// (one round trip for the indices, one for the issue times), so a step
+// reads LDS only.  Completions (and the completion times of claimed refresh
+// quanta) are staged in LDS and written out OUTB at a time by the whole
+// wave, so a step issues no global memory operation either.
+constexpr int RING = 32;
+constexpr int CHUNK_R = 16;
+constexpr int RSTRIDE = RING + 1;   // padded: lanes' rings start in different banks
+constexpr int OUTB = 256;           // staged completions per write-out
+constexpr int QB = 64;              // staged quantum completions per write-out
+
+// One wave per channel (blockIdx.x); lane j = die queue c*Dk + j.
+//   DDw / IX: die-ordered request indices (packed word's low half when the
+//   cell shift is <= 32, else IX); seg_start / totals: each die queue's run.
+//   ref: refresh quanta pending (each die queue's first ref_pend admissions
+//   claim one, tQ before the read; the quantum's completion is written).
+__global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DDw, const uint32_t *__restrict__ IX,
+                                                 const int64_t *__restrict__ issue,
+                                                 const uint32_t *__restrict__ seg_start,
+                                                 const uint32_t *__restrict__ totals, Geo g, DevState *st,
+                                                 CallCtl *ctl, int64_t *__restrict__ complete,
+                                                 int64_t *__restrict__ dfnew, int64_t *__restrict__ cfnew, int ref) {
+  __shared__ uint32_t ring_idx[64 * RSTRIDE];
+  __shared__ int64_t ring_iss[64 * RSTRIDE];
+  __shared__ uint32_t out_idx[OUTB];
+  __shared__ int64_t out_cpl[OUTB];
+  __shared__ uint32_t q_die[QB], q_rank[QB];
+  __shared__ int64_t q_val[QB];
+  if (__hip_atomic_load(&ctl->err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+  const uint32_t c = blockIdx.x, lane = __lane_id(), Dk = g.Dk;
+  const bool on = lane < Dk;
+  const uint32_t k = c * Dk + (on ? lane : 0);
+  const bool narrow = ctl->shift <= 32;
+  const int64_t tR = g.tR, tQ = g.tQ, xfer = g.xfer;
+  const uint32_t total = on ? totals[k] : 0;
+  const uint32_t base = on ? seg_start[k] : 0;
+  const uint32_t R = (on && ref) ? st->ref_pend[k] : 0;
+  uint32_t err = 0;
+
+  auto lds_sync = [&]() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  // request indices: the low half of each packed die-order word, or IX
+  const uint32_t *ixs = narrow ? reinterpret_cast<const uint32_t *>(DDw) : IX;
+  const uint32_t ixstride = narrow ? 2u : 1u;
+  uint32_t loaded = 0;     // requests of this die queue copied into the ring
+  uint32_t admitted = 0;   // requests whose read has been scheduled
+  // every lane with room tops its ring up by CHUNK_R requests (wave-uniform call)
+  auto refill = [&]() {
+    const bool go = on && loaded < total && loaded - admitted <= (uint32_t)(RING - CHUNK_R);
+    uint32_t ix[CHUNK_R];
+    int64_t is[CHUNK_R];
+    // unconditional loads (entry 0 stands in for the unused ones) so that
+    // all of them are in flight at once
+#pragma unroll
+    for (int j = 0; j < CHUNK_R; j++) {
+      const uint32_t r = loaded + j;
+      ix[j] = ixs[(go && r < total) ? (size_t)(base + r) * ixstride : 0];
+    }
+#pragma unroll
+    for (int j = 0; j < CHUNK_R; j++) {
+      const uint32_t r = loaded + j;
+      is[j] = issue[(go && r < total) ? ix[j] : 0u];
+    }
+#pragma unroll
+    for (int j = 0; j < CHUNK_R; j++) {
+      const uint32_t r = loaded + j;
+      if (go && r < total) {
+        ring_idx[lane * RSTRIDE + r % RING] = ix[j];
+        ring_iss[lane * RSTRIDE + r % RING] = is[j];
+      }
+    }
+    if (go) loaded = min(total, loaded + CHUNK_R);
+    lds_sync();
+  };
+
+  uint32_t nout = 0, nq = 0;   // staged completions / quantum completions (uniform)
+  auto flush_out = [&]() {     // wave-uniform
+    lds_sync();
+    for (uint32_t j = lane; j < nout; j += 64) complete[out_idx[j]] = out_cpl[j];
+    nout = 0;
+    lds_sync();
+  };
+  auto flush_q = [&]() {       // wave-uniform
+    lds_sync();
+    for (uint32_t j = lane; j < nq; j += 64) {
+      const uint32_t kk = q_die[j];
+      *st->ref_slot[st->ref_off[kk] + st->ref_head[kk] + q_rank[j]] = q_val[j];
+    }
+    nq = 0;
+    lds_sync();
+  };
+
+  int64_t dd = INT64_MAX;  // die-done of the pending page
+  uint32_t pidx = UINT32_MAX;
+  int64_t free_at = on ? st->die_free[k] : NEG;  // NEG: idle since minus infinity
+  // the die reads its next request; returns whether it claimed a quantum
+  auto admit = [&]() -> bool {
+    const uint32_t sl = lane * RSTRIDE + admitted % RING;
+    const bool claim = admitted < R;
+    int64_t s0 = max64(ring_iss[sl], free_at);
+    if (claim) s0 += tQ;
+    dd = s0 + tR;
+    pidx = ring_idx[sl];
+    if (dd >= TIME_LIMIT) err |= ERR_OVERFLOW;
+    admitted++;
+    return claim;
+  };
+  refill();
+  {  // every die queue's first read; claims staged in lane order
+    const bool cl = total ? admit() : false;
+    const uint64_t cm = __ballot(cl);
+    if (cl) {
+      const uint32_t slot = (uint32_t)__popcll(cm & ((1ull << lane) - 1));
+      q_die[slot] = k;
+      q_rank[slot] = 0;
+      q_val[slot] = dd - tR;
+    }
+    nq = (uint32_t)__popcll(cm);
+    if (nq) flush_q();
+  }
+
+  uint32_t left = total;             // not yet transferred
+  int64_t cfree = st->chan_free[c];  // NEG: idle since minus infinity
+  bool any = false;
+  for (;;) {
+    const int64_t key = left ? dd : INT64_MAX;
+    const int64_t m = wave_min64(key);
+    if (m == INT64_MAX) break;
+    const bool tie = left && dd == m;
+    const uint64_t tied = __ballot(tie);
+    // several pages reached the channel at the same time: the lowest request
+    // index goes first.  The reduction runs on every lane (a collective must
+    // not sit behind a per-lane condition); the branch on `tied` is uniform.
+    const bool several = __popcll(tied) > 1;
+    const uint32_t first = several ? wave_min32(tie ? pidx : UINT32_MAX) : 0u;
+    const bool win = tie && (!several || pidx == first);
+    const int64_t cpl = max64(m, cfree) + xfer;
+    cfree = cpl;
+    any = true;
+    if (win) {
+      out_idx[nout] = pidx;
+      out_cpl[nout] = cpl;
+      left--;
+      free_at = cpl;  // the page has left the register
+    }
+    if (cpl >= TIME_LIMIT) err |= on ? ERR_OVERFLOW : 0u;
+    if (++nout == OUTB) flush_out();
+    // the winner's next request must be in its ring; top rings up early
+    if (__ballot(win && left && loaded - admitted < 4)) refill();
+    bool cl = false;
+    if (win && left) cl = admit();
+    if (__ballot(cl)) {   // at most the winner
+      if (cl) {
+        q_die[nq] = k;
+        q_rank[nq] = admitted - 1;
+        q_val[nq] = dd - tR;
+      }
+      if (++nq == QB) flush_q();
+    }
+  }
+  if (nout) flush_out();
+  if (nq) flush_q();
+  if (on && total) dfnew[k] = free_at;
+  if (lane == 0) {
+    cfnew[c] = cfree;
+    if (any) atomicMax((long long *)&ctl->max_cpl, (long long)cfree);
+  }
+  if (__ballot(err != 0)) {
+    uint32_t e = err;
+    for (int d = 32; d >= 1; d >>= 1) e |= (uint32_t)__shfl_xor((int)e, d);
+    if (lane == 0) atomicOr(&ctl->err, e);
+  }
+}
+
+hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue,
+                           const uint32_t *seg_start, const uint32_t *totals, DevState *st, CallCtl *ctl,
+                           int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref, hipStream_t s) {
+  hipLaunchKernelGGL(k_regblock, dim3(g.C), dim3(64), 0, s, DDw, IX, issue, seg_start, totals, g, st, ctl, complete,
+                     dfnew, cfnew, ref ? 1 : 0);
+  return hipGetLastError();
+}
+
+}  // namespace hbf

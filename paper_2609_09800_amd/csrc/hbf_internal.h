@@ -68,6 +68,8 @@ struct Geo {
   uint32_t lg_tR;     // floor(log2(tR)): bucket width of the channel merge
   int64_t tR, xfer;
   int64_t tQ;         // die time of one refresh quantum (tR + tPROG), 0 if unset
+  uint32_t reg_block; // media variant: die page-register blocking
+  uint32_t pad;
 };
 
 // Persistent device state of a model.  Refresh quanta pending at die queue
@@ -123,6 +125,10 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
                                 DevState *st, const uint64_t *addr, const int64_t *issue,
                                 int64_t *complete, hipStream_t s, hipEvent_t *ev, int n_ev,
                                 bool refresh);
+// Register-blocking channel stage (hbf_blocking.hip): one wave per channel.
+hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue,
+                           const uint32_t *seg_start, const uint32_t *totals, DevState *st, CallCtl *ctl,
+                           int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref, hipStream_t s);
 hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s);
 hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
 hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, const uint64_t *addr,

@@ -1599,7 +1599,15 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
-  {
+  if (g.reg_block) {
+    // media variant: the channel stage simulated per channel in service
+    // order (timed in the first channel-stage slot)
+    if ((e = launch_regblock(g, (const uint64_t *)DD, IX, issue, seg, totals, st, ctl, complete, dfnew, cfnew,
+                             refresh, s)) != hipSuccess)
+      return e;
+    mark();
+    mark();
+  } else {
     // channel stage: enough one-wave blocks to fill the chip, a multiple of
     // the XCD count, and no more than there can be cells
     int dev = 0, ncu = 256, per_cu = 0;

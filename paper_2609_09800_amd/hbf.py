@@ -22,6 +22,7 @@ HBF_EHIP = -7
 HBF_ENOMEM = -8
 HBF_TIME_ERROR = -(1 << 63)
 HBF_FLAG_PLANE_PARALLEL = 1
+HBF_FLAG_REGISTER_BLOCKING = 2
 
 EXPORTED = [
     "hbf_model_create", "hbf_model_destroy", "hbf_xfer_ns", "hbf_n_die_queues", "hbf_model_reset",
