@@ -217,6 +217,61 @@ def capacity_leg(torch, hbf, wl, reps=2):
                                       enumerate(zip(frames, pref)) if p in (0, 7, 63)}))
 
 
+def blocking_leg(torch, hbf, wl, w, addr, issue, complete, reps=2):
+    """The media-variant row: die page-register blocking (a die reads again
+    only once its last page has crossed the channel).  The large mixed
+    stream is timed on a blocking model and checked against the reference
+    digest; config 2's stream is timed and checked against the reference
+    model on the host."""
+    from oracle import oracle
+    s = torch.cuda.current_stream()
+
+    def timed(model, a, i, c):
+        ts = []
+        for r in range(reps + 1):
+            model.reset(s)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            assert model.time_requests(a, i, c, s) == 0
+            e1.record(s)
+            torch.cuda.synchronize()
+            if r:
+                ts.append(e0.elapsed_time(e1))
+        assert model.get_status() == 0
+        return float(np.median(ts))
+
+    m5 = hbf.Model(**dict(w.params, flags=hbf.HBF_FLAG_REGISTER_BLOCKING))
+    for b, nb in w.ranges:
+        assert m5.register_range(b, nb)[0] == 0
+    ms5 = timed(m5, addr, issue, complete)
+    parity5 = None
+    gold_p = os.path.join(ROOT, "tests", "golden", "oracle_digests.json")
+    if w.n == 1 << 28 and os.path.exists(gold_p):
+        gold = json.load(open(gold_p)).get("config5_blocking")
+        if gold:
+            parity5 = sha(complete.cpu().numpy()) == gold["complete_sha256"]
+    m5.close()
+    w2 = wl.config2()
+    p2 = dict(w2.params, flags=hbf.HBF_FLAG_REGISTER_BLOCKING)
+    m2 = hbf.Model(**p2)
+    o2 = oracle.OracleModel(**p2)
+    for b, nb in w2.ranges:
+        assert m2.register_range(b, nb)[0] == 0 and o2.register_range(b, nb) == 0
+    a2 = torch.from_numpy(w2.addr.view(np.int64)).cuda()
+    i2 = torch.from_numpy(w2.issue).cuda()
+    c2 = torch.empty_like(i2)
+    ms2 = timed(m2, a2, i2, c2)
+    t = time.perf_counter()
+    rc, want = o2.time_requests(w2.addr, w2.issue)
+    cpu2 = time.perf_counter() - t
+    parity2 = rc == 0 and bool(np.array_equal(c2.cpu().numpy(), want))
+    return dict(variant="die page-register blocking",
+                large=dict(requests=int(w.n), ms_per_call=ms5, requests_per_s=w.n / (ms5 / 1e3),
+                           parity_vs_reference_digest=parity5),
+                config2=dict(requests=int(w2.n), ms_per_call=ms2, requests_per_s=w2.n / (ms2 / 1e3),
+                             parity_vs_reference=parity2, reference_cpu_s=cpu2, reference_cores=1))
+
+
 def cpu_baseline(w, n_sample):
     from oracle import oracle
     m = oracle.OracleModel(**w.params)
@@ -248,6 +303,7 @@ def main():
     ap.add_argument("--no-closed-loop", action="store_true", help="skip the closed-loop decode report")
     ap.add_argument("--no-refresh", action="store_true", help="skip the refresh-plan report")
     ap.add_argument("--no-capacity", action="store_true", help="skip the capacity-mode frame cache report")
+    ap.add_argument("--no-blocking", action="store_true", help="skip the register-blocking report")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -393,6 +449,9 @@ def main():
     if not args.no_capacity:
         log("capacity-mode frame cache timing")
         out["capacity"] = capacity_leg(torch, hbf, wl)
+    if not args.no_blocking:
+        log("register-blocking timing")
+        out["register_blocking"] = blocking_leg(torch, hbf, wl, w, addr, issue, complete)
     if not args.no_cpu:
         log("timing the reference model on the CPU sample")
         out["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, n))

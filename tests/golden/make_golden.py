@@ -1,6 +1,7 @@
 """Write tests/golden/oracle_digests.json: SHA-256 digests of the reference
 model's outputs on the seeded workloads (configs 1, 2, 3 and 5, and config
-5 with a refresh plan pending: argument "5r").
+5 with a refresh plan pending: argument "5r"; config 5 with die
+page-register blocking: "5b").
 
 Calls only ``oracle/`` and the input generators; nothing here comes from
 the HIP path.  Usage:  python tests/golden/make_golden.py [config ...]
@@ -75,6 +76,24 @@ def digest_refresh():
     return rec
 
 
+def digest_blocking():
+    """The large mixed stream with die page-register blocking (flag 2)."""
+    w = wl.config5()
+    params = dict(w.params, flags=2)
+    m = oracle.OracleModel(**params)
+    for b, n in w.ranges:
+        assert m.register_range(b, n) == 0
+    t = time.time()
+    rc, c = m.time_requests(w.addr, w.issue)
+    to = time.time() - t
+    assert rc == 0
+    d, ch = m.state()
+    rec = dict(n=w.n, complete_sha256=sha(c), die_free_sha256=sha(d), chan_free_sha256=sha(ch),
+               max_complete=int(c.max()), oracle_s=round(to, 1))
+    print("config5_blocking", rec, flush=True)
+    return rec
+
+
 def main(cfgs):
     data = json.load(open(OUT)) if os.path.exists(OUT) else {}
     data["_comment"] = ("SHA-256 of the reference model's outputs (int64 little endian) on the "
@@ -82,10 +101,12 @@ def main(cfgs):
     for c in cfgs:
         if c == "5r":
             data["config5_refresh"] = digest_refresh()
+        elif c == "5b":
+            data["config5_blocking"] = digest_blocking()
         else:
             data[f"config{c}"] = digest(int(c))
         json.dump(data, open(OUT, "w"), indent=1, sort_keys=True)
 
 
 if __name__ == "__main__":
-    main(sys.argv[1:] or ["1", "2", "3", "5", "5r"])
+    main(sys.argv[1:] or ["1", "2", "3", "5", "5r", "5b"])

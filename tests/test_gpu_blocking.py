@@ -150,3 +150,40 @@ def test_closed_loop_with_blocking(torch):
     assert rc == 0
     assert np.array_equal(iss.cpu().numpy(), wi) and np.array_equal(c.cpu().numpy(), wc)
     assert np.array_equal(d.cpu().numpy(), wd)
+
+
+def test_large_mixed_stream_blocking_digest(torch):
+    """2^28 requests of the large mixed stream with blocking, against the
+    digest the reference model wrote (tests/golden/make_golden.py 5b)."""
+    import hashlib
+    import json
+    import os
+    from paper_2609_09800_amd import hbf
+
+    def sha(*arrays):
+        h = hashlib.sha256()
+        for a in arrays:
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()
+
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "oracle_digests.json")))
+    gold = gold["config5_blocking"]
+    say(f"config5 + blocking: generating {gold['n']} requests")
+    w = wl.config5()
+    g = hbf.Model(**dict(w.params, flags=BLOCK))
+    for b, nb in w.ranges:
+        assert g.register_range(b, nb)[0] == 0
+    a = dev(torch, w.addr)
+    i = dev(torch, w.issue)
+    del w
+    c = torch.empty_like(i)
+    say("config5 + blocking: timing on the GPU")
+    assert g.time_requests(a, i, c) == 0
+    assert g.get_status() == 0
+    del a, i
+    got = c.cpu().numpy()
+    assert int(got.max()) == gold["max_complete"]
+    assert sha(got) == gold["complete_sha256"]
+    d, ch = g.get_state()
+    assert sha(d) == gold["die_free_sha256"] and sha(ch) == gold["chan_free_sha256"]
+    g.close()
