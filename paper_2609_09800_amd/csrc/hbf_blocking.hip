@@ -64,25 +64,43 @@ __device__ __forceinline__ uint32_t wave_min32(uint32_t x) {
 
 }  // namespace
 
+// Issue times in die order, so that each die queue's requests are two
+// contiguous runs (indices, issue times) for the sequential stage.
+__global__ __launch_bounds__(256) void k_regblock_gather(const uint64_t *__restrict__ DDw,
+                                                         const uint32_t *__restrict__ IX,
+                                                         const int64_t *__restrict__ issue,
+                                                         int64_t *__restrict__ issue_do, int64_t n,
+                                                         const CallCtl *ctl) {
+  if (__hip_atomic_load(&ctl->err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+  const bool narrow = ctl->shift <= 32;
+  const int64_t m = ctl->n_in;
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < m && p < n; p += (int64_t)gridDim.x * 256) {
+    const uint32_t ix = narrow ? (uint32_t)DDw[p] : IX[p];
+    issue_do[p] = issue[ix];
+  }
+}
+
 // Per lane, the die queue's upcoming requests (index, issue time) wait in an
-// LDS ring of RING entries, refilled CHUNK_R at a time for every lane at once
-// (one round trip for the indices, one for the issue times), so a step
-// reads LDS only.  Completions (and the completion times of claimed refresh
-// quanta) are staged in LDS and written out OUTB at a time by the whole
-// wave, so a step issues no global memory operation either.
-constexpr int RING = 32;
-constexpr int CHUNK_R = 16;
+// LDS ring of RING entries.  The next CHUNK_R of them are always in flight
+// in registers: a top-up writes them to the ring and starts loading the
+// following CHUNK_R, so their memory latency overlaps the steps in between
+// and a step reads LDS only.  Completions (and the completion times of
+// claimed refresh quanta) are staged in LDS and written out by the whole
+// wave, OUTB at a time.
+constexpr int RING = 64;
+constexpr int CHUNK_R = 32;
 constexpr int RSTRIDE = RING + 1;   // padded: lanes' rings start in different banks
 constexpr int OUTB = 256;           // staged completions per write-out
 constexpr int QB = 64;              // staged quantum completions per write-out
 
 // One wave per channel (blockIdx.x); lane j = die queue c*Dk + j.
 //   DDw / IX: die-ordered request indices (packed word's low half when the
-//   cell shift is <= 32, else IX); seg_start / totals: each die queue's run.
-//   ref: refresh quanta pending (each die queue's first ref_pend admissions
-//   claim one, tQ before the read; the quantum's completion is written).
+//   cell shift is <= 32, else IX); issue_do: their issue times; seg_start /
+//   totals: each die queue's run.  ref: refresh quanta pending (each die
+//   queue's first ref_pend admissions claim one, tQ before the read; the
+//   quantum's completion is written).
 __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DDw, const uint32_t *__restrict__ IX,
-                                                 const int64_t *__restrict__ issue,
+                                                 const int64_t *__restrict__ issue_do,
                                                  const uint32_t *__restrict__ seg_start,
                                                  const uint32_t *__restrict__ totals, Geo g, DevState *st,
                                                  CallCtl *ctl, int64_t *__restrict__ complete,
@@ -102,6 +120,8 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
   const uint32_t total = on ? totals[k] : 0;
   const uint32_t base = on ? seg_start[k] : 0;
   const uint32_t R = (on && ref) ? st->ref_pend[k] : 0;
+  int64_t free_at = on ? st->die_free[k] : NEG;  // NEG: idle since minus infinity
+  int64_t cfree = st->chan_free[c];              // NEG: idle since minus infinity
   uint32_t err = 0;
 
   auto lds_sync = [&]() {
@@ -112,34 +132,35 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
   // request indices: the low half of each packed die-order word, or IX
   const uint32_t *ixs = narrow ? reinterpret_cast<const uint32_t *>(DDw) : IX;
   const uint32_t ixstride = narrow ? 2u : 1u;
-  uint32_t loaded = 0;     // requests of this die queue copied into the ring
+  uint32_t loaded = 0;     // requests of this die queue written to the ring
   uint32_t admitted = 0;   // requests whose read has been scheduled
-  // every lane with room tops its ring up by CHUNK_R requests (wave-uniform call)
-  auto refill = [&]() {
+  uint32_t nix[CHUNK_R];   // in flight: requests loaded .. loaded + CHUNK_R - 1
+  int64_t nis[CHUNK_R];
+  auto fetch = [&]() {     // per lane: start loading the chunk after `loaded`
+#pragma unroll
+    for (int j = 0; j < CHUNK_R; j++) {
+      const uint32_t r = loaded + j;
+      const bool v = on && r < total;
+      nix[j] = ixs[v ? (size_t)(base + r) * ixstride : 0];
+      nis[j] = issue_do[v ? base + r : 0];
+    }
+  };
+  // wave-uniform: every lane whose ring has room for the chunk in flight
+  // writes it and starts the next one
+  auto top_up = [&]() {
     const bool go = on && loaded < total && loaded - admitted <= (uint32_t)(RING - CHUNK_R);
-    uint32_t ix[CHUNK_R];
-    int64_t is[CHUNK_R];
-    // unconditional loads (entry 0 stands in for the unused ones) so that
-    // all of them are in flight at once
+    if (go) {
 #pragma unroll
-    for (int j = 0; j < CHUNK_R; j++) {
-      const uint32_t r = loaded + j;
-      ix[j] = ixs[(go && r < total) ? (size_t)(base + r) * ixstride : 0];
-    }
-#pragma unroll
-    for (int j = 0; j < CHUNK_R; j++) {
-      const uint32_t r = loaded + j;
-      is[j] = issue[(go && r < total) ? ix[j] : 0u];
-    }
-#pragma unroll
-    for (int j = 0; j < CHUNK_R; j++) {
-      const uint32_t r = loaded + j;
-      if (go && r < total) {
-        ring_idx[lane * RSTRIDE + r % RING] = ix[j];
-        ring_iss[lane * RSTRIDE + r % RING] = is[j];
+      for (int j = 0; j < CHUNK_R; j++) {
+        const uint32_t r = loaded + j;
+        if (r < total) {
+          ring_idx[lane * RSTRIDE + r % RING] = nix[j];
+          ring_iss[lane * RSTRIDE + r % RING] = nis[j];
+        }
       }
+      loaded = min(total, loaded + CHUNK_R);
+      fetch();
     }
-    if (go) loaded = min(total, loaded + CHUNK_R);
     lds_sync();
   };
 
@@ -162,7 +183,6 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
 
   int64_t dd = INT64_MAX;  // die-done of the pending page
   uint32_t pidx = UINT32_MAX;
-  int64_t free_at = on ? st->die_free[k] : NEG;  // NEG: idle since minus infinity
   // the die reads its next request; returns whether it claimed a quantum
   auto admit = [&]() -> bool {
     const uint32_t sl = lane * RSTRIDE + admitted % RING;
@@ -175,7 +195,8 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     admitted++;
     return claim;
   };
-  refill();
+  fetch();
+  top_up();
   {  // every die queue's first read; claims staged in lane order
     const bool cl = total ? admit() : false;
     const uint64_t cm = __ballot(cl);
@@ -188,9 +209,9 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     nq = (uint32_t)__popcll(cm);
     if (nq) flush_q();
   }
+  top_up();   // second chunk into the ring, third in flight
 
   uint32_t left = total;             // not yet transferred
-  int64_t cfree = st->chan_free[c];  // NEG: idle since minus infinity
   bool any = false;
   for (;;) {
     const int64_t key = left ? dd : INT64_MAX;
@@ -215,8 +236,8 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     }
     if (cpl >= TIME_LIMIT) err |= on ? ERR_OVERFLOW : 0u;
     if (++nout == OUTB) flush_out();
-    // the winner's next request must be in its ring; top rings up early
-    if (__ballot(win && left && loaded - admitted < 4)) refill();
+    // the winner's next request must be in its ring
+    if (__ballot(win && left && loaded - admitted < 8)) top_up();
     bool cl = false;
     if (win && left) cl = admit();
     if (__ballot(cl)) {   // at most the winner
@@ -243,10 +264,17 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
 }
 
 hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue,
-                           const uint32_t *seg_start, const uint32_t *totals, DevState *st, CallCtl *ctl,
-                           int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref, hipStream_t s) {
-  hipLaunchKernelGGL(k_regblock, dim3(g.C), dim3(64), 0, s, DDw, IX, issue, seg_start, totals, g, st, ctl, complete,
-                     dfnew, cfnew, ref ? 1 : 0);
+                           int64_t *issue_do, int64_t n, const uint32_t *seg_start, const uint32_t *totals,
+                           DevState *st, CallCtl *ctl, int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref,
+                           hipStream_t s) {
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_regblock_gather, dim3((uint32_t)blocks), dim3(256), 0, s, DDw, IX, issue, issue_do, n, ctl);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_regblock, dim3(g.C), dim3(64), 0, s, DDw, IX, issue_do, seg_start, totals, g, st, ctl,
+                     complete, dfnew, cfnew, ref ? 1 : 0);
   return hipGetLastError();
 }
 

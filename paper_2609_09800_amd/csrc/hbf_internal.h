@@ -112,6 +112,7 @@ struct Layout {
   size_t off_totals, off_seg, off_dfnew, off_cfnew;
   size_t off_dd, off_ix, off_kr, off_lb;
   size_t off_cagg, off_cgin;  // per (channel, time cell): aggregate, entering term
+  size_t off_iss;             // register blocking: issue times in die order (n int64)
   size_t total;
 };
 
@@ -127,8 +128,9 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
                                 bool refresh);
 // Register-blocking channel stage (hbf_blocking.hip): one wave per channel.
 hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue,
-                           const uint32_t *seg_start, const uint32_t *totals, DevState *st, CallCtl *ctl,
-                           int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref, hipStream_t s);
+                           int64_t *issue_do, int64_t n, const uint32_t *seg_start, const uint32_t *totals,
+                           DevState *st, CallCtl *ctl, int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref,
+                           hipStream_t s);
 hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s);
 hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
 hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, const uint64_t *addr,

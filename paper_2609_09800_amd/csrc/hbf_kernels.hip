@@ -1602,8 +1602,8 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   if (g.reg_block) {
     // media variant: the channel stage simulated per channel in service
     // order (timed in the first channel-stage slot)
-    if ((e = launch_regblock(g, (const uint64_t *)DD, IX, issue, seg, totals, st, ctl, complete, dfnew, cfnew,
-                             refresh, s)) != hipSuccess)
+    if ((e = launch_regblock(g, (const uint64_t *)DD, IX, issue, (int64_t *)(ws + Lo.off_iss), Lo.n, seg, totals,
+                             st, ctl, complete, dfnew, cfnew, refresh, s)) != hipSuccess)
       return e;
     mark();
     mark();
