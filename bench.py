@@ -205,6 +205,24 @@ def capacity_leg(torch, hbf, wl, reps=2):
     assert hbf.cache_sweep(frames, pref, R, pd, sc, s) == 0
     sweep_s = time.perf_counter() - t
     sv = sc.cpu().numpy()
+    # caches small enough to live in LDS (the prefetcher example's scale:
+    # hundreds of frames), many at once
+    frs = [64, 128, 256, 512, 1024, 2048, 4096]
+    pfs = [0, 1, 2, 3, 5, 7, 11, 15, 23, 31, 47, 63]
+    sframes = [f for f in frs for p in pfs if p < f]
+    spref = [p for f in frs for p in pfs if p < f]
+    ssc = torch.zeros((len(sframes), 5), dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    assert hbf.cache_sweep(sframes, spref, R, pd, ssc, s) == 0
+    small_s = time.perf_counter() - t
+    ssv = ssc.cpu().numpy()
+    o256 = oracle.OracleCache(256, 7, R)
+    t = time.perf_counter()
+    o256.access(pages, pf_cap=0)
+    cpu256 = time.perf_counter() - t
+    b256 = [b for b, (f, p) in enumerate(zip(sframes, spref)) if (f, p) == (256, 7)][0]
+    small_parity = bool(np.array_equal(ssv[b256], o256.counts()))
     h, m, pr, used, unused = (int(x) for x in got[:5])
     return dict(workload=f"two config-3 decode steps at batch 8 as a capacity stream: {n} accesses over {R} "
                          f"expert pages, {F} frames (half), prefetch {d} pages per fault",
@@ -214,7 +232,12 @@ def capacity_leg(torch, hbf, wl, reps=2):
                 sweep=dict(caches=len(frames), seconds=sweep_s,
                            cache_accesses_per_s=len(frames) * n / sweep_s,
                            hit_share={f"{f}f/{p}p": float(sv[b, 0] / n) for b, (f, p) in
-                                      enumerate(zip(frames, pref)) if p in (0, 7, 63)}))
+                                      enumerate(zip(frames, pref)) if p in (0, 7, 63)}),
+                small_sweep=dict(caches=len(sframes), frames=frs, prefetch=pfs, seconds=small_s,
+                                 cache_accesses_per_s=len(sframes) * n / small_s,
+                                 reference_cpu_s_one_cache_256f_7p=cpu256, parity_256f_7p=small_parity,
+                                 hit_share_7p={str(f): float(ssv[b, 0] / n) for b, (f, p) in
+                                               enumerate(zip(sframes, spref)) if p == 7}))
 
 
 def blocking_leg(torch, hbf, wl, w, addr, issue, complete, reps=2):

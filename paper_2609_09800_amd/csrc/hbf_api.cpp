@@ -507,6 +507,7 @@ struct hbf_cache {
   void *mem = nullptr;         // frames | flags | slots | ctl | cfg | status, n_pf
   CacheCfg *dcfg = nullptr;
   int64_t *status = nullptr;   // [0] status, [1] prefetch reads of the call
+  int *dids = nullptr;
 };
 
 static bool cache_params_ok(uint32_t F, uint32_t d, uint64_t R) {
@@ -515,16 +516,18 @@ static bool cache_params_ok(uint32_t F, uint32_t d, uint64_t R) {
 
 // Device state of n caches in one allocation; returns the config array.
 static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, void **mem, CacheCfg **dcfg,
-                       int64_t **status) {
+                       int64_t **status, int **dids) {
   size_t o = 0;
   std::vector<size_t> off(n);
   for (int b = 0; b < n; b++) {
     off[b] = o;
     o = up256(o + (size_t)F[b] * 8);
     o = up256(o + (size_t)F[b] * 4);
-    o = up256(o + (size_t)R * 4);
+    o = up256(o + (F[b] > CACHE_LDS_MAX ? (size_t)R * 4 : 0));
     o = up256(o + sizeof(CacheCtl));
   }
+  const size_t oids = o;
+  o = up256(o + sizeof(int) * n);
   const size_t ocfg = o;
   o = up256(o + sizeof(CacheCfg) * n);
   const size_t ost = o;
@@ -539,19 +542,28 @@ static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, 
     q = up256(q + (size_t)F[b] * 8);
     cfg[b].frame_pf = (uint32_t *)(base + q);
     q = up256(q + (size_t)F[b] * 4);
-    cfg[b].slot = (int32_t *)(base + q);
-    q = up256(q + (size_t)R * 4);
+    cfg[b].slot = F[b] > CACHE_LDS_MAX ? (int32_t *)(base + q) : nullptr;
+    q = up256(q + (F[b] > CACHE_LDS_MAX ? (size_t)R * 4 : 0));
     cfg[b].ctl = (CacheCtl *)(base + q);
     cfg[b].F = F[b];
     cfg[b].d = d[b];
   }
-  if (hipMemcpy(base + ocfg, cfg.data(), sizeof(CacheCfg) * n, hipMemcpyHostToDevice) != hipSuccess) {
+  // cache ids grouped: the LDS-resident ones first, then the others
+  std::vector<int> ids;
+  for (int b = 0; b < n; b++)
+    if (F[b] <= CACHE_LDS_MAX) ids.push_back(b);
+  for (int b = 0; b < n; b++)
+    if (F[b] > CACHE_LDS_MAX) ids.push_back(b);
+  if (hipMemcpy(base + ocfg, cfg.data(), sizeof(CacheCfg) * n, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(base + oids, ids.data(), sizeof(int) * n, hipMemcpyHostToDevice) != hipSuccess ||
+      cache_set_lds_limit() != hipSuccess) {
     hipFree(p);
     return HBF_EHIP;
   }
   *mem = p;
   *dcfg = (CacheCfg *)(base + ocfg);
   *status = (int64_t *)(base + ost);
+  *dids = (int *)(base + oids);
   return HBF_OK;
 }
 
@@ -564,7 +576,7 @@ int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pa
   c->F = frames;
   c->d = prefetch_pages;
   c->R = range_pages;
-  int rc = cache_alloc(&c->F, &c->d, 1, c->R, &c->mem, &c->dcfg, &c->status);
+  int rc = cache_alloc(&c->F, &c->d, 1, c->R, &c->mem, &c->dcfg, &c->status, &c->dids);
   if (rc) {
     delete c;
     return rc;
@@ -596,8 +608,8 @@ int hbf_cache_access(hbf_cache_t c, const uint64_t *pages, int64_t n, uint8_t *h
   if ((pf_page == nullptr) != (pf_src == nullptr) || pf_cap < 0) return HBF_EINVAL;
   const hipStream_t s = (hipStream_t)stream;
   if (launch_fill(c->status, 2, 0, s) != hipSuccess) return HBF_EHIP;
-  if (n > 0 && launch_cache_run(c->dcfg, 1, c->R, pages, n, hit, pf_page, pf_src, pf_page ? pf_cap : 0, c->status,
-                                c->status + 1, s) != hipSuccess)
+  if (n > 0 && launch_cache_run(c->dcfg, c->dids, 1, c->F <= CACHE_LDS_MAX, c->F, c->R, pages, n, hit, pf_page,
+                                pf_src, pf_page ? pf_cap : 0, c->status, c->status + 1, s) != hipSuccess)
     return HBF_EHIP;
   return launch_cache_report(c->dcfg, 1, c->status + 1, c->status, counts, 8, s) == hipSuccess ? HBF_OK
                                                                                               : HBF_EHIP;
@@ -615,14 +627,30 @@ int hbf_cache_sweep(const uint32_t *frames, const uint32_t *prefetch, int n_cfg,
   void *mem = nullptr;
   CacheCfg *dcfg = nullptr;
   int64_t *status = nullptr;
-  int rc = cache_alloc(frames, prefetch, n_cfg, range_pages, &mem, &dcfg, &status);
+  int *dids = nullptr;
+  int rc = cache_alloc(frames, prefetch, n_cfg, range_pages, &mem, &dcfg, &status, &dids);
   if (rc) return rc;
   const hipStream_t s = (hipStream_t)stream;
+  int n_lds = 0;
+  uint32_t max_lds = 0, max_big = 0;
+  for (int b = 0; b < n_cfg; b++) {
+    if (frames[b] <= CACHE_LDS_MAX) {
+      n_lds++;
+      max_lds = std::max(max_lds, frames[b]);
+    } else {
+      max_big = std::max(max_big, frames[b]);
+    }
+  }
   bool ok = launch_fill(status, 2, 0, s) == hipSuccess &&
-            launch_cache_clear(dcfg, n_cfg, range_pages, max_f, s) == hipSuccess &&
-            (n == 0 || launch_cache_run(dcfg, n_cfg, range_pages, pages, n, nullptr, nullptr, nullptr, 0, status,
-                                        nullptr, s) == hipSuccess) &&
-            launch_cache_report(dcfg, n_cfg, nullptr, status, counts, 5, s) == hipSuccess;
+            launch_cache_clear(dcfg, n_cfg, range_pages, max_f, s) == hipSuccess;
+  // one launch for the LDS-resident caches, one for the others (both queued)
+  if (ok && n > 0 && n_lds > 0)
+    ok = launch_cache_run(dcfg, dids, n_lds, true, max_lds, range_pages, pages, n, nullptr, nullptr, nullptr, 0,
+                          status, nullptr, s) == hipSuccess;
+  if (ok && n > 0 && n_lds < n_cfg)
+    ok = launch_cache_run(dcfg, dids + n_lds, n_cfg - n_lds, false, max_big, range_pages, pages, n, nullptr, nullptr,
+                          nullptr, 0, status, nullptr, s) == hipSuccess;
+  ok = ok && launch_cache_report(dcfg, n_cfg, nullptr, status, counts, 5, s) == hipSuccess;
   // the temporary state is freed once the sweep has run
   ok = hipStreamSynchronize(s) == hipSuccess && ok;
   int64_t st = 0;

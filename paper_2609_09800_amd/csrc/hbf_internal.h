@@ -162,10 +162,17 @@ struct CacheCfg {
   uint32_t F, d;
 };
 constexpr uint32_t CACHE_MAX_PREFETCH = 63;  // one fault's candidates fit one wave
+// Caches of up to this many frames run with their whole state in LDS (a hash
+// of the resident pages); larger ones keep a page -> frame table in memory.
+constexpr uint32_t CACHE_LDS_MAX = 4096;
 hipError_t launch_cache_clear(CacheCfg *dev_cfgs, int n_cfg, uint64_t R, uint32_t max_f, hipStream_t s);
-hipError_t launch_cache_run(const CacheCfg *dev_cfgs, int n_cfg, uint64_t R, const uint64_t *pages, int64_t n,
-                            uint8_t *hit, uint64_t *pf_page, int64_t *pf_src, int64_t pf_cap, int64_t *status,
-                            int64_t *n_pf_out, hipStream_t s);
+// cfg_ids: the caches to run (device, n_cfg entries); every one of them has
+// F <= CACHE_LDS_MAX when lds is set, else F > CACHE_LDS_MAX.  max_f: their
+// largest frame count.
+hipError_t launch_cache_run(const CacheCfg *dev_cfgs, const int *cfg_ids, int n_cfg, bool lds, uint32_t max_f,
+                            uint64_t R, const uint64_t *pages, int64_t n, uint8_t *hit, uint64_t *pf_page,
+                            int64_t *pf_src, int64_t pf_cap, int64_t *status, int64_t *n_pf_out, hipStream_t s);
+hipError_t cache_set_lds_limit();
 hipError_t launch_cache_report(const CacheCfg *dev_cfgs, int n_cfg, const int64_t *n_pf, const int64_t *status,
                                int64_t *out, int per_cfg, hipStream_t s);
 

@@ -4,8 +4,9 @@ prefetch read (page and faulting access), the counters, and the sweep of
 many caches over one stream.  Parameters include tight caches (frames =
 prefetch depth + 1) where a fault often evicts one of its own later
 candidates (the in-order replay), the widest prefetch (63 pages), long
-streams spanning many 64-access batches, calls that continue one cache, and
-an out-of-range page.
+streams spanning many 64-access batches, calls that continue one cache, an
+out-of-range page, and both homes of the cache state (LDS up to 4,096 frames,
+device memory above).
 """
 import sys
 
@@ -79,8 +80,10 @@ def test_belady_anomaly(torch):
     assert faults == {3: 9, 4: 10}
 
 
+# up to 4,096 frames the cache lives in LDS (hash of resident pages); above,
+# in device memory (page -> frame table)
 CASES = [(8, 7, 40), (9, 7, 30), (4, 3, 12), (64, 63, 200), (16, 8, 64), (256, 7, 1033), (1000, 0, 5000),
-         (4096, 31, 1 << 20)]
+         (4096, 31, 1 << 20), (1, 0, 5), (2, 1, 3), (4097, 7, 12000), (6000, 63, 9000), (20000, 15, 1 << 20)]
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
@@ -134,8 +137,8 @@ def test_sweep_matches_reference(torch):
     rng = np.random.default_rng(9)
     R = 3000
     pages = np.array(runs_stream(rng, 30000, R, 16), dtype=np.int64)
-    frames = [16, 64, 256, 257, 1024, 2999, 3000, 8]
-    pref = [0, 7, 7, 15, 63, 1, 0, 7]
+    frames = [16, 64, 256, 257, 1024, 2999, 3000, 8, 4096, 4097, 2500]
+    pref = [0, 7, 7, 15, 63, 1, 0, 7, 31, 31, 63]
     say(f"cache sweep: {len(frames)} caches over {pages.size} accesses")
     cnt = torch.full((len(frames), 5), -9, dtype=torch.int64, device="cuda")
     assert hbf.cache_sweep(frames, pref, R, torch.from_numpy(pages).cuda(), cnt) == 0
