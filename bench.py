@@ -295,6 +295,49 @@ def blocking_leg(torch, hbf, wl, w, addr, issue, complete, reps=2):
                              parity_vs_reference=parity2, reference_cpu_s=cpu2, reference_cores=1))
 
 
+def gemv_leg(torch, hbf, wl, sets=16, reps=3):
+    """Row a5's bandwidth with no delay injected: the 8-expert grouped GEMV
+    (8 x [768 x 2048] bf16, 24 MiB) over `sets` distinct weight sets in turn
+    (16 x 24 MiB = 384 MiB, more than the 256 MB MALL, so the weights come
+    from HBM), at batch 1, 4 and 16.  Bytes = weights + activations +
+    outputs; peak 8 TB/s."""
+    page = 16384
+    W, _ = wl.config4_operands(batch=1)
+    E, N, K = W.shape
+    wbytes = W.nbytes
+    buf = torch.empty(sets * wbytes + page, dtype=torch.uint8, device="cuda")
+    off = (-buf.data_ptr()) % page
+    Wall = buf[off:off + sets * wbytes].view(torch.int16).view(sets, E, N, K)
+    for k in range(sets):
+        Wk, _ = wl.config4_operands(seed=100 + k, batch=1)
+        Wall[k].copy_(torch.from_numpy(Wk.view(np.int16)))
+    gm = hbf.Model(**wl.geometry(16, 8, 4))
+    assert gm.register_range(Wall.data_ptr(), sets * wbytes)[0] == 0
+    s = torch.cuda.current_stream()
+    out = {}
+    for B in (1, 4, 16):
+        _, X = wl.config4_operands(batch=B)
+        Xd = torch.from_numpy(X.view(np.int16)).cuda()
+        Yd = torch.empty((E, B, N), dtype=torch.float32, device="cuda")
+        for k in range(sets):  # warm-up
+            assert gm.gemv_instrumented(Wall[k], Xd, Yd, stream=s) == 0
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            for k in range(sets):
+                gm.gemv_instrumented(Wall[k], Xd, Yd, stream=s)
+        e1.record(s)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / (reps * sets)
+        nbytes = wbytes + X.nbytes + E * B * N * 4
+        gbps = nbytes / (ms / 1e3) / 1e9
+        out[f"batch{B}"] = dict(us_per_call=ms * 1e3, GBps=gbps, frac_of_hbm_peak=gbps / HBM_PEAK_GBPS,
+                                TFLOPs=2 * E * B * N * K / (ms / 1e3) / 1e12)
+    assert gm.get_status() == 0
+    return dict(workload=f"8 experts x [768 x 2048] bf16 per call, {sets} weight sets rotated "
+                         f"({sets * wbytes >> 20} MiB), no injected delay", **out)
+
+
 def cpu_baseline(w, n_sample):
     from oracle import oracle
     m = oracle.OracleModel(**w.params)
@@ -472,6 +515,9 @@ def main():
     if not args.no_capacity:
         log("capacity-mode frame cache timing")
         out["capacity"] = capacity_leg(torch, hbf, wl)
+    if not args.no_gemv:
+        log("GEMV bandwidth, no delay")
+        out["gemv_bandwidth"] = gemv_leg(torch, hbf, wl)
     if not args.no_blocking:
         log("register-blocking timing")
         out["register_blocking"] = blocking_leg(torch, hbf, wl, w, addr, issue, complete)

@@ -11,7 +11,8 @@
 // involved, so no clock origins are mixed.
 //
 // Y[e][b][n] = sum_k X[e][b][k] * W[e][n][k], bf16 inputs, fp32 accumulate.
-// Bandwidth bound (B flop per weight byte): plain FMA, no matrix cores.
+// Bandwidth bound (B flop per weight byte): packed bf16 dot instructions
+// (two products per instruction, fp32 accumulate), no matrix cores.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -24,18 +25,19 @@ constexpr int GEMV_MAXV = 8;  // 16-byte weight vectors held per lane
 // reported (HBF_ERANGE_TIME) so that a bad time array can never stall the GPU.
 constexpr int64_t MAX_PAGE_DELAY_NS = 1000000000;
 
-__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
+__device__ __forceinline__ float dot2(uint32_t w, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, x), acc,
+                                         false);
+}
+
+// 8 bf16 products summed in fp32 (four packed two-product dot instructions)
 __device__ __forceinline__ float dot8(uint4 w, uint4 x) {
-  float s = bf16_lo(w.x) * bf16_lo(x.x);
-  s = fmaf(bf16_hi(w.x), bf16_hi(x.x), s);
-  s = fmaf(bf16_lo(w.y), bf16_lo(x.y), s);
-  s = fmaf(bf16_hi(w.y), bf16_hi(x.y), s);
-  s = fmaf(bf16_lo(w.z), bf16_lo(x.z), s);
-  s = fmaf(bf16_hi(w.z), bf16_hi(x.z), s);
-  s = fmaf(bf16_lo(w.w), bf16_lo(x.w), s);
-  s = fmaf(bf16_hi(w.w), bf16_hi(x.w), s);
+  float s = dot2(w.x, x.x, 0.0f);
+  s = dot2(w.y, x.y, s);
+  s = dot2(w.z, x.z, s);
+  s = dot2(w.w, x.w, s);
   return s;
 }
 
@@ -114,11 +116,114 @@ __global__ __launch_bounds__(256) void k_gemv_instrumented(
   }
 }
 
+// Transposing butterfly over the 64 lanes of a wave on C values per lane:
+// at the step with lane distance O a lane keeps the upper half of its values
+// if bit O of its lane index is set, the lower half if not, and adds the
+// partner's copy of the half it keeps.  Once one value is left, the
+// remaining steps are a plain xor reduction.  Afterwards every lane holds the
+// wave sum of value index (lane >> (6 - log2 C)).
+template <int C, int O>
+__device__ __forceinline__ void butterfly(float *val, int lane) {
+  if constexpr (O >= 1) {
+    if constexpr (C > 1) {
+      constexpr int H = C / 2;
+      const bool upper = (lane & O) != 0;
+#pragma unroll
+      for (int i = 0; i < H; i++) {
+        const float keep = upper ? val[i + H] : val[i];
+        const float send = upper ? val[i] : val[i + H];
+        val[i] = keep + __shfl_xor(send, O);
+      }
+      butterfly<H, O / 2>(val, lane);
+    } else {
+      val[0] += __shfl_xor(val[0], O);
+      butterfly<1, O / 2>(val, lane);
+    }
+  }
+}
+
+// The same operation for the expert shape of the MoE workloads (K = 2048,
+// 16 KiB pages of 4 rows) at batch BB = 1, 2, 4, 8 or 16.  Thread t of the
+// page's block holds the 16-byte column slice t of all 4 rows and of every
+// activation row, so each activation vector is read once per block (not once
+// per row) and feeds 4 dot products.  The activations are loaded right after
+// the page, before the wait.  The 4*BB partial sums of a lane are reduced
+// across the wave by a transposing butterfly (63 exchanges for 64 values
+// instead of 6 per value), then across the 4 waves through LDS.  (Blocks of
+// 2 or 4 pages, sharing one activation load, measured slower at every batch:
+// fewer blocks in flight.)
+template <int BB>
+__global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__ W, int N,
+                                                    const uint16_t *__restrict__ X, float *__restrict__ Y,
+                                                    const int64_t *__restrict__ pi, const int64_t *__restrict__ pc,
+                                                    int64_t *__restrict__ meas, int64_t tick_ps, DevState *st) {
+  constexpr int K = 2048, R = 4, V = R * BB;
+  constexpr int LGV = V == 4 ? 2 : V == 8 ? 3 : V == 16 ? 4 : V == 32 ? 5 : 6;
+  __shared__ float red[4][64];
+  const int q = blockIdx.x;
+  const int row0 = q * R;
+  const int e = row0 / N;
+  const int nb = row0 - e * N;
+  const int t = threadIdx.x, w = t >> 6, lane = t & 63;
+
+  int64_t d = 0;
+  if (pi) {
+    d = pc[q] - pi[q];
+    if (d < 0) d = 0;
+    if (d > MAX_PAGE_DELAY_NS) {
+      d = MAX_PAGE_DELAY_NS;
+      if (t == 0) atomicOr(&st->sticky, ERR_RANGE_TIME);
+    }
+  }
+  const uint64_t ticks = (uint64_t)((d * 1000 + tick_ps - 1) / tick_ps);
+
+  // ---- issue: clock, then every load of this page, then the activations
+  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  uint4 v[R];
+#pragma unroll
+  for (int r = 0; r < R; r++) v[r] = *(const uint4 *)(W + (size_t)(row0 + r) * K + (size_t)t * 8);
+  const uint16_t *xe = X + (size_t)e * BB * K + (size_t)t * 8;
+  uint4 xv[BB];
+#pragma unroll
+  for (int b = 0; b < BB; b++) xv[b] = *(const uint4 *)(xe + (size_t)b * K);
+
+  // ---- consumption point: wait for the modeled completion
+  uint64_t now = __builtin_amdgcn_s_memrealtime();
+  while (now - t0 < ticks) {
+    __builtin_amdgcn_s_sleep(1);
+    now = __builtin_amdgcn_s_memrealtime();
+  }
+  if (meas && t == 0) meas[q] = (int64_t)((now - t0) * (uint64_t)tick_ps / 1000);
+
+  // ---- consume: value index r*BB + b
+  float val[V];
+#pragma unroll
+  for (int b = 0; b < BB; b++)
+#pragma unroll
+    for (int r = 0; r < R; r++) val[r * BB + b] = dot8(v[r], xv[b]);
+  butterfly<V, 32>(val, lane);
+  red[w][lane] = val[0];
+  __syncthreads();
+  // the lane holding value index i has i's bits in its top log2(V) bits
+  if (t < V) {
+    const int src = t << (6 - LGV);
+    const float sum = red[0][src] + red[1][src] + red[2][src] + red[3][src];
+    const int r = t / BB, b = t - r * BB;
+    Y[((size_t)e * BB + b) * N + nb + r] = sum;
+  }
+}
+
 hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
                        int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
                        int64_t tick_ps, DevState *st, hipStream_t s) {
   const int R = page_bytes / (2 * K);
   const int64_t pages = (int64_t)E * N / R;
+  if (K == 2048 && R == 4 && (B == 1 || B == 2 || B == 4 || B == 8 || B == 16)) {
+    auto kfn = B == 1 ? k_gemv_k2048<1> : B == 2 ? k_gemv_k2048<2> : B == 4 ? k_gemv_k2048<4>
+             : B == 8 ? k_gemv_k2048<8> : k_gemv_k2048<16>;
+    hipLaunchKernelGGL(kfn, dim3((uint32_t)pages), dim3(256), 0, s, W, N, X, Y, pi, pc, meas, tick_ps, st);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(k_gemv_instrumented, dim3((uint32_t)pages), dim3(256), 0, s, W, K, N, R, X, B, Y, pi,
                      pc, meas, tick_ps, st);
   return hipGetLastError();
