@@ -283,8 +283,8 @@ int hbf_refresh_pending(hbf_model_t model, uint32_t *host_pending, void *stream)
 /* ---- Capacity mode: frame cache and next-page prefetcher (Section "D5:
  * Capacity": a capacity range is served from a bounded frame cache in HBM,
  * a miss reads the page from the media; Section "D6: Speculative
- * Prefetcher": the pages that follow a served fault are fetched too, and
- * prefetch reads never enter the timing path).  This step decides which
+ * Prefetcher": once a fault is served, the next pages are read ahead,
+ * and prefetch reads never enter the timing path).  This step decides which
  * accesses become media reads; a faulting access is then timed like any
  * other read (e.g. by hbf_time_requests on the faulting accesses).
  * Reading used here (the paper names no replacement policy or depth):
@@ -301,8 +301,8 @@ int hbf_refresh_pending(hbf_model_t model, uint32_t *host_pending, void *stream)
  * device and persists across calls until reset. */
 typedef struct hbf_cache *hbf_cache_t;  /* opaque, owned by the library */
 
-/* Create an empty cache (allocates frames*12 + range_pages*4 bytes of device
- * memory; synchronous). */
+/* Create an empty cache (allocates frames*12 bytes of device memory for up
+ * to 4,096 frames, range_pages*8 + frames*2 bytes above; synchronous). */
 int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pages, hbf_cache_t *out);
 void hbf_cache_destroy(hbf_cache_t cache);
 /* Empty every frame and zero the counters (asynchronous on `stream`). */

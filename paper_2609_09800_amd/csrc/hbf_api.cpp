@@ -521,9 +521,14 @@ static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, 
   std::vector<size_t> off(n);
   for (int b = 0; b < n; b++) {
     off[b] = o;
-    o = up256(o + (size_t)F[b] * 8);
-    o = up256(o + (size_t)F[b] * 4);
-    o = up256(o + (F[b] > CACHE_LDS_MAX ? (size_t)R * 4 : 0));
+    if (F[b] <= CACHE_LDS_MAX) {  // frame pages and flags
+      o = up256(o + (size_t)F[b] * 8);
+      o = up256(o + (size_t)F[b] * 4);
+    } else {  // latest insertion per page, two flags per frame
+      o = up256(o + (size_t)R * 8);
+      o = up256(o + (size_t)F[b]);
+      o = up256(o + (size_t)F[b]);
+    }
     o = up256(o + sizeof(CacheCtl));
   }
   const size_t oids = o;
@@ -538,12 +543,20 @@ static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, 
   std::vector<CacheCfg> cfg(n);
   for (int b = 0; b < n; b++) {
     size_t q = off[b];
-    cfg[b].frame_page = (int64_t *)(base + q);
-    q = up256(q + (size_t)F[b] * 8);
-    cfg[b].frame_pf = (uint32_t *)(base + q);
-    q = up256(q + (size_t)F[b] * 4);
-    cfg[b].slot = F[b] > CACHE_LDS_MAX ? (int32_t *)(base + q) : nullptr;
-    q = up256(q + (F[b] > CACHE_LDS_MAX ? (size_t)R * 4 : 0));
+    cfg[b] = CacheCfg{};
+    if (F[b] <= CACHE_LDS_MAX) {
+      cfg[b].frame_page = (int64_t *)(base + q);
+      q = up256(q + (size_t)F[b] * 8);
+      cfg[b].frame_pf = (uint32_t *)(base + q);
+      q = up256(q + (size_t)F[b] * 4);
+    } else {
+      cfg[b].pins = (int64_t *)(base + q);
+      q = up256(q + (size_t)R * 8);
+      cfg[b].fpf = (uint8_t *)(base + q);
+      q = up256(q + (size_t)F[b]);
+      cfg[b].fhit = (uint8_t *)(base + q);
+      q = up256(q + (size_t)F[b]);
+    }
     cfg[b].ctl = (CacheCtl *)(base + q);
     cfg[b].F = F[b];
     cfg[b].d = d[b];

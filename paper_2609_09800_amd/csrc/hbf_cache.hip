@@ -11,14 +11,11 @@
 // order while p + k < range_pages, each p + k not resident at that moment.
 //
 // The outcome of an access depends on every earlier one, so one wave runs
-// one cache over the stream.  It takes the accesses 64 at a time: all 64
-// look their pages up at once; every access before the first fault is a
-// hit (hits change nothing); the fault's insertions are done by up to d+1
-// lanes at once (FIFO slots are head, head+1, ...); the accesses after it
-// look up again.  A fault whose insertion would evict one of its own later
-// candidates (which was resident when the fault began) is replayed by one
-// lane in order.  Many caches -- a sweep over frame budgets and prefetch
-// depths -- run as independent waves.
+// one cache over the stream, 64 accesses per round; many caches -- a sweep
+// over frame budgets and prefetch depths -- run as independent waves.
+// Caches of up to CACHE_LDS_MAX frames keep their whole state in LDS;
+// larger ones keep, in device memory, the number of each page's latest
+// insertion (under FIFO, residency is a window over the insertion count).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -30,20 +27,23 @@ namespace {
 
 __device__ __forceinline__ uint32_t lane_no() { return __lane_id(); }
 
+// Device-memory accesses of the cache state, as global (not flat)
+// instructions: a flat access also counts against the LDS wait counter, so
+// every later LDS wait would wait for it too.
+template <typename T>
+using gptr = __attribute__((address_space(1))) T *;
 template <typename T>
 __device__ __forceinline__ T ld(const T *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load((gptr<const T>)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 template <typename T>
 __device__ __forceinline__ void st(T *p, T v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store((gptr<T>)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ uint32_t take_flag(uint32_t *p) {
-  return __hip_atomic_exchange(p, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void wave_fence() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "agent");
+__device__ __forceinline__ void lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 __device__ __forceinline__ int64_t read_lane(int64_t v, uint32_t l) {
   const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, (int)l);
@@ -66,137 +66,270 @@ __global__ __launch_bounds__(256) void k_cache_clear(CacheCfg *cfgs, uint64_t R)
   const CacheCfg c = cfgs[blockIdx.y];
   const uint64_t t = (uint64_t)blockIdx.x * 256 + threadIdx.x, stride = (uint64_t)gridDim.x * 256;
   for (uint64_t f = t; f < c.F; f += stride) {
-    c.frame_page[f] = -1;
-    c.frame_pf[f] = 0;
+    if (c.frame_page) {
+      c.frame_page[f] = -1;
+      c.frame_pf[f] = 0;
+    } else {
+      c.fpf[f] = 0;
+      c.fhit[f] = 0;
+    }
   }
-  if (c.slot)
-    for (uint64_t q = t; q < R; q += stride) c.slot[q] = -1;
+  if (c.pins)
+    for (uint64_t q = t; q < R; q += stride) c.pins[q] = PINS_NEVER;
   if (t == 0) {
     c.ctl->head = 0;
     for (int k = 0; k < 5; k++) c.ctl->count[k] = 0;
+    c.ctl->ins = 0;
+    c.ctl->pend = 0;
   }
 }
 
-// One wave per cache (cache cfg_ids[blockIdx.x], or blockIdx.x).  hit:
-// per-access flags of cache b at hit + b * n (nullable); the prefetch list
-// (nullable) is kept for cache 0.
+// ---- caches of more than CACHE_LDS_MAX frames: state in device memory
+//
+// With FIFO replacement the resident pages are exactly the last F pages
+// inserted (a page is inserted only when absent, so those F are distinct):
+// after I insertions, the page of insertion x is resident iff x >= I - F.
+// The state is therefore the number of each page's latest insertion (pins,
+// PINS_NEVER if none) and the counter I; insertion x fills frame x mod F,
+// which keeps two flags (prefetched; hit since then), and eviction needs no
+// bookkeeping of its own.  One wave runs one cache, 64 accesses per round:
+//  - one gather of the pins of the round's pages; one of the candidates
+//    (p+1 .. p+d) of the pages that miss at the start of the round; the
+//    flags of the frames the round may refill, copied to LDS;
+//  - the faults are then resolved in order inside the wave: a fault's
+//    candidate k is inserted iff its latest insertion is below
+//    I + c_k - F, with c_k the insertions of this fault before it (the
+//    page itself first).  The condition is monotone in the set of
+//    insertions, so iterating it from the candidates absent at the start
+//    reaches the sequential answer in a few steps.  Later lanes and later
+//    candidates see the round's insertions through a per-round list of
+//    (page, first insertion, inserted-candidate mask);
+//  - a page that becomes absent during the round (evicted by its own
+//    round) loads its candidates when it faults.
+// Evicting insertion x - F while inserting x counts a prefetched page
+// evicted unused when its frame's flags say prefetched and not hit; the
+// prefetched pages used are the prefetch reads minus those evicted unused
+// minus those still resident and never hit (k_cache_pending).
+constexpr int SNAP_CHUNK = 256;        // frame flags copied per chunk
+constexpr int SNAP_MAX = 64 * 64;      // insertions in one round: 64 faults x (1 + 63 candidates)
+
 __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ cfgs, const int *cfg_ids, uint64_t R,
                                                   const uint64_t *__restrict__ pages, int64_t n,
                                                   uint8_t *__restrict__ hit, uint64_t *__restrict__ pf_page,
                                                   int64_t *__restrict__ pf_src, int64_t pf_cap,
                                                   const int64_t *status, int64_t *n_pf_out) {
+  __shared__ int64_t s_cand[64 * 64];   // [slot][k]: latest insertion of candidate k of the slot-th start miss
+  __shared__ int64_t s_page[64], s_cod[64];
+  __shared__ uint32_t s_mlane[64];
+  __shared__ int64_t s_fpm[64], s_fbase[64];
+  __shared__ uint64_t s_fmask[64];
+  __shared__ uint8_t s_snpf[SNAP_MAX], s_snhit[SNAP_MAX];
   if (ld(status)) return;  // a page outside the range: nothing changes
   const int id = cfg_ids ? cfg_ids[blockIdx.x] : (int)blockIdx.x;
   const CacheCfg c = cfgs[id];
-  const uint32_t lane = lane_no(), F = c.F, d = c.d;
+  const uint32_t lane = lane_no(), d = c.d;
+  const int64_t F = c.F;
   uint8_t *myhit = hit ? hit + (size_t)id * n : nullptr;
   const bool keep_pf = pf_page && id == 0;
-  uint32_t head = c.ctl->head;
-  int64_t hits = 0, faults = 0, pfr = 0, used = 0, unused = 0, npf = 0;
+  int64_t I = c.ctl->ins;
+  int64_t Imod = (int64_t)((uint64_t)I % (uint64_t)F);
+  int64_t hits = 0, faults = 0, pfr = 0, npf = 0, unused_l = 0;
 
   for (int64_t b0 = 0; b0 < n; b0 += 64) {
     const int64_t i = b0 + lane;
-    const int64_t p = i < n ? (int64_t)pages[i] : 0;
-    uint64_t active = __ballot(i < n);
-    while (active) {
-      const bool act = (active >> lane) & 1;
-      const int32_t s = act ? ld(&c.slot[p]) : -1;
-      const uint64_t miss = __ballot(act && s < 0);
-      const uint32_t f = miss ? (uint32_t)__builtin_ctzll(miss) : 64u;
-      // accesses before the first fault hit the current contents
-      const bool h = act && lane < f;
-      bool first_use = false;
+    const bool act = i < n;
+    const int64_t a = act ? (int64_t)pages[i] : -1;
+    int64_t view = act ? ld(&c.pins[a]) : PINS_NEVER;
+    const int64_t I_rs = I, Imod_rs = Imod;
+    // flags of the frames (Imod_rs + u) mod F, u < snap: they hold insertions
+    // I_rs - F + u, which the round's insertions I_rs + u evict
+    uint32_t snap = 0;
+    auto load_snap = [&]() {
+      uint8_t pf[SNAP_CHUNK / 64], hh[SNAP_CHUNK / 64];
+#pragma unroll
+      for (int u = 0; u < SNAP_CHUNK / 64; u++) {
+        int64_t fr = Imod_rs + (int64_t)(snap + u * 64 + lane);
+        if (fr >= F) fr -= F;
+        pf[u] = ld(&c.fpf[fr]);
+        hh[u] = ld(&c.fhit[fr]);
+      }
+#pragma unroll
+      for (int u = 0; u < SNAP_CHUNK / 64; u++) {
+        s_snpf[snap + u * 64 + lane] = pf[u];
+        s_snhit[snap + u * 64 + lane] = hh[u];
+      }
+      snap += SNAP_CHUNK;
+    };
+    if (I_rs + 64 * (int64_t)(d + 1) > F) load_snap();  // the round may evict
+    const uint64_t miss0 = __ballot(act && view < I_rs - F);
+    int64_t fr = view >= 0 ? (int64_t)((uint64_t)view % (uint64_t)F) : 0;  // frame of this lane's page
+    // candidates of the pages missing at the start of the round
+    if (d > 0 && miss0) {
+      s_page[lane] = a;
+      if ((miss0 >> lane) & 1) s_mlane[__builtin_amdgcn_mbcnt_hi((uint32_t)(miss0 >> 32),
+                                       __builtin_amdgcn_mbcnt_lo((uint32_t)miss0, 0u))] = lane;
+      lds_fence();
+      const uint32_t total = (uint32_t)__popcll(miss0) * d;
+      for (uint32_t e0 = 0; e0 < total; e0 += 512) {
+        int64_t v[8];
+        uint32_t at[8];
+#pragma unroll
+        for (int u = 0; u < 8; u++) {
+          const uint32_t e = e0 + (uint32_t)u * 64 + lane;
+          v[u] = PINS_NEVER;
+          at[u] = 0xFFFFFFFFu;
+          if (e < total) {
+            const uint32_t sl = e / d, k = e - sl * d + 1;
+            const int64_t q = s_page[s_mlane[sl]] + (int64_t)k;
+            at[u] = sl * 64 + k;
+            if ((uint64_t)q < R) v[u] = ld(&c.pins[q]);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; u++)
+          if (at[u] != 0xFFFFFFFFu) s_cand[at[u]] = v[u];
+      }
+      lds_fence();
+    }
+
+    uint32_t cursor = 0, J = 0;
+    uint8_t hflag = 0;
+    while (true) {
+      const bool later = act && lane >= cursor;
+      const uint64_t mm = __ballot(later && view < I - F);
+      const uint32_t f = mm ? (uint32_t)__builtin_ctzll(mm) : 64u;
+      // the accesses before the next fault hit
+      const bool h = later && lane < f;
       if (h) {
-        if (myhit) myhit[i] = 1;
-        first_use = take_flag(&c.frame_pf[s]) != 0;
+        hflag = 1;
+        st(&c.fhit[fr], (uint8_t)1);
+        const int64_t u = view - (I_rs - F);
+        if (u >= 0 && u < (int64_t)snap) s_snhit[u] = 1;
       }
       hits += __popcll(__ballot(h));
-      used += __popcll(__ballot(first_use));
       if (f == 64) break;
-      // the fault at lane f: candidates p_f + k, k = lane = 0..d
-      const int64_t pm = read_lane(p, f);
-      const int64_t im = b0 + f;
-      if (lane == f && myhit) myhit[i] = 0;
       faults++;
-      const int64_t cand = pm + (int64_t)lane;
-      const bool cv = lane <= d && (uint64_t)cand < R;
-      const bool res = cv && lane > 0 && ld(&c.slot[cand]) >= 0;
-      const bool ins = cv && !res;
-      const uint64_t insm = __ballot(ins);
-      const uint32_t pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(insm >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)insm, 0u));
-      const uint32_t m = (uint32_t)__popcll(insm);
-      const uint32_t fs = (uint32_t)(((uint64_t)head + pos) % F);
-      const int64_t ev = ins ? ld(&c.frame_page[fs]) : -1;
-      // does this insertion evict a later candidate that was resident (it
-      // would have to be fetched again when its turn comes)?
-      const int64_t k = ev - pm;
-      const bool later = ins && k > (int64_t)lane && k <= (int64_t)d;
-      const uint32_t kk = later ? (uint32_t)k : lane;
-      const bool kres = __shfl(res ? 1 : 0, (int)kk) != 0;
-      if (__ballot(later && kres)) {
-        // replay this fault in order on one lane
-        if (lane == 0) {
-          for (uint32_t j = 0; j <= d && (uint64_t)(pm + j) < R; j++) {
-            const int64_t q = pm + j;
-            if (j > 0 && ld(&c.slot[q]) >= 0) continue;
-            const int64_t old = ld(&c.frame_page[head]);
-            if (old >= 0) {
-              st(&c.slot[old], -1);
-              if (take_flag(&c.frame_pf[head])) unused++;
-            }
-            st(&c.frame_page[head], q);
-            st(&c.frame_pf[head], j > 0 ? 1u : 0u);
-            st(&c.slot[q], (int32_t)head);
-            if (j > 0) {
-              if (keep_pf && npf < pf_cap) {
-                pf_page[npf] = (uint64_t)q;
-                pf_src[npf] = im;
-              }
-              npf++;
-              pfr++;
-            }
-            head = head + 1 == F ? 0 : head + 1;
-          }
-        }
-        head = (uint32_t)__shfl((int)head, 0);
-        npf = read_lane(npf, 0);
-        pfr = read_lane(pfr, 0);
-        unused = read_lane(unused, 0);
+      const int64_t pm = read_lane(a, f);
+      const int64_t im = b0 + f;
+      // candidate k = lane (lane 0: the page itself)
+      const bool cv = lane <= d && (uint64_t)(pm + (int64_t)lane) < R;
+      int64_t L = PINS_NEVER;
+      if ((miss0 >> f) & 1) {
+        const uint32_t slot = (uint32_t)__popcll(miss0 & ((1ull << f) - 1));
+        if (lane >= 1 && cv) L = s_cand[slot * 64 + lane];
       } else {
-        bool lost = false;
-        if (ins) {
-          if (ev >= 0) {
-            st(&c.slot[ev], -1);
-            lost = take_flag(&c.frame_pf[fs]) != 0;
-          }
-          st(&c.frame_page[fs], cand);
-          st(&c.frame_pf[fs], lane > 0 ? 1u : 0u);
-          st(&c.slot[cand], (int32_t)fs);
-          if (lane > 0 && keep_pf) {
-            const int64_t j = npf + (int64_t)pos - 1;
-            if (j < pf_cap) {
-              pf_page[j] = (uint64_t)cand;
-              pf_src[j] = im;
+        // absent since earlier in this round: read the candidates now (through
+        // LDS, so that only this rare branch waits for device memory)
+        if (lane >= 1 && cv) s_cod[lane] = ld(&c.pins[pm + (int64_t)lane]);
+        lds_fence();
+        if (lane >= 1 && cv) L = s_cod[lane];
+      }
+      if (lane >= 1 && cv) {
+        for (int j = (int)J - 1; j >= 0; j--) {
+          const int64_t off = pm + (int64_t)lane - s_fpm[j];
+          if (off >= 0 && off <= (int64_t)d) {
+            const uint64_t fm = s_fmask[j];
+            if ((fm >> off) & 1) {
+              L = s_fbase[j] + __popcll(fm & ((1ull << off) - 1));
+              break;
             }
           }
         }
-        unused += __popcll(__ballot(lost));
-        npf += m - 1;
-        pfr += m - 1;
-        head = (uint32_t)(((uint64_t)head + m) % F);
       }
-      wave_fence();
-      active &= ~((f == 63 ? ~0ull : ((1ull << (f + 1)) - 1)));
+      // insertions: the least fixed point of ins_k = (L_k < I + c_k - F)
+      uint64_t msk = __ballot(cv && (lane == 0 || L < I + 1 - F));
+      while (true) {
+        const int64_t ck = (int64_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(msk >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
+        const uint64_t m2 = __ballot(cv && (lane == 0 || L < I + ck - F));
+        if (m2 == msk) break;
+        msk = m2;
+      }
+      const uint32_t m = (uint32_t)__popcll(msk);
+      // the flags of the frames these insertions take
+      if (I + (int64_t)m > F) {
+        const int64_t need = I + (int64_t)m - I_rs;
+        while ((int64_t)snap < need) load_snap();
+        lds_fence();
+      }
+      if ((msk >> lane) & 1) {
+        const uint32_t off = __builtin_amdgcn_mbcnt_hi((uint32_t)(msk >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
+        const int64_t x = I + off;
+        int64_t fx = Imod + off;
+        if (fx >= F) fx -= F;
+        if (x >= F) {
+          const uint32_t u = (uint32_t)(x - I_rs);
+          if (s_snpf[u] && !s_snhit[u]) unused_l++;
+        }
+        const int64_t q = pm + (int64_t)lane;
+        st(&c.pins[q], x);
+        st(&c.fpf[fx], (uint8_t)(lane > 0 ? 1 : 0));
+        st(&c.fhit[fx], (uint8_t)0);
+        if (lane > 0 && keep_pf) {
+          const int64_t j = npf + (int64_t)off - 1;
+          if (j < pf_cap) {
+            pf_page[j] = (uint64_t)q;
+            pf_src[j] = im;
+          }
+        }
+      }
+      npf += m - 1;
+      pfr += m - 1;
+      if (lane == 0) {
+        s_fpm[J] = pm;
+        s_fbase[J] = I;
+        s_fmask[J] = msk;
+      }
+      // the later accesses see this fault's insertions
+      {
+        const int64_t off = a - pm;
+        if (act && lane > f && off >= 0 && off <= (int64_t)d && ((msk >> off) & 1)) {
+          const int64_t o = __popcll(msk & ((1ull << off) - 1));
+          view = I + o;
+          fr = Imod + o;
+          if (fr >= F) fr -= F;
+        }
+      }
+      J++;
+      I += m;
+      Imod += m;
+      if (Imod >= F) Imod -= F;
+      lds_fence();
+      cursor = f + 1;
     }
+    if (act && myhit) myhit[i] = hflag;
+    lds_fence();
   }
+  int64_t unused = unused_l;
+  for (int o = 32; o >= 1; o >>= 1) unused += __shfl_xor(unused, o);
   if (lane == 0) {
-    c.ctl->head = head;
+    c.ctl->ins = I;
+    c.ctl->head = (uint32_t)Imod;
     c.ctl->count[0] += hits;
     c.ctl->count[1] += faults;
     c.ctl->count[2] += pfr;
-    c.ctl->count[3] += used;
     c.ctl->count[4] += unused;
+    c.ctl->pend = 0;
     if (id == 0 && n_pf_out) *n_pf_out = npf;
+  }
+}
+
+// Prefetched pages still resident and never hit, per cache (after k_cache_run).
+__global__ __launch_bounds__(256) void k_cache_pending(const CacheCfg *__restrict__ cfgs, const int *cfg_ids,
+                                                      const int64_t *status) {
+  __shared__ int64_t part[4];
+  if (ld(status)) return;  // the run changed nothing
+  const CacheCfg c = cfgs[cfg_ids ? cfg_ids[blockIdx.y] : (int)blockIdx.y];
+  int64_t cnt = 0;
+  for (uint64_t f = (uint64_t)blockIdx.x * 256 + threadIdx.x; f < c.F; f += (uint64_t)gridDim.x * 256)
+    cnt += (c.fpf[f] && !c.fhit[f]) ? 1 : 0;
+  for (int o = 32; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int64_t s = part[0] + part[1] + part[2] + part[3];
+    if (s) atomicAdd((unsigned long long *)&c.ctl->pend, (unsigned long long)s);
   }
 }
 
@@ -260,11 +393,6 @@ struct LdsCache {
   }
 };
 
-__device__ __forceinline__ void lds_fence() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
 }  // namespace
 
 static __host__ __device__ uint32_t cache_tab_size(uint32_t F) {
@@ -470,6 +598,8 @@ __global__ void k_cache_report(const CacheCfg *__restrict__ cfgs, int n_cfg, con
   if (b >= n_cfg) return;
   const CacheCtl *ctl = cfgs[b].ctl;
   for (int k = 0; k < 5; k++) out[(size_t)b * per_cfg + k] = ctl->count[k];
+  // device-memory caches: prefetched used = reads - evicted unused - still pending
+  if (cfgs[b].pins) out[(size_t)b * per_cfg + 3] = ctl->count[2] - ctl->count[4] - ctl->pend;
   if (per_cfg >= 7) {
     out[(size_t)b * per_cfg + 5] = n_pf ? *n_pf : 0;
     out[(size_t)b * per_cfg + 6] = *status;
@@ -505,9 +635,15 @@ hipError_t launch_cache_run(const CacheCfg *dev_cfgs, const int *cfg_ids, int n_
   if (lds)
     hipLaunchKernelGGL(k_cache_run_lds, dim3((uint32_t)n_cfg), dim3(64), cache_lds_bytes(max_f), s, dev_cfgs,
                        cfg_ids, R, pages, n, hit, pf_page, pf_src, pf_cap, status, n_pf_out);
-  else
+  else {
     hipLaunchKernelGGL(k_cache_run, dim3((uint32_t)n_cfg), dim3(64), 0, s, dev_cfgs, cfg_ids, R, pages, n, hit,
                        pf_page, pf_src, pf_cap, status, n_pf_out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    uint64_t pb = ((uint64_t)max_f + 255) / 256;
+    if (pb > 256) pb = 256;
+    hipLaunchKernelGGL(k_cache_pending, dim3((uint32_t)pb, (uint32_t)n_cfg), dim3(256), 0, s, dev_cfgs, cfg_ids, status);
+  }
   return hipGetLastError();
 }
 

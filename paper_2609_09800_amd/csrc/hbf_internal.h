@@ -144,23 +144,30 @@ hipError_t launch_layer_done(const CallCtl *ctl, int64_t count, const int64_t *p
 hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
                        int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
                        int64_t tick_ps, DevState *st, hipStream_t s);
-// Capacity-mode frame cache (hbf_cache.hip): per cache, the page held by
-// each frame (-1 empty), a prefetched-and-not-yet-hit flag per frame, the
-// frame holding each page of the range (-1 not resident), the FIFO head and
-// the counters (hits, faults, prefetch reads, prefetched used, evicted
-// unused).
+// Capacity-mode frame cache (hbf_cache.hip).  Caches of up to
+// CACHE_LDS_MAX frames: the page held by each frame (-1 empty) and a
+// prefetched-and-not-yet-hit flag per frame, loaded into LDS per call.
+// Larger caches: the number of each page's latest insertion (PINS_NEVER if
+// none) and, per frame, a prefetched flag and a hit-since-insertion flag.
+// Both: the FIFO head, the counters (hits, faults, prefetch reads,
+// prefetched used, evicted unused), the insertion count and the prefetched
+// pages resident and unhit (device-memory caches, after each run).
 struct CacheCtl {
   uint32_t head;
   uint32_t pad;
   int64_t count[5];
+  int64_t ins;
+  int64_t pend;
 };
 struct CacheCfg {
   int64_t *frame_page;
   uint32_t *frame_pf;
-  int32_t *slot;
+  int64_t *pins;
+  uint8_t *fpf, *fhit;
   CacheCtl *ctl;
   uint32_t F, d;
 };
+constexpr int64_t PINS_NEVER = INT64_MIN / 4;
 constexpr uint32_t CACHE_MAX_PREFETCH = 63;  // one fault's candidates fit one wave
 // Caches of up to this many frames run with their whole state in LDS (a hash
 // of the resident pages); larger ones keep a page -> frame table in memory.

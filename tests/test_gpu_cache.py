@@ -83,7 +83,8 @@ def test_belady_anomaly(torch):
 # up to 4,096 frames the cache lives in LDS (hash of resident pages); above,
 # in device memory (page -> frame table)
 CASES = [(8, 7, 40), (9, 7, 30), (4, 3, 12), (64, 63, 200), (16, 8, 64), (256, 7, 1033), (1000, 0, 5000),
-         (4096, 31, 1 << 20), (1, 0, 5), (2, 1, 3), (4097, 7, 12000), (6000, 63, 9000), (20000, 15, 1 << 20)]
+         (4096, 31, 1 << 20), (1, 0, 5), (2, 1, 3), (4097, 7, 12000), (6000, 63, 9000), (20000, 15, 1 << 20),
+         (4097, 63, 4200), (5000, 0, 20000), (4100, 63, 1 << 20), (100000, 7, 150000), (4099, 1, 4101)]
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
@@ -98,6 +99,30 @@ def test_calls_continue_one_cache(torch):
     rng = np.random.default_rng(7)
     s = runs_stream(rng, 9000, 300, 9)
     run_both(torch, 32, 7, 300, [s[:100], s[100:101], [], s[101:5000], s[5000:]], "multi-call")
+
+
+def test_calls_continue_device_memory_cache(torch):
+    """A cache above the LDS limit carried over several calls (its
+    insertion count and frame flags persist), one of them empty."""
+    rng = np.random.default_rng(17)
+    s = runs_stream(rng, 60000, 20000, 9)
+    run_both(torch, 5000, 7, 20000, [s[:63], s[63:64], [], s[64:30000], s[30000:]], "multi-call-dm")
+
+
+def test_pages_evicted_within_their_round(torch):
+    """Near-full FIFO with the widest prefetch: each fault inserts up to 64
+    pages, so one 64-access round can evict a page that was resident when
+    the round began and that a later access of the same round touches (that
+    access then faults and reads its candidates on the spot)."""
+    rng = np.random.default_rng(18)
+    R = 1 << 20
+    pages = []
+    for t in range(40000):
+        if t >= 120 and rng.random() < 0.5:
+            pages.append(pages[t - int(rng.integers(60, 130))])
+        else:
+            pages.append(int(rng.integers(0, R)))
+    run_both(torch, 4097, 63, R, [pages], "evict-in-round")
 
 
 def test_moe_expert_stream(torch):
