@@ -161,6 +161,41 @@ def refresh_leg(torch, hbf, wl, w, model, addr, issue, complete, reps=3):
                 ms_per_call=ms, requests_per_s=w.n / (ms / 1e3), parity_vs_reference_digest=parity)
 
 
+def small_configs_leg(torch, hbf, wl, reps=20):
+    """The two small streams (4,096 and 1,048,576 requests): their inputs and
+    outputs (at most 48 MB) stay in the 256 MB MALL, so these rates are
+    cache-resident, not HBM-bound.  Median of `reps` timed calls of reset +
+    hbf_time_requests each, checked against the reference digests."""
+    gold_p = os.path.join(ROOT, "tests", "golden", "oracle_digests.json")
+    gold = json.load(open(gold_p)) if os.path.exists(gold_p) else {}
+    out = {}
+    s = torch.cuda.current_stream()
+    for name, w in (("config1", wl.config1()), ("config2", wl.config2())):
+        m = hbf.Model(**w.params)
+        for b, nb in w.ranges:
+            assert m.register_range(b, nb)[0] == 0
+        a = torch.from_numpy(w.addr.view(np.int64)).cuda()
+        i = torch.from_numpy(w.issue).cuda()
+        c = torch.empty_like(i)
+        times = []
+        for r in range(reps + 1):
+            m.reset(s)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            assert m.time_requests(a, i, c, s) == 0
+            e1.record(s)
+            torch.cuda.synchronize()
+            if r:
+                times.append(e0.elapsed_time(e1))
+        assert m.get_status() == 0
+        ms = float(np.median(times))
+        g = gold.get(name)
+        out[name] = dict(requests=int(w.n), ms_per_call=ms, requests_per_s=w.n / (ms / 1e3),
+                         residency="cache-resident (MALL)",
+                         parity_vs_reference_digest=(sha(c.cpu().numpy()) == g["complete_sha256"]) if g else None)
+    return out
+
+
 def capacity_leg(torch, hbf, wl, reps=2):
     """The capacity row (Sections D5, D6): two config-3 decode steps at batch
     8 as a capacity-mode stream through one frame cache holding half of the
@@ -329,13 +364,26 @@ def gemv_leg(torch, hbf, wl, sets=16, reps=3):
         e1.record(s)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / (reps * sets)
+        # the same calls instrumented, every page's delay zero: the cost of
+        # the clock reads and the (immediately satisfied) wait
+        zi = torch.zeros(E * N * K * 2 // page, dtype=torch.int64, device="cuda")
+        e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e2.record(s)
+        for _ in range(reps):
+            for k in range(sets):
+                gm.gemv_instrumented(Wall[k], Xd, Yd, zi, zi, None, stream=s)
+        e3.record(s)
+        torch.cuda.synchronize()
+        ms0 = e2.elapsed_time(e3) / (reps * sets)
         nbytes = wbytes + X.nbytes + E * B * N * 4
         gbps = nbytes / (ms / 1e3) / 1e9
         out[f"batch{B}"] = dict(us_per_call=ms * 1e3, GBps=gbps, frac_of_hbm_peak=gbps / HBM_PEAK_GBPS,
-                                TFLOPs=2 * E * B * N * K / (ms / 1e3) / 1e12)
+                                TFLOPs=2 * E * B * N * K / (ms / 1e3) / 1e12,
+                                us_per_call_zero_delay=ms0 * 1e3)
     assert gm.get_status() == 0
     return dict(workload=f"8 experts x [768 x 2048] bf16 per call, {sets} weight sets rotated "
-                         f"({sets * wbytes >> 20} MiB), no injected delay", **out)
+                         f"({sets * wbytes >> 20} MiB), no instrumentation; us_per_call_zero_delay: "
+                         f"instrumented with every delay zero", **out)
 
 
 def cpu_baseline(w, n_sample):
@@ -348,9 +396,18 @@ def cpu_baseline(w, n_sample):
     rc, _ = m.time_requests(a, i)
     dt = time.perf_counter() - t
     assert rc == 0
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return dict(value=n_sample / dt, unit="requests/s", cores=1, kind="oracle",
                 sample=f"first {n_sample} requests of the same stream, single-threaded C reference "
-                       f"(gcc -O2), {dt:.2f} s")
+                       f"(gcc -O2), {dt:.2f} s",
+                host_cpu=cpu, host_threads=os.cpu_count())
 
 
 def main():
@@ -366,6 +423,7 @@ def main():
                     help="directory to keep the generated stream in (.npy) for repeated runs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--no-gemv", action="store_true", help="time only hbf_time_requests (diagnostic)")
+    ap.add_argument("--no-small", action="store_true", help="skip the cache-resident small streams")
     ap.add_argument("--no-closed-loop", action="store_true", help="skip the closed-loop decode report")
     ap.add_argument("--no-refresh", action="store_true", help="skip the refresh-plan report")
     ap.add_argument("--no-capacity", action="store_true", help="skip the capacity-mode frame cache report")
@@ -506,6 +564,9 @@ def main():
     if pt:  # counter-measured HBM bytes of the whole call / its kernels' time
         out["path_counter_GBps"] = pt / (tr_ms / 1e3) / 1e9
         out["path_counter_frac"] = out["path_counter_GBps"] / HBM_PEAK_GBPS
+    if not args.no_small:
+        log("small streams (cache-resident)")
+        out["small_configs"] = small_configs_leg(torch, hbf, wl)
     if not args.no_closed_loop:
         log("closed-loop decode timing")
         out["closed_loop"] = closed_loop(torch, hbf, wl)
