@@ -113,6 +113,14 @@ __global__ __launch_bounds__(256) void k_cache_clear(CacheCfg *cfgs, uint64_t R)
 constexpr int SNAP_CHUNK = 256;        // frame flags copied per chunk
 constexpr int SNAP_MAX = 64 * 64;      // insertions in one round: 64 faults x (1 + 63 candidates)
 
+// One wave runs one cache, and a wave's LDS operations execute in issue
+// order, so between its own LDS writes and reads only the compiler must be
+// kept from reordering or caching them (no wait is needed).
+__device__ __forceinline__ void wave_lds_order() {
+  __builtin_amdgcn_wave_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ cfgs, const int *cfg_ids, uint64_t R,
                                                   const uint64_t *__restrict__ pages, int64_t n,
                                                   uint8_t *__restrict__ hit, uint64_t *__restrict__ pf_page,
@@ -193,6 +201,7 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
     }
 
     uint32_t cursor = 0, J = 0;
+    int64_t fmin = 0, fmax = 0;  // least and greatest faulting page of the round (with candidates)
     uint8_t hflag = 0;
     while (true) {
       const bool later = act && lane >= cursor;
@@ -224,7 +233,10 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
         lds_fence();
         if (lane >= 1 && cv) L = s_cod[lane];
       }
-      if (lane >= 1 && cv) {
+      // an earlier fault of this round can have inserted pm + lane only if
+      // its page lies in [pm + 1 - d, pm + d]
+      const bool near = J > 0 && fmin <= pm + (int64_t)d && fmax + (int64_t)d >= pm + 1;
+      if (near && lane >= 1 && cv) {
         for (int j = (int)J - 1; j >= 0; j--) {
           const int64_t off = pm + (int64_t)lane - s_fpm[j];
           if (off >= 0 && off <= (int64_t)d) {
@@ -246,11 +258,15 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
         msk = m2;
       }
       const uint32_t m = (uint32_t)__popcll(msk);
-      // the flags of the frames these insertions take
+      // the flags of the frames these insertions take must be in the copy
+      // before any later hit of this round could touch them (counted at the
+      // end of the round)
       if (I + (int64_t)m > F) {
         const int64_t need = I + (int64_t)m - I_rs;
-        while ((int64_t)snap < need) load_snap();
-        lds_fence();
+        if ((int64_t)snap < need) {
+          while ((int64_t)snap < need) load_snap();
+          lds_fence();
+        }
       }
       if ((msk >> lane) & 1) {
         const uint32_t off = __builtin_amdgcn_mbcnt_hi((uint32_t)(msk >> 32),
@@ -258,10 +274,6 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
         const int64_t x = I + off;
         int64_t fx = Imod + off;
         if (fx >= F) fx -= F;
-        if (x >= F) {
-          const uint32_t u = (uint32_t)(x - I_rs);
-          if (s_snpf[u] && !s_snhit[u]) unused_l++;
-        }
         const int64_t q = pm + (int64_t)lane;
         st(&c.pins[q], x);
         st(&c.fpf[fx], (uint8_t)(lane > 0 ? 1 : 0));
@@ -276,10 +288,14 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       }
       npf += m - 1;
       pfr += m - 1;
-      if (lane == 0) {
-        s_fpm[J] = pm;
-        s_fbase[J] = I;
-        s_fmask[J] = msk;
+      if (d > 0) {
+        if (lane == 0) {
+          s_fpm[J] = pm;
+          s_fbase[J] = I;
+          s_fmask[J] = msk;
+        }
+        fmin = J ? (pm < fmin ? pm : fmin) : pm;
+        fmax = J ? (pm > fmax ? pm : fmax) : pm;
       }
       // the later accesses see this fault's insertions
       {
@@ -295,10 +311,17 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       I += m;
       Imod += m;
       if (Imod >= F) Imod -= F;
-      lds_fence();
+      wave_lds_order();
       cursor = f + 1;
     }
     if (act && myhit) myhit[i] = hflag;
+    // evictions of the round: its insertions I_rs + u with I_rs + u >= F took
+    // the frames of insertions I_rs - F + u; every hit on those happened
+    // before their eviction and is in the copy
+    {
+      const int64_t lo = F - I_rs > 0 ? F - I_rs : 0, hi = I - I_rs;
+      for (int64_t u = lo + lane; u < hi; u += 64) unused_l += (s_snpf[u] && !s_snhit[u]) ? 1 : 0;
+    }
     lds_fence();
   }
   int64_t unused = unused_l;
