@@ -143,6 +143,58 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
   int64_t Imod = (int64_t)((uint64_t)I % (uint64_t)F);
   int64_t hits = 0, faults = 0, pfr = 0, npf = 0, unused_l = 0;
 
+  if (d == 0) {
+    // No prefetch: a fault inserts only its own page, no frame is ever
+    // prefetched, so only the insertion numbers matter.  Lane l of a round
+    // faults iff no earlier lane of the round faulted on its page (such a
+    // page stays resident for the rest of the round: a round inserts at most
+    // 64 < F pages) and its latest insertion is below I + c_l - F, with c_l
+    // the faults of the lanes before it.  Each lane's outcome depends only
+    // on those of the lanes before it, so the equations have one solution,
+    // and iterating them from any guess reaches it after at most 64 steps
+    // (after step k the first k lanes are settled); usually after 2.
+    for (int64_t b0 = 0; b0 < n; b0 += 64) {
+      const int64_t i = b0 + lane;
+      const bool act = i < n;
+      const uint32_t a = act ? (uint32_t)pages[i] : 0xFFFFFFFFu;
+      const int64_t view = act ? ld(&c.pins[a]) : PINS_NEVER;
+      // earlier lanes of the round with the same page
+      uint64_t same = 0;
+      for (uint32_t j = 0; j < 64; j++) {
+        const uint32_t aj = (uint32_t)__builtin_amdgcn_readlane((int)a, (int)j);
+        same |= (j < lane && aj == a) ? (1ull << j) : 0ull;
+      }
+      uint64_t fm = __ballot(act && view < I - F);
+      for (int it = 0; it <= 64; it++) {
+        const int64_t cl = (int64_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(fm >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)fm, 0u));
+        const uint64_t nf = __ballot(act && !(same & fm) && view < I + cl - F);
+        if (nf == fm) break;
+        fm = nf;
+      }
+      const bool flt = (fm >> lane) & 1;
+      if (flt) {
+        const int64_t cl = (int64_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(fm >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)fm, 0u));
+        st(&c.pins[a], I + cl);
+      }
+      if (act && myhit) myhit[i] = flt ? 0 : 1;
+      const int64_t m = __popcll(fm);
+      faults += m;
+      hits += __popcll(__ballot(act)) - m;
+      I += m;
+    }
+    if (lane == 0) {
+      c.ctl->ins = I;
+      c.ctl->head = (uint32_t)((uint64_t)I % (uint64_t)F);
+      c.ctl->count[0] += hits;
+      c.ctl->count[1] += faults;
+      c.ctl->pend = 0;
+      if (id == 0 && n_pf_out) *n_pf_out = 0;
+    }
+    return;
+  }
+
   for (int64_t b0 = 0; b0 < n; b0 += 64) {
     const int64_t i = b0 + lane;
     const bool act = i < n;

@@ -125,6 +125,28 @@ def test_pages_evicted_within_their_round(torch):
     run_both(torch, 4097, 63, R, [pages], "evict-in-round")
 
 
+@pytest.mark.parametrize("F", [4097, 5000])
+def test_no_prefetch_device_memory_cache(torch, F):
+    """Depth 0 above the LDS limit (each round's faults found together):
+    cyclic scans just shorter and just longer than the cache (all hits /
+    all faults under FIFO), then a cycle near the cache size with repeats
+    inside a round, so that faults earlier in a round decide whether a
+    page is still resident later in it."""
+    rng = np.random.default_rng(19 + F)
+    R = 3 * F
+    calls = [list(range(F - 1)) * 3, list(range(F + 1)) * 3]
+    mix = []
+    cyc = list(range(F + 16))
+    for t in range(12 * F):
+        if t >= 8 and rng.random() < 0.2:
+            mix.append(mix[-int(rng.integers(1, 8))])
+        else:
+            mix.append(cyc[t % len(cyc)])
+    calls.append(mix)
+    calls.append([int(x) for x in rng.integers(0, R, 30000)])
+    run_both(torch, F, 0, R, calls, f"no-prefetch-{F}")
+
+
 def test_moe_expert_stream(torch):
     """Expert weight pages in layer order (8 pages per expert, 64 experts per
     layer, a few active per step), 256 frames, prefetch 7: the shape of the
