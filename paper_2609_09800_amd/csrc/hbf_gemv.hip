@@ -116,28 +116,54 @@ __global__ __launch_bounds__(256) void k_gemv_instrumented(
   }
 }
 
-// Transposing butterfly over the 64 lanes of a wave on C values per lane:
-// at the step with lane distance O a lane keeps the upper half of its values
-// if bit O of its lane index is set, the lower half if not, and adds the
-// partner's copy of the half it keeps.  Once one value is left, the
-// remaining steps are a plain xor reduction.  Afterwards every lane holds the
-// wave sum of value index (lane >> (6 - log2 C)).
-template <int C, int O>
+// Transposing butterfly over the 64 lanes of a wave on C values per lane,
+// in six steps that pair each lane with lane ^ 32, ^ 16, ^ 15, ^ 7, ^ 2 and
+// ^ 1 (the masks span all six lane bits, so every lane's result sums all 64
+// lanes).  While a lane has more than one value, a step halves them: the
+// lane keeps the upper half if its decision bit (5, 4, 3, 2, 1, 0 in step
+// order) is set, the lower half if not, and adds the partner's copy of that
+// half.  The first two steps use gfx950's cross-row swaps, which hand each
+// lane exactly the partner's copy of the half it keeps (no selects); the
+// others use DPP lane permutations (row mirror, half-row mirror, quad
+// permutes).  Once one value is left the remaining steps are plain sums.
+// Afterwards the lane holds the wave sum of value index lane >> (6 - log2 C).
+__device__ __forceinline__ float swap_sum(float a, float b, int step) {
+  const auto r = step == 0 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false)
+                           : __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int STEP>
+__device__ __forceinline__ float partner(float v) {
+  return dpp_f<STEP == 2 ? 0x140 : STEP == 3 ? 0x141 : STEP == 4 ? 0x4E : 0xB1>(v);
+}
+template <int C, int STEP>
 __device__ __forceinline__ void butterfly(float *val, int lane) {
-  if constexpr (O >= 1) {
+  if constexpr (STEP < 6) {
     if constexpr (C > 1) {
       constexpr int H = C / 2;
-      const bool upper = (lane & O) != 0;
+      if constexpr (STEP < 2) {
 #pragma unroll
-      for (int i = 0; i < H; i++) {
-        const float keep = upper ? val[i + H] : val[i];
-        const float send = upper ? val[i] : val[i + H];
-        val[i] = keep + __shfl_xor(send, O);
+        for (int i = 0; i < H; i++) val[i] = swap_sum(val[i], val[i + H], STEP);
+      } else {
+        const bool up = ((lane >> (5 - STEP)) & 1) != 0;
+#pragma unroll
+        for (int i = 0; i < H; i++) {
+          const float lo = val[i] + partner<STEP>(val[i]);
+          const float hi = val[i + H] + partner<STEP>(val[i + H]);
+          val[i] = up ? hi : lo;
+        }
       }
-      butterfly<H, O / 2>(val, lane);
+      butterfly<H, STEP + 1>(val, lane);
     } else {
-      val[0] += __shfl_xor(val[0], O);
-      butterfly<1, O / 2>(val, lane);
+      if constexpr (STEP < 2)
+        val[0] = swap_sum(val[0], val[0], STEP);
+      else
+        val[0] += partner<STEP>(val[0]);
+      butterfly<1, STEP + 1>(val, lane);
     }
   }
 }
@@ -149,7 +175,8 @@ __device__ __forceinline__ void butterfly(float *val, int lane) {
 // per row) and feeds 4 dot products.  The activations are loaded right after
 // the page, before the wait.  The 4*BB partial sums of a lane are reduced
 // across the wave by a transposing butterfly (63 exchanges for 64 values
-// instead of 6 per value), then across the 4 waves through LDS.  (Blocks of
+// instead of 6 per value, all in registers), then across the 4 waves
+// through LDS.  (Blocks of
 // 2 or 4 pages, sharing one activation load, measured slower at every batch:
 // fewer blocks in flight.)
 template <int BB>
@@ -201,7 +228,7 @@ __global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__
   for (int b = 0; b < BB; b++)
 #pragma unroll
     for (int r = 0; r < R; r++) val[r * BB + b] = dot8(v[r], xv[b]);
-  butterfly<V, 32>(val, lane);
+  butterfly<V, 0>(val, lane);
   red[w][lane] = val[0];
   __syncthreads();
   // the lane holding value index i has i's bits in its top log2(V) bits
