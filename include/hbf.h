@@ -302,7 +302,7 @@ int hbf_refresh_pending(hbf_model_t model, uint32_t *host_pending, void *stream)
 typedef struct hbf_cache *hbf_cache_t;  /* opaque, owned by the library */
 
 /* Create an empty cache (allocates frames*12 bytes of device memory for up
- * to 4,096 frames, range_pages*8 + frames*2 bytes above; synchronous). */
+ * to 63 frames, range_pages*8 + frames*2 bytes above; synchronous). */
 int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pages, hbf_cache_t *out);
 void hbf_cache_destroy(hbf_cache_t cache);
 /* Empty every frame and zero the counters (asynchronous on `stream`). */

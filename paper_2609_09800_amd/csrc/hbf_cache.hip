@@ -132,11 +132,12 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
   __shared__ int64_t s_fpm[64], s_fbase[64];
   __shared__ uint64_t s_fmask[64];
   __shared__ uint8_t s_snpf[SNAP_MAX], s_snhit[SNAP_MAX];
+  __shared__ uint8_t s_ipf[SNAP_MAX], s_ihit[SNAP_MAX];  // the round's own insertions I_rs + u
   if (ld(status)) return;  // a page outside the range: nothing changes
   const int id = cfg_ids ? cfg_ids[blockIdx.x] : (int)blockIdx.x;
   const CacheCfg c = cfgs[id];
   const uint32_t lane = lane_no(), d = c.d;
-  const int64_t F = c.F;
+  const int64_t F = c.F;  // >= 64: an insertion offset within one fault (<= 63) is below F
   uint8_t *myhit = hit ? hit + (size_t)id * n : nullptr;
   const bool keep_pf = pf_page && id == 0;
   int64_t I = c.ctl->ins;
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
     // prefetched, so only the insertion numbers matter.  Lane l of a round
     // faults iff no earlier lane of the round faulted on its page (such a
     // page stays resident for the rest of the round: a round inserts at most
-    // 64 < F pages) and its latest insertion is below I + c_l - F, with c_l
+    // 64 <= F pages) and its latest insertion is below I + c_l - F, with c_l
     // the faults of the lanes before it.  Each lane's outcome depends only
     // on those of the lanes before it, so the equations have one solution,
     // and iterating them from any guess reaches it after at most 64 steps
@@ -208,8 +209,7 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       uint8_t pf[SNAP_CHUNK / 64], hh[SNAP_CHUNK / 64];
 #pragma unroll
       for (int u = 0; u < SNAP_CHUNK / 64; u++) {
-        int64_t fr = Imod_rs + (int64_t)(snap + u * 64 + lane);
-        if (fr >= F) fr -= F;
+        const int64_t fr = (int64_t)((uint32_t)(Imod_rs + (int64_t)(snap + u * 64 + lane)) % (uint32_t)F);
         pf[u] = ld(&c.fpf[fr]);
         hh[u] = ld(&c.fhit[fr]);
       }
@@ -264,8 +264,12 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       if (h) {
         hflag = 1;
         st(&c.fhit[fr], (uint8_t)1);
-        const int64_t u = view - (I_rs - F);
-        if (u >= 0 && u < (int64_t)snap) s_snhit[u] = 1;
+        if (view >= I_rs) {
+          s_ihit[view - I_rs] = 1;
+        } else {
+          const int64_t u = view - (I_rs - F);
+          if (u >= 0 && u < (int64_t)snap) s_snhit[u] = 1;
+        }
       }
       hits += __popcll(__ballot(h));
       if (f == 64) break;
@@ -314,7 +318,8 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       // before any later hit of this round could touch them (counted at the
       // end of the round)
       if (I + (int64_t)m > F) {
-        const int64_t need = I + (int64_t)m - I_rs;
+        int64_t need = I + (int64_t)m - I_rs;
+        if (need > F) need = F;  // beyond F the evicted insertions are the round's own
         if ((int64_t)snap < need) {
           while ((int64_t)snap < need) load_snap();
           lds_fence();
@@ -326,6 +331,8 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
         const int64_t x = I + off;
         int64_t fx = Imod + off;
         if (fx >= F) fx -= F;
+        s_ipf[x - I_rs] = lane > 0 ? 1 : 0;
+        s_ihit[x - I_rs] = 0;
         const int64_t q = pm + (int64_t)lane;
         st(&c.pins[q], x);
         st(&c.fpf[fx], (uint8_t)(lane > 0 ? 1 : 0));
@@ -368,11 +375,15 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
     }
     if (act && myhit) myhit[i] = hflag;
     // evictions of the round: its insertions I_rs + u with I_rs + u >= F took
-    // the frames of insertions I_rs - F + u; every hit on those happened
-    // before their eviction and is in the copy
+    // the frames of insertions I_rs - F + u -- made before the round (their
+    // flags are in the copy) or, when u >= F, by the round itself (in its
+    // own records); every hit on an evicted insertion preceded its eviction
     {
       const int64_t lo = F - I_rs > 0 ? F - I_rs : 0, hi = I - I_rs;
-      for (int64_t u = lo + lane; u < hi; u += 64) unused_l += (s_snpf[u] && !s_snhit[u]) ? 1 : 0;
+      for (int64_t u = lo + lane; u < hi; u += 64) {
+        const bool gone_unused = u >= F ? (s_ipf[u - F] && !s_ihit[u - F]) : (s_snpf[u] && !s_snhit[u]);
+        unused_l += gone_unused ? 1 : 0;
+      }
     }
     lds_fence();
   }

@@ -169,9 +169,12 @@ struct CacheCfg {
 };
 constexpr int64_t PINS_NEVER = INT64_MIN / 4;
 constexpr uint32_t CACHE_MAX_PREFETCH = 63;  // one fault's candidates fit one wave
-// Caches of up to this many frames run with their whole state in LDS (a hash
-// of the resident pages); larger ones keep a page -> frame table in memory.
-constexpr uint32_t CACHE_LDS_MAX = 4096;
+// Caches of up to this many frames run with their whole state in LDS (a
+// hash of the resident pages); larger ones keep each page's latest
+// insertion number in device memory, which needs at least 64 frames (a
+// round of 64 accesses without prefetch then never evicts a page it
+// inserted, and one fault's insertion offsets, at most 63, stay below F).
+constexpr uint32_t CACHE_LDS_MAX = 63;
 hipError_t launch_cache_clear(CacheCfg *dev_cfgs, int n_cfg, uint64_t R, uint32_t max_f, hipStream_t s);
 // cfg_ids: the caches to run (device, n_cfg entries); every one of them has
 // F <= CACHE_LDS_MAX when lds is set, else F > CACHE_LDS_MAX.  max_f: their

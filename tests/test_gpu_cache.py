@@ -5,7 +5,7 @@ many caches over one stream.  Parameters include tight caches (frames =
 prefetch depth + 1) where a fault often evicts one of its own later
 candidates (the in-order replay), the widest prefetch (63 pages), long
 streams spanning many 64-access batches, calls that continue one cache, an
-out-of-range page, and both homes of the cache state (LDS up to 4,096 frames,
+out-of-range page, and both homes of the cache state (LDS up to 63 frames,
 device memory above).
 """
 import sys
@@ -80,11 +80,13 @@ def test_belady_anomaly(torch):
     assert faults == {3: 9, 4: 10}
 
 
-# up to 4,096 frames the cache lives in LDS (hash of resident pages); above,
-# in device memory (page -> frame table)
+# up to 63 frames the cache lives in LDS (hash of resident pages); above, in
+# device memory (latest insertion number per page)
 CASES = [(8, 7, 40), (9, 7, 30), (4, 3, 12), (64, 63, 200), (16, 8, 64), (256, 7, 1033), (1000, 0, 5000),
          (4096, 31, 1 << 20), (1, 0, 5), (2, 1, 3), (4097, 7, 12000), (6000, 63, 9000), (20000, 15, 1 << 20),
-         (4097, 63, 4200), (5000, 0, 20000), (4100, 63, 1 << 20), (100000, 7, 150000), (4099, 1, 4101)]
+         (4097, 63, 4200), (5000, 0, 20000), (4100, 63, 1 << 20), (100000, 7, 150000), (4099, 1, 4101),
+         (65, 63, 300), (65, 0, 200), (100, 63, 1 << 20), (127, 31, 5000), (63, 62, 400),
+         (64, 63, 300), (64, 0, 150)]
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
@@ -101,12 +103,13 @@ def test_calls_continue_one_cache(torch):
     run_both(torch, 32, 7, 300, [s[:100], s[100:101], [], s[101:5000], s[5000:]], "multi-call")
 
 
-def test_calls_continue_device_memory_cache(torch):
+@pytest.mark.parametrize("F", [100, 5000])
+def test_calls_continue_device_memory_cache(torch, F):
     """A cache above the LDS limit carried over several calls (its
     insertion count and frame flags persist), one of them empty."""
     rng = np.random.default_rng(17)
     s = runs_stream(rng, 60000, 20000, 9)
-    run_both(torch, 5000, 7, 20000, [s[:63], s[63:64], [], s[64:30000], s[30000:]], "multi-call-dm")
+    run_both(torch, F, 7, 20000, [s[:63], s[63:64], [], s[64:30000], s[30000:]], f"multi-call-dm-{F}")
 
 
 def test_pages_evicted_within_their_round(torch):
@@ -125,7 +128,7 @@ def test_pages_evicted_within_their_round(torch):
     run_both(torch, 4097, 63, R, [pages], "evict-in-round")
 
 
-@pytest.mark.parametrize("F", [4097, 5000])
+@pytest.mark.parametrize("F", [64, 65, 200, 4097, 5000])
 def test_no_prefetch_device_memory_cache(torch, F):
     """Depth 0 above the LDS limit (each round's faults found together):
     cyclic scans just shorter and just longer than the cache (all hits /
