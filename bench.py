@@ -240,8 +240,8 @@ def capacity_leg(torch, hbf, wl, reps=2):
     assert hbf.cache_sweep(frames, pref, R, pd, sc, s) == 0
     sweep_s = time.perf_counter() - t
     sv = sc.cpu().numpy()
-    # caches small enough to live in LDS (the prefetcher example's scale:
-    # hundreds of frames), many at once
+    # small caches (the prefetcher example's scale: hundreds of frames),
+    # many at once
     frs = [64, 128, 256, 512, 1024, 2048, 4096]
     pfs = [0, 1, 2, 3, 5, 7, 11, 15, 23, 31, 47, 63]
     sframes = [f for f in frs for p in pfs if p < f]
