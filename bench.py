@@ -123,6 +123,45 @@ def closed_loop(torch, hbf, wl, steps=2, reps=3):
                 modeled_decode_step_ns=step_ns)
 
 
+def size_sweep_leg(torch, hbf, w, addr, issue, complete, reps=5):
+    """hbf_time_requests on prefixes of the large stream (2^20 .. its full
+    length): how the rate grows with the call size.  Median of `reps` calls
+    of reset + time_requests each; the two smallest prefixes are checked
+    against the reference model on the host."""
+    from oracle import oracle
+    s = torch.cuda.current_stream()
+    m = hbf.Model(**w.params)
+    for b, nb in w.ranges:
+        assert m.register_range(b, nb)[0] == 0
+    out = {}
+    k = 20
+    while (1 << k) <= w.n:
+        n = 1 << k
+        a, i, c = addr[:n], issue[:n], complete[:n]
+        times = []
+        for r in range(reps + 1):
+            m.reset(s)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            assert m.time_requests(a, i, c, s) == 0
+            e1.record(s)
+            torch.cuda.synchronize()
+            if r:
+                times.append(e0.elapsed_time(e1))
+        assert m.get_status() == 0
+        ms = float(np.median(times))
+        row = dict(ms_per_call=ms, requests_per_s=n / (ms / 1e3))
+        if k <= 22:
+            o = oracle.OracleModel(**w.params)
+            for b, nb in w.ranges:
+                o.register_range(b, nb)
+            rc, want = o.time_requests(w.addr[:n], w.issue[:n])
+            row["parity_vs_reference"] = bool(rc == 0 and np.array_equal(c.cpu().numpy(), want))
+        out[f"2^{k}"] = row
+        k += 2
+    return out
+
+
 def refresh_leg(torch, hbf, wl, w, model, addr, issue, complete, reps=3):
     """The refresh row: the same stream timed with a refresh plan pending
     (Section D4), which adds a counting pass and rank-dependent die service.
@@ -423,7 +462,7 @@ def main():
                     help="directory to keep the generated stream in (.npy) for repeated runs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline")
     ap.add_argument("--no-gemv", action="store_true", help="time only hbf_time_requests (diagnostic)")
-    ap.add_argument("--no-small", action="store_true", help="skip the cache-resident small streams")
+    ap.add_argument("--no-small", action="store_true", help="skip the small streams and the size sweep")
     ap.add_argument("--no-closed-loop", action="store_true", help="skip the closed-loop decode report")
     ap.add_argument("--no-refresh", action="store_true", help="skip the refresh-plan report")
     ap.add_argument("--no-capacity", action="store_true", help="skip the capacity-mode frame cache report")
@@ -567,6 +606,8 @@ def main():
     if not args.no_small:
         log("small streams (cache-resident)")
         out["small_configs"] = small_configs_leg(torch, hbf, wl)
+        log("prefixes of the large stream")
+        out["size_sweep"] = size_sweep_leg(torch, hbf, w, addr, issue, complete)
     if not args.no_closed_loop:
         log("closed-loop decode timing")
         out["closed_loop"] = closed_loop(torch, hbf, wl)
