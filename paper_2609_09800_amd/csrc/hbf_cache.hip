@@ -223,13 +223,17 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
     if (I_rs + 64 * (int64_t)(d + 1) > F) load_snap();  // the round may evict
     const uint64_t miss0 = __ballot(act && view < I_rs - F);
     int64_t fr = view >= 0 ? (int64_t)((uint64_t)view % (uint64_t)F) : 0;  // frame of this lane's page
-    // candidates of the pages missing at the start of the round
-    if (d > 0 && miss0) {
+    // candidates of the first pages missing at the start of the round, as
+    // many as one 512-entry gather holds (the earliest misses are the
+    // likeliest faults: later ones are often filled by an earlier fault's
+    // prefetch); a fault beyond them reads its candidates when it happens
+    const uint32_t n_pre = d > 0 ? min((uint32_t)__popcll(miss0), 512u / d) : 0u;
+    if (n_pre > 0) {
       s_page[lane] = a;
       if ((miss0 >> lane) & 1) s_mlane[__builtin_amdgcn_mbcnt_hi((uint32_t)(miss0 >> 32),
                                        __builtin_amdgcn_mbcnt_lo((uint32_t)miss0, 0u))] = lane;
       lds_fence();
-      const uint32_t total = (uint32_t)__popcll(miss0) * d;
+      const uint32_t total = n_pre * d;
       for (uint32_t e0 = 0; e0 < total; e0 += 512) {
         int64_t v[8];
         uint32_t at[8];
@@ -279,12 +283,12 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       // candidate k = lane (lane 0: the page itself)
       const bool cv = lane <= d && (uint64_t)(pm + (int64_t)lane) < R;
       int64_t L = PINS_NEVER;
-      if ((miss0 >> f) & 1) {
-        const uint32_t slot = (uint32_t)__popcll(miss0 & ((1ull << f) - 1));
+      const uint32_t slot = (uint32_t)__popcll(miss0 & ((1ull << f) - 1));
+      if (((miss0 >> f) & 1) && slot < n_pre) {
         if (lane >= 1 && cv) L = s_cand[slot * 64 + lane];
       } else {
-        // absent since earlier in this round: read the candidates now (through
-        // LDS, so that only this rare branch waits for device memory)
+        // not among the gathered misses: read the candidates now (through
+        // LDS, so that only this branch waits for device memory)
         if (lane >= 1 && cv) s_cod[lane] = ld(&c.pins[pm + (int64_t)lane]);
         lds_fence();
         if (lane >= 1 && cv) L = s_cod[lane];
