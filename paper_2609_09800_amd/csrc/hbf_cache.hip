@@ -258,24 +258,16 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
 
     uint32_t cursor = 0, J = 0;
     int64_t fmin = 0, fmax = 0;  // least and greatest faulting page of the round (with candidates)
-    uint8_t hflag = 0;
+    uint64_t hitmask = 0;
     while (true) {
       const bool later = act && lane >= cursor;
       const uint64_t mm = __ballot(later && view < I - F);
       const uint32_t f = mm ? (uint32_t)__builtin_ctzll(mm) : 64u;
-      // the accesses before the next fault hit
-      const bool h = later && lane < f;
-      if (h) {
-        hflag = 1;
-        st(&c.fhit[fr], (uint8_t)1);
-        if (view >= I_rs) {
-          s_ihit[view - I_rs] = 1;
-        } else {
-          const int64_t u = view - (I_rs - F);
-          if (u >= 0 && u < (int64_t)snap) s_snhit[u] = 1;
-        }
-      }
-      hits += __popcll(__ballot(h));
+      // the accesses before the next fault hit (their bookkeeping is done at
+      // the end of the round: a lane's view no longer changes after its turn)
+      const uint64_t hm = __ballot(later && lane < f);
+      hitmask |= hm;
+      hits += __popcll(hm);
       if (f == 64) break;
       faults++;
       const int64_t pm = read_lane(a, f);
@@ -377,7 +369,20 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       wave_lds_order();
       cursor = f + 1;
     }
-    if (act && myhit) myhit[i] = hflag;
+    const bool hl = (hitmask >> lane) & 1;
+    if (act && myhit) myhit[i] = hl ? 1 : 0;
+    if (hl) {
+      // mark the hit insertion in the round's records or the flag copy, and
+      // in device memory if it is still resident (else its frame was refilled)
+      if (view >= I_rs) {
+        s_ihit[view - I_rs] = 1;
+      } else {
+        const int64_t u = view - (I_rs - F);
+        if (u >= 0 && u < (int64_t)snap) s_snhit[u] = 1;
+      }
+      if (view >= I - F) st(&c.fhit[fr], (uint8_t)1);
+    }
+    wave_lds_order();
     // evictions of the round: its insertions I_rs + u with I_rs + u >= F took
     // the frames of insertions I_rs - F + u -- made before the round (their
     // flags are in the copy) or, when u >= F, by the round itself (in its
