@@ -363,7 +363,7 @@ DEVI int64_t svc_sum(uint32_t g, uint32_t R, int64_t tR, int64_t tQ) {
 // depends on its rank in the call, so the tile aggregate is kept in global
 // form, max over the tile of issue - svc_sum(global rank), with the global
 // ranks of the tile's first requests taken from a count pass (tin_base).
-// LDS: ranges | wcnt[DWAVES][K] u16 | tot[K] u16 | cnt[K] u32 | amax[K] i64
+// LDS: ranges | amax[K] i64 | cmax[K] i64 | cnt[K] u32 | wcnt[DWAVES][K] u16 | tot[K] u16 | refp[K] u32
 template <bool POW2, bool REF>
 __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict__ addr,
                                                     const int64_t *__restrict__ issue, int64_t n,
@@ -382,6 +382,8 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
   uint32_t *cnt = (uint32_t *)(cmax + K);
   uint16_t *wcnt = (uint16_t *)(cnt + K);
   uint16_t *tot = wcnt + DWAVES * K;
+  // REF: pending quanta per key, read once per block (4-byte aligned: K may be odd)
+  uint32_t *refp = (uint32_t *)(((uintptr_t)(tot + K) + 3) & ~(uintptr_t)3);
 
   load_ranges(lr, rt);
   for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
@@ -389,6 +391,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
     cnt[k] = REF ? tin_base[(size_t)blockIdx.x * K + k] : 0;
     amax[k] = NEG;
     cmax[k] = NEG;
+    if (REF) refp[k] = st->ref_pend[k];
   }
   __syncthreads();
 
@@ -461,7 +464,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
         const uint32_t rc = mycnt[k] + rank[e];  // rank among key k in the chunk
         if (REF)
           atomicMax((long long *)&amax[k],
-                    (long long)(iss[e] - svc_sum(cnt[k] + rc, st->ref_pend[k], tR, g.tQ)));
+                    (long long)(iss[e] - svc_sum(cnt[k] + rc, refp[k], tR, g.tQ)));
         else
           atomicMax((long long *)&cmax[k], (long long)(iss[e] - (int64_t)mul32(rc, (uint32_t)tR)));
         KR[i] = (k << 16) | rc;
@@ -694,7 +697,7 @@ __global__ __launch_bounds__(BLK) void k_key_scan(const uint32_t *__restrict__ t
 //   KW[k] = {rbase: die rank (within the call) of k's first request in the
 //            chunk, pbase: its die-order position, lbo: k's column in the
 //            cell table, tot: k's requests in the call}
-// LDS: sval[CHUNKP] i64 | KA[K] | KW[K] | hist[K] u32 | skey, srank,
+// LDS: sval[CHUNKP] i64 | KA[K] | KW[K] | hist[K] u32 | refp[K] u32 | skey, srank,
 //      sloc [CHUNKP] u16
 constexpr int CHUNKP = CHUNK + CHUNK / 16;
 // Runs up to this length are scanned by one thread each; a chunk with a
@@ -730,7 +733,8 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
   KeyA *KA = (KeyA *)(sval + CHUNKP);
   KeyW *KW = (KeyW *)(KA + K);
   uint32_t *hist = (uint32_t *)(KW + K);
-  uint16_t *skey = (uint16_t *)(hist + K);
+  uint32_t *refp = hist + K;  // REF: pending quanta per key, read once per block
+  uint16_t *skey = (uint16_t *)(refp + K);
   uint16_t *srank = skey + CHUNKP;
   uint16_t *sloc = srank + CHUNKP;
 
@@ -741,6 +745,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
     KA[k] = KeyA{0u, 0u, tin_L[row + k]};
     const uint32_t ch = k / Dk;
     KW[k] = KeyW{base, seg_start[k] + base, ch * (gmax + 1) * Dk + (k - ch * Dk), totals[k]};
+    if (REF) refp[k] = st->ref_pend[k];
   }
   const int64_t cbase = ctl->cbase;
   const uint32_t shift = ctl->shift, G = ctl->G;
@@ -807,7 +812,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
         const uint32_t P = pad16(ka.koff + rc);
         int64_t v;
         if (REF) {
-          const uint32_t R = st->ref_pend[k], g0 = KW[k].rbase;
+          const uint32_t R = refp[k], g0 = KW[k].rbase;
           v = iss[e] - svc_sum(g0 + rc, R, g.tR, g.tQ);
           if (rc == 0) v = imax(v, ka.L - svc_sum(g0, R, g.tR, g.tQ));
         } else {
@@ -832,7 +837,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
         const KeyA ka = KA[k];
         int64_t run = NEG;
         if (REF) {
-          const uint32_t R = st->ref_pend[k], g0 = KW[k].rbase;
+          const uint32_t R = refp[k], g0 = KW[k].rbase;
           for (uint32_t q = 0; q < t; q++) {
             const uint32_t P = pad16(ka.koff + q);
             run = imax(run, sval[P]);
@@ -870,7 +875,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
           run = (rc == 0) ? vals[q] : imax(run, vals[q]);
           const uint32_t kk = skey[pad16(p)];
           if (REF)
-            sval[pad16(p)] = svc_sum(KW[kk].rbase + rc + 1, st->ref_pend[kk], g.tR, g.tQ) + run;
+            sval[pad16(p)] = svc_sum(KW[kk].rbase + rc + 1, refp[kk], g.tR, g.tQ) + run;
           else
             sval[pad16(p)] = (int64_t)mul32(KA[kk].cnt + rc + 1, tR) + run;
         }
@@ -895,7 +900,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
           IX[gpos] = ix;
         }
       }
-      if (REF && r < st->ref_pend[k])  // this admission claimed quantum r of k's pending ones
+      if (REF && r < refp[k])  // this admission claimed quantum r of k's pending ones
         *st->ref_slot[st->ref_off[k] + st->ref_head[k] + r] = dd - g.tR;
       const int64_t prev = (rc > 0) ? sval[pad16(p - 1)] : KA[k].L;
       const int64_t cell = imin((dd - cbase) >> shift, (int64_t)G);
@@ -1520,11 +1525,11 @@ static size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
 
 // LDS of pass 1: range table | amax[K], cmax[K] i64 | cnt[K] | wcnt[DWAVES][K] u16 | tot[K] u16
 size_t lds_die_reduce(uint32_t K) {
-  return align16(sizeof(LdsRanges)) + K * (8 + 8 + 4) + DWAVES * K * 2 + K * 2;
+  return align16(sizeof(LdsRanges)) + K * (8 + 8 + 4) + DWAVES * K * 2 + K * 2 + 4 + K * 4;
 }
 size_t lds_die_count(uint32_t K) { return align16(sizeof(LdsRanges)) + K * 4; }
 size_t lds_die_scatter(uint32_t K) {
-  return (size_t)CHUNKP * 8 + (size_t)K * (sizeof(KeyA) + sizeof(KeyW) + 4) + (size_t)CHUNKP * 6;
+  return (size_t)CHUNKP * 8 + (size_t)K * (sizeof(KeyA) + sizeof(KeyW) + 4 + 4) + (size_t)CHUNKP * 6;
 }
 
 hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout &Lo, char *ws,
