@@ -123,6 +123,35 @@ def closed_loop(torch, hbf, wl, steps=2, reps=3):
                 modeled_decode_step_ns=step_ns)
 
 
+def classify_leg(torch, model, w, addr, reps=5):
+    """Row a0 on its own: hbf_classify_map over the large stream (read the
+    address 8 B, write the map word 8 B per request), median of `reps` calls;
+    the words of a sample of requests are checked against the reference."""
+    from oracle import oracle
+    s = torch.cuda.current_stream()
+    mp = torch.empty_like(addr)
+    times = []
+    for r in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        assert model.classify_map(addr, mp, s) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+        if r:
+            times.append(e0.elapsed_time(e1))
+    assert model.get_status() == 0
+    ms = float(np.median(times))
+    o = oracle.OracleModel(**w.params)
+    for b, nb in w.ranges:
+        o.register_range(b, nb)
+    idx = np.random.default_rng(5).integers(0, w.n, 1 << 16)
+    rc, want = o.classify_map(w.addr[idx])
+    got = mp.cpu().numpy().view(np.uint64)[idx]
+    gbps = 16 * w.n / (ms / 1e3) / 1e9
+    return dict(requests=int(w.n), ms_per_call=ms, GBps=gbps, frac_of_hbm_peak=gbps / HBM_PEAK_GBPS,
+                parity_vs_reference_sample=bool(rc == 0 and np.array_equal(got, want)), sample=int(idx.size))
+
+
 def size_sweep_leg(torch, hbf, w, addr, issue, complete, reps=5):
     """hbf_time_requests on prefixes of the large stream (2^20 .. its full
     length): how the rate grows with the call size.  Median of `reps` calls
@@ -608,6 +637,8 @@ def main():
         out["small_configs"] = small_configs_leg(torch, hbf, wl)
         log("prefixes of the large stream")
         out["size_sweep"] = size_sweep_leg(torch, hbf, w, addr, issue, complete)
+        log("classify + map alone")
+        out["classify"] = classify_leg(torch, model, w, addr)
     if not args.no_closed_loop:
         log("closed-loop decode timing")
         out["closed_loop"] = closed_loop(torch, hbf, wl)

@@ -110,6 +110,26 @@ def test_config_classify_parity(torch, cfg):
     g.close()
 
 
+@pytest.mark.parametrize("start,count", [(0, 4095), (1, 4094), (1, 4095), (0, 1), (1, 1)])
+def test_classify_alignment_and_odd_lengths(torch, start, count):
+    """Both classify kernels: 16-byte-aligned arrays take two requests per
+    thread (an odd last one on its own); other alignments one each."""
+    w = wl.config1()
+    say(f"classify slice start={start} count={count}")
+    g = gpu_model(w.params, w.ranges)
+    o = oracle_model(w.params, w.ranges)
+    a = dev(torch, w.addr)
+    out = torch.full_like(a, -3)
+    assert g.classify_map(a[start:start + count], out[start:start + count]) == 0
+    assert g.get_status() == 0
+    rc, want = o.classify_map(w.addr[start:start + count])
+    assert rc == 0
+    got = out.cpu().numpy()
+    assert np.array_equal(got[start:start + count].view(np.uint64), want)
+    assert (got[:start] == -3).all() and (got[start + count:] == -3).all()
+    g.close()
+
+
 # ---------------------------------------------------------------- random suites
 
 GEOMS = [
