@@ -500,7 +500,7 @@ def main():
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); "
               "the timing path would shard by channel across GPUs, which is not built here.")
         sys.exit(2)
 
