@@ -169,19 +169,19 @@ __device__ __forceinline__ void butterfly(float *val, int lane) {
 }
 
 // The same operation for the expert shape of the MoE workloads (K = 2048,
-// 16 KiB pages of 4 rows) at batch BB = 1, 2, 4, 8 or 16.  Thread t of the
+// 16 KiB pages of 4 rows) at batch B <= BB, BB = 1, 2, 4, 8 or 16 (rows
+// b >= B are zero and not written).  Thread t of the
 // page's block holds the 16-byte column slice t of all 4 rows and of every
 // activation row, so each activation vector is read once per block (not once
 // per row) and feeds 4 dot products.  The activations are loaded right after
 // the page, before the wait.  The 4*BB partial sums of a lane are reduced
 // across the wave by a transposing butterfly (63 exchanges for 64 values
 // instead of 6 per value, all in registers), then across the 4 waves
-// through LDS.  (Blocks of
-// 2 or 4 pages, sharing one activation load, measured slower at every batch:
-// fewer blocks in flight.)
-template <int BB>
+// through LDS.  (Blocks of 2 or 4 pages, sharing one activation load,
+// measured slower at every batch: fewer blocks in flight.)
+template <int BB, bool PAD>
 __global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__ W, int N,
-                                                    const uint16_t *__restrict__ X, float *__restrict__ Y,
+                                                    const uint16_t *__restrict__ X, int B_, float *__restrict__ Y,
                                                     const int64_t *__restrict__ pi, const int64_t *__restrict__ pc,
                                                     int64_t *__restrict__ meas, int64_t tick_ps, DevState *st) {
   constexpr int K = 2048, R = 4, V = R * BB;
@@ -209,10 +209,11 @@ __global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__
   uint4 v[R];
 #pragma unroll
   for (int r = 0; r < R; r++) v[r] = *(const uint4 *)(W + (size_t)(row0 + r) * K + (size_t)t * 8);
-  const uint16_t *xe = X + (size_t)e * BB * K + (size_t)t * 8;
+  const int B = PAD ? B_ : BB;  // the batch (PAD: B_ < BB rows, the rest zero)
+  const uint16_t *xe = X + (size_t)e * B * K + (size_t)t * 8;
   uint4 xv[BB];
 #pragma unroll
-  for (int b = 0; b < BB; b++) xv[b] = *(const uint4 *)(xe + (size_t)b * K);
+  for (int b = 0; b < BB; b++) xv[b] = b < B ? *(const uint4 *)(xe + (size_t)b * K) : make_uint4(0, 0, 0, 0);
 
   // ---- consumption point: wait for the modeled completion
   uint64_t now = __builtin_amdgcn_s_memrealtime();
@@ -236,7 +237,7 @@ __global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__
     const int src = t << (6 - LGV);
     const float sum = red[0][src] + red[1][src] + red[2][src] + red[3][src];
     const int r = t / BB, b = t - r * BB;
-    Y[((size_t)e * BB + b) * N + nb + r] = sum;
+    if (b < B) Y[((size_t)e * B + b) * N + nb + r] = sum;
   }
 }
 
@@ -245,10 +246,12 @@ hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, c
                        int64_t tick_ps, DevState *st, hipStream_t s) {
   const int R = page_bytes / (2 * K);
   const int64_t pages = (int64_t)E * N / R;
-  if (K == 2048 && R == 4 && (B == 1 || B == 2 || B == 4 || B == 8 || B == 16)) {
-    auto kfn = B == 1 ? k_gemv_k2048<1> : B == 2 ? k_gemv_k2048<2> : B == 4 ? k_gemv_k2048<4>
-             : B == 8 ? k_gemv_k2048<8> : k_gemv_k2048<16>;
-    hipLaunchKernelGGL(kfn, dim3((uint32_t)pages), dim3(256), 0, s, W, N, X, Y, pi, pc, meas, tick_ps, st);
+  if (K == 2048 && R == 4 && B >= 1 && B <= 16) {
+    auto kfn = B == 1 ? k_gemv_k2048<1, false> : B == 2 ? k_gemv_k2048<2, false>
+             : B == 4 ? k_gemv_k2048<4, false> : B == 8 ? k_gemv_k2048<8, false>
+             : B == 16 ? k_gemv_k2048<16, false> : B < 4 ? k_gemv_k2048<4, true>
+             : B < 8 ? k_gemv_k2048<8, true> : k_gemv_k2048<16, true>;
+    hipLaunchKernelGGL(kfn, dim3((uint32_t)pages), dim3(256), 0, s, W, N, X, B, Y, pi, pc, meas, tick_ps, st);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_gemv_instrumented, dim3((uint32_t)pages), dim3(256), 0, s, W, K, N, R, X, B, Y, pi,

@@ -47,10 +47,11 @@ def rel_l2(y, ref):
     return float(np.linalg.norm(y - ref) / np.linalg.norm(ref))
 
 
-@pytest.mark.parametrize("batch", [1, 2, 3, 4, 8, 16])
+@pytest.mark.parametrize("batch", [1, 2, 3, 4, 5, 8, 12, 16, 17])
 def test_gemv_with_modeled_delays(torch, batch):
     """Config 4: 8 experts x [768 x 2048] bf16, delays from the config-3 model
-    (batch 3 takes the general kernel, the others the K = 2048 one)."""
+    (batches up to 16 take the K = 2048 kernel, padded to 1, 2, 4, 8 or 16
+    rows; batch 17 the general one)."""
     from oracle import oracle
     from paper_2609_09800_amd import hbf
     say(f"gemv config4 batch={batch}")
