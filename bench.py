@@ -326,6 +326,17 @@ def capacity_leg(torch, hbf, wl, reps=2):
     cpu256 = time.perf_counter() - t
     b256 = [b for b, (f, p) in enumerate(zip(sframes, spref)) if (f, p) == (256, 7)][0]
     small_parity = bool(np.array_equal(ssv[b256], o256.counts()))
+
+    # every sweep member's five counters against the reference model (host)
+    def sweep_parity(fs, ps, got_counts):
+        ok, t0 = True, time.perf_counter()
+        for b, (f, p) in enumerate(zip(fs, ps)):
+            oc = oracle.OracleCache(f, p, R)
+            oc.access(pages, pf_cap=0)
+            ok = ok and bool(np.array_equal(got_counts[b], oc.counts()))
+        return ok, time.perf_counter() - t0
+    sweep_ok, sweep_cpu = sweep_parity(frames, pref, sv)
+    small_ok, small_cpu = sweep_parity(sframes, spref, ssv)
     h, m, pr, used, unused = (int(x) for x in got[:5])
     return dict(workload=f"two config-3 decode steps at batch 8 as a capacity stream: {n} accesses over {R} "
                          f"expert pages, {F} frames (half), prefetch {d} pages per fault",
@@ -334,11 +345,13 @@ def capacity_leg(torch, hbf, wl, reps=2):
                 parity_vs_reference=parity, reference_cpu_s=cpu_s, reference_cores=1,
                 sweep=dict(caches=len(frames), seconds=sweep_s,
                            cache_accesses_per_s=len(frames) * n / sweep_s,
+                           parity_vs_reference_all=sweep_ok, reference_cpu_s_all=sweep_cpu,
                            hit_share={f"{f}f/{p}p": float(sv[b, 0] / n) for b, (f, p) in
                                       enumerate(zip(frames, pref)) if p in (0, 7, 63)}),
                 small_sweep=dict(caches=len(sframes), frames=frs, prefetch=pfs, seconds=small_s,
                                  cache_accesses_per_s=len(sframes) * n / small_s,
                                  reference_cpu_s_one_cache_256f_7p=cpu256, parity_256f_7p=small_parity,
+                                 parity_vs_reference_all=small_ok, reference_cpu_s_all=small_cpu,
                                  hit_share_7p={str(f): float(ssv[b, 0] / n) for b, (f, p) in
                                                enumerate(zip(sframes, spref)) if p == 7}))
 
