@@ -3,8 +3,8 @@
 //
 // A capacity range is served from a bounded frame cache in HBM: an access
 // whose page is resident is a hit; otherwise it faults and its page is read
-// from the media.  The prefetcher then fetches the pages that follow the
-// faulting page.  Prefetch reads never enter the timing path, so this step
+// from the media.  The prefetcher then reads ahead the pages after the
+// faulting one.  Prefetch reads never enter the timing path, so this step
 // only decides which accesses become media reads.  Reading: F frames with
 // FIFO replacement (each insertion takes the frame filled longest ago; a hit
 // changes nothing); a fault on page p inserts p and then, for k = 1..d in
