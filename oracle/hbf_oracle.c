@@ -537,8 +537,8 @@ void orc_refresh_done(const orc_model *m, int64_t *done) {
 /* ---------------------------------------------------------------- capacity
  * Sections D5 and D6: a capacity range is served from a bounded frame cache
  * in HBM; an access whose page is not resident faults and reads it from the
- * media; the speculative prefetcher then fetches the pages that follow the
- * faulting page.  Prefetch reads never enter the timing path (D6), so the
+ * media; the speculative prefetcher then reads ahead the pages after the
+ * faulting one.  Prefetch reads never enter the timing path (D6), so the
  * cache only decides which accesses become media reads.  Readings (the paper
  * names no replacement policy and no prefetch depth):
  *  - pages are numbered within the capacity range, [0, range_pages);
