@@ -1,8 +1,8 @@
 /*
  * hbf.h -- C ABI of the MI355X (gfx950) HBF service-model hot path.
  *
- * HBFSim (arXiv 2609.09800) models High-Bandwidth Flash under real GPU
- * execution: applications register HBF address ranges, every access is
+ * HBFSim (arXiv 2609.09800) models High-Bandwidth Flash as a running GPU
+ * program sees it: applications register HBF address ranges, every access is
  * classified against them, and each in-range access is given a modeled
  * completion time by an online media model; the running kernel pays that
  * delay where it first consumes the value.  This library implements that
@@ -213,8 +213,8 @@ int hbf_gemv_instrumented(hbf_model_t model, const uint16_t *dev_W, int E, int K
 
 /* ---- Refresh traffic in the same queues (Section "D4: Retention, Refresh,
  * and Wear as Injected Latency": refresh read-rewrite pairs get ids of their
- * own, enter the same queues as the application's reads, and an admission
- * claims at most one refresh quantum, served before its own service).
+ * own, enter the same queues as the application's reads, and one
+ * admission can take a single refresh quantum along, served ahead of it).
  * Reading used here (the paper gives no refresh timing):
  *  - one quantum = the read and the rewrite of one device page; it occupies
  *    that page's die queue for tQ = t_read_ns + t_prog_ns and no channel

@@ -1,9 +1,9 @@
 // Instrumented bf16 grouped GEMV with HBF delay injection at consumption.
 //
 // HBFSim (arXiv 2609.09800, Section "D2: Preserving GPU Asynchrony") splits
-// an access into issue and consumption: the load is issued and the program
-// keeps going; the modeled latency is paid only where the loaded value is
-// first used.  Here each workgroup owns one weight page: its waves read the
+// an access into issue and consumption: after issuing a load the program
+// continues, and the modeled latency is charged only at the first use of the
+// loaded value.  Here each workgroup owns one weight page: its waves read the
 // wall clock, issue every load of the page, and only then wait -- right
 // before the first multiply that consumes the data -- until the page's
 // modeled delay has elapsed since the issue.  The wait is measured against
