@@ -300,9 +300,10 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
           }
         }
       }
-      // insertions: the least fixed point of ins_k = (L_k < I + c_k - F)
+      // insertions: the least fixed point of ins_k = (L_k < I + c_k - F);
+      // the first guess takes c_k = 1, which is exact for depth 1
       uint64_t msk = __ballot(cv && (lane == 0 || L < I + 1 - F));
-      while (true) {
+      while (d > 1) {
         const int64_t ck = (int64_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(msk >> 32),
                                                                __builtin_amdgcn_mbcnt_lo((uint32_t)msk, 0u));
         const uint64_t m2 = __ballot(cv && (lane == 0 || L < I + ck - F));
