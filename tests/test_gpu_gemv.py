@@ -86,6 +86,34 @@ def test_gemv_with_modeled_delays(torch, batch):
     assert derr <= 0.01, derr
 
 
+@pytest.mark.parametrize("K,N,batch", [(512, 64, 3), (4096, 32, 2), (1024, 48, 16)])
+def test_gemv_other_shapes_with_delays(torch, K, N, batch):
+    """The general kernel (16, 2 or 8 rows per 16 KiB page) with a delay per
+    page: every consumer waits at least its page's delay, and the product is
+    right."""
+    from oracle import oracle
+    from paper_2609_09800_amd import hbf
+    say(f"gemv K={K} N={N} batch={batch} with delays")
+    W, X = wl.config4_operands(seed=11, batch=batch, experts=2, K=K, N=N)
+    buf, Wd = device_weights(torch, W)
+    Xd = torch.from_numpy(X.view(np.int16)).cuda()
+    Y = torch.empty((2, batch, N), dtype=torch.float32, device="cuda")
+    m = hbf.Model(**wl.geometry(16, 8, 4))
+    assert m.register_range(Wd.data_ptr(), W.nbytes)[0] == 0
+    n_pages = W.nbytes // PAGE
+    rng = np.random.default_rng(K + N)
+    req = rng.integers(2_000, 60_000, n_pages).astype(np.int64)
+    pi = torch.zeros(n_pages, dtype=torch.int64, device="cuda")
+    pc = torch.from_numpy(req).cuda()
+    meas = torch.zeros(n_pages, dtype=torch.int64, device="cuda")
+    assert m.gemv_instrumented(Wd, Xd, Y, pi, pc, meas) == 0
+    assert m.get_status() == 0
+    assert rel_l2(Y.cpu().numpy().astype(np.float64), oracle.gemv_bf16(W, X)) <= 1e-3
+    got = meas.cpu().numpy()
+    assert np.all(got >= req)
+    assert abs(got.mean() - req.mean()) / req.mean() <= 0.01
+
+
 def test_gemv_without_delays(torch):
     """Both time pointers NULL: no wait, same numbers."""
     from oracle import oracle
