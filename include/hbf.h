@@ -197,14 +197,21 @@ int hbf_time_layers(hbf_model_t model, const uint64_t *dev_addr, int64_t n,
  *   16 rows per page, and N a multiple of the rows per page.
  * dev_page_issue_ns / dev_page_complete_ns: int64 per weight page
  *   (E*N*K*2 / page_bytes entries, page order of W), e.g. from
- *   hbf_time_requests.  Page q's consumer waits until
- *   (complete[q] - issue[q]) ns have elapsed since its loads were issued,
- *   measured on the GPU's constant-rate wall clock.  Both NULL: no delay.
- *   A page delay above 1 s is clamped to 1 s and reported as
- *   HBF_ERANGE_TIME by hbf_get_status (the GPU never spins longer).
- * dev_measured_delay_ns (nullable): int64 per page, the delay the
- *   consumer actually waited (wall-clock ticks * tick length), for
- *   injection-fidelity checks.
+ *   hbf_time_requests.  Every page of the call is issued at the call's
+ *   start: its time origin is the GPU wall clock (constant rate, see
+ *   hbf_wall_clock_tick_ps) at which the call's earliest workgroup began.
+ *   Page q's loads are issued before its first use, and that use waits
+ *   until origin + (complete[q] - issue[q]) ns.  The call runs on at most
+ *   as many workgroups as the GPU holds at once, each taking its pages in
+ *   ascending order of delay, so no page waits behind another page's delay.
+ *   Both NULL: no delay (one workgroup per page, no clock reads).  Times
+ *   outside [0, 2^62) or complete[q] < issue[q]: no wait for that page and
+ *   HBF_ERANGE_TIME from hbf_get_status; a delay above 1 s is clamped to
+ *   1 s and reported the same way (the GPU never spins longer).
+ * dev_measured_delay_ns (nullable, needs the time arrays): int64 per page,
+ *   the time from the call's origin to the page's release (wall-clock
+ *   ticks * tick length), for injection-fidelity checks.  Calls with delays
+ *   on one model must not overlap (they share the origin record).
  * 1 <= B <= 64, E >= 1. */
 int hbf_gemv_instrumented(hbf_model_t model, const uint16_t *dev_W, int E, int K, int N,
                           const uint16_t *dev_X, int B, float *dev_Y,

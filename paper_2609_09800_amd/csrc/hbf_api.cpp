@@ -107,6 +107,7 @@ static int ensure_device(hbf_model *m) {
   for (int c = 0; c < MAX_CHANNELS; c++) host[0].chan_free[c] = NEG;
   host[0].sticky = 0;
   host[0].pad = 0;
+  host[0].gemv_origin = 0;
   if (hipMemcpy(m->st, host.data(), sizeof(DevState), hipMemcpyHostToDevice) != hipSuccess) return HBF_EHIP;
   if (set_lds_limits(m->g.K) != hipSuccess) return HBF_EHIP;
   if (hipDeviceGetAttribute(&m->ncu, hipDeviceAttributeMultiprocessorCount, m->dev) != hipSuccess)
@@ -677,7 +678,7 @@ int hbf_gemv_instrumented(hbf_model_t m, const uint16_t *W, int E, int K, int N,
                           int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
                           void *stream) {
   if (!m || !W || !X || !Y || E < 1 || K < 1 || N < 1 || B < 1 || B > 64) return HBF_EINVAL;
-  if ((pi == nullptr) != (pc == nullptr)) return HBF_EINVAL;
+  if ((pi == nullptr) != (pc == nullptr) || (meas && !pi)) return HBF_EINVAL;
   const uint64_t pb = m->p.page_bytes;
   if (K % 512 || K > 4096 || pb % ((uint64_t)K * 2)) return HBF_EINVAL;
   const uint64_t rows_per_page = pb / ((uint64_t)K * 2);
@@ -685,8 +686,8 @@ int hbf_gemv_instrumented(hbf_model_t m, const uint16_t *W, int E, int K, int N,
   if (((uintptr_t)W) % pb || ((uintptr_t)X) % 16 || ((uintptr_t)Y) % 4) return HBF_EINVAL;
   int rc = ensure_device(m);
   if (rc) return rc;
-  return launch_gemv(W, E, K, N, (int)pb, X, B, Y, pi, pc, meas, m->tick_ps, m->st, (hipStream_t)stream) ==
-                 hipSuccess
+  return launch_gemv(W, E, K, N, (int)pb, X, B, Y, pi, pc, meas, m->tick_ps, m->st, m->ncu,
+                     (hipStream_t)stream) == hipSuccess
              ? HBF_OK
              : HBF_EHIP;
 }

@@ -3,12 +3,21 @@
 // HBFSim (arXiv 2609.09800, Section "D2: Preserving GPU Asynchrony") splits
 // an access into issue and consumption: after issuing a load the program
 // continues, and the modeled latency is charged only at the first use of the
-// loaded value.  Here each workgroup owns one weight page: its waves read the
-// wall clock, issue every load of the page, and only then wait -- right
-// before the first multiply that consumes the data -- until the page's
-// modeled delay has elapsed since the issue.  The wait is measured against
-// the GPU's constant-rate wall clock (s_memrealtime); no host clock is
-// involved, so no clock origins are mixed.
+// loaded value.  Here a workgroup issues every load of a weight page and
+// only then waits -- right before the first multiply that consumes the data
+// -- until the page's modeled completion.  Waits are measured on the GPU's
+// constant-rate wall clock (s_memrealtime); no host clock is involved, so no
+// clock origins are mixed.
+//
+// One time origin per call.  Every page of a call is issued at the call's
+// start, so page q is released at origin + (complete[q] - issue[q]), where
+// origin is one wall-clock reading taken by the call's first kernel (a
+// single thread, before any consumer starts).  With delays, the call runs
+// on persistent workgroups (at most as many as the GPU holds at once, so
+// none starts late behind a waiting one), each taking its pages in
+// ascending delay order.  No workgroup writes anything shared with another
+// (the origin is read-only to them); a last kernel turns the recorded
+// release clocks into delays from the origin.
 //
 // Y[e][b][n] = sum_k X[e][b][k] * W[e][n][k], bf16 inputs, fp32 accumulate.
 // Bandwidth bound (B flop per weight byte): packed bf16 dot instructions
@@ -24,6 +33,8 @@ constexpr int GEMV_MAXV = 8;  // 16-byte weight vectors held per lane
 // Longest delay one page may inject; longer requests are clamped to it and
 // reported (HBF_ERANGE_TIME) so that a bad time array can never stall the GPU.
 constexpr int64_t MAX_PAGE_DELAY_NS = 1000000000;
+// Pages one persistent workgroup may take (one per thread when ordering).
+constexpr int GEMV_MAXP = 256;
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
@@ -41,14 +52,64 @@ __device__ __forceinline__ float dot8(uint4 w, uint4 x) {
   return s;
 }
 
-// One block (4 wave64) per weight page of R = page_bytes / (2K) rows.
-// Wave w takes rows w, w+4, ...; lane l takes the 16-byte vectors
-// l, l+64, ... of each row (VPL = K/512 of them).
-__global__ __launch_bounds__(256) void k_gemv_instrumented(
-    const uint16_t *__restrict__ W, int K, int N, int R, const uint16_t *__restrict__ X, int B,
-    float *__restrict__ Y, const int64_t *__restrict__ pi, const int64_t *__restrict__ pc,
-    int64_t *__restrict__ meas, int64_t tick_ps, DevState *st) {
-  const int q = blockIdx.x;
+// ------------------------------------------------------------------ timing
+
+// Wall-clock ticks page q must wait: ceil((complete - issue) / tick).  Times
+// outside [0, 2^62) or a completion before the issue are errors (no wait,
+// HBF_ERANGE_TIME); delays above MAX_PAGE_DELAY_NS are clamped and reported.
+__device__ __forceinline__ uint64_t page_ticks(const int64_t *pi, const int64_t *pc, int q, int64_t tick_ps,
+                                               uint32_t *errb) {
+  const int64_t a = pi[q], b = pc[q];
+  if (a < 0 || b < 0 || a >= TIME_LIMIT || b >= TIME_LIMIT || b < a) {
+    *errb |= ERR_RANGE_TIME;
+    return 0;
+  }
+  int64_t d = b - a;
+  if (d > MAX_PAGE_DELAY_NS) {
+    d = MAX_PAGE_DELAY_NS;
+    *errb |= ERR_RANGE_TIME;
+  }
+  return (uint64_t)((d * 1000 + tick_ps - 1) / tick_ps);
+}
+
+// Consumption point of a delayed page: spin until `ticks` have passed since
+// the call's origin.  Returns the release clock.
+__device__ __forceinline__ uint64_t wait_release(uint64_t origin, uint64_t ticks) {
+  uint64_t now = __builtin_amdgcn_s_memrealtime();
+  while (now < origin || now - origin < ticks) {  // (a clock read below the origin waits too)
+    __builtin_amdgcn_s_sleep(1);
+    now = __builtin_amdgcn_s_memrealtime();
+  }
+  return now;
+}
+
+// First kernel of a delayed call: its time origin.
+__global__ void k_gemv_origin(DevState *st) {
+  if (threadIdx.x == 0) st->gemv_origin = __builtin_amdgcn_s_memrealtime();
+}
+
+// Last kernel of a delayed call with measurements: release clock -> delay
+// from the origin, in ns.
+__global__ __launch_bounds__(256) void k_gemv_measured(int64_t *__restrict__ meas, int npages, int64_t tick_ps,
+                                                       const DevState *st) {
+  const uint64_t o = st->gemv_origin;
+  const int q = blockIdx.x * 256 + threadIdx.x;
+  if (q < npages) {
+    const uint64_t rel = (uint64_t)meas[q];
+    meas[q] = rel < o ? 0 : (int64_t)((rel - o) * (uint64_t)tick_ps / 1000);
+  }
+}
+
+// ------------------------------------------------------------------ page bodies
+
+// General shape: one page of R = page_bytes / (2K) rows by one 256-thread
+// workgroup.  Wave w takes rows w, w+4, ...; lane l takes the 16-byte
+// vectors l, l+64, ... of each row (VPL = K/512 of them).  `wait` runs
+// between the page's loads and its first use.
+template <typename Wait>
+__device__ __forceinline__ void page_general(int q, const uint16_t *__restrict__ W, int K, int N, int R,
+                                             const uint16_t *__restrict__ X, int B, float *__restrict__ Y,
+                                             Wait wait) {
   const int row0 = q * R;
   const int e = row0 / N;
   const int nb = row0 - e * N;
@@ -57,20 +118,7 @@ __global__ __launch_bounds__(256) void k_gemv_instrumented(
   const int lane = threadIdx.x & 63;
   const int RPW = (R + 3) >> 2;
 
-  int64_t d = 0;
-  if (pi) {
-    d = pc[q] - pi[q];
-    if (d < 0) d = 0;
-    if (d > MAX_PAGE_DELAY_NS) {
-      d = MAX_PAGE_DELAY_NS;
-      if (threadIdx.x == 0) atomicOr(&st->sticky, ERR_RANGE_TIME);
-    }
-  }
-  // ceil(d ns / tick), tick in ps
-  const uint64_t ticks = (uint64_t)((d * 1000 + tick_ps - 1) / tick_ps);
-
-  // ---- issue: clock, then every load of this page
-  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  // ---- issue: every load of this page
   uint4 v[GEMV_MAXV];
 #pragma unroll
   for (int s = 0; s < GEMV_MAXV; s++) {
@@ -81,13 +129,8 @@ __global__ __launch_bounds__(256) void k_gemv_instrumented(
     else
       v[s] = make_uint4(0, 0, 0, 0);
   }
-  // ---- consumption point: wait for the modeled completion
-  uint64_t now = __builtin_amdgcn_s_memrealtime();
-  while (now - t0 < ticks) {
-    __builtin_amdgcn_s_sleep(1);
-    now = __builtin_amdgcn_s_memrealtime();
-  }
-  if (meas && w == 0 && lane == 0) meas[q] = (int64_t)((now - t0) * (uint64_t)tick_ps / 1000);
+  // ---- consumption point
+  wait();
 
   // ---- consume
   const uint16_t *xe = X + (size_t)e * B * K;
@@ -168,44 +211,29 @@ __device__ __forceinline__ void butterfly(float *val, int lane) {
   }
 }
 
-// The same operation for the expert shape of the MoE workloads (K = 2048,
-// 16 KiB pages of 4 rows) at batch B <= BB, BB = 1, 2, 4, 8 or 16 (rows
-// b >= B are zero and not written).  Thread t of the
-// page's block holds the 16-byte column slice t of all 4 rows and of every
-// activation row, so each activation vector is read once per block (not once
-// per row) and feeds 4 dot products.  The activations are loaded right after
-// the page, before the wait.  The 4*BB partial sums of a lane are reduced
-// across the wave by a transposing butterfly (63 exchanges for 64 values
-// instead of 6 per value, all in registers), then across the 4 waves
-// through LDS.  (Blocks of 2 or 4 pages, sharing one activation load,
-// measured slower at every batch: fewer blocks in flight.)
-template <int BB, bool PAD>
-__global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__ W, int N,
-                                                    const uint16_t *__restrict__ X, int B_, float *__restrict__ Y,
-                                                    const int64_t *__restrict__ pi, const int64_t *__restrict__ pc,
-                                                    int64_t *__restrict__ meas, int64_t tick_ps, DevState *st) {
+// The expert shape of the MoE workloads (K = 2048, 16 KiB pages of 4 rows)
+// at batch B <= BB, BB = 1, 2, 4, 8 or 16 (rows b >= B are zero and not
+// written).  Thread t of the page's workgroup holds the 16-byte column slice
+// t of all 4 rows and of every activation row, so each activation vector is
+// read once per workgroup (not once per row) and feeds 4 dot products.  The
+// activations are loaded right after the page, before the wait.  The 4*BB
+// partial sums of a lane are reduced across the wave by a transposing
+// butterfly (63 exchanges for 64 values instead of 6 per value, all in
+// registers), then across the 4 waves through LDS.  (Workgroups of 2 or 4
+// pages, sharing one activation load, measured slower at every batch: fewer
+// workgroups in flight.)
+template <int BB, bool PAD, typename Wait>
+__device__ __forceinline__ void page_k2048(int q, const uint16_t *__restrict__ W, int N,
+                                           const uint16_t *__restrict__ X, int B_, float *__restrict__ Y,
+                                           float (*red)[64], Wait wait) {
   constexpr int K = 2048, R = 4, V = R * BB;
   constexpr int LGV = V == 4 ? 2 : V == 8 ? 3 : V == 16 ? 4 : V == 32 ? 5 : 6;
-  __shared__ float red[4][64];
-  const int q = blockIdx.x;
   const int row0 = q * R;
   const int e = row0 / N;
   const int nb = row0 - e * N;
   const int t = threadIdx.x, w = t >> 6, lane = t & 63;
 
-  int64_t d = 0;
-  if (pi) {
-    d = pc[q] - pi[q];
-    if (d < 0) d = 0;
-    if (d > MAX_PAGE_DELAY_NS) {
-      d = MAX_PAGE_DELAY_NS;
-      if (t == 0) atomicOr(&st->sticky, ERR_RANGE_TIME);
-    }
-  }
-  const uint64_t ticks = (uint64_t)((d * 1000 + tick_ps - 1) / tick_ps);
-
-  // ---- issue: clock, then every load of this page, then the activations
-  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  // ---- issue: every load of this page, then the activations
   uint4 v[R];
 #pragma unroll
   for (int r = 0; r < R; r++) v[r] = *(const uint4 *)(W + (size_t)(row0 + r) * K + (size_t)t * 8);
@@ -215,13 +243,8 @@ __global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__
 #pragma unroll
   for (int b = 0; b < BB; b++) xv[b] = b < B ? *(const uint4 *)(xe + (size_t)b * K) : make_uint4(0, 0, 0, 0);
 
-  // ---- consumption point: wait for the modeled completion
-  uint64_t now = __builtin_amdgcn_s_memrealtime();
-  while (now - t0 < ticks) {
-    __builtin_amdgcn_s_sleep(1);
-    now = __builtin_amdgcn_s_memrealtime();
-  }
-  if (meas && t == 0) meas[q] = (int64_t)((now - t0) * (uint64_t)tick_ps / 1000);
+  // ---- consumption point
+  wait();
 
   // ---- consume: value index r*BB + b
   float val[V];
@@ -239,24 +262,150 @@ __global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__
     const int r = t / BB, b = t - r * BB;
     if (b < B) Y[((size_t)e * B + b) * N + nb + r] = sum;
   }
+  __syncthreads();  // red is reused by the workgroup's next page
+}
+
+// ------------------------------------------------------------------ schedulers
+
+// No delays: one workgroup per page, no clock reads.
+__global__ __launch_bounds__(256) void k_gemv_general(const uint16_t *__restrict__ W, int K, int N, int R,
+                                                      const uint16_t *__restrict__ X, int B,
+                                                      float *__restrict__ Y) {
+  page_general(blockIdx.x, W, K, N, R, X, B, Y, [] {});
+}
+
+template <int BB, bool PAD>
+__global__ __launch_bounds__(256) void k_gemv_k2048(const uint16_t *__restrict__ W, int N,
+                                                    const uint16_t *__restrict__ X, int B_,
+                                                    float *__restrict__ Y) {
+  __shared__ float red[4][64];
+  page_k2048<BB, PAD>(blockIdx.x, W, N, X, B_, Y, red, [] {});
+}
+
+// With delays: persistent workgroups.  Workgroup g owns pages g + i*G
+// (i < m <= GEMV_MAXP, G = gridDim.x) and serves them in ascending order of
+// their wait (ties by page).  `page(q, wait)` runs one page.
+template <typename Page>
+__device__ __forceinline__ void timed_pages(int npages, const int64_t *__restrict__ pi,
+                                            const int64_t *__restrict__ pc, int64_t *__restrict__ meas,
+                                            int64_t tick_ps, DevState *st, Page page) {
+  __shared__ uint64_t s_ticks[GEMV_MAXP];
+  __shared__ int s_order[GEMV_MAXP];
+  const int t = threadIdx.x;
+  const int G = gridDim.x, g = blockIdx.x;
+  const uint64_t origin = st->gemv_origin;
+  const int m = (npages - g + G - 1) / G;
+  uint32_t errb = 0;
+  uint64_t mine = 0;
+  if (t < m) {
+    mine = page_ticks(pi, pc, g + t * G, tick_ps, &errb);
+    s_ticks[t] = mine;
+  }
+  __syncthreads();
+  if (t < m) {  // rank among the workgroup's pages by (ticks, position)
+    int r = 0;
+    for (int j = 0; j < m; j++) {
+      const uint64_t o = s_ticks[j];
+      r += (o < mine || (o == mine && j < t)) ? 1 : 0;
+    }
+    s_order[r] = t;
+  }
+  __syncthreads();
+  for (int i = 0; i < m; i++) {
+    const int li = s_order[i];
+    const int q = g + li * G;
+    const uint64_t ticks = s_ticks[li];
+    page(q, [&] {
+      const uint64_t rel = wait_release(origin, ticks);
+      if (meas && t == 0) meas[q] = (int64_t)rel;  // release clock; a delay after k_gemv_measured
+    });
+  }
+  if (errb) atomicOr(&st->sticky, errb);
+}
+
+__global__ __launch_bounds__(256) void k_gemv_general_timed(const uint16_t *__restrict__ W, int K, int N, int R,
+                                                            const uint16_t *__restrict__ X, int B,
+                                                            float *__restrict__ Y, int npages,
+                                                            const int64_t *__restrict__ pi,
+                                                            const int64_t *__restrict__ pc,
+                                                            int64_t *__restrict__ meas, int64_t tick_ps,
+                                                            DevState *st) {
+  timed_pages(npages, pi, pc, meas, tick_ps, st,
+              [&](int q, auto wait) { page_general(q, W, K, N, R, X, B, Y, wait); });
+}
+
+template <int BB, bool PAD>
+__global__ __launch_bounds__(256) void k_gemv_k2048_timed(const uint16_t *__restrict__ W, int N,
+                                                          const uint16_t *__restrict__ X, int B_,
+                                                          float *__restrict__ Y, int npages,
+                                                          const int64_t *__restrict__ pi,
+                                                          const int64_t *__restrict__ pc,
+                                                          int64_t *__restrict__ meas, int64_t tick_ps,
+                                                          DevState *st) {
+  __shared__ float red[4][64];
+  timed_pages(npages, pi, pc, meas, tick_ps, st,
+              [&](int q, auto wait) { page_k2048<BB, PAD>(q, W, N, X, B_, Y, red, wait); });
+}
+
+// Persistent grid of a timed kernel: as many workgroups as the GPU holds at
+// once, but at least enough that none owns more than GEMV_MAXP pages.
+static hipError_t timed_grid(const void *fn, int ncu, int64_t pages, uint32_t *grid) {
+  int per_cu = 0;
+  const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 256, 0);
+  if (e != hipSuccess) return e;
+  int64_t gsz = (int64_t)(per_cu > 0 ? per_cu : 1) * (ncu > 0 ? ncu : 1);
+  if (gsz > pages) gsz = pages;
+  const int64_t need = (pages + GEMV_MAXP - 1) / GEMV_MAXP;
+  if (gsz < need) gsz = need;
+  *grid = (uint32_t)gsz;
+  return hipSuccess;
+}
+
+static hipError_t finish_measured(int64_t *meas, int64_t pages, int64_t tick_ps, const DevState *st,
+                                  hipStream_t s) {
+  if (meas)
+    hipLaunchKernelGGL(k_gemv_measured, dim3((uint32_t)((pages + 255) / 256)), dim3(256), 0, s, meas, (int)pages,
+                       tick_ps, st);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
                        int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
-                       int64_t tick_ps, DevState *st, hipStream_t s) {
+                       int64_t tick_ps, DevState *st, int ncu, hipStream_t s) {
   const int R = page_bytes / (2 * K);
   const int64_t pages = (int64_t)E * N / R;
+  const bool timed = pi != nullptr;
   if (K == 2048 && R == 4 && B >= 1 && B <= 16) {
-    auto kfn = B == 1 ? k_gemv_k2048<1, false> : B == 2 ? k_gemv_k2048<2, false>
-             : B == 4 ? k_gemv_k2048<4, false> : B == 8 ? k_gemv_k2048<8, false>
-             : B == 16 ? k_gemv_k2048<16, false> : B < 4 ? k_gemv_k2048<4, true>
-             : B < 8 ? k_gemv_k2048<8, true> : k_gemv_k2048<16, true>;
-    hipLaunchKernelGGL(kfn, dim3((uint32_t)pages), dim3(256), 0, s, W, N, X, B, Y, pi, pc, meas, tick_ps, st);
+    if (!timed) {
+      auto kfn = B == 1 ? k_gemv_k2048<1, false> : B == 2 ? k_gemv_k2048<2, false>
+               : B == 4 ? k_gemv_k2048<4, false> : B == 8 ? k_gemv_k2048<8, false>
+               : B == 16 ? k_gemv_k2048<16, false> : B < 4 ? k_gemv_k2048<4, true>
+               : B < 8 ? k_gemv_k2048<8, true> : k_gemv_k2048<16, true>;
+      hipLaunchKernelGGL(kfn, dim3((uint32_t)pages), dim3(256), 0, s, W, N, X, B, Y);
+      return hipGetLastError();
+    }
+    auto kfn = B == 1 ? k_gemv_k2048_timed<1, false> : B == 2 ? k_gemv_k2048_timed<2, false>
+             : B == 4 ? k_gemv_k2048_timed<4, false> : B == 8 ? k_gemv_k2048_timed<8, false>
+             : B == 16 ? k_gemv_k2048_timed<16, false> : B < 4 ? k_gemv_k2048_timed<4, true>
+             : B < 8 ? k_gemv_k2048_timed<8, true> : k_gemv_k2048_timed<16, true>;
+    uint32_t grid = 0;
+    hipError_t e = timed_grid((const void *)kfn, ncu, pages, &grid);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_gemv_origin, dim3(1), dim3(64), 0, s, st);
+    hipLaunchKernelGGL(kfn, dim3(grid), dim3(256), 0, s, W, N, X, B, Y, (int)pages, pi, pc, meas, tick_ps, st);
+    return finish_measured(meas, pages, tick_ps, st, s);
+  }
+  if (!timed) {
+    hipLaunchKernelGGL(k_gemv_general, dim3((uint32_t)pages), dim3(256), 0, s, W, K, N, R, X, B, Y);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_gemv_instrumented, dim3((uint32_t)pages), dim3(256), 0, s, W, K, N, R, X, B, Y, pi,
-                     pc, meas, tick_ps, st);
-  return hipGetLastError();
+  uint32_t grid = 0;
+  hipError_t e = timed_grid((const void *)k_gemv_general_timed, ncu, pages, &grid);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_gemv_origin, dim3(1), dim3(64), 0, s, st);
+  hipLaunchKernelGGL(k_gemv_general_timed, dim3(grid), dim3(256), 0, s, W, K, N, R, X, B, Y, (int)pages, pi, pc,
+                     meas, tick_ps, st);
+  return finish_measured(meas, pages, tick_ps, st, s);
 }
 
 }  // namespace hbf

@@ -85,6 +85,9 @@ struct DevState {
   uint32_t ref_head[MAX_KEYS];
   uint32_t ref_off[MAX_KEYS];
   int64_t **ref_slot;
+  // Instrumented GEMV with delays: the time origin of the current call
+  // (wall-clock ticks, read by the call's first kernel).
+  uint64_t gemv_origin;
 };
 
 // Completion cell of a refresh quantum that has not been served.
@@ -143,7 +146,7 @@ hipError_t launch_layer_done(const CallCtl *ctl, int64_t count, const int64_t *p
                              int64_t compute_ns, int64_t *done, hipStream_t s);
 hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, const uint16_t *X,
                        int B, float *Y, const int64_t *pi, const int64_t *pc, int64_t *meas,
-                       int64_t tick_ps, DevState *st, hipStream_t s);
+                       int64_t tick_ps, DevState *st, int ncu, hipStream_t s);
 // Capacity-mode frame cache (hbf_cache.hip).  Caches of up to
 // CACHE_LDS_MAX frames: the page held by each frame (-1 empty) and a
 // prefetched-and-not-yet-hit flag per frame, loaded into LDS per call.

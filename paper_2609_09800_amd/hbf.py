@@ -124,6 +124,35 @@ def _check(code, what):
     return code
 
 
+def _dev(t, what, dtypes, numel=None, shape=None, at_least=False):
+    """Fail-closed argument check (Section D1) before any pointer reaches the
+    library, which cannot see array lengths: `t` must be a contiguous tensor
+    on the GPU with one of `dtypes` (names) and, when given, exactly `numel`
+    elements (at least that many with at_least) or exactly `shape`.  Raises
+    HbfError(HBF_EINVAL) otherwise."""
+    import torch
+    bad = None
+    if not isinstance(t, torch.Tensor):
+        bad = f"not a tensor ({type(t).__name__})"
+    elif not t.is_cuda:
+        bad = "not in GPU memory"
+    elif str(t.dtype).replace("torch.", "") not in dtypes:
+        bad = f"dtype {t.dtype}, expected {'/'.join(dtypes)}"
+    elif not t.is_contiguous():
+        bad = "not contiguous"
+    elif shape is not None and tuple(t.shape) != tuple(shape):
+        bad = f"shape {tuple(t.shape)}, expected {tuple(shape)}"
+    elif numel is not None and (t.numel() < numel if at_least else t.numel() != numel):
+        bad = f"{t.numel()} elements, expected {'at least ' if at_least else ''}{numel}"
+    if bad is not None:
+        raise HbfError(HBF_EINVAL, f"{what}: {bad}")
+    return t
+
+
+_W64 = ("int64", "uint64")   # 8-byte words (addresses are uint64 bit patterns)
+_I64 = ("int64",)
+
+
 class Model:
     """An HBF device model on the current GPU (owns one C handle)."""
 
@@ -183,16 +212,20 @@ class Model:
     def set_workspace(self, tensor):
         if tensor is None:
             return self._lib.hbf_set_workspace(self._h, None, 0)
+        _dev(tensor, "workspace", ("uint8", "int8", "int16", "int32", "int64", "float32"))
         return self._lib.hbf_set_workspace(self._h, _dp(tensor), tensor.numel() * tensor.element_size())
 
     def classify_map(self, addr, out, stream=None):
         """addr: uint64-valued int64 tensor [n] (device); out: int64 tensor [n]."""
+        _dev(addr, "addr", _W64)
+        _dev(out, "map_out", _W64, numel=addr.numel())
         return self._lib.hbf_classify_map(self._h, _dp(addr), addr.numel(), _dp(out), _sp(stream))
 
     def time_requests(self, addr, issue, complete, stream=None):
         """addr/issue/complete: int64 device tensors [n] (addr holds uint64 bit patterns)."""
-        n = addr.numel()
-        assert issue.numel() == n and complete.numel() == n
+        n = _dev(addr, "addr", _W64).numel()
+        _dev(issue, "issue_ns", _I64, numel=n)
+        _dev(complete, "complete_ns", _I64, numel=n)
         return self._lib.hbf_time_requests(self._h, _dp(addr), _dp(issue), n, _dp(complete), _sp(stream))
 
     def time_layers(self, addr, layer_start, t_start_ns, compute_ns, issue, complete, layer_done, stream=None):
@@ -201,16 +234,38 @@ class Model:
         import numpy as np
         ls = np.ascontiguousarray(layer_start, dtype=np.int64)
         L = ls.size - 1
-        n = addr.numel()
-        assert issue.numel() == n and complete.numel() == n and layer_done.numel() >= L
+        n = _dev(addr, "addr", _W64).numel()
+        _dev(issue, "issue_ns", _I64, numel=n)
+        _dev(complete, "complete_ns", _I64, numel=n)
+        _dev(layer_done, "layer_done_ns", _I64, numel=max(L, 0), at_least=True)
+        if ls.ndim != 1 or L < 0:
+            raise HbfError(HBF_EINVAL, "layer_start: one-dimensional, at least one entry")
         return self._lib.hbf_time_layers(self._h, _dp(addr), n, ls.ctypes.data_as(ctypes.c_void_p), L,
                                          t_start_ns, compute_ns, _dp(issue), _dp(complete), _dp(layer_done),
                                          _sp(stream))
 
     def gemv_instrumented(self, W, X, Y, page_issue=None, page_complete=None, measured=None, stream=None):
-        """W: int16 [E,N,K] (bf16 bits); X: int16 [E,B,K]; Y: float32 [E,B,N]."""
+        """W: int16 [E,N,K] (bf16 bits); X: int16 [E,B,K]; Y: float32 [E,B,N];
+        page_issue / page_complete (both or neither) and measured: int64
+        [E*N*K*2 / page_bytes], one entry per weight page."""
+        _dev(W, "W", ("int16", "uint16", "bfloat16"))
+        if W.dim() != 3:
+            raise HbfError(HBF_EINVAL, f"W: shape {tuple(W.shape)}, expected [E, N, K]")
         E, N, K = W.shape
+        _dev(X, "X", ("int16", "uint16", "bfloat16"))
+        if X.dim() != 3 or X.shape[0] != E or X.shape[2] != K:
+            raise HbfError(HBF_EINVAL, f"X: shape {tuple(X.shape)}, expected [{E}, B, {K}]")
         B = X.shape[1]
+        _dev(Y, "Y", ("float32",), shape=(E, B, N))
+        if (page_issue is None) != (page_complete is None):
+            raise HbfError(HBF_EINVAL, "page_issue and page_complete: both or neither")
+        if measured is not None and page_issue is None:
+            raise HbfError(HBF_EINVAL, "measured needs page_issue and page_complete")
+        pages = E * N * K * 2 // self.params.page_bytes
+        for t, nm in ((page_issue, "page_issue_ns"), (page_complete, "page_complete_ns"),
+                      (measured, "measured_delay_ns")):
+            if t is not None:
+                _dev(t, nm, _I64, numel=pages)
         return self._lib.hbf_gemv_instrumented(self._h, _dp(W), E, K, N, _dp(X), B, _dp(Y), _dp(page_issue),
                                                _dp(page_complete), _dp(measured), _sp(stream))
 
@@ -247,7 +302,8 @@ class Model:
         device tensor [len(pages)] receiving each quantum's completion."""
         import numpy as np
         pg = np.ascontiguousarray(pages, dtype=np.uint64)
-        assert done is None or done.numel() >= pg.size
+        if done is not None:
+            _dev(done, "done_ns", _I64, numel=pg.size, at_least=True)
         return self._lib.hbf_refresh_submit(self._h, pg.ctypes.data_as(ctypes.c_void_p) if pg.size else None,
                                             pg.size, _dp(done), _sp(stream))
 
@@ -300,7 +356,15 @@ class Cache:
     def access(self, pages, hit, counts, pf_page=None, pf_src=None, stream=None):
         """pages: int64 device tensor [n] (page numbers); hit: uint8 [n];
         counts: int64 [8]; pf_page / pf_src: int64 [cap] or None."""
+        n = _dev(pages, "pages", _W64).numel()
+        _dev(hit, "hit", ("uint8",), numel=n, at_least=True)
+        _dev(counts, "counts", _I64, numel=8, at_least=True)
+        if (pf_page is None) != (pf_src is None):
+            raise HbfError(HBF_EINVAL, "pf_page and pf_src: both or neither")
         cap = 0 if pf_page is None else pf_page.numel()
+        if pf_page is not None:
+            _dev(pf_page, "pf_page", _W64)
+            _dev(pf_src, "pf_src", _I64, numel=cap)
         return self._lib.hbf_cache_access(self._h, _dp(pages), pages.numel(), _dp(hit), _dp(pf_page), _dp(pf_src),
                                           cap, _dp(counts), _sp(stream))
 
@@ -312,7 +376,10 @@ def cache_sweep(frames, prefetch, range_pages, pages, counts, stream=None):
     lib = load_library()
     f = np.ascontiguousarray(frames, dtype=np.uint32)
     d = np.ascontiguousarray(prefetch, dtype=np.uint32)
-    assert f.size == d.size and counts.numel() >= 5 * f.size
+    if f.size != d.size:
+        raise HbfError(HBF_EINVAL, "frames and prefetch: one entry per cache each")
+    _dev(pages, "pages", _W64)
+    _dev(counts, "counts", _I64, numel=5 * f.size, at_least=True)
     return lib.hbf_cache_sweep(f.ctypes.data_as(ctypes.c_void_p), d.ctypes.data_as(ctypes.c_void_p), f.size,
                                range_pages, _dp(pages), pages.numel(), _dp(counts), _sp(stream))
 
