@@ -257,7 +257,10 @@ typedef struct {
  * served last, lowest first) that still has pages; a die's pages go in
  * (zone, block, plane, page) order.  host_pages_out receives
  * n_blocks * pages_per_block entries (capacity `cap`, else HBF_EINVAL).
- * Block fields out of the geometry: HBF_EINVAL. */
+ * Block fields out of the geometry: HBF_EINVAL.  A physical block
+ * (channel, die, plane, block) is eligible at most once per epoch, so a
+ * plan listing one twice in an epoch (under any zone) is refused with
+ * HBF_EINVAL; in different epochs it is refreshed once per epoch. */
 int hbf_refresh_plan(const hbf_params *params, const hbf_refresh_block *host_blocks, int64_t n_blocks,
                      uint32_t pages_per_block, uint64_t *host_pages_out, int64_t cap);
 

@@ -313,9 +313,20 @@ def refresh_plan(params, blocks, pages_per_block):
     that still have pages in ascending order; each visit takes one page from
     the channel's next die (cyclically after the die it served last, lowest
     first) that still has pages.  Within a die, pages follow (zone, block,
-    plane, page); a block listed twice is refreshed twice, entries in list
-    order."""
+    plane, page).
+
+    A physical block (channel, die, plane, block) is eligible at most once
+    per epoch: the order above places each eligible block once, so a plan
+    that lists one block twice in an epoch has no place in it and is
+    rejected (ValueError).  The same block in different epochs is refreshed
+    once per epoch."""
     C, D, P = params.channels, params.dies_per_channel, params.planes_per_die
+    seen = set()
+    for (e, zone, ch, die, plane, blk) in blocks:
+        if (e, ch, die, plane, blk) in seen:
+            raise ValueError(f"block (channel {ch}, die {die}, plane {plane}, block {blk}) listed twice "
+                             f"in epoch {e}")
+        seen.add((e, ch, die, plane, blk))
     out = []
     for epoch in sorted({b[0] for b in blocks}):
         per_die = {}

@@ -7,6 +7,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <new>
+#include <tuple>
 #include <vector>
 
 #include "hbf.h"
@@ -365,9 +366,20 @@ int hbf_refresh_plan(const hbf_params *params, const hbf_refresh_block *blocks, 
   if ((unsigned __int128)n_blocks * ppb > (unsigned __int128)cap) return HBF_EINVAL;
   for (int64_t b = 0; b < n_blocks; b++)
     if (blocks[b].channel >= C || blocks[b].die >= D || blocks[b].plane >= P) return HBF_EINVAL;
-  // per epoch: each die's pages in (zone, block, plane, page) order
   std::vector<int64_t> idx(n_blocks);
   for (int64_t b = 0; b < n_blocks; b++) idx[b] = b;
+  // a physical block is eligible at most once per epoch: the order places
+  // each eligible block once, so a block listed twice in an epoch is refused
+  {
+    auto phys = [&](int64_t x) {
+      const hbf_refresh_block &a = blocks[x];
+      return std::make_tuple(a.epoch, a.channel, a.die, a.plane, a.block);
+    };
+    std::sort(idx.begin(), idx.end(), [&](int64_t x, int64_t y) { return phys(x) < phys(y); });
+    for (int64_t i = 1; i < n_blocks; i++)
+      if (phys(idx[i - 1]) == phys(idx[i])) return HBF_EINVAL;
+  }
+  // per epoch: each die's pages in (zone, block, plane, page) order
   std::sort(idx.begin(), idx.end(), [&](int64_t x, int64_t y) {
     const hbf_refresh_block &a = blocks[x], &c = blocks[y];
     if (a.epoch != c.epoch) return a.epoch < c.epoch;

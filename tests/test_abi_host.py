@@ -192,6 +192,12 @@ def test_refresh_plan_hand_example(lib):
     assert rc == -1
     rc, out = hbf.refresh_plan(_plan_params(2, 2, 1), [], 4)
     assert rc == 0 and out.size == 0
+    # a block listed twice in one epoch (here under two zones) is refused;
+    # in two epochs it is refreshed once per epoch
+    rc, out = hbf.refresh_plan(_plan_params(2, 2, 1), [(0, 0, 1, 0, 0, 3), (0, 2, 1, 0, 0, 3)], 2)
+    assert rc == -1
+    rc, out = hbf.refresh_plan(_plan_params(2, 2, 1), [(1, 0, 1, 0, 0, 3), (0, 0, 1, 0, 0, 3)], 1)
+    assert rc == 0 and list(out) == [13, 13]
 
 
 @pytest.mark.parametrize("seed", range(6))
@@ -202,13 +208,25 @@ def test_refresh_plan_matches_reference(lib, oracle_mod, seed):
     C, D, P = [(4, 3, 2), (1, 1, 4), (8, 4, 1), (3, 5, 2), (2, 8, 4), (16, 2, 1)][seed]
     ppb = int(rng.integers(1, 5))
     nb = int(rng.integers(0, 60))
-    blocks = [(int(rng.integers(0, 3)), int(rng.integers(0, 3)), int(rng.integers(0, C)), int(rng.integers(0, D)),
-               int(rng.integers(0, P)), int(rng.integers(0, 6))) for _ in range(nb)]
-    rc, out = hbf.refresh_plan(_plan_params(C, D, P), blocks, ppb)
-    assert rc == 0
+    drawn = [(int(rng.integers(0, 3)), int(rng.integers(0, 3)), int(rng.integers(0, C)), int(rng.integers(0, D)),
+              int(rng.integers(0, P)), int(rng.integers(0, 6))) for _ in range(nb)]
 
     class Prm:
         channels, dies_per_channel, planes_per_die = C, D, P
+    # a block listed twice in one epoch: refused by both
+    key = lambda b: (b[0], b[2], b[3], b[4], b[5])   # noqa: E731
+    if len({key(b) for b in drawn}) < len(drawn):
+        rc, _ = hbf.refresh_plan(_plan_params(C, D, P), drawn, ppb)
+        assert rc == -1
+        with pytest.raises(ValueError):
+            oracle_mod.refresh_plan(Prm, drawn, ppb)
+    first = {}
+    for b in drawn:
+        first.setdefault(key(b), b)
+    blocks = list(first.values())
+    rng.shuffle(blocks)
+    rc, out = hbf.refresh_plan(_plan_params(C, D, P), blocks, ppb)
+    assert rc == 0
     assert [int(x) for x in out] == oracle_mod.refresh_plan(Prm, blocks, ppb)
 
 

@@ -208,6 +208,26 @@ def test_plan_order_hand_example(oracle_mod):
     assert oracle_mod.refresh_plan(_P(2, 2, 1), blocks, 2) == [8, 25, 2, 29, 12, 6, 0, 4]
 
 
+def test_plan_rejects_a_block_listed_twice_in_an_epoch(oracle_mod):
+    # Section D4 orders an epoch's eligible blocks by zone, block and page:
+    # each physical block (channel, die, plane, block) has one place in
+    # that order, so listing it twice in one epoch -- even under another
+    # zone -- names no order and is refused.  In two epochs it is two
+    # refreshes, one per epoch.
+    import pytest
+    twice = [(0, 0, 1, 0, 0, 3), (0, 2, 1, 0, 0, 3)]
+    with pytest.raises(ValueError):
+        oracle_mod.refresh_plan(_P(2, 2, 1), twice, 2)
+    with pytest.raises(ValueError):
+        oracle_mod.refresh_plan(_P(2, 2, 1), [(0, 0, 0, 1, 0, 0)] * 2, 1)
+    # epochs 0 and 1: C=2, D=2, P=1, 1 page per block; block 3 of (ch1, die0)
+    # is plane page 3 -> device page (3*2 + 0)*2 + 1 = 13, once per epoch
+    assert oracle_mod.refresh_plan(_P(2, 2, 1), [(1, 0, 1, 0, 0, 3), (0, 0, 1, 0, 0, 3)], 1) == [13, 13]
+    # the same block index on another plane, die or channel is another block
+    assert oracle_mod.refresh_plan(_P(2, 2, 2), [(0, 0, 1, 0, 0, 3), (0, 0, 1, 0, 1, 3)], 1) == [
+        ((3 * 2 + 0) * 2 + 0) * 2 + 1, ((3 * 2 + 1) * 2 + 0) * 2 + 1]
+
+
 def test_plan_order_zone_then_block_then_plane(oracle_mod):
     # one die, two planes: zone first, then block, then plane, then page
     blocks = [(0, 1, 0, 0, 0, 0), (0, 0, 0, 0, 1, 2), (0, 0, 0, 0, 0, 2), (0, 0, 0, 0, 1, 1)]
@@ -218,9 +238,13 @@ def test_plan_order_zone_then_block_then_plane(oracle_mod):
 def test_plan_order_properties(oracle_mod):
     rng = np.random.default_rng(9)
     C, D, P, ppb = 4, 3, 2, 3
-    blocks = sorted({(int(rng.integers(0, 3)), int(rng.integers(0, 2)), int(rng.integers(0, C)),
-                      int(rng.integers(0, D)), int(rng.integers(0, P)), int(rng.integers(0, 5)))
-                     for _ in range(40)})
+    drawn = [(int(rng.integers(0, 3)), int(rng.integers(0, 2)), int(rng.integers(0, C)),
+              int(rng.integers(0, D)), int(rng.integers(0, P)), int(rng.integers(0, 5))) for _ in range(40)]
+    # one entry per physical block and epoch (the first zone drawn)
+    first = {}
+    for b in drawn:
+        first.setdefault((b[0], b[2], b[3], b[4], b[5]), b)
+    blocks = sorted(first.values())
     out = oracle_mod.refresh_plan(_P(C, D, P), blocks, ppb)
 
     def dev(pl, b, j, d, c):
