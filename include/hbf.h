@@ -165,6 +165,26 @@ int hbf_classify_map(hbf_model_t model, const uint64_t *dev_addr, int64_t n, uin
 int hbf_time_requests(hbf_model_t model, const uint64_t *dev_addr, const int64_t *dev_issue_ns,
                       int64_t n, int64_t *dev_complete_ns, void *stream);
 
+/* ---- The same call without any allocation, for callers that cannot
+ * allocate (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid device allocation).  Arguments, results, device-detected
+ * errors and the model's clocks are those of hbf_time_requests; the call
+ * allocates nothing (no hipMalloc / hipFree, no workspace of the model, no
+ * profiling events).  Its scratch is one static device array of
+ * HBF_NOALLOC_SCRATCH_BYTES per GPU, held from the first such call on that
+ * GPU until the process ends and shared by every such call on it: calls
+ * that overlap on one GPU (other streams, other models) race on it and must
+ * be ordered by the caller.  Host-detected errors, before any launch:
+ * HBF_EINVAL for the arguments hbf_time_requests refuses, or if the
+ * model's device state does not exist yet on the current HIP device (any
+ * earlier call that launches work creates it, e.g. hbf_model_reset);
+ * HBF_ENOWORKSPACE if hbf_workspace_bytes(model, n) exceeds
+ * HBF_NOALLOC_SCRATCH_BYTES (up to about 4 M requests on the 16 x 8 x 4
+ * geometry, 2.9 M with 2,048 die queues). */
+#define HBF_NOALLOC_SCRATCH_BYTES (64ull << 20)
+int hbf_time_requests_noalloc(hbf_model_t model, const uint64_t *dev_addr, const int64_t *dev_issue_ns,
+                              int64_t n, int64_t *dev_complete_ns, void *stream);
+
 /* Closed-loop timing of a layered decode: the running program pays each
  * layer's modeled delays before it issues the next layer's reads (Section
  * "Introduction": delays are paid by the running program; Section D2: the

@@ -110,7 +110,8 @@ static int ensure_device(hbf_model *m) {
   host[0].pad = 0;
   host[0].gemv_origin = 0;
   if (hipMemcpy(m->st, host.data(), sizeof(DevState), hipMemcpyHostToDevice) != hipSuccess) return HBF_EHIP;
-  if (set_lds_limits(m->g.K) != hipSuccess) return HBF_EHIP;
+  // (for the largest die-queue count: models of any size may follow)
+  if (set_lds_limits(MAX_KEYS) != hipSuccess) return HBF_EHIP;
   if (hipDeviceGetAttribute(&m->ncu, hipDeviceAttributeMultiprocessorCount, m->dev) != hipSuccess)
     return HBF_EHIP;
   int rate_khz = 0;
@@ -121,13 +122,14 @@ static int ensure_device(hbf_model *m) {
   return HBF_OK;
 }
 
+// (no heap allocation: the no-allocation entry point takes snapshots too)
 static RangeTable snapshot(const hbf_model *m) {
   RangeTable rt;
   std::memset(&rt, 0, sizeof(rt));
   const int n = (int)m->rbase.size();
-  std::vector<int> idx(n);
+  int idx[MAX_RANGES];
   for (int i = 0; i < n; i++) idx[i] = i;
-  std::sort(idx.begin(), idx.end(), [&](int a, int b) { return m->rbase[a] < m->rbase[b]; });
+  std::sort(idx, idx + n, [&](int a, int b) { return m->rbase[a] < m->rbase[b]; });
   for (int i = 0; i < n; i++) {
     rt.base[i] = m->rbase[idx[i]];
     rt.bytes[i] = m->rbytes[idx[i]];
@@ -314,6 +316,22 @@ int hbf_time_requests(hbf_model_t m, const uint64_t *addr, const int64_t *issue,
   if (n == 0) return HBF_OK;
   if ((rc = ensure_ws(m, n))) return rc;
   return time_call(m, snapshot(m), addr, issue, n, complete, stream);
+}
+
+int hbf_time_requests_noalloc(hbf_model_t m, const uint64_t *addr, const int64_t *issue, int64_t n,
+                              int64_t *complete, void *stream) {
+  if (!m || n < 0 || n > N_LIMIT || (n > 0 && (!addr || !issue || !complete))) return HBF_EINVAL;
+  int dev = -1;
+  if (!m->st || hipGetDevice(&dev) != hipSuccess || dev != m->dev) return HBF_EINVAL;
+  if (n == 0) return HBF_OK;
+  const Layout L = make_layout(m->g, n);
+  if (L.total > HBF_NOALLOC_SCRATCH_BYTES) return HBF_ENOWORKSPACE;
+  char *ws = nullptr;
+  if (noalloc_scratch(dev, &ws) != hipSuccess) return HBF_EHIP;
+  return launch_time_requests(m->g, snapshot(m), L, ws, m->st, addr, issue, complete, (hipStream_t)stream,
+                              nullptr, 0, m->ref_maybe) == hipSuccess
+             ? HBF_OK
+             : HBF_EHIP;
 }
 
 int hbf_time_layers(hbf_model_t m, const uint64_t *addr, int64_t n, const int64_t *ls, int L,

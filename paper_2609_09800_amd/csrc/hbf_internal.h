@@ -136,6 +136,9 @@ hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX
                            hipStream_t s);
 hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s);
 hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
+// Device address of this GPU's static scratch of hbf_time_requests_noalloc
+// (HBF_NOALLOC_SCRATCH_BYTES); `dev` must be the current device.
+hipError_t noalloc_scratch(int dev, char **ptr);
 hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, const uint64_t *addr,
                            int64_t n, uint64_t *map, hipStream_t s);
 hipError_t launch_reset(DevState *st, hipStream_t s);

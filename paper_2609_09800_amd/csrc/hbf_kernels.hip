@@ -35,6 +35,8 @@
 // of width 2^floor(log2 t_read_ns) at most one: cells are bounded by
 // construction and merge without searching.
 #include <hip/hip_runtime.h>
+
+#include <mutex>
 #include <stdint.h>
 
 #include "hbf_internal.h"
@@ -1769,6 +1771,31 @@ hipError_t set_lds_limits(uint32_t K) {
 hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s) {
   hipLaunchKernelGGL(k_refresh_drain, dim3((g.K + BLK - 1) / BLK), dim3(BLK), 0, s, st, g.K, g.tQ, t_from, t_to);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ static scratch
+
+// Scratch of hbf_time_requests_noalloc: one array per GPU, held until the
+// process ends.  In host code `scratch` names a host-side stand-in, not a
+// device address; the device address comes from hipGetSymbolAddress, once
+// per device, with that device current.
+static __device__ __align__(256) char scratch[HBF_NOALLOC_SCRATCH_BYTES];
+constexpr int SCRATCH_DEVICES = 64;
+
+hipError_t noalloc_scratch(int dev, char **ptr) {
+  static std::mutex mu;
+  static char *addr[SCRATCH_DEVICES] = {};
+  if (dev < 0 || dev >= SCRATCH_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || (uintptr_t)p % 256) return hipErrorInvalidValue;
+    addr[dev] = (char *)p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s) {

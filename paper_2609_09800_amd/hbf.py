@@ -31,7 +31,9 @@ EXPORTED = [
     "hbf_get_state", "hbf_set_state", "hbf_profile", "hbf_kernel_times", "hbf_strerror",
     "hbf_refresh_plan", "hbf_refresh_configure", "hbf_refresh_submit", "hbf_refresh_drain", "hbf_refresh_pending",
     "hbf_cache_create", "hbf_cache_destroy", "hbf_cache_reset", "hbf_cache_access", "hbf_cache_sweep",
+    "hbf_time_requests_noalloc",
 ]
+HBF_NOALLOC_SCRATCH_BYTES = 64 << 20
 REFRESH_PENDING = -1
 
 
@@ -70,6 +72,7 @@ def load_library(path=LIB_PATH):
         "hbf_set_workspace": ([vp, vp, ctypes.c_size_t], i32),
         "hbf_classify_map": ([vp, vp, i64, vp, vp], i32),
         "hbf_time_requests": ([vp, vp, vp, i64, vp, vp], i32),
+        "hbf_time_requests_noalloc": ([vp, vp, vp, i64, vp, vp], i32),
         "hbf_gemv_instrumented": ([vp, vp, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp], i32),
         "hbf_wall_clock_tick_ps": ([vp, ctypes.POINTER(i64)], i32),
         "hbf_get_status": ([vp, vp], i32),
@@ -227,6 +230,16 @@ class Model:
         _dev(issue, "issue_ns", _I64, numel=n)
         _dev(complete, "complete_ns", _I64, numel=n)
         return self._lib.hbf_time_requests(self._h, _dp(addr), _dp(issue), n, _dp(complete), _sp(stream))
+
+    def time_requests_noalloc(self, addr, issue, complete, stream=None):
+        """hbf_time_requests through the entry point that allocates nothing
+        (static per-GPU scratch of HBF_NOALLOC_SCRATCH_BYTES; calls on one GPU
+        must not overlap)."""
+        n = _dev(addr, "addr", _W64).numel()
+        _dev(issue, "issue_ns", _I64, numel=n)
+        _dev(complete, "complete_ns", _I64, numel=n)
+        return self._lib.hbf_time_requests_noalloc(self._h, _dp(addr), _dp(issue), n, _dp(complete),
+                                                   _sp(stream))
 
     def time_layers(self, addr, layer_start, t_start_ns, compute_ns, issue, complete, layer_done, stream=None):
         """Closed-loop layers.  addr/issue/complete: int64 device tensors [n];
