@@ -9,6 +9,15 @@ One step = one pass of the whole hot path over one batch of synthetic input:
      grouped GEMV (8 x [768 x 2048], batch 16) that waits for those modeled
      completions at the point of consumption.
 Inputs are resident in HBM before timing starts.  Prints one JSON line.
+
+Beside the headline: the roofline of the dominant kernel (24 algorithmic
+bytes per request over its mean launch time), the whole call's algorithmic
+and counter-measured bandwidth, delay-injection fidelity from the call's
+common origin and the paper's paired 1,000 / 200 us increment timed with HIP
+events, config 3's open-loop MoE decode trace (44.6 M requests), the small
+streams, the next rows (closed loop, refresh, capacity cache, register
+blocking), and the reference model timed on the host on configs 1, 2, 3 and
+the large stream, with the SHA-256 of each of its outputs.
 """
 import argparse
 import hashlib
@@ -411,6 +420,109 @@ def blocking_leg(torch, hbf, wl, w, addr, issue, complete, reps=2):
                              parity_vs_reference=parity2, reference_cpu_s=cpu2, reference_cores=1))
 
 
+def config3_leg(torch, hbf, wl, reps=5, oracle_too=True):
+    """Config 3 open loop: the MoE decode weight-streaming trace (16 steps x
+    48 layers, Zipf(1.1) top-8 routing at batch 64, every active expert's
+    576 pages issued at its layer's time, 2 us per layer), about 44.6 M
+    requests in one hbf_time_requests call.  Median of `reps` calls of reset
+    + time_requests, checked against the reference digest; the reference
+    model times the same stream on one host core."""
+    gold_p = os.path.join(ROOT, "tests", "golden", "oracle_digests.json")
+    gold = json.load(open(gold_p)).get("config3") if os.path.exists(gold_p) else None
+    t = time.time()
+    w = wl.config3()
+    gen_s = time.time() - t
+    m = hbf.Model(**w.params)
+    for b, nb in w.ranges:
+        assert m.register_range(b, nb)[0] == 0
+    a = torch.from_numpy(w.addr.view(np.int64)).cuda()
+    i = torch.from_numpy(w.issue).cuda()
+    c = torch.empty_like(i)
+    s = torch.cuda.current_stream()
+    times = []
+    m.profile(True)
+    for r in range(reps + 1):
+        m.reset(s)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        assert m.time_requests(a, i, c, s) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+        if r:
+            times.append(e0.elapsed_time(e1))
+    kern = dict(m.kernel_times())
+    m.profile(False)
+    assert m.get_status() == 0
+    got_sha = sha(c.cpu().numpy())
+    ms = float(np.median(times))
+    n = int(w.n)
+    out = dict(workload="MoE decode weight-streaming trace (Qwen3-30B-A3B-shaped: 48 layers x 128 experts, "
+                        "top-8, Zipf 1.1, batch 64, 16 steps, 576 pages per expert, 2 us per layer), open loop, "
+                        "16ch x 8die x 4plane, tR 3000 ns, 8 GB/s/ch",
+               requests=n, ms_per_call=ms, requests_per_s=n / (ms / 1e3),
+               path_algorithmic_GBps=PATH_ALG_BYTES * n / (ms / 1e3) / 1e9,
+               path_algorithmic_frac=PATH_ALG_BYTES * n / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS,
+               kernel_ms=kern, complete_sha256=got_sha,
+               parity_vs_reference_digest=(got_sha == gold["complete_sha256"]) if gold else None,
+               input_gen_s=gen_s)
+    if oracle_too:
+        rate, dt, digest = oracle_time(w)
+        out["reference"] = dict(requests_per_s=rate, seconds=dt, cores=1, complete_sha256=digest,
+                                matches_gpu=digest == got_sha)
+    return out
+
+
+def small_oracle(wl):
+    """The reference model on configs 1 and 2 (whole streams, one core)."""
+    out = {}
+    for name, w in (("config1", wl.config1()), ("config2", wl.config2())):
+        rate, dt, digest = oracle_time(w)
+        out[name] = dict(requests=int(w.n), requests_per_s=rate, seconds=dt, cores=1, complete_sha256=digest)
+    return out
+
+
+def delay_increment_leg(torch, gm, Wd, Xd, Yd, pairs=36):
+    """The paper's paired increment (Section EQ1): every weight page of the
+    8-expert call injected with 1,000 us, then with 200 us, `pairs` times,
+    each call timed with HIP events on its stream (events never read the
+    wall clock the kernel waits on).  Error = |mean(t_1000 - t_200) - 800 us|
+    / 800 us.  Also reports the kernel's own mean measurement of the
+    1,000 us calls (from the call's common origin)."""
+    page = 16384
+    n_pages = Wd.numel() * 2 // page
+    s = torch.cuda.current_stream()
+    pi = torch.zeros(n_pages, dtype=torch.int64, device="cuda")
+    hi = torch.full((n_pages,), 1_000_000, dtype=torch.int64, device="cuda")
+    lo = torch.full((n_pages,), 200_000, dtype=torch.int64, device="cuda")
+    meas = torch.zeros(n_pages, dtype=torch.int64, device="cuda")
+
+    def call(pc):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        assert gm.gemv_instrumented(Wd, Xd, Yd, pi, pc, meas, stream=s) == 0
+        e1.record(s)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e6  # ns
+    call(lo)
+    inc, t_hi, own = [], [], []
+    for _ in range(pairs):
+        th = call(hi)
+        own.append(float(meas.cpu().numpy().mean()))
+        tl = call(lo)
+        inc.append(th - tl)
+        t_hi.append(th)
+    assert gm.get_status() == 0
+    inc = np.array(inc)
+    return dict(pairs=pairs, pages=n_pages, requested_increment_ns=800_000,
+                mean_increment_ns=float(inc.mean()),
+                increment_error_pct=float(abs(inc.mean() - 800_000) / 800_000 * 100),
+                increment_p5_p50_p95_ns=[float(np.percentile(inc, q)) for q in (5, 50, 95)],
+                call_1000us_hip_event_us=[float(min(t_hi) / 1e3), float(np.median(t_hi) / 1e3)],
+                kernel_mean_measured_1000us_ns=float(np.mean(own)),
+                paper_context="0.152 % on an NVIDIA RTX PRO 6000 Blackwell Server Edition (TMA, 8192 B, "
+                              "36 paired blocks); context only")
+
+
 def gemv_leg(torch, hbf, wl, sets=16, reps=3):
     """Row a5's bandwidth with no delay injected: the 8-expert grouped GEMV
     (8 x [768 x 2048] bf16, 24 MiB) over `sets` distinct weight sets in turn
@@ -467,28 +579,55 @@ def gemv_leg(torch, hbf, wl, sets=16, reps=3):
                          f"instrumented with every delay zero", **out)
 
 
-def cpu_baseline(w, n_sample):
+def host_cpu():
+    """The host CPU as lscpu names it, and the threads this process may use."""
+    import subprocess
+    model = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if model is None:
+        try:
+            for line in open("/proc/cpuinfo"):
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            model = "unknown"
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return dict(lscpu_model=model, nproc=usable, os_cpu_count=os.cpu_count())
+
+
+def oracle_time(w, n=None):
+    """The reference model (single-threaded C, gcc -O2) on the first n
+    requests of workload w: (requests/s, seconds, SHA-256 of complete_ns)."""
     from oracle import oracle
     m = oracle.OracleModel(**w.params)
     for b, nb in w.ranges:
         m.register_range(b, nb)
-    a, i = w.addr[:n_sample].copy(), w.issue[:n_sample].copy()
+    n = w.n if n is None else n
+    a, i = w.addr[:n].copy(), w.issue[:n].copy()
     t = time.perf_counter()
-    rc, _ = m.time_requests(a, i)
+    rc, c = m.time_requests(a, i)
     dt = time.perf_counter() - t
     assert rc == 0
-    cpu = "unknown"
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
-    return dict(value=n_sample / dt, unit="requests/s", cores=1, kind="oracle",
+    return n / dt, dt, sha(c)
+
+
+def cpu_baseline(w, n_sample, per_config):
+    rate, dt, digest = oracle_time(w, n_sample)
+    return dict(value=rate, unit="requests/s", cores=1, kind="oracle",
                 sample=f"first {n_sample} requests of the same stream, single-threaded C reference "
                        f"(gcc -O2), {dt:.2f} s",
-                host_cpu=cpu, host_threads=os.cpu_count())
+                complete_sha256=digest, host=host_cpu(), per_config=per_config)
 
 
 def main():
@@ -509,6 +648,7 @@ def main():
     ap.add_argument("--no-refresh", action="store_true", help="skip the refresh-plan report")
     ap.add_argument("--no-capacity", action="store_true", help="skip the capacity-mode frame cache report")
     ap.add_argument("--no-blocking", action="store_true", help="skip the register-blocking report")
+    ap.add_argument("--no-config3", action="store_true", help="skip the config 3 open-loop report")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -600,24 +740,40 @@ def main():
         if gold:
             parity = sha(complete.cpu().numpy()) == gold["complete_sha256"]
 
-    # delay injection fidelity of the last step
+    # delay injection fidelity of the last step: each page's release measured
+    # from the call's common origin, against its requested delay
     delay = None
     if not args.no_gemv:
         req = (pc_d - pi_d).cpu().numpy().astype(np.float64)
         got = meas.cpu().numpy().astype(np.float64)
-        delay = dict(pages=int(req.size), mean_requested_ns=float(req.mean()),
-                     mean_measured_ns=float(got.mean()),
+        late = got - req
+        # the GEMV call alone, timed with HIP events
+        gd = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            assert gm.gemv_instrumented(Wd, Xd, Yd, pi_d, pc_d, meas, stream) == 0
+            e1.record(stream)
+            e1.synchronize()
+            gd.append(e0.elapsed_time(e1) * 1e3)
+        delay = dict(pages=int(req.size), origin="one wall-clock reading per call, before any consumer starts",
+                     mean_requested_ns=float(req.mean()), mean_measured_ns=float(got.mean()),
                      error_pct=float(abs(got.mean() - req.mean()) / req.mean() * 100),
-                     mean_abs_rel_err_pct=float(np.mean(np.abs(got - req) / req) * 100),
-                     p50_err_ns=float(np.median(got - req)), p95_abs_err_ns=float(np.percentile(np.abs(got - req), 95)),
+                     mean_lateness_ns=float(late.mean()), p99_lateness_ns=float(np.percentile(late, 99)),
+                     max_lateness_ns=float(late.max()), released_early=int((late < 0).sum()),
+                     largest_requested_us=float(req.max() / 1e3),
+                     call_hip_event_us_median=float(np.median(gd)),
                      tick_ps=gm.wall_clock_tick_ps())
 
     n = w.n
     n_timed = n + (0 if args.no_gemv else n_pages)
     value = n_timed / (ms / 1e3)
-    dom = max(ALG_BYTES, key=lambda k: per_kernel.get(k, 0.0))
+    # roofline of the dominant kernel: the path's algorithmic bytes (24 B per
+    # request: read addr + issue, write complete) over that kernel's mean
+    # launch time, against 8 TB/s
+    dom = max(per_kernel, key=lambda k: per_kernel[k])
     dom_ms = per_kernel[dom]
-    achieved = ALG_BYTES[dom] * n / (dom_ms / 1e3) / 1e9
+    achieved = PATH_ALG_BYTES * n / (dom_ms / 1e3) / 1e9
     traffic = traffic_for(dom, n)
     tr_ms = sum(per_kernel.values())
     out = {
@@ -629,15 +785,18 @@ def main():
                                f"8x768x2048 batch {args.batch} with modeled delays",
                    "requests": n, "gemv_pages": 0 if args.no_gemv else n_pages},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": traffic, "alg_bytes_per_request": ALG_BYTES[dom]},
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+                     "alg_bytes_per_request": PATH_ALG_BYTES, "kernel_ms": dom_ms,
+                     "formula": "24 B x requests / dominant kernel mean launch time / 8000 GB/s"},
         "time_requests_ms": tr_ms,
         "time_requests_req_per_s": n / (tr_ms / 1e3),
         "path_algorithmic_GBps": PATH_ALG_BYTES * n / (tr_ms / 1e3) / 1e9,
         "path_algorithmic_frac": PATH_ALG_BYTES * n / (tr_ms / 1e3) / 1e9 / HBM_PEAK_GBPS,
         "path_counter_GBps": None,
         "path_counter_frac": None,
+        "path_traffic_over_algorithmic": None,
         "kernel_ms": per_kernel,
+        "kernel_alg_bytes_per_request": ALG_BYTES,
         "parity_vs_reference_digest": parity,
         "delay": delay,
     }
@@ -645,6 +804,13 @@ def main():
     if pt:  # counter-measured HBM bytes of the whole call / its kernels' time
         out["path_counter_GBps"] = pt / (tr_ms / 1e3) / 1e9
         out["path_counter_frac"] = out["path_counter_GBps"] / HBM_PEAK_GBPS
+        out["path_traffic_over_algorithmic"] = pt / (PATH_ALG_BYTES * n)
+    if not args.no_gemv:
+        log("paired delay increment (1,000 us vs 200 us)")
+        out["delay_increment"] = delay_increment_leg(torch, gm, Wd, Xd, Yd)
+    if not args.no_config3:
+        log("config 3 open loop (MoE decode trace)")
+        out["config3_open_loop"] = config3_leg(torch, hbf, wl, oracle_too=not args.no_cpu)
     if not args.no_small:
         log("small streams (cache-resident)")
         out["small_configs"] = small_configs_leg(torch, hbf, wl)
@@ -668,8 +834,12 @@ def main():
         log("register-blocking timing")
         out["register_blocking"] = blocking_leg(torch, hbf, wl, w, addr, issue, complete)
     if not args.no_cpu:
-        log("timing the reference model on the CPU sample")
-        out["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, n))
+        log("timing the reference model on the CPU sample and on configs 1 and 2")
+        per = small_oracle(wl)
+        if "config3_open_loop" in out and "reference" in out["config3_open_loop"]:
+            per["config3"] = dict(requests=out["config3_open_loop"]["requests"],
+                                  **out["config3_open_loop"]["reference"])
+        out["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, n), per)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out))
