@@ -55,6 +55,9 @@ Layout make_layout(const Geo &g, int64_t n) {
   L.off_lb = o;       o = up256(o + C * ((size_t)L.gmax + 1) * g.Dk * 4);
   L.off_cagg = o;     o = up256(o + C * (size_t)L.gmax * 8);
   L.off_cgin = o;     o = up256(o + C * (size_t)L.gmax * 8);
+  L.off_cmin = o;     o = up256(o + C * (size_t)L.gmax * 4);
+  L.off_cr0 = o;      o = up256(o + C * (size_t)L.gmax * 4);
+  L.off_nbl = o;      o = up256(o + C * (size_t)L.gmax * 4);
   L.off_iss = o;      o = up256(o + (g.reg_block ? (size_t)n * 8 : 0));
   L.total = o;
   return L;

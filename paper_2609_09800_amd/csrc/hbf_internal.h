@@ -102,6 +102,8 @@ struct CallCtl {
   int64_t max_dd;     // largest die-done time of the call
   int64_t max_cpl;    // largest in-range completion of the call (NEG if none)
   int64_t cbase;      // origin of the cell grid (= first issue time)
+  uint32_t n_rest;    // cells the window output pass leaves to k_cell_rest
+  uint32_t pad;
 };
 
 // Workspace layout of one hbf_time_requests call.
@@ -115,6 +117,8 @@ struct Layout {
   size_t off_totals, off_seg, off_dfnew, off_cfnew;
   size_t off_dd, off_ix, off_kr, off_lb;
   size_t off_cagg, off_cgin;  // per (channel, time cell): aggregate, entering term
+  size_t off_cmin, off_cr0;   // per cell: smallest request index (window staging), first channel rank
+  size_t off_nbl;             // cells the window output pass leaves to k_cell_rest
   size_t off_iss;             // register blocking: issue times in die order (n int64)
   size_t total;
 };

@@ -26,8 +26,10 @@
 //   k_cell_agg     per (channel, time cell): merge the cell's die runs by
 //                  (die-done, index) and reduce them to one channel term.
 //   k_cell_scan    per channel, the running maximum of those terms.
-//   k_cell_out     every cell again, with its entering term: write
-//                  complete[] in request order.
+//   k_cell_win     every cell again, with its entering term, one workgroup
+//                  per time window: write complete[] in request order
+//                  (staged by index in LDS where the window's requests
+//                  cluster); k_cell_rest takes the cells off the bucket path.
 //   k_finalize     fail-closed error fill, or commit of the new clocks.
 //
 // A die emits at most one request per t_read_ns, so a time cell of width
@@ -348,6 +350,7 @@ __global__ void k_prologue(CallCtl *ctl) {
     ctl->max_dd = NEG;
     ctl->max_cpl = NEG;
     ctl->cbase = 0;
+    ctl->n_rest = 0;
   }
 }
 
@@ -1129,7 +1132,8 @@ DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, bool
 // j' < j).  The stage runs as reduce, scan, reduce again:
 //   k_cell_agg   M_j of every cell;
 //   k_cell_scan  per channel, the running maximum of M_j seeded with f0;
-//   k_cell_out   every cell again, now writing complete[] with its term.
+//   k_cell_win   every cell again, now writing complete[] with its term
+//                (k_cell_rest: the cells the bucket path cannot take).
 // No block ever waits for another.
 //
 // One wave per cell.  The bucket path (buckets of width 2^lg_tR <= tR hold
@@ -1137,40 +1141,14 @@ DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, bool
 // die d's is at 1 + the byte the LDS table holds for (q, d) -- sorts them
 // in registers, and owns merged positions boff..boff+cnt-1 of the cell.
 // Cells that are too wide or too full stream through the LDS instead.
-#ifndef HBF_OUT_WCH
-#define HBF_OUT_WCH 0
-#endif
-constexpr uint32_t OUT_WCH = HBF_OUT_WCH;
 
-#ifndef HBF_OUT_WAVES_PER_CU
-#define HBF_OUT_WAVES_PER_CU 8
-#endif
-constexpr int OUT_WAVES_PER_CU = HBF_OUT_WAVES_PER_CU;
-
-// Cell of iteration `it` of this block.  OUT_WCH == 0: (window, channel)
-// order, grid-stride, so all blocks move along one common time front and
-// the scattered complete[] stores of requests that finish close in time
-// (close in request order, as a rule) meet in a bounded span of lines.
-// OUT_WCH > 0: XCD space x = block mod NXCD takes runs of OUT_WCH
-// consecutive windows (all channels), runs dealt round robin, so those
-// stores meet in one L2.
+// Cell of iteration `it` of this block: (window, channel) order,
+// grid-stride, so all blocks move along one common time front.
 DEVI bool cell_at(uint32_t it, uint32_t N, uint32_t C, uint32_t G, uint32_t &c, uint32_t &j) {
-  if (OUT_WCH == 0) {
-    const uint64_t cell = (uint64_t)blockIdx.x + (uint64_t)it * gridDim.x;
-    if (cell >= N) return false;
-    j = (uint32_t)cell / C;
-    c = (uint32_t)cell - j * C;
-    return true;
-  }
-  const uint32_t xcd = blockIdx.x % NXCD;
-  const uint32_t nfull = G / OUT_WCH, wrem = G % OUT_WCH;
-  const uint32_t wins = (nfull / NXCD + (xcd < nfull % NXCD ? 1u : 0u)) * OUT_WCH +
-                        (nfull % NXCD == xcd ? wrem : 0u);
-  const uint64_t i = (uint64_t)(blockIdx.x / NXCD) + (uint64_t)it * (gridDim.x / NXCD);
-  if (i >= (uint64_t)wins * C) return false;
-  const uint32_t lw = (uint32_t)i / C;
-  c = (uint32_t)i - lw * C;
-  j = ((lw / OUT_WCH) * NXCD + xcd) * OUT_WCH + lw % OUT_WCH;
+  const uint64_t cell = (uint64_t)blockIdx.x + (uint64_t)it * gridDim.x;
+  if (cell >= N) return false;
+  j = (uint32_t)cell / C;
+  c = (uint32_t)cell - j * C;
   return true;
 }
 
@@ -1215,6 +1193,15 @@ DEVI void load_runs(const int64_t *__restrict__ DD, const CellRuns &cr, int R, u
   }
 }
 
+// Whether the cell grid allows the bucket path at all: buckets of width
+// 2^lg_tR, at most 64 of them per cell, packed 32-bit cell offsets, and at
+// most SL die runs per channel.  A cell then takes it if no run holds more
+// than 64 of its requests.
+template <int SL>
+DEVI bool grid_bucketable(const Geo &g, uint32_t shift) {
+  return (shift - g.lg_tR <= 6) && shift <= 32 && g.lg_tR <= 20 && (int)g.Dk <= SL;
+}
+
 template <int SL, bool EMIT>
 DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX,
                        const CellRuns &cr, const uint64_t (&xv)[SL], const Geo &g, uint32_t shift,
@@ -1223,7 +1210,7 @@ DEVI int64_t cell_pass(CellLds &S, const int64_t *__restrict__ DD, const uint32_
   const uint32_t lane = lane_id();
   const uint32_t Dk = g.Dk;
   const uint32_t lgt = g.lg_tR;
-  const bool bucketable = (shift - lgt <= 6) && shift <= 32 && lgt <= 20 && (int)Dk <= SL;
+  const bool bucketable = grid_bucketable<SL>(g, shift);
   const int R = (int)Dk;
   const int64_t xfer = g.xfer;
   const int64_t cstart = cbase + ((int64_t)j << shift);
@@ -1333,22 +1320,49 @@ DEVI void cell_loop(const int64_t *__restrict__ DD, const uint32_t *__restrict__
   }
 }
 
+// Per cell, besides M_j: its first channel rank (CR0) and, for cells on the
+// bucket path, its smallest request index (CMIN; the heads of its die runs,
+// each run ascending in index), else CMIN_NONE -- cells with requests off
+// the bucket path are listed for k_cell_rest.
+constexpr uint32_t CMIN_NONE = 0xFFFFFFFFu;
+
 template <int SL>
 __global__ __launch_bounds__(64) void k_cell_agg(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals, Geo g,
-    const CallCtl *ctl, int64_t *__restrict__ AGG, uint32_t gmax, uint32_t n) {
+    CallCtl *ctl, int64_t *__restrict__ AGG, uint32_t *__restrict__ CMIN, uint32_t *__restrict__ CR0,
+    uint32_t *__restrict__ NBL, uint32_t gmax, uint32_t n) {
   extern __shared__ __align__(16) unsigned char smem[];
   CellLds &S = *(CellLds *)smem;
   if (agent_load32(&ctl->err)) return;
   const uint32_t G = ctl->G, N = G * g.C, shift = ctl->shift;
   const int64_t cbase = ctl->cbase;
+  const bool gb = grid_bucketable<SL>(g, shift);
   uint32_t errb = 0;
   cell_loop<SL>(DD, LB, seg_start, totals, g, gmax, N, G,
                 [&](uint32_t c, uint32_t j, const CellRuns &cr, const uint64_t (&xv)[SL]) {
                   const int64_t M = cell_pass<SL, false>(S, DD, IX, cr, xv, g, shift, cbase, j, NEG,
                                                          nullptr, n, &errb);
-                  if (lane_id() == 0) AGG[(size_t)c * gmax + j] = M;
+                  const uint32_t lane = lane_id();
+                  const uint32_t len = cr.hi - cr.lo;
+                  const uint32_t m = wave_sum(len);
+                  const uint32_t maxlen = wave_umax(lane < g.Dk ? len : 0u);
+                  uint32_t head = CMIN_NONE;
+#pragma unroll
+                  for (int d = 0; d < SL; d++) {
+                    const uint32_t lend = __builtin_amdgcn_readlane(len, d);
+                    const uint32_t ix = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)xv[d], 0);
+                    if (d < (int)g.Dk && lend > 0) head = min(head, ix);
+                  }
+                  const bool bk = gb && maxlen <= 64;
+                  const size_t cell = (size_t)c * gmax + j;
+                  const uint32_t rank0 = wave_sum(cr.r0);
+                  if (lane == 0) {
+                    AGG[cell] = M;
+                    CR0[cell] = rank0;
+                    CMIN[cell] = (bk && m > 0) ? head : CMIN_NONE;
+                    if (m > 0 && !bk) NBL[atomicAdd(&ctl->n_rest, 1u)] = j * g.C + c;
+                  }
                 });
 }
 
@@ -1384,23 +1398,228 @@ __global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ A
   }
 }
 
+// ---- Output pass.  The completions of one time window, over all channels,
+// fall in a narrow band of request indices (every die queue is served at
+// its own pace, so a window holds each queue's next few dozen requests).
+// One workgroup takes a whole window: its waves merge the window's cells
+// (bucket path) and stage each completion in LDS at its index's offset in
+// the band, as a 32-bit offset from a window base; the workgroup then
+// writes the band in index order, so each wave stores whole 128-byte lines
+// instead of one scattered 8-byte value per request (scattered stores are
+// served one address at a time, and several channels' stores landing in
+// one line from different XCDs cost partial-line writes).  Completions
+// outside the staged span, or whose offset does not fit 32 bits, are
+// stored directly.  Cells off the bucket path go to k_cell_rest.
+constexpr int WIN_WAVES = 16;
+constexpr int WIN_THREADS = WIN_WAVES * 64;
+constexpr uint32_t WIN_SLOTS = 32768;
+constexpr uint32_t WIN_EMPTY = 0xFFFFFFFFu;
+
+struct WinLds {
+  uint32_t stage[WIN_SLOTS];                         // completion - wbase at index lo + slot
+  uint8_t tbl[WIN_WAVES][MAX_BUCKETS][SLOTS_MAX];   // per wave: 1 + position in run d of bucket q's entry
+  uint32_t rmin[WIN_WAVES];
+  int64_t rbase[WIN_WAVES];
+  uint32_t top;                                      // staged slots in use
+};
+
+// Stage slot of band offset r.  One channel's requests often sit at a
+// fixed stride in the index space (sequential streams stripe over the
+// channels), so the offsets one store instruction writes can share their
+// low bits; XOR-ing in the next six bits spreads them over the LDS banks,
+// while each aligned group of 64 consecutive offsets stays a permutation of
+// itself (the write-out reads them conflict-free).
+DEVI uint32_t win_slot(uint32_t r) { return r ^ ((r >> 6) & 63u); }
+
+DEVI uint32_t wave_umin(uint32_t x) { return ~wave_umax(~x); }
+DEVI int64_t wave_min(int64_t x) { return -wave_max(-x); }
+
+// One bucketable cell of the window: merge its die runs in registers (lane q
+// gathers bucket q's entries from the lanes holding them, sorts them, and
+// owns merged positions boff..boff+cnt-1) and stage every completion.
 template <int SL>
-__global__ __launch_bounds__(64) void k_cell_out(
+DEVI void cell_emit_win(uint8_t (*tbl)[SLOTS_MAX], const CellRuns &cr, const uint64_t (&xv)[SL], const Geo &g,
+                        uint32_t shift, int64_t cbase, uint32_t j, int64_t gin, uint32_t lo, int64_t wbase,
+                        uint32_t *stage, int64_t *__restrict__ complete, uint32_t n, uint32_t *errb,
+                        uint32_t *top) {
+  const uint32_t lane = lane_id();
+  const int R = (int)g.Dk;
+  const uint32_t lgt = g.lg_tR;
+  const int64_t xfer = g.xfer;
+  const uint32_t len = cr.hi - cr.lo;
+  const uint32_t m = wave_sum(len);
+  if (m == 0) return;
+  const uint32_t maxlen = wave_umax(lane < (uint32_t)R ? len : 0u);
+  if (maxlen > 64) return;  // off the bucket path: k_cell_rest
+  const int64_t rank0 = wave_sum(cr.r0);
+  const int64_t cstart = cbase + ((int64_t)j << shift);
+  reinterpret_cast<uint4 *>(&tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
+  wave_sync();
+  // sort key of entry `lane` of run d: offset in its bucket (< 2^20) << 31 | index
+  const uint64_t offmask = (uint64_t(1) << lgt) - 1;
+  uint64_t key[SL];
+#pragma unroll
+  for (int d = 0; d < SL; d++) {
+    const uint32_t lend = __builtin_amdgcn_readlane(len, d);
+    const uint64_t rel = xv[d] >> 32;
+    key[d] = KEY_ONE | (rel & offmask) << 31 | (xv[d] & 0xFFFFFFFFull);
+    if (d < R && lane < lend) tbl[rel >> lgt][d] = (uint8_t)(lane + 1);
+  }
+  wave_sync();
+  uint64_t slot[SL];
+  uint32_t cnt = 0;
+  {
+    const uint4 row = reinterpret_cast<const uint4 *>(&tbl[0][0])[lane];
+    const uint32_t rw[4] = {row.x, row.y, row.z, row.w};
+#pragma unroll
+    for (int d = 0; d < SL; d++) {
+      const uint32_t y = (rw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
+      const uint64_t v = __shfl(key[d], y ? (int)(y - 1) : 0);
+      slot[d] = y ? v : KEY_EMPTY;
+      cnt += y ? 1u : 0u;
+    }
+  }
+  sort_slots<SL>(slot);
+  const uint32_t boff = wave_excl_sum(cnt);
+  const int64_t cst = cstart + ((int64_t)lane << lgt) - rank0 * xfer;
+  int64_t loc = NEG;
+#pragma unroll
+  for (int i = 0; i < SL; i++) {
+    if ((uint32_t)i < cnt) {
+      const int64_t v = cst + (int64_t)((slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+      loc = imax(loc, v);
+    }
+  }
+  int64_t carry = __shfl_up(wave_incl_max(loc), 1);
+  if (lane == 0) carry = NEG;
+  carry = imax(carry, gin);
+  const int64_t r0x = rank0 * xfer;
+  uint32_t mytop = 0;
+#pragma unroll
+  for (int i = 0; i < SL; i++) {
+    if ((uint32_t)i < cnt) {
+      const int64_t v = cst + (int64_t)((slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+      carry = imax(carry, v);
+      const int64_t cpl = r0x + (int64_t)mul32(boff + i + 1, (uint32_t)xfer) + carry;
+      if (cpl >= TIME_LIMIT) *errb |= ERR_OVERFLOW;
+      const uint32_t ix = (uint32_t)slot[i] & 0x7FFFFFFFu;
+      if (ix < n) {
+        const uint32_t rel = ix - lo;
+        const uint64_t off = (uint64_t)(cpl - wbase);
+        if (ix >= lo && rel < WIN_SLOTS && off < WIN_EMPTY) {
+          stage[win_slot(rel)] = (uint32_t)off;
+          mytop = max(mytop, rel + 1);
+        } else {
+          complete[ix] = cpl;
+        }
+      }
+    }
+  }
+  *top = max(*top, mytop);
+}
+
+template <int SL>
+__global__ __launch_bounds__(WIN_THREADS) void k_cell_win(
+    const int64_t *__restrict__ DD, const uint32_t *__restrict__ LB, const uint32_t *__restrict__ seg_start,
+    const uint32_t *__restrict__ totals, Geo g, CallCtl *ctl, const int64_t *__restrict__ GIN,
+    const uint32_t *__restrict__ CMIN, const uint32_t *__restrict__ CR0, int64_t *__restrict__ complete,
+    uint32_t gmax, uint32_t n) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  WinLds &S = *(WinLds *)smem;
+  if (agent_load32(&ctl->err)) return;
+  const uint32_t G = ctl->G, shift = ctl->shift, C = g.C;
+  if (!grid_bucketable<SL>(g, shift)) return;  // every cell is k_cell_rest's
+  const int64_t cbase = ctl->cbase, xfer = g.xfer;
+  const uint32_t t = threadIdx.x, w = t >> 6, lane = t & 63;
+  for (uint32_t q = t; q < WIN_SLOTS; q += WIN_THREADS) S.stage[q] = WIN_EMPTY;
+  uint32_t errb = 0;
+  // windows by rounds of gridDim.x; within a round each XCD (workgroup
+  // b runs on XCD b mod NXCD) takes a contiguous run of windows, so the
+  // direct stores of neighbouring windows, which share cache lines, meet in
+  // one L2 (measured: 2.71 ms against 2.78 ms round robin)
+  const uint32_t nb = gridDim.x;
+  const uint32_t first = nb % NXCD == 0 ? (blockIdx.x % NXCD) * (nb / NXCD) + blockIdx.x / NXCD : blockIdx.x;
+  for (uint32_t j = first; j < G; j += nb) {
+    // the window's band start (smallest index of its bucket-path cells) and
+    // completion base (a lower bound of every completion in them)
+    uint32_t mn = CMIN_NONE;
+    int64_t bmin = INT64_MAX;
+    for (uint32_t c = t; c < C; c += WIN_THREADS) {
+      const size_t cell = (size_t)c * gmax + j;
+      const uint32_t h = CMIN[cell];
+      if (h != CMIN_NONE) {
+        mn = min(mn, h);
+        bmin = imin(bmin, (int64_t)(CR0[cell] + 1u) * xfer + GIN[cell]);
+      }
+    }
+    mn = wave_umin(mn);
+    bmin = wave_min(bmin);
+    if (lane == 0) {
+      S.rmin[w] = mn;
+      S.rbase[w] = bmin;
+    }
+    if (t == 0) S.top = 0;
+    __syncthreads();
+    uint32_t lo = CMIN_NONE;
+    int64_t wbase = INT64_MAX;
+#pragma unroll
+    for (int k = 0; k < WIN_WAVES; k++) {
+      lo = min(lo, S.rmin[k]);
+      wbase = imin(wbase, S.rbase[k]);
+    }
+    if (lo != CMIN_NONE) {
+      uint32_t top = 0;
+      for (uint32_t c = w; c < C; c += WIN_WAVES) {
+        const CellRuns cr = cell_runs(LB, seg_start, totals, g.Dk, gmax, c, j);
+        uint64_t xv[SL];
+        load_runs<SL>(DD, cr, (int)g.Dk, xv);
+        cell_emit_win<SL>(S.tbl[w], cr, xv, g, shift, cbase, j, GIN[(size_t)c * gmax + j], lo, wbase, S.stage,
+                          complete, n, &errb, &top);
+        wave_sync();
+      }
+      top = wave_umax(top);
+      if (lane == 0 && top) atomicMax(&S.top, top);
+      __syncthreads();
+      const uint32_t used = S.top;
+      for (uint32_t q = t; q < used; q += WIN_THREADS) {
+        const uint32_t sq = win_slot(q);
+        const uint32_t v = S.stage[sq];
+        if (v != WIN_EMPTY) {
+          complete[lo + q] = wbase + (int64_t)v;
+          S.stage[sq] = WIN_EMPTY;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (errb) atomicOr(&ctl->err, errb);
+}
+
+// The cells the window pass leaves (off the bucket path): one wave each,
+// streamed through the LDS, completions stored directly.
+template <int SL>
+__global__ __launch_bounds__(64) void k_cell_rest(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals, Geo g, CallCtl *ctl,
-    const int64_t *__restrict__ GIN, int64_t *__restrict__ complete, uint32_t gmax, uint32_t n) {
+    const int64_t *__restrict__ GIN, const uint32_t *__restrict__ NBL, int64_t *__restrict__ complete,
+    uint32_t gmax, uint32_t n) {
   extern __shared__ __align__(16) unsigned char smem[];
   CellLds &S = *(CellLds *)smem;
   if (agent_load32(&ctl->err)) return;
-  const uint32_t G = ctl->G, N = G * g.C, shift = ctl->shift;
+  const uint32_t nr = agent_load32(&ctl->n_rest);
+  const uint32_t shift = ctl->shift;
   const int64_t cbase = ctl->cbase;
   uint32_t errb = 0;
-  cell_loop<SL>(DD, LB, seg_start, totals, g, gmax, N, G,
-                [&](uint32_t c, uint32_t j, const CellRuns &cr, const uint64_t (&xv)[SL]) {
-                  cell_pass<SL, true>(S, DD, IX, cr, xv, g, shift, cbase, j, GIN[(size_t)c * gmax + j],
-                                      complete, n, &errb);
-                });
-  if (errb && lane_id() == 0) atomicOr(&ctl->err, errb);
+  for (uint32_t i = blockIdx.x; i < nr; i += gridDim.x) {
+    const uint32_t id = NBL[i];
+    const uint32_t j = id / g.C, c = id - j * g.C;
+    const CellRuns cr = cell_runs(LB, seg_start, totals, g.Dk, gmax, c, j);
+    uint64_t xv[SL];
+    load_runs<SL>(DD, cr, (int)g.Dk, xv);
+    cell_pass<SL, true>(S, DD, IX, cr, xv, g, shift, cbase, j, GIN[(size_t)c * gmax + j], complete, n, &errb);
+    wave_sync();
+  }
+  if (errb) atomicOr(&ctl->err, errb);
 }
 
 // ------------------------------------------------------------------ k_finalize
@@ -1512,10 +1731,10 @@ __global__ __launch_bounds__(BLK) void k_fill(int64_t *__restrict__ p, int64_t n
 
 // ------------------------------------------------------------------ launchers
 
-const char *const kKernelNames[] = {"k_prologue",  "k_die_reduce", "k_tile_scan",
-                                    "k_key_scan",  "k_die_scatter", "k_cell_agg",
-                                    "k_cell_scan", "k_cell_out",    "k_finalize"};
-const int kNumTimedKernels = 9;
+const char *const kKernelNames[] = {"k_prologue",  "k_die_reduce", "k_tile_scan", "k_key_scan",
+                                    "k_die_scatter", "k_cell_agg",  "k_cell_scan", "k_cell_win",
+                                    "k_cell_rest", "k_finalize"};
+const int kNumTimedKernels = 10;
 
 static uint32_t bits_for(uint32_t K) {
   uint32_t b = 0;
@@ -1614,6 +1833,7 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
       return e;
     mark();
     mark();
+    mark();
   } else {
     // channel stage: enough one-wave blocks to fill the chip, a multiple of
     // the XCD count, and no more than there can be cells
@@ -1634,33 +1854,53 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
       if (blocks < NXCD) blocks = NXCD;
       return dim3((uint32_t)blocks);
     };
-    // the aggregate pass runs at full occupancy; the output pass keeps fewer
-    // cells in flight, which narrows the time front its scattered stores
-    // cover (measured: 8 waves per CU beat 4 and 15-24)
-    const dim3 gr = grid_of(per_cu), gro = grid_of(per_cu < OUT_WAVES_PER_CU ? per_cu : OUT_WAVES_PER_CU);
+    const dim3 gr = grid_of(per_cu);
     const dim3 bl(64);
     const size_t lds = sizeof(CellLds);
     const uint32_t nn = (uint32_t)Lo.n;
+    uint32_t *CMIN = (uint32_t *)(ws + Lo.off_cmin), *CR0 = (uint32_t *)(ws + Lo.off_cr0);
+    uint32_t *NBL = (uint32_t *)(ws + Lo.off_nbl);
     if (sl == 4)
-      hipLaunchKernelGGL(k_cell_agg<4>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, Lo.gmax, nn);
+      hipLaunchKernelGGL(k_cell_agg<4>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, CMIN, CR0, NBL,
+                         Lo.gmax, nn);
     else if (sl == 8)
-      hipLaunchKernelGGL(k_cell_agg<8>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, Lo.gmax, nn);
+      hipLaunchKernelGGL(k_cell_agg<8>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, CMIN, CR0, NBL,
+                         Lo.gmax, nn);
     else
-      hipLaunchKernelGGL(k_cell_agg<16>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, Lo.gmax, nn);
+      hipLaunchKernelGGL(k_cell_agg<16>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, CMIN, CR0, NBL,
+                         Lo.gmax, nn);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     mark();
     hipLaunchKernelGGL(k_cell_scan, dim3(g.C), dim3(BLK), 0, s, AGG, GIN, totals, g, ctl, st, cfnew, Lo.gmax);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     mark();
-    if (sl == 4)
-      hipLaunchKernelGGL(k_cell_out<4>, gro, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
-                         Lo.gmax, nn);
-    else if (sl == 8)
-      hipLaunchKernelGGL(k_cell_out<8>, gro, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
-                         Lo.gmax, nn);
-    else
-      hipLaunchKernelGGL(k_cell_out<16>, gro, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, complete,
-                         Lo.gmax, nn);
+    // output: one workgroup per window (one per CU: its LDS holds the
+    // window's band), then the cells off the bucket path
+    {
+      const dim3 gw((uint32_t)ncu), bw(WIN_THREADS);
+      const size_t lw = sizeof(WinLds);
+      if (sl == 4)
+        hipLaunchKernelGGL(k_cell_win<4>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, GIN, CMIN, CR0, complete,
+                           Lo.gmax, nn);
+      else if (sl == 8)
+        hipLaunchKernelGGL(k_cell_win<8>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, GIN, CMIN, CR0, complete,
+                           Lo.gmax, nn);
+      else
+        hipLaunchKernelGGL(k_cell_win<16>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, GIN, CMIN, CR0, complete,
+                           Lo.gmax, nn);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      mark();
+      const dim3 gx = grid_of(4);
+      if (sl == 4)
+        hipLaunchKernelGGL(k_cell_rest<4>, gx, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, NBL, complete,
+                           Lo.gmax, nn);
+      else if (sl == 8)
+        hipLaunchKernelGGL(k_cell_rest<8>, gx, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, NBL, complete,
+                           Lo.gmax, nn);
+      else
+        hipLaunchKernelGGL(k_cell_rest<16>, gx, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, NBL, complete,
+                           Lo.gmax, nn);
+    }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
@@ -1765,6 +2005,10 @@ hipError_t set_lds_limits(uint32_t K) {
   const void *fc[] = {(const void *)k_die_count<true>, (const void *)k_die_count<false>};
   for (const void *f : fc)
     if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, c)) != hipSuccess) return e;
+  const void *fw[] = {(const void *)k_cell_win<4>, (const void *)k_cell_win<8>, (const void *)k_cell_win<16>};
+  for (const void *f : fw)
+    if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(WinLds))) != hipSuccess)
+      return e;
   return hipSuccess;
 }
 
