@@ -33,6 +33,8 @@
  *  - die queue key = (ch, die); with the plane-parallel flag (ch, die, plane).
  *  - media variant (flag): die page-register blocking, see
  *    orc_blocking_stage.
+ *  - timing source (flag): the calibrated end-to-end vmem burst curve
+ *    instead of the media model, see orc_vmem_stage.
  *  - xfer = ceil(page_bytes * 1e9 / channel_bytes_per_s) in integer ns.
  *  - times are int64 ns; "idle since minus infinity" at create/reset.
  *
@@ -59,6 +61,7 @@
 #define ORC_TIME_ERROR    INT64_MIN
 #define ORC_FLAG_PLANE_PARALLEL 1u
 #define ORC_FLAG_REGISTER_BLOCKING 2u
+#define ORC_FLAG_VMEM_CURVE 4u
 #define ORC_MAX_RANGES    64
 
 /* Issue times must lie in [0, 2^61); any modeled time reaching 2^62 is an
@@ -96,6 +99,13 @@ typedef struct {
   struct orc_fifo *fifo;
   int64_t *qdone;
   int64_t nq, qcap;
+  /* vmem curve: burst cost at the knots, the route's clock, the device
+   * page of the last access and the length of the burst it ended */
+  int64_t vknot[6];
+  int64_t vfree;
+  uint8_t vbusy, vhave;
+  uint64_t vlast;
+  int64_t vburst;
 } orc_model;
 
 typedef struct orc_fifo { int64_t *id; int64_t head, len, cap; } orc_fifo;
@@ -113,7 +123,8 @@ int orc_create(const orc_params *p, orc_model **out) {
   if (p->page_bytes == 0) return ORC_EINVAL;
   if (p->t_read_ns < 1 || p->t_read_ns > ORC_SERVICE_LIMIT) return ORC_EINVAL;
   if (p->channel_bytes_per_s == 0) return ORC_EINVAL;
-  if (p->flags & ~(ORC_FLAG_PLANE_PARALLEL | ORC_FLAG_REGISTER_BLOCKING)) return ORC_EINVAL;
+  if (p->flags & ~(ORC_FLAG_PLANE_PARALLEL | ORC_FLAG_REGISTER_BLOCKING | ORC_FLAG_VMEM_CURVE)) return ORC_EINVAL;
+  if ((p->flags & ORC_FLAG_VMEM_CURVE) && (p->flags & ORC_FLAG_REGISTER_BLOCKING)) return ORC_EINVAL;
   if ((uint64_t)p->channels * p->dies_per_channel * p->planes_per_die > 65536u) return ORC_EINVAL;
   /* transfer time: ceil(page_bytes * 1e9 / bytes_per_s), exact integers */
   unsigned __int128 num = (unsigned __int128)p->page_bytes * 1000000000u;
@@ -123,6 +134,9 @@ int orc_create(const orc_params *p, orc_model **out) {
   if (!m) return ORC_ENOMEM;
   m->p = *p;
   m->xfer_ns = (int64_t)q;
+  /* vmem curve until configured: every page of a burst costs the
+   * single-page value the paper prints (11,133 ns), i.e. no burst benefit */
+  for (int k = 0; k < 6; k++) m->vknot[k] = 11133 * (int64_t[]){1, 4, 16, 64, 256, 512}[k];
   m->n_die_keys = orc_n_die_keys(p);
   m->die_free = (int64_t *)calloc(m->n_die_keys, sizeof(int64_t));
   m->die_busy = (uint8_t *)calloc(m->n_die_keys, 1);
@@ -156,6 +170,11 @@ void orc_reset(orc_model *m) {
   memset(m->chan_busy, 0, m->p.channels);
   memset(m->die_free, 0, sizeof(int64_t) * m->n_die_keys);
   memset(m->chan_free, 0, sizeof(int64_t) * m->p.channels);
+  m->vfree = 0;
+  m->vbusy = 0;
+  m->vhave = 0;
+  m->vlast = 0;
+  m->vburst = 0;
 }
 
 /* Range registration (Section D1): explicit [base, base+bytes) intervals,
@@ -313,6 +332,93 @@ static int orc_blocking_stage(orc_model *m, const int64_t *issue, int64_t n, int
   return overflow;
 }
 
+/* ---------------------------------------------------------------- vmem curve
+ * Section "Discussion": a second timing source, a calibrated end-to-end curve
+ * measured on a host paging path that presents an SSD as memory.  The curve
+ * prices a sequential burst of L pages; its knots are at 1, 4, 16, 64, 256
+ * and 512 pages, and beyond the last knot it keeps the final segment's slope.
+ * An access that jumps elsewhere, steps back, re-reads the same page or
+ * switches operation does not extend a burst: it begins a fresh one-page
+ * burst at the single-page price the paper prints, 11,133 ns.  Readings (the paper prints only that one knot value and
+ * does not say how a burst becomes per-access completion times):
+ *  - T(L), the cost of a burst of L pages: T(0) = 0; the six knot values are
+ *    parameters (orc_vmem_configure); between knots T is linear in L,
+ *    rounded down to whole ns; past 512, T(512) + floor((T(512) - T(256)) *
+ *    (L - 512) / 256);
+ *  - an access continues the burst iff its device page is the page right
+ *    after the previous in-range access's page (request order, across calls
+ *    until reset); every other access (any other page: random, reverse,
+ *    repeated) starts a new burst.  Every request is a page read, so the
+ *    operation never changes and no cross-operation reset arises;
+ *  - the route serves one access at a time in request order: the access at
+ *    burst position L occupies it for T(L) - T(L-1), so a back-to-back burst
+ *    of L pages takes T(L) and a lone access T(1);
+ *  - complete = max(issue, route free) + that service; the route's clock
+ *    persists across calls like the media model's (idle after reset);
+ *    out-of-range requests take the native path (complete = issue). */
+static const int64_t ORC_VKNOT_PAGES[6] = {1, 4, 16, 64, 256, 512};
+
+/* T(L): cost of a sequential burst of L pages. */
+int64_t orc_vmem_burst_ns(const orc_model *m, int64_t L) {
+  const int64_t *T = m->vknot;
+  if (L <= 0) return 0;
+  if (L > 512)
+    return T[5] + (int64_t)((__int128)(T[5] - T[4]) * (L - 512) / 256);
+  int s = 0;  /* the segment [knot s, knot s+1] holding L */
+  while (s < 4 && L > ORC_VKNOT_PAGES[s + 1]) s++;
+  const int64_t La = ORC_VKNOT_PAGES[s], Lb = ORC_VKNOT_PAGES[s + 1];
+  return T[s] + (int64_t)((__int128)(T[s + 1] - T[s]) * (L - La) / (Lb - La));
+}
+
+/* Knot values T(1), T(4), T(16), T(64), T(256), T(512) in ns: T(1) >= 1,
+ * nondecreasing, and no page of any segment (nor a lone page) costing more
+ * than 2^29 ns on average. */
+int orc_vmem_configure(orc_model *m, const int64_t *knot) {
+  if (!m || !knot) return ORC_EINVAL;
+  if (knot[0] < 1 || knot[0] > ORC_SERVICE_LIMIT) return ORC_EINVAL;
+  for (int k = 1; k < 6; k++) {
+    if (knot[k] < knot[k - 1]) return ORC_EINVAL;
+    if (knot[k] - knot[k - 1] > ORC_SERVICE_LIMIT * (ORC_VKNOT_PAGES[k] - ORC_VKNOT_PAGES[k - 1])) return ORC_EINVAL;
+  }
+  for (int k = 0; k < 6; k++) m->vknot[k] = knot[k];
+  return ORC_OK;
+}
+
+/* The route's state: {clock (INT64_MIN if idle), last device page (-1 if
+ * none), length of the burst that page ended (0 if none)}. */
+void orc_vmem_state(const orc_model *m, int64_t *out) {
+  out[0] = m->vbusy ? m->vfree : INT64_MIN;
+  out[1] = m->vhave ? (int64_t)m->vlast : -1;
+  out[2] = m->vhave ? m->vburst : 0;
+}
+
+/* Requests in index order on the vmem route (validation done by the caller).
+ * Returns 1 on a time-domain overflow (state then untouched). */
+static int orc_vmem_stage(orc_model *m, const uint64_t *addr, const int64_t *issue, int64_t n,
+                          int64_t *complete) {
+  int64_t vf = m->vfree, L = m->vburst;
+  uint8_t vb = m->vbusy, have = m->vhave;
+  uint64_t last = m->vlast;
+  int overflow = 0;
+  for (int64_t i = 0; i < n; i++) {
+    int r = orc_classify(m, addr[i]);
+    if (r < 0) { complete[i] = issue[i]; continue; }
+    uint64_t page = m->ranges[r].dev_page_base + (addr[i] - m->ranges[r].base) / m->p.page_bytes;
+    L = (have && page == last + 1) ? L + 1 : 1;
+    last = page;
+    have = 1;
+    int64_t service = orc_vmem_burst_ns(m, L) - orc_vmem_burst_ns(m, L - 1);
+    int64_t start = vb ? orc_max(issue[i], vf) : issue[i];
+    complete[i] = start + service;
+    if (complete[i] >= ORC_TIME_LIMIT) overflow = 1;
+    vf = complete[i];
+    vb = 1;
+  }
+  if (overflow) return 1;
+  m->vfree = vf; m->vbusy = vb; m->vhave = have; m->vlast = last; m->vburst = L;
+  return 0;
+}
+
 /*
  * The timing call.  Steps, in the model's order:
  *  1. validate every issue time (0 <= t < 2^61, nondecreasing in index);
@@ -342,6 +448,13 @@ int orc_time_requests(orc_model *m, const uint64_t *addr, const int64_t *issue, 
   if (bad_range || bad_order) {
     for (int64_t i = 0; i < n; i++) complete[i] = ORC_TIME_ERROR;
     return bad_range ? ORC_ERANGE_TIME : ORC_EUNSORTED;
+  }
+  if (p->flags & ORC_FLAG_VMEM_CURVE) {
+    if (orc_vmem_stage(m, addr, issue, n, complete)) {
+      for (int64_t i = 0; i < n; i++) complete[i] = ORC_TIME_ERROR;
+      return ORC_ERANGE_TIME;
+    }
+    return ORC_OK;
   }
 
   /* working copies of the clocks: committed only if the call succeeds */
@@ -476,6 +589,7 @@ int orc_refresh_configure(orc_model *m, int64_t t_prog_ns) {
  * *first_id .. *first_id + nq - 1. */
 int orc_refresh_submit(orc_model *m, const uint64_t *pages, int64_t nq, int64_t *first_id) {
   if (!m || nq < 0 || (nq > 0 && !pages)) return ORC_EINVAL;
+  if (m->p.flags & ORC_FLAG_VMEM_CURVE) return ORC_EINVAL;  /* no die queues on the vmem route */
   if (!m->fifo) {
     m->fifo = (orc_fifo *)calloc(m->n_die_keys, sizeof(orc_fifo));
     if (!m->fifo) return ORC_ENOMEM;

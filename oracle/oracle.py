@@ -25,6 +25,8 @@ OK, EINVAL, EALIGN, EOVERLAP, ENOWORKSPACE, EUNSORTED, ERANGE_TIME, EHIP, ENOMEM
 TIME_ERROR = np.iinfo(np.int64).min
 FLAG_PLANE_PARALLEL = 1
 FLAG_REGISTER_BLOCKING = 2
+FLAG_VMEM_CURVE = 4
+VMEM_KNOT_PAGES = (1, 4, 16, 64, 256, 512)
 
 
 def build(force=False):
@@ -88,6 +90,12 @@ def _load():
         lib.orc_refresh_count.restype = i64
         lib.orc_refresh_done.argtypes = [vp, vp]
         lib.orc_refresh_done.restype = None
+        lib.orc_vmem_configure.argtypes = [vp, vp]
+        lib.orc_vmem_configure.restype = i32
+        lib.orc_vmem_burst_ns.argtypes = [vp, i64]
+        lib.orc_vmem_burst_ns.restype = i64
+        lib.orc_vmem_state.argtypes = [vp, vp]
+        lib.orc_vmem_state.restype = None
         lib.orc_cache_create.argtypes = [i64, i64, i64, ctypes.POINTER(vp)]
         lib.orc_cache_create.restype = i32
         lib.orc_cache_destroy.argtypes = [vp]
@@ -219,6 +227,24 @@ class OracleModel:
         return int(self._lib.orc_set_state(self._h, _ptr(d), _ptr(c)))
 
     # -- refresh (Section D4; readings in hbf_oracle.c)
+
+    # -- the calibrated vmem curve (Section "Discussion"; see hbf_oracle.c)
+
+    def vmem_configure(self, knots):
+        """Knot values T(1), T(4), T(16), T(64), T(256), T(512) in ns."""
+        k = np.ascontiguousarray(knots, dtype=np.int64)
+        assert k.size == 6
+        return self._lib.orc_vmem_configure(self._h, _ptr(k))
+
+    def vmem_burst_ns(self, L):
+        """T(L): cost of a sequential burst of L pages."""
+        return self._lib.orc_vmem_burst_ns(self._h, int(L))
+
+    def vmem_state(self):
+        """(clock or INT64_MIN if idle, last device page or -1, burst length)."""
+        out = np.zeros(3, dtype=np.int64)
+        self._lib.orc_vmem_state(self._h, _ptr(out))
+        return tuple(int(x) for x in out)
 
     def refresh_configure(self, t_prog_ns):
         return int(self._lib.orc_refresh_configure(self._h, int(t_prog_ns)))

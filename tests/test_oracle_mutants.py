@@ -80,6 +80,27 @@ MUTANTS = {
     "blocking-channel-tie-reversed": (
         "(dd[i] == dd[best] && i < best)",
         "(dd[i] == dd[best] && i > best)"),
+    "vmem-charges-whole-burst": (
+        "int64_t service = orc_vmem_burst_ns(m, L) - orc_vmem_burst_ns(m, L - 1);",
+        "int64_t service = orc_vmem_burst_ns(m, L);"),
+    "vmem-reverse-continues": (
+        "L = (have && page == last + 1) ? L + 1 : 1;",
+        "L = (have && (page == last + 1 || page + 1 == last)) ? L + 1 : 1;"),
+    "vmem-native-breaks-burst": (
+        "if (r < 0) { complete[i] = issue[i]; continue; }\n    uint64_t page",
+        "if (r < 0) { complete[i] = issue[i]; have = 0; continue; }\n    uint64_t page"),
+    "vmem-tail-slope-from-wrong-segment": (
+        "return T[5] + (int64_t)((__int128)(T[5] - T[4]) * (L - 512) / 256);",
+        "return T[5] + (int64_t)((__int128)(T[5] - T[3]) * (L - 512) / 448);"),
+    "vmem-route-never-busy": (
+        "int64_t start = vb ? orc_max(issue[i], vf) : issue[i];",
+        "int64_t start = issue[i];"),
+    "vmem-interpolation-rounds-up": (
+        "return T[s] + (int64_t)((__int128)(T[s + 1] - T[s]) * (L - La) / (Lb - La));",
+        "return T[s] + (int64_t)(((__int128)(T[s + 1] - T[s]) * (L - La) + (Lb - La) - 1) / (Lb - La));"),
+    "vmem-burst-state-not-kept": (
+        "m->vfree = vf; m->vbusy = vb; m->vhave = have; m->vlast = last; m->vburst = L;",
+        "m->vfree = vf; m->vbusy = vb; m->vhave = 0; m->vlast = last; m->vburst = L;"),
     "extra-service-term": (
         "complete[i] = start + xfer;",
         "complete[i] = start + xfer + (start > dd[i] ? 1 : 0);"),
@@ -101,6 +122,7 @@ def test_pins_catch_mutant(tmp_path, name):
                         os.path.join(ROOT, "tests", "test_oracle_events.py"),
                         os.path.join(ROOT, "tests", "test_oracle_refresh.py"),
                         os.path.join(ROOT, "tests", "test_oracle_cache.py"),
-                        os.path.join(ROOT, "tests", "test_oracle_blocking.py")],
+                        os.path.join(ROOT, "tests", "test_oracle_blocking.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_vmem.py")],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"

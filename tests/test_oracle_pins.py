@@ -79,7 +79,7 @@ def test_xfer_is_ceiling_of_page_over_bandwidth(oracle_mod):
 @pytest.mark.parametrize("kw", [
     dict(channels=0), dict(dies_per_channel=0), dict(planes_per_die=0), dict(page_bytes=0),
     dict(t_read_ns=0), dict(t_read_ns=1 << 30), dict(channel_bytes_per_s=0),
-    dict(channel_bytes_per_s=1), dict(flags=4)])
+    dict(channel_bytes_per_s=1), dict(flags=8), dict(flags=6)])
 def test_invalid_params(oracle_mod, kw):
     base = dict(channels=2, dies_per_channel=2, planes_per_die=1, page_bytes=16384, t_read_ns=3,
                 channel_bytes_per_s=16384 * 250_000_000)
