@@ -16,7 +16,7 @@ and counter-measured bandwidth, delay-injection fidelity from the call's
 common origin and the paper's paired 1,000 / 200 us increment timed with HIP
 events, config 3's open-loop MoE decode trace (44.6 M requests), the small
 streams, the next rows (closed loop, refresh, capacity cache, register
-blocking), and the reference model timed on the host on configs 1, 2, 3 and
+blocking, the vmem burst curve), and the reference model timed on the host on configs 1, 2, 3 and
 the large stream, with the SHA-256 of each of its outputs.
 """
 import argparse
@@ -523,6 +523,40 @@ def delay_increment_leg(torch, gm, Wd, Xd, Yd, pairs=36):
                               "36 paired blocks); context only")
 
 
+def vmem_leg(torch, hbf, wl, w, addr, issue, complete, reps=3):
+    """The vmem timing source (Section "Discussion"): the large mixed stream
+    on the calibrated end-to-end burst curve (illustrative knots, the first
+    one the paper's), checked against the reference digest."""
+    m = hbf.Model(**dict(w.params, flags=hbf.HBF_FLAG_VMEM_CURVE))
+    for b, nb in w.ranges:
+        assert m.register_range(b, nb)[0] == 0
+    assert m.vmem_configure(wl.VMEM_KNOTS) == 0
+    s = torch.cuda.current_stream()
+    times = []
+    for r in range(reps + 1):
+        m.reset(s)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        assert m.time_requests(addr, issue, complete, s) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+        if r:
+            times.append(e0.elapsed_time(e1))
+    assert m.get_status() == 0
+    parity = None
+    gold_p = os.path.join(ROOT, "tests", "golden", "oracle_digests.json")
+    if w.n == 1 << 28 and os.path.exists(gold_p):
+        gold = json.load(open(gold_p)).get("config5_vmem")
+        if gold:
+            parity = sha(complete.cpu().numpy()) == gold["complete_sha256"]
+    m.close()
+    ms = float(np.median(times))
+    return dict(workload=f"the same {w.n} requests on the vmem route, knots {list(wl.VMEM_KNOTS)} ns",
+                ms_per_call=ms, requests_per_s=w.n / (ms / 1e3),
+                path_algorithmic_frac=PATH_ALG_BYTES * w.n / (ms / 1e3) / 1e9 / HBM_PEAK_GBPS,
+                parity_vs_reference_digest=parity)
+
+
 def gemv_leg(torch, hbf, wl, sets=16, reps=3):
     """Row a5's bandwidth with no delay injected: the 8-expert grouped GEMV
     (8 x [768 x 2048] bf16, 24 MiB) over `sets` distinct weight sets in turn
@@ -649,6 +683,7 @@ def main():
     ap.add_argument("--no-capacity", action="store_true", help="skip the capacity-mode frame cache report")
     ap.add_argument("--no-blocking", action="store_true", help="skip the register-blocking report")
     ap.add_argument("--no-config3", action="store_true", help="skip the config 3 open-loop report")
+    ap.add_argument("--no-vmem", action="store_true", help="skip the vmem-curve report")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -830,6 +865,9 @@ def main():
     if not args.no_gemv:
         log("GEMV bandwidth, no delay")
         out["gemv_bandwidth"] = gemv_leg(torch, hbf, wl)
+    if not args.no_vmem:
+        log("vmem curve timing")
+        out["vmem_curve"] = vmem_leg(torch, hbf, wl, w, addr, issue, complete)
     if not args.no_blocking:
         log("register-blocking timing")
         out["register_blocking"] = blocking_leg(torch, hbf, wl, w, addr, issue, complete)

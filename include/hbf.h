@@ -82,6 +82,25 @@ extern "C" {
  * channel in service order (one wave per channel): slower than the default
  * unblocked model, which needs no such order. */
 #define HBF_FLAG_REGISTER_BLOCKING 2u
+/* Timing source: the calibrated end-to-end vmem curve (Section
+ * "Discussion") instead of the media model.  That curve was measured on a
+ * host paging path presenting an SSD as memory; it prices a sequential
+ * burst of L pages, T(L), from knots at 1, 4, 16, 64, 256 and 512 pages
+ * (hbf_vmem_configure).  Reading used here: between knots T is linear in L,
+ * rounded down to whole ns; past 512 pages T(L) = T(512) +
+ * floor((T(512) - T(256)) * (L - 512) / 256).  An in-range access continues
+ * the burst iff its device page is the one after the previous in-range
+ * access's page (request order, across calls until reset); any other access
+ * (a jump, a step back, the same page again) starts a burst of one.  The
+ * route serves one access at a time in request order, the access at burst
+ * position L taking T(L) - T(L-1):
+ *   complete = max(issue, route free) + T(L) - T(L-1).
+ * Out-of-range requests take the native path (complete = issue).  No die or
+ * channel queues: refresh calls return HBF_EINVAL; not combinable with
+ * HBF_FLAG_REGISTER_BLOCKING (HBF_EINVAL at create).  The route's clock and
+ * burst persist across calls and are cleared by hbf_model_reset;
+ * hbf_get_state / hbf_set_state cover the media clocks only. */
+#define HBF_FLAG_VMEM_CURVE 4u
 
 typedef struct hbf_model *hbf_model_t;  /* opaque, owned by the library */
 
@@ -237,6 +256,15 @@ int hbf_gemv_instrumented(hbf_model_t model, const uint16_t *dev_W, int E, int K
                           const uint16_t *dev_X, int B, float *dev_Y,
                           const int64_t *dev_page_issue_ns, const int64_t *dev_page_complete_ns,
                           int64_t *dev_measured_delay_ns, void *stream);
+
+/* Knot values of the vmem curve (model created with HBF_FLAG_VMEM_CURVE):
+ * host_knot_ns[6] = T(1), T(4), T(16), T(64), T(256), T(512) in ns.  The
+ * paper prints T(1) = 11,133 ns and none of the others; until configured a
+ * model uses T(L) = 11,133 * L at every knot (no burst benefit).  Requires
+ * 1 <= T(1) <= 2^29, nondecreasing knots, and at most 2^29 ns per page on
+ * average over every segment (else HBF_EINVAL).  Host only; applies to
+ * calls made after it returns. */
+int hbf_vmem_configure(hbf_model_t model, const int64_t *host_knot_ns);
 
 /* ---- Refresh traffic in the same queues (Section "D4: Retention, Refresh,
  * and Wear as Injected Latency": refresh read-rewrite pairs get ids of their

@@ -21,6 +21,21 @@ static size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 Layout make_layout(const Geo &g, int64_t n) {
   Layout L{};
   L.n = n;
+  if (g.vmem) {  // the vmem route: tile summaries and one service per request
+    const size_t nt = (size_t)((n + VM_TILE - 1) / VM_TILE);
+    size_t o = 0;
+    L.off_ctl = o;   o = up256(o + sizeof(CallCtl));
+    L.off_vsum = o;  o = up256(o + nt * 32);
+    L.off_vin = o;   o = up256(o + nt * 32);
+    L.off_vpair = o; o = up256(o + nt * 16);
+    L.off_vfin = o;  o = up256(o + nt * 8);
+    L.off_vcost = o; o = up256(o + (size_t)n * 4);
+    L.off_vend = o;  o = up256(o + 64);
+    L.off_vwsum = o; o = up256(o + nt * (VM_THREADS / 64) * 32);
+    L.off_vwpair = o; o = up256(o + nt * (VM_THREADS / 64) * 16);
+    L.total = o;
+    return L;
+  }
   int64_t te = (n + TARGET_TILES - 1) / TARGET_TILES;
   te = ((te + CHUNK - 1) / CHUNK) * CHUNK;
   if (te < CHUNK) te = CHUNK;
@@ -112,6 +127,11 @@ static int ensure_device(hbf_model *m) {
   host[0].sticky = 0;
   host[0].pad = 0;
   host[0].gemv_origin = 0;
+  host[0].vfree = NEG;
+  host[0].vlast = 0;
+  host[0].vburst = 0;
+  host[0].vhave = 0;
+  host[0].vpad = 0;
   if (hipMemcpy(m->st, host.data(), sizeof(DevState), hipMemcpyHostToDevice) != hipSuccess) return HBF_EHIP;
   // (for the largest die-queue count: models of any size may follow)
   if (set_lds_limits(MAX_KEYS) != hipSuccess) return HBF_EHIP;
@@ -154,7 +174,8 @@ int hbf_model_create(const hbf_params *params, hbf_model_t *out) {
   if (p.page_bytes == 0) return HBF_EINVAL;
   if (p.t_read_ns < 1 || p.t_read_ns > SERVICE_LIMIT) return HBF_EINVAL;
   if (p.channel_bytes_per_s == 0) return HBF_EINVAL;
-  if (p.flags & ~(HBF_FLAG_PLANE_PARALLEL | HBF_FLAG_REGISTER_BLOCKING)) return HBF_EINVAL;
+  if (p.flags & ~(HBF_FLAG_PLANE_PARALLEL | HBF_FLAG_REGISTER_BLOCKING | HBF_FLAG_VMEM_CURVE)) return HBF_EINVAL;
+  if ((p.flags & HBF_FLAG_VMEM_CURVE) && (p.flags & HBF_FLAG_REGISTER_BLOCKING)) return HBF_EINVAL;
   const uint64_t cdp = (uint64_t)p.channels * p.dies_per_channel * p.planes_per_die;
   if (cdp > 65536) return HBF_EINVAL;
   const bool pp = (p.flags & HBF_FLAG_PLANE_PARALLEL) != 0;
@@ -176,6 +197,11 @@ int hbf_model_create(const hbf_params *params, hbf_model_t *out) {
   g.page_bytes = p.page_bytes;
   g.plane_parallel = pp;
   g.reg_block = (p.flags & HBF_FLAG_REGISTER_BLOCKING) != 0;
+  g.vmem = (p.flags & HBF_FLAG_VMEM_CURVE) != 0;
+  {  // until configured: every page of a burst at the printed single-page cost
+    const int64_t kp[6] = {1, 4, 16, 64, 256, 512};
+    for (int k = 0; k < 6; k++) g.vknot[k] = 11133 * kp[k];
+  }
   g.pow2 = is_pow2(p.page_bytes) && is_pow2(p.channels) && is_pow2(p.dies_per_channel) &&
            is_pow2(p.planes_per_die);
   g.lg_page = lg2(p.page_bytes);
@@ -298,7 +324,7 @@ static int time_call(hbf_model_t m, const RangeTable &rt, const uint64_t *addr, 
                      int64_t n, int64_t *complete, void *stream) {
   const Layout L = make_layout(m->g, n);
   hipEvent_t *ev = nullptr;
-  if (m->prof) {
+  if (m->prof && !m->g.vmem) {  // (per-kernel timing covers the media model's kernels)
     hipEvent_t *set = m->ev[m->prof_calls % hbf_model::RING];
     for (int k = 0; k <= kNumTimedKernels; k++)
       if (!set[k] && hipEventCreate(&set[k]) != hipSuccess) return HBF_EHIP;
@@ -307,7 +333,7 @@ static int time_call(hbf_model_t m, const RangeTable &rt, const uint64_t *addr, 
   hipError_t e = launch_time_requests(m->g, rt, L, (char *)m->ws, m->st, addr, issue, complete,
                                       (hipStream_t)stream, ev, kNumTimedKernels + 1, m->ref_maybe);
   if (e != hipSuccess) return HBF_EHIP;
-  if (m->prof) m->prof_calls++;
+  if (ev) m->prof_calls++;
   return HBF_OK;
 }
 
@@ -449,8 +475,20 @@ int hbf_refresh_plan(const hbf_params *params, const hbf_refresh_block *blocks, 
   return HBF_OK;
 }
 
+int hbf_vmem_configure(hbf_model_t m, const int64_t *knot) {
+  if (!m || !knot || !m->g.vmem) return HBF_EINVAL;
+  const int64_t kp[6] = {1, 4, 16, 64, 256, 512};
+  if (knot[0] < 1 || knot[0] > SERVICE_LIMIT) return HBF_EINVAL;
+  for (int k = 1; k < 6; k++) {
+    if (knot[k] < knot[k - 1]) return HBF_EINVAL;
+    if (knot[k] - knot[k - 1] > SERVICE_LIMIT * (kp[k] - kp[k - 1])) return HBF_EINVAL;
+  }
+  for (int k = 0; k < 6; k++) m->g.vknot[k] = knot[k];
+  return HBF_OK;
+}
+
 int hbf_refresh_configure(hbf_model_t m, int64_t t_prog_ns) {
-  if (!m || t_prog_ns < 0 || 2 * m->g.tR + t_prog_ns > SERVICE_LIMIT) return HBF_EINVAL;
+  if (!m || m->g.vmem || t_prog_ns < 0 || 2 * m->g.tR + t_prog_ns > SERVICE_LIMIT) return HBF_EINVAL;
   m->t_prog = t_prog_ns;
   m->g.tQ = m->g.tR + t_prog_ns;
   return HBF_OK;

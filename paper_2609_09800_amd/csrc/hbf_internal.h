@@ -69,7 +69,8 @@ struct Geo {
   int64_t tR, xfer;
   int64_t tQ;         // die time of one refresh quantum (tR + tPROG), 0 if unset
   uint32_t reg_block; // media variant: die page-register blocking
-  uint32_t pad;
+  uint32_t vmem;      // timing source: the calibrated end-to-end vmem curve
+  int64_t vknot[6];   // vmem burst cost T(L) at L = 1, 4, 16, 64, 256, 512 pages
 };
 
 // Persistent device state of a model.  Refresh quanta pending at die queue
@@ -88,6 +89,13 @@ struct DevState {
   // Instrumented GEMV with delays: the time origin of the current call
   // (wall-clock ticks, read by the call's first kernel).
   uint64_t gemv_origin;
+  // vmem route: its clock (NEG = idle), the device page of the last
+  // in-range access and the length of the burst it ended (vhave = 0: none)
+  int64_t vfree;
+  uint64_t vlast;
+  int64_t vburst;
+  uint32_t vhave;
+  uint32_t vpad;
 };
 
 // Completion cell of a refresh quantum that has not been served.
@@ -120,6 +128,11 @@ struct Layout {
   size_t off_cmin, off_cr0;   // per cell: smallest request index (window staging), first channel rank
   size_t off_nbl;             // cells the window output pass leaves to k_cell_rest
   size_t off_iss;             // register blocking: issue times in die order (n int64)
+  // vmem route (tiles of VM_TILE requests): per tile its burst summary, the
+  // summary of everything before it, its route-clock pair and entering
+  // clock; per request its service (u32); the call's closing state
+  size_t off_vsum, off_vin, off_vpair, off_vfin, off_vcost, off_vend;
+  size_t off_vwsum, off_vwpair;  // the same summary and pair per wave span of a tile
   size_t total;
 };
 
@@ -138,6 +151,13 @@ hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX
                            int64_t *issue_do, int64_t n, const uint32_t *seg_start, const uint32_t *totals,
                            DevState *st, CallCtl *ctl, int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref,
                            hipStream_t s);
+// Calibrated vmem curve (hbf_vmem.hip): the whole timing call on the vmem
+// route (classification, burst lengths, route clock, complete[]).
+constexpr int VM_THREADS = 256;
+constexpr int VM_ITEMS = 16;
+constexpr int64_t VM_TILE = VM_THREADS * VM_ITEMS;
+hipError_t launch_vmem(const Geo &g, const RangeTable &rt, const Layout &L, char *ws, DevState *st,
+                       const uint64_t *addr, const int64_t *issue, int64_t *complete, hipStream_t s);
 hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s);
 hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
 // Device address of this GPU's static scratch of hbf_time_requests_noalloc

@@ -23,6 +23,7 @@ HBF_ENOMEM = -8
 HBF_TIME_ERROR = -(1 << 63)
 HBF_FLAG_PLANE_PARALLEL = 1
 HBF_FLAG_REGISTER_BLOCKING = 2
+HBF_FLAG_VMEM_CURVE = 4
 
 EXPORTED = [
     "hbf_model_create", "hbf_model_destroy", "hbf_xfer_ns", "hbf_n_die_queues", "hbf_model_reset",
@@ -31,7 +32,7 @@ EXPORTED = [
     "hbf_get_state", "hbf_set_state", "hbf_profile", "hbf_kernel_times", "hbf_strerror",
     "hbf_refresh_plan", "hbf_refresh_configure", "hbf_refresh_submit", "hbf_refresh_drain", "hbf_refresh_pending",
     "hbf_cache_create", "hbf_cache_destroy", "hbf_cache_reset", "hbf_cache_access", "hbf_cache_sweep",
-    "hbf_time_requests_noalloc",
+    "hbf_time_requests_noalloc", "hbf_vmem_configure",
 ]
 HBF_NOALLOC_SCRATCH_BYTES = 64 << 20
 REFRESH_PENDING = -1
@@ -73,6 +74,7 @@ def load_library(path=LIB_PATH):
         "hbf_classify_map": ([vp, vp, i64, vp, vp], i32),
         "hbf_time_requests": ([vp, vp, vp, i64, vp, vp], i32),
         "hbf_time_requests_noalloc": ([vp, vp, vp, i64, vp, vp], i32),
+        "hbf_vmem_configure": ([vp, vp], i32),
         "hbf_gemv_instrumented": ([vp, vp, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp], i32),
         "hbf_wall_clock_tick_ps": ([vp, ctypes.POINTER(i64)], i32),
         "hbf_get_status": ([vp, vp], i32),
@@ -304,6 +306,16 @@ class Model:
         c = np.ascontiguousarray(chan_free, dtype=np.int64)
         return self._lib.hbf_set_state(self._h, d.ctypes.data_as(ctypes.c_void_p),
                                        c.ctypes.data_as(ctypes.c_void_p), _sp(stream))
+
+    # -- the calibrated vmem curve (Section "Discussion"; reading in include/hbf.h)
+
+    def vmem_configure(self, knots_ns):
+        """T(1), T(4), T(16), T(64), T(256), T(512) in ns (HBF_FLAG_VMEM_CURVE models)."""
+        import numpy as np
+        k = np.ascontiguousarray(knots_ns, dtype=np.int64)
+        if k.size != 6:
+            raise HbfError(HBF_EINVAL, "vmem knots: six values")
+        return self._lib.hbf_vmem_configure(self._h, k.ctypes.data_as(ctypes.c_void_p))
 
     # -- refresh traffic (Section D4; reading in include/hbf.h)
 

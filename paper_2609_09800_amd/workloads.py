@@ -374,3 +374,11 @@ def random_stream(seed, n, params, range_pages, mean_gap, out_frac=0.0, run_frac
 
 
 ALL_CONFIGS = {1: config1, 2: config2, 3: config3, 5: config5}
+
+
+# An illustrative calibrated vmem curve for the vmem timing source (T(L) in
+# ns at 1, 4, 16, 64, 256 and 512 pages).  Only the first value is the
+# paper's (the single-page cost it prints); the others are inputs of this
+# project's workloads, chosen to cheapen the pages of a sequential burst
+# until 64 pages and rise faster beyond, not values from the paper.
+VMEM_KNOTS = (11_133, 14_500, 26_000, 80_000, 300_000, 640_000)

@@ -1,7 +1,7 @@
 """Write tests/golden/oracle_digests.json: SHA-256 digests of the reference
 model's outputs on the seeded workloads (configs 1, 2, 3 and 5, and config
 5 with a refresh plan pending: argument "5r"; config 5 with die
-page-register blocking: "5b").
+page-register blocking: "5b"; config 5 on the vmem timing source: "5v").
 
 Calls only ``oracle/`` and the input generators; nothing here comes from
 the HIP path.  Usage:  python tests/golden/make_golden.py [config ...]
@@ -94,6 +94,25 @@ def digest_blocking():
     return rec
 
 
+def digest_vmem():
+    """The large mixed stream on the vmem timing source (flag 4) with the
+    illustrative knots of workloads.VMEM_KNOTS."""
+    w = wl.config5()
+    params = dict(w.params, flags=oracle.FLAG_VMEM_CURVE)
+    m = oracle.OracleModel(**params)
+    for b, n in w.ranges:
+        assert m.register_range(b, n) == 0
+    assert m.vmem_configure(wl.VMEM_KNOTS) == 0
+    t = time.time()
+    rc, c = m.time_requests(w.addr, w.issue)
+    to = time.time() - t
+    assert rc == 0
+    rec = dict(n=w.n, knots=list(wl.VMEM_KNOTS), complete_sha256=sha(c), route_state=list(m.vmem_state()),
+               max_complete=int(c.max()), oracle_s=round(to, 1))
+    print("config5_vmem", rec, flush=True)
+    return rec
+
+
 def main(cfgs):
     data = json.load(open(OUT)) if os.path.exists(OUT) else {}
     data["_comment"] = ("SHA-256 of the reference model's outputs (int64 little endian) on the "
@@ -103,10 +122,12 @@ def main(cfgs):
             data["config5_refresh"] = digest_refresh()
         elif c == "5b":
             data["config5_blocking"] = digest_blocking()
+        elif c == "5v":
+            data["config5_vmem"] = digest_vmem()
         else:
             data[f"config{c}"] = digest(int(c))
         json.dump(data, open(OUT, "w"), indent=1, sort_keys=True)
 
 
 if __name__ == "__main__":
-    main(sys.argv[1:] or ["1", "2", "3", "5", "5r", "5b"])
+    main(sys.argv[1:] or ["1", "2", "3", "5", "5r", "5b", "5v"])

@@ -62,7 +62,8 @@ def create(lib, **kw):
 @pytest.mark.parametrize("kw", [
     dict(channels=0), dict(channels=1025), dict(dies_per_channel=0), dict(planes_per_die=65),
     dict(page_bytes=0), dict(t_read_ns=0), dict(t_read_ns=(1 << 29) + 1), dict(channel_bytes_per_s=0),
-    dict(channel_bytes_per_s=1), dict(flags=4), dict(dies_per_channel=128),  # 128 dies > 64 queues per channel
+    dict(channel_bytes_per_s=1), dict(flags=8), dict(flags=6),            # unknown flag; vmem + blocking
+    dict(dies_per_channel=128),                                            # 128 dies > 64 queues per channel
     dict(channels=64, dies_per_channel=64),                                # 4096 die queues
     dict(flags=1, dies_per_channel=32),                                    # 32*4 queues per channel
 ])
@@ -175,6 +176,27 @@ def test_refresh_validation_is_host_side(lib):
     assert lib.hbf_refresh_drain(h, 6, 5, None) == -1
     assert lib.hbf_refresh_drain(h, 0, 1 << 61, None) == -1
     assert lib.hbf_refresh_pending(h, None, None) == -1
+    lib.hbf_model_destroy(h)
+
+
+def test_vmem_validation_is_host_side(lib):
+    """The vmem curve's knots are checked on the host; media models refuse
+    them, and vmem models refuse refresh traffic."""
+    knots = lambda *k: (ctypes.c_int64 * 6)(*k)   # noqa: E731
+    rc, media = create(lib)
+    assert rc == 0
+    assert lib.hbf_vmem_configure(media, knots(11133, 20000, 40000, 90000, 300000, 700000)) == -1
+    lib.hbf_model_destroy(media)
+    rc, h = create(lib, flags=4)
+    assert rc == 0
+    assert lib.hbf_vmem_configure(h, None) == -1
+    assert lib.hbf_vmem_configure(h, knots(0, 1, 2, 3, 4, 5)) == -1                  # T(1) >= 1
+    assert lib.hbf_vmem_configure(h, knots((1 << 29) + 1, 1 << 30, 1 << 31, 1 << 32, 1 << 33, 1 << 34)) == -1
+    assert lib.hbf_vmem_configure(h, knots(10, 9, 20, 30, 40, 50)) == -1               # decreasing
+    assert lib.hbf_vmem_configure(h, knots(10, 20, 30, 40, 50, 50 + 256 * (1 << 29) + 1)) == -1  # > 2^29/page
+    assert lib.hbf_vmem_configure(h, knots(10, 20, 30, 40, 50, 50 + 256 * (1 << 29))) == 0
+    assert lib.hbf_vmem_configure(h, knots(5, 5, 5, 5, 5, 5)) == 0
+    assert lib.hbf_refresh_configure(h, 1000) == -1
     lib.hbf_model_destroy(h)
 
 
