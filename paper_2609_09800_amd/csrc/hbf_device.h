@@ -249,6 +249,28 @@ DEVI uint64_t dev_page(const Geo &g, const LdsRanges *lr, int r, uint64_t a) {
   return lr->pbase[r] + (POW2 ? (off >> g.lg_page) : off / g.page_bytes);
 }
 
+// LDS slot of die queue k in the die passes: die-major, slot = die * C +
+// channel (k = channel * Dk + die).  Device pages stripe over the channels
+// first, so the die queues of consecutive pages -- the common case inside a
+// wave -- sit in consecutive slots instead of Dk apart, which would put a
+// wave's per-queue LDS accesses into a few banks.  lkey inverts it.
+DEVI uint32_t lslot(const Geo &g, uint32_t k) {
+  if (g.pow2) {
+    const uint32_t s = (uint32_t)__builtin_ctz(g.Dk);
+    return ((k & (g.Dk - 1)) << g.lg_C) | (k >> s);
+  }
+  const uint32_t c = k / g.Dk;
+  return (k - c * g.Dk) * g.C + c;
+}
+DEVI uint32_t lkey(const Geo &g, uint32_t li) {
+  if (g.pow2) {
+    const uint32_t s = (uint32_t)__builtin_ctz(g.Dk);
+    return ((li & (g.C - 1)) << s) | (li >> g.lg_C);
+  }
+  const uint32_t d = li / g.C;
+  return (li - d * g.C) * g.Dk + d;
+}
+
 // Die-queue key of an address, or KEY_NONE for the native path.
 template <bool POW2>
 DEVI uint32_t key_of(const Geo &g, const LdsRanges *lr, uint64_t a) {

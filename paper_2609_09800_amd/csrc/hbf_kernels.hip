@@ -141,13 +141,16 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
   // REF: pending quanta per key, read once per block (4-byte aligned: K may be odd)
   uint32_t *refp = (uint32_t *)(((uintptr_t)(tot + K) + 3) & ~(uintptr_t)3);
 
+  // per-queue LDS state is indexed by the queue's LDS slot (lslot); global
+  // per-queue arrays by the queue itself
   load_ranges(lr, rt);
-  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+  for (uint32_t li = threadIdx.x; li < K; li += DBLK) {
+    const uint32_t k = lkey(g, li);
     // REF: cnt holds the call-wide rank of the tile's next request of k
-    cnt[k] = REF ? tin_base[(size_t)blockIdx.x * K + k] : 0;
-    amax[k] = NEG;
-    cmax[k] = NEG;
-    if (REF) refp[k] = st->ref_pend[k];
+    cnt[li] = REF ? tin_base[(size_t)blockIdx.x * K + k] : 0;
+    amax[li] = NEG;
+    cmax[li] = NEG;
+    if (REF) refp[li] = st->ref_pend[k];
   }
   __syncthreads();
 
@@ -205,7 +208,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
       }
       uint32_t k = v ? key_of<POW2>(g, lr, a) : KEY_NONE;
       if (v && k == KEY_NONE) complete[i] = x;  // native path: no modeled delay
-      key[e] = k;
+      key[e] = k == KEY_NONE ? KEY_NONE : lslot(g, k);
       iss[e] = x;
     }
     wave_rank(key, rank, mycnt, kbits);
@@ -243,13 +246,14 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
     __syncthreads();
   }
   const size_t row = (size_t)blockIdx.x * K;
-  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+  for (uint32_t li = threadIdx.x; li < K; li += DBLK) {
+    const uint32_t k = lkey(g, li);
     if (REF) {  // global form; the counts came from the count pass
-      agg_A[row + k] = amax[k];
+      agg_A[row + k] = amax[li];
     } else {    // departure of the tile's last request of k from an idle die
-      const uint32_t c = cnt[k];
+      const uint32_t c = cnt[li];
       agg_cnt[row + k] = c;
-      agg_A[row + k] = c ? (int64_t)c * tR + amax[k] : NEG;
+      agg_A[row + k] = c ? (int64_t)c * tR + amax[li] : NEG;
     }
   }
   if (errb) atomicOr(&ctl->err, errb);
@@ -272,10 +276,10 @@ __global__ __launch_bounds__(DBLK) void k_die_count(const uint64_t *__restrict__
   const int64_t t1 = imin(n, t0 + tile_elems);
   for (int64_t i = t0 + threadIdx.x; i < t1; i += DBLK) {
     const uint32_t k = key_of<POW2>(g, lr, addr[i]);
-    if (k != KEY_NONE) atomicAdd(&cnt[k], 1u);
+    if (k != KEY_NONE) atomicAdd(&cnt[lslot(g, k)], 1u);
   }
   __syncthreads();
-  for (uint32_t k = threadIdx.x; k < K; k += DBLK) agg_cnt[(size_t)blockIdx.x * K + k] = cnt[k];
+  for (uint32_t li = threadIdx.x; li < K; li += DBLK) agg_cnt[(size_t)blockIdx.x * K + lkey(g, li)] = cnt[li];
 }
 
 // Refresh path: per die queue, the call-wide rank of each tile's first
@@ -496,12 +500,15 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
 
   const uint32_t Dk = g.Dk;
   const size_t row = (size_t)blockIdx.x * K;
-  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+  // per-queue LDS records by LDS slot (lslot), as in pass 1, whose ranks
+  // carry the slot
+  for (uint32_t li = threadIdx.x; li < K; li += DBLK) {
+    const uint32_t k = lkey(g, li);
     const uint32_t base = tin_base[row + k];  // die rank of the tile's first request of k
-    KA[k] = KeyA{0u, 0u, tin_L[row + k]};
+    KA[li] = KeyA{0u, 0u, tin_L[row + k]};
     const uint32_t ch = k / Dk;
-    KW[k] = KeyW{base, seg_start[k] + base, ch * (gmax + 1) * Dk + (k - ch * Dk), totals[k]};
-    if (REF) refp[k] = st->ref_pend[k];
+    KW[li] = KeyW{base, seg_start[k] + base, ch * (gmax + 1) * Dk + (k - ch * Dk), totals[k]};
+    if (REF) refp[li] = st->ref_pend[k];
   }
   const int64_t cbase = ctl->cbase;
   const uint32_t shift = ctl->shift, G = ctl->G;
@@ -656,8 +663,10 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
           IX[gpos] = ix;
         }
       }
-      if (REF && r < refp[k])  // this admission claimed quantum r of k's pending ones
-        *st->ref_slot[st->ref_off[k] + st->ref_head[k] + r] = dd - g.tR;
+      if (REF && r < refp[k]) {  // this admission claimed quantum r of its queue's pending ones
+        const uint32_t kq = lkey(g, k);
+        *st->ref_slot[st->ref_off[kq] + st->ref_head[kq] + r] = dd - g.tR;
+      }
       const int64_t prev = (rc > 0) ? sval[pad16(p - 1)] : KA[k].L;
       const int64_t cell = imin((dd - cbase) >> shift, (int64_t)G);
       const int64_t pcell = (r == 0) ? -1 : imin((prev - cbase) >> shift, (int64_t)G);
