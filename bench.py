@@ -37,7 +37,7 @@ HBM_PEAK_GBPS = 8000.0
 # writes the kernel cannot avoid), and of the whole call.
 # (The die-order entry is one 8-byte word whenever time cells are at most 2^32 ns
 # wide, as on this workload.)
-ALG_BYTES = {"k_die_reduce": 20, "k_die_scatter": 20, "k_cell_agg": 8, "k_cell_win": 16}
+ALG_BYTES = {"k_die_reduce": 20, "k_die_scatter": 20, "k_cell_chan": 16, "k_cell_agg": 8, "k_cell_rest": 16}
 PATH_ALG_BYTES = 24  # read addr + issue, write complete
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic_config5.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_09800_amd", "csrc", "hbf_kernels.hip")

@@ -68,6 +68,8 @@ extern "C" {
                                  reached 2^62 (device-detected) */
 #define HBF_EHIP          -7  /* a HIP runtime call failed */
 #define HBF_ENOMEM        -8  /* host or device allocation failed */
+#define HBF_EINTERNAL     -9  /* a bounded device-side wait ran out (an internal
+                                 fault: the call failed closed) */
 
 /* complete_ns value written for every request of a failed call. */
 #define HBF_TIME_ERROR    INT64_MIN
@@ -394,8 +396,9 @@ int hbf_cache_sweep(const uint32_t *host_frames, const uint32_t *host_prefetch, 
 int hbf_wall_clock_tick_ps(hbf_model_t model, int64_t *tick_ps);
 
 /* Synchronise `stream`, then return and clear the sticky device status:
- * HBF_OK, HBF_ERANGE_TIME, HBF_EUNSORTED or HBF_EINVAL (in that order of
- * precedence); HBF_EHIP if synchronising or reading the status fails. */
+ * HBF_OK, HBF_ERANGE_TIME, HBF_EUNSORTED, HBF_EINVAL or HBF_EINTERNAL (in
+ * that order of precedence); HBF_EHIP if synchronising or reading the
+ * status fails. */
 int hbf_get_status(hbf_model_t model, void *stream);
 
 /* Copy the resource clocks to host memory after synchronising `stream`:

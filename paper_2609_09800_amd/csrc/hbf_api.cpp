@@ -70,8 +70,7 @@ Layout make_layout(const Geo &g, int64_t n) {
   L.off_lb = o;       o = up256(o + C * ((size_t)L.gmax + 1) * g.Dk * 4);
   L.off_cagg = o;     o = up256(o + C * (size_t)L.gmax * 8);
   L.off_cgin = o;     o = up256(o + C * (size_t)L.gmax * 8);
-  L.off_cmin = o;     o = up256(o + C * (size_t)L.gmax * 4);
-  L.off_cr0 = o;      o = up256(o + C * (size_t)L.gmax * 4);
+  L.off_wst = o;      o = up256(o + 2 * C * (size_t)L.gmax * 8);
   L.off_nbl = o;      o = up256(o + C * (size_t)L.gmax * 4);
   L.off_iss = o;      o = up256(o + (g.reg_block ? (size_t)n * 8 : 0));
   L.total = o;
@@ -782,6 +781,7 @@ int hbf_get_status(hbf_model_t m, void *stream) {
   if (s & (ERR_RANGE_TIME | ERR_OVERFLOW)) return HBF_ERANGE_TIME;
   if (s & ERR_UNSORTED) return HBF_EUNSORTED;
   if (s & ERR_MAP) return HBF_EINVAL;
+  if (s & ERR_INTERNAL) return HBF_EINTERNAL;
   return HBF_OK;
 }
 
@@ -859,6 +859,7 @@ const char *hbf_strerror(int code) {
     case HBF_ERANGE_TIME: return "time outside the model's domain";
     case HBF_EHIP: return "HIP runtime error";
     case HBF_ENOMEM: return "out of memory";
+    case HBF_EINTERNAL: return "internal wait bound exceeded";
     default: return "unknown status";
   }
 }

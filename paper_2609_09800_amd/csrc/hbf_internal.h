@@ -26,6 +26,7 @@ constexpr uint32_t ERR_RANGE_TIME = 1u;
 constexpr uint32_t ERR_UNSORTED = 2u;
 constexpr uint32_t ERR_OVERFLOW = 4u;
 constexpr uint32_t ERR_MAP = 8u;
+constexpr uint32_t ERR_INTERNAL = 16u;  // a bounded internal wait ran out (never expected)
 
 // Die stage: 256 threads (4 wave64), 16 items per thread per chunk.
 constexpr int BLK = 256;            // threads per block of the small kernels
@@ -110,8 +111,8 @@ struct CallCtl {
   int64_t max_dd;     // largest die-done time of the call
   int64_t max_cpl;    // largest in-range completion of the call (NEG if none)
   int64_t cbase;      // origin of the cell grid (= first issue time)
-  uint32_t n_rest;    // cells the window output pass leaves to k_cell_rest
-  uint32_t pad;
+  uint32_t n_rest;    // cells k_cell_agg lists for k_cell_rest (grids off the bucket path)
+  uint32_t wctr;      // next unit of the fused channel stage
 };
 
 // Workspace layout of one hbf_time_requests call.
@@ -125,8 +126,8 @@ struct Layout {
   size_t off_totals, off_seg, off_dfnew, off_cfnew;
   size_t off_dd, off_ix, off_kr, off_lb;
   size_t off_cagg, off_cgin;  // per (channel, time cell): aggregate, entering term
-  size_t off_cmin, off_cr0;   // per cell: smallest request index (window staging), first channel rank
-  size_t off_nbl;             // cells the window output pass leaves to k_cell_rest
+  size_t off_wst;             // fused channel stage: published aggregate and inclusive term per cell
+  size_t off_nbl;             // cells k_cell_agg lists for k_cell_rest
   size_t off_iss;             // register blocking: issue times in die order (n int64)
   // vmem route (tiles of VM_TILE requests): per tile its burst summary, the
   // summary of everything before it, its route-clock pair and entering

@@ -23,13 +23,15 @@
 //   k_die_scatter  pass 2: exact die-done times, written in die-queue order
 //                  (an LDS-staged stable multisplit) plus, per (channel,
 //                  time cell, die), the first die rank in that cell.
-//   k_cell_agg     per (channel, time cell): merge the cell's die runs by
-//                  (die-done, index) and reduce them to one channel term.
-//   k_cell_scan    per channel, the running maximum of those terms.
-//   k_cell_win     every cell again, with its entering term, one workgroup
-//                  per time window: write complete[] in request order
-//                  (staged by index in LDS where the window's requests
-//                  cluster); k_cell_rest takes the cells off the bucket path.
+//   k_cell_chan    per (time window, channel group), in window order: merge
+//                  each cell's die runs by (die-done, index), publish the
+//                  cell's channel term, take the term entering it by a
+//                  decoupled look-back over earlier windows, and write
+//                  complete[] in request order (staged by index in LDS
+//                  where the window's requests cluster).
+//   k_cell_agg, k_cell_scan, k_cell_rest
+//                  the same stage as reduce, scan and reduce again, for
+//                  grids whose cells are too wide for the bucket merge.
 //   k_finalize     fail-closed error fill, or commit of the new clocks.
 //
 // A die emits at most one request per t_read_ns, so a time cell of width
@@ -102,6 +104,7 @@ __global__ void k_prologue(CallCtl *ctl) {
     ctl->max_cpl = NEG;
     ctl->cbase = 0;
     ctl->n_rest = 0;
+    ctl->wctr = 0;
   }
 }
 
@@ -482,7 +485,7 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
     int64_t tile_elems, const int64_t *__restrict__ tin_L, const uint32_t *__restrict__ tin_base,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals,
     int64_t *__restrict__ DD, uint32_t *__restrict__ IX, uint32_t *__restrict__ LB, uint32_t gmax,
-    CallCtl *ctl, const DevState *st) {
+    CallCtl *ctl, const DevState *st, uint64_t *__restrict__ WST) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ SegMax shseg[DWAVES];
   __shared__ uint32_t shsum[DWAVES];
@@ -513,6 +516,14 @@ __global__ __launch_bounds__(DBLK) void k_die_scatter(
   const int64_t cbase = ctl->cbase;
   const uint32_t shift = ctl->shift, G = ctl->G;
   const bool narrow = shift <= 32;
+  if (G) {  // clear the fused channel stage's look-back words of this call's cells (channel-major)
+    const size_t nw = (size_t)G * g.C, step = (size_t)gridDim.x * DBLK;
+    for (size_t q = (size_t)blockIdx.x * DBLK + threadIdx.x; q < nw; q += step) {
+      const size_t c = q / G, at = c * gmax + (q - c * G);
+      WST[at] = 0;
+      WST[(size_t)gmax * g.C + at] = 0;
+    }
+  }
   const uint64_t relmask = narrow ? (uint64_t(1) << shift) - 1 : 0;
   const int64_t t0 = (int64_t)blockIdx.x * tile_elems;
   const int64_t t1 = imin(n, t0 + tile_elems);
@@ -889,12 +900,12 @@ DEVI int64_t stream_cell(CellLds &S, const int64_t *DD, const uint32_t *IX, bool
 // A cell knows its first rank from the cell table (the sum of its row), so
 // its aggregate is one number, M_j = max over its requests of
 // (dd - (rank-1)*xfer), and the term entering cell j is max(f0, M_j' for
-// j' < j).  The stage runs as reduce, scan, reduce again:
+// j' < j).  On the bucket path k_cell_chan merges each cell once and finds
+// the entering term by a look-back over earlier windows.  Grids off the
+// bucket path run reduce, scan, reduce again:
 //   k_cell_agg   M_j of every cell;
 //   k_cell_scan  per channel, the running maximum of M_j seeded with f0;
-//   k_cell_win   every cell again, now writing complete[] with its term
-//                (k_cell_rest: the cells the bucket path cannot take).
-// No block ever waits for another.
+//   k_cell_rest  every cell again, now writing complete[] with its term.
 //
 // One wave per cell.  The bucket path (buckets of width 2^lg_tR <= tR hold
 // at most one request per die): lane q gathers the requests of bucket q --
@@ -1080,50 +1091,35 @@ DEVI void cell_loop(const int64_t *__restrict__ DD, const uint32_t *__restrict__
   }
 }
 
-// Per cell, besides M_j: its first channel rank (CR0) and, for cells on the
-// bucket path, its smallest request index (CMIN; the heads of its die runs,
-// each run ascending in index), else CMIN_NONE -- cells with requests off
-// the bucket path are listed for k_cell_rest.
 constexpr uint32_t CMIN_NONE = 0xFFFFFFFFu;
 
+// Grids off the bucket path (cells too wide for 64 buckets, or more die
+// queues per channel than SL): M_j of every cell, which is listed for
+// k_cell_rest.  On the bucket path k_cell_chan does the whole stage and
+// this kernel returns at once.
 template <int SL>
 __global__ __launch_bounds__(64) void k_cell_agg(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals, Geo g,
-    CallCtl *ctl, int64_t *__restrict__ AGG, uint32_t *__restrict__ CMIN, uint32_t *__restrict__ CR0,
-    uint32_t *__restrict__ NBL, uint32_t gmax, uint32_t n) {
+    CallCtl *ctl, int64_t *__restrict__ AGG, uint32_t *__restrict__ NBL, uint32_t gmax, uint32_t n) {
   extern __shared__ __align__(16) unsigned char smem[];
   CellLds &S = *(CellLds *)smem;
   if (agent_load32(&ctl->err)) return;
   const uint32_t G = ctl->G, N = G * g.C, shift = ctl->shift;
+  if (grid_bucketable<SL>(g, shift)) return;
   const int64_t cbase = ctl->cbase;
-  const bool gb = grid_bucketable<SL>(g, shift);
   uint32_t errb = 0;
   cell_loop<SL>(DD, LB, seg_start, totals, g, gmax, N, G,
                 [&](uint32_t c, uint32_t j, const CellRuns &cr, const uint64_t (&xv)[SL]) {
                   const int64_t M = cell_pass<SL, false>(S, DD, IX, cr, xv, g, shift, cbase, j, NEG,
                                                          nullptr, n, &errb);
-                  const uint32_t lane = lane_id();
-                  const uint32_t len = cr.hi - cr.lo;
-                  const uint32_t m = wave_sum(len);
-                  const uint32_t maxlen = wave_umax(lane < g.Dk ? len : 0u);
-                  uint32_t head = CMIN_NONE;
-#pragma unroll
-                  for (int d = 0; d < SL; d++) {
-                    const uint32_t lend = __builtin_amdgcn_readlane(len, d);
-                    const uint32_t ix = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)xv[d], 0);
-                    if (d < (int)g.Dk && lend > 0) head = min(head, ix);
-                  }
-                  const bool bk = gb && maxlen <= 64;
-                  const size_t cell = (size_t)c * gmax + j;
-                  const uint32_t rank0 = wave_sum(cr.r0);
-                  if (lane == 0) {
-                    AGG[cell] = M;
-                    CR0[cell] = rank0;
-                    CMIN[cell] = (bk && m > 0) ? head : CMIN_NONE;
-                    if (m > 0 && !bk) NBL[atomicAdd(&ctl->n_rest, 1u)] = j * g.C + c;
+                  const uint32_t m = wave_sum(cr.hi - cr.lo);
+                  if (lane_id() == 0) {
+                    AGG[(size_t)c * gmax + j] = M;
+                    if (m > 0) NBL[atomicAdd(&ctl->n_rest, 1u)] = j * g.C + c;
                   }
                 });
+  if (errb) atomicOr(&ctl->err, errb);
 }
 
 // Per channel: GIN[j] = max(f0, M_j' for j' < j); the channel clock after the
@@ -1135,6 +1131,7 @@ __global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ A
                                                    int64_t *__restrict__ cfnew, uint32_t gmax) {
   __shared__ int64_t sh[WAVES];
   if (agent_load32(&ctl->err)) return;
+  if (grid_bucketable<SLOTS_MAX>(g, ctl->shift)) return;  // the bucket path is k_cell_chan's
   const uint32_t c = blockIdx.x, G = ctl->G;
   const size_t row = (size_t)c * gmax;
   const uint32_t per = (G + BLK - 1) / BLK;
@@ -1158,22 +1155,35 @@ __global__ __launch_bounds__(BLK) void k_cell_scan(const int64_t *__restrict__ A
   }
 }
 
-// ---- Output pass.  The completions of one time window, over all channels,
-// fall in a narrow band of request indices (every die queue is served at
-// its own pace, so a window holds each queue's next few dozen requests).
-// One workgroup takes a whole window: its waves merge the window's cells
-// (bucket path) and stage each completion in LDS at its index's offset in
-// the band, as a 32-bit offset from a window base; the workgroup then
-// writes the band in index order, so each wave stores whole 128-byte lines
-// instead of one scattered 8-byte value per request (scattered stores are
-// served one address at a time, and several channels' stores landing in
-// one line from different XCDs cost partial-line writes).  Completions
-// outside the staged span, or whose offset does not fit 32 bits, are
-// stored directly.  Cells off the bucket path go to k_cell_rest.
+// ---- Fused channel stage (grids on the bucket path).  The work is cut into
+// units: a unit is one time window j and a group of up to CH_GROUP channels
+// (all of them when C <= CH_GROUP), and units are claimed in (window, group)
+// order from a counter of the call.  One 1,024-thread workgroup per unit:
+//   1. each wave merges two of the unit's cells (bucket path, kept in
+//      registers) and publishes each cell's term M_j;
+//   2. per channel, the term entering the cell, max(f0, M_j' for j' < j),
+//      by a decoupled look-back over the earlier windows' published words:
+//      the nearest inclusive term plus the aggregates in between;
+//   3. it publishes the inclusive term max(entering, M_j);
+//   4. it writes the completions.  Those of one window fall in a band of
+//      request indices (each die queue serves its next requests), so each
+//      completion is staged in LDS at its index's offset from the band start
+//      as a 32-bit offset from a base, and the band is written in index
+//      order (whole lines); completions outside the staged span, or whose
+//      offset does not fit, are stored directly.
+// A unit waits only for units claimed before it: their workgroups are
+// running and publish their aggregates without waiting, so every wait ends.
+// The wait is bounded all the same; running past the bound fails the call
+// with ERR_INTERNAL instead of hanging.  The published words are single
+// 64-bit atomics that carry their own validity (0 = not yet), cleared by
+// k_die_scatter for the cells of the call and laid out channel-major, so a
+// half-wave polling 32 consecutive windows of one channel reads two lines.
 constexpr int WIN_WAVES = 16;
 constexpr int WIN_THREADS = WIN_WAVES * 64;
+constexpr int CH_GROUP = 2 * WIN_WAVES;
 constexpr uint32_t WIN_SLOTS = 32768;
 constexpr uint32_t WIN_EMPTY = 0xFFFFFFFFu;
+constexpr uint32_t LOOKBACK_ROUNDS = 1u << 22;
 
 struct WinLds {
   uint32_t stage[WIN_SLOTS];                         // completion - wbase at index lo + slot
@@ -1181,6 +1191,7 @@ struct WinLds {
   uint32_t rmin[WIN_WAVES];
   int64_t rbase[WIN_WAVES];
   uint32_t top;                                      // staged slots in use
+  uint32_t unit;
 };
 
 // Stage slot of band offset r.  One channel's requests often sit at a
@@ -1194,40 +1205,165 @@ DEVI uint32_t win_slot(uint32_t r) { return r ^ ((r >> 6) & 63u); }
 DEVI uint32_t wave_umin(uint32_t x) { return ~wave_umax(~x); }
 DEVI int64_t wave_min(int64_t x) { return -wave_max(-x); }
 
-// One bucketable cell of the window: merge its die runs in registers (lane q
-// gathers bucket q's entries from the lanes holding them, sorts them, and
-// owns merged positions boff..boff+cnt-1) and stage every completion.
+// Look-back words: 0 = not yet published, else the value + 2^62 (every
+// published value lies in [NEG, 2^62)).
+DEVI uint64_t enc_time(int64_t x) { return (uint64_t)x + (uint64_t(1) << 62); }
+DEVI int64_t dec_time(uint64_t w) { return (int64_t)(w - (uint64_t(1) << 62)); }
+DEVI uint64_t agent_load64(const uint64_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+DEVI void agent_store64(uint64_t *p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Inclusive maximum within each half (32 lanes) of the wave: lanes 31 and
+// 63 end up holding the two halves' maxima.
+DEVI int64_t half_incl_max(int64_t x) {
+  x = imax(x, dpp64<DPP_ROW_SHR1, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR2, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR4, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_SHR8, 0xF>(NEG, x));
+  x = imax(x, dpp64<DPP_ROW_BCAST15, 0xA>(NEG, x));
+  return x;
+}
+DEVI int64_t lane_i64(int64_t x, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), l);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// The terms entering window j of two channels, one per half-wave (lanes
+// 0-31: channel ca, 32-63: channel cb; a channel >= C is skipped).  Lane s
+// of a half inspects window base - s: its inclusive word, else its
+// aggregate.  A round ends at the nearest inclusive word (or before window
+// 0, where the term is the channel's clock f0) if no aggregate before it is
+// missing; otherwise the half folds what precedes the first missing one and
+// polls again from there.
+DEVI void look_back2(const uint64_t *WAGG, const uint64_t *WINC, uint32_t C, uint32_t gmax, uint32_t j,
+                     uint32_t ca, uint32_t cb, int64_t f0a, int64_t f0b, int64_t &ga, int64_t &gb,
+                     uint32_t *errb) {
+  const uint32_t lane = lane_id(), s = lane & 31;
+  const bool hi = lane >= 32;
+  const uint32_t c = hi ? cb : ca;
+  const int64_t f0 = hi ? f0b : f0a;
+  int64_t acc0 = NEG, acc1 = NEG;
+  int64_t base0 = (int64_t)j - 1, base1 = (int64_t)j - 1;
+  bool done0 = ca >= C, done1 = cb >= C;
+  uint32_t rounds = 0;
+  while (!(done0 && done1)) {
+    const bool mine_done = hi ? done1 : done0;
+    const int64_t jj = (hi ? base1 : base0) - (int64_t)s;
+    int stt = 2;  // 2: inclusive (or nothing left to fold), 1: aggregate, 0: not yet published
+    int64_t v = NEG;
+    if (!mine_done) {
+      if (jj < 0) {
+        v = f0;
+      } else {
+        const size_t at = (size_t)c * gmax + (size_t)jj;  // a half reads 32 consecutive words
+        const uint64_t wi = agent_load64(&WINC[at]);
+        if (wi) {
+          v = dec_time(wi);
+        } else {
+          const uint64_t wa = agent_load64(&WAGG[at]);
+          stt = wa ? 1 : 0;
+          if (wa) v = dec_time(wa);
+        }
+      }
+    }
+    const uint64_t incl = __ballot(stt == 2), none = __ballot(stt == 0);
+    const uint32_t bi0 = (uint32_t)incl, bi1 = (uint32_t)(incl >> 32);
+    const uint32_t bn0 = (uint32_t)none, bn1 = (uint32_t)(none >> 32);
+    const uint32_t fi0 = bi0 ? (uint32_t)__builtin_ctz(bi0) : 32u, fi1 = bi1 ? (uint32_t)__builtin_ctz(bi1) : 32u;
+    const uint32_t fn0 = bn0 ? (uint32_t)__builtin_ctz(bn0) : 32u, fn1 = bn1 ? (uint32_t)__builtin_ctz(bn1) : 32u;
+    // fold: through the inclusive word if it precedes every gap, else up to the gap
+    const uint32_t fi = hi ? fi1 : fi0, fn = hi ? fn1 : fn0;
+    const uint32_t lim = (fi < fn) ? fi + 1 : fn;
+    const int64_t red = half_incl_max(s < lim ? v : NEG);
+    bool stalled = false;
+    if (!done0) {
+      acc0 = imax(acc0, lane_i64(red, 31));
+      if (fi0 < fn0) done0 = true;
+      else {
+        base0 -= fn0;
+        stalled |= fn0 == 0;
+      }
+    }
+    if (!done1) {
+      acc1 = imax(acc1, lane_i64(red, 63));
+      if (fi1 < fn1) done1 = true;
+      else {
+        base1 -= fn1;
+        stalled |= fn1 == 0;
+      }
+    }
+    if (stalled) {
+      if (++rounds > LOOKBACK_ROUNDS) {
+        *errb |= ERR_INTERNAL;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  ga = acc0;
+  gb = acc1;
+}
+
+// A merged cell, held in registers: lane q owns bucket q's entries, sorted
+// (slot), their count and first merged position; plus the cell's size, its
+// smallest request index, the channel rank of its first request, and per
+// lane the maximum of dd - (rank0 + position) * xfer over its entries.
 template <int SL>
-DEVI void cell_emit_win(uint8_t (*tbl)[SLOTS_MAX], const CellRuns &cr, const uint64_t (&xv)[SL], const Geo &g,
-                        uint32_t shift, int64_t cbase, uint32_t j, int64_t gin, uint32_t lo, int64_t wbase,
-                        uint32_t *stage, int64_t *__restrict__ complete, uint32_t n, uint32_t *errb,
-                        uint32_t *top) {
+struct Merged {
+  uint64_t slot[SL];
+  uint32_t cnt, boff;
+  uint32_t m, head;
+  int64_t rank0, loc;
+};
+
+// Merge one bucketable cell (lane q gathers bucket q's entries from the
+// lanes that loaded them, sorts them, and takes merged positions
+// boff..boff+cnt-1).  Its run of die d holds at most one entry per bucket.
+template <int SL>
+DEVI void cell_merge(uint8_t (*tbl)[SLOTS_MAX], const CellRuns &cr, const uint64_t (&xv)[SL], const Geo &g,
+                     int64_t cstart, Merged<SL> &M, uint32_t *errb) {
   const uint32_t lane = lane_id();
   const int R = (int)g.Dk;
   const uint32_t lgt = g.lg_tR;
   const int64_t xfer = g.xfer;
   const uint32_t len = cr.hi - cr.lo;
-  const uint32_t m = wave_sum(len);
-  if (m == 0) return;
-  const uint32_t maxlen = wave_umax(lane < (uint32_t)R ? len : 0u);
-  if (maxlen > 64) return;  // off the bucket path: k_cell_rest
-  const int64_t rank0 = wave_sum(cr.r0);
-  const int64_t cstart = cbase + ((int64_t)j << shift);
+  M.m = wave_sum(len);
+  M.cnt = 0;
+  M.boff = 0;
+  M.head = CMIN_NONE;
+  M.rank0 = 0;
+  M.loc = NEG;
+#pragma unroll
+  for (int d = 0; d < SL; d++) M.slot[d] = KEY_EMPTY;
+  if (M.m == 0) return;
+  if (wave_umax(lane < (uint32_t)R ? len : 0u) > 64) {  // impossible on a bucketable grid
+    *errb |= ERR_INTERNAL;
+    M.m = 0;
+    return;
+  }
+  M.rank0 = wave_sum(cr.r0);
   reinterpret_cast<uint4 *>(&tbl[0][0])[lane] = make_uint4(0, 0, 0, 0);
   wave_sync();
   // sort key of entry `lane` of run d: offset in its bucket (< 2^20) << 31 | index
   const uint64_t offmask = (uint64_t(1) << lgt) - 1;
   uint64_t key[SL];
+  uint32_t head = CMIN_NONE;
 #pragma unroll
   for (int d = 0; d < SL; d++) {
     const uint32_t lend = __builtin_amdgcn_readlane(len, d);
     const uint64_t rel = xv[d] >> 32;
     key[d] = KEY_ONE | (rel & offmask) << 31 | (xv[d] & 0xFFFFFFFFull);
     if (d < R && lane < lend) tbl[rel >> lgt][d] = (uint8_t)(lane + 1);
+    // a run's first entry has its smallest index (die order is index order)
+    const uint32_t ix0 = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)xv[d], 0);
+    if (d < R && lend > 0) head = min(head, ix0);
   }
+  M.head = head;
   wave_sync();
-  uint64_t slot[SL];
-  uint32_t cnt = 0;
   {
     const uint4 row = reinterpret_cast<const uint4 *>(&tbl[0][0])[lane];
     const uint32_t rw[4] = {row.x, row.y, row.z, row.w};
@@ -1235,34 +1371,45 @@ DEVI void cell_emit_win(uint8_t (*tbl)[SLOTS_MAX], const CellRuns &cr, const uin
     for (int d = 0; d < SL; d++) {
       const uint32_t y = (rw[d >> 2] >> (8 * (d & 3))) & 0xFFu;
       const uint64_t v = __shfl(key[d], y ? (int)(y - 1) : 0);
-      slot[d] = y ? v : KEY_EMPTY;
-      cnt += y ? 1u : 0u;
+      M.slot[d] = y ? v : KEY_EMPTY;
+      M.cnt += y ? 1u : 0u;
     }
   }
-  sort_slots<SL>(slot);
-  const uint32_t boff = wave_excl_sum(cnt);
-  const int64_t cst = cstart + ((int64_t)lane << lgt) - rank0 * xfer;
-  int64_t loc = NEG;
+  sort_slots<SL>(M.slot);
+  M.boff = wave_excl_sum(M.cnt);
+  const int64_t cst = cstart + ((int64_t)lane << lgt) - M.rank0 * xfer;
 #pragma unroll
   for (int i = 0; i < SL; i++) {
-    if ((uint32_t)i < cnt) {
-      const int64_t v = cst + (int64_t)((slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(boff + i, (uint32_t)xfer);
-      loc = imax(loc, v);
+    if ((uint32_t)i < M.cnt) {
+      const int64_t v = cst + (int64_t)((M.slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(M.boff + i, (uint32_t)xfer);
+      M.loc = imax(M.loc, v);
     }
   }
-  int64_t carry = __shfl_up(wave_incl_max(loc), 1);
+  wave_sync();  // tbl is reused by the wave's next cell
+}
+
+// Completions of a merged cell given its entering term gin: staged in the
+// band when they fit, else stored directly.  mytop: staged span used.
+template <int SL>
+DEVI void cell_emit(const Merged<SL> &M, const Geo &g, int64_t cstart, int64_t gin, uint32_t lo, int64_t wbase,
+                    uint32_t *stage, int64_t *__restrict__ complete, uint32_t n, uint32_t *errb,
+                    uint32_t &mytop) {
+  if (M.m == 0) return;
+  const uint32_t lane = lane_id();
+  const int64_t xfer = g.xfer;
+  const int64_t cst = cstart + ((int64_t)lane << g.lg_tR) - M.rank0 * xfer;
+  int64_t carry = __shfl_up(wave_incl_max(M.loc), 1);
   if (lane == 0) carry = NEG;
   carry = imax(carry, gin);
-  const int64_t r0x = rank0 * xfer;
-  uint32_t mytop = 0;
+  const int64_t r0x = M.rank0 * xfer;
 #pragma unroll
   for (int i = 0; i < SL; i++) {
-    if ((uint32_t)i < cnt) {
-      const int64_t v = cst + (int64_t)((slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(boff + i, (uint32_t)xfer);
+    if ((uint32_t)i < M.cnt) {
+      const int64_t v = cst + (int64_t)((M.slot[i] >> 31) & 0x1FFFFFu) - (int64_t)mul32(M.boff + i, (uint32_t)xfer);
       carry = imax(carry, v);
-      const int64_t cpl = r0x + (int64_t)mul32(boff + i + 1, (uint32_t)xfer) + carry;
+      const int64_t cpl = r0x + (int64_t)mul32(M.boff + i + 1, (uint32_t)xfer) + carry;
       if (cpl >= TIME_LIMIT) *errb |= ERR_OVERFLOW;
-      const uint32_t ix = (uint32_t)slot[i] & 0x7FFFFFFFu;
+      const uint32_t ix = (uint32_t)M.slot[i] & 0x7FFFFFFFu;
       if (ix < n) {
         const uint32_t rel = ix - lo;
         const uint64_t off = (uint64_t)(cpl - wbase);
@@ -1275,45 +1422,85 @@ DEVI void cell_emit_win(uint8_t (*tbl)[SLOTS_MAX], const CellRuns &cr, const uin
       }
     }
   }
-  *top = max(*top, mytop);
+}
+
+// Requests of channel c in the call (lanes < Dk read one die queue each).
+DEVI uint32_t chan_total(const uint32_t *__restrict__ totals, uint32_t Dk, uint32_t c) {
+  const uint32_t lane = lane_id();
+  return wave_sum(lane < Dk ? totals[c * Dk + lane] : 0u);
 }
 
 template <int SL>
-__global__ __launch_bounds__(WIN_THREADS) void k_cell_win(
+__global__ __launch_bounds__(WIN_THREADS) void k_cell_chan(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ LB, const uint32_t *__restrict__ seg_start,
-    const uint32_t *__restrict__ totals, Geo g, CallCtl *ctl, const int64_t *__restrict__ GIN,
-    const uint32_t *__restrict__ CMIN, const uint32_t *__restrict__ CR0, int64_t *__restrict__ complete,
-    uint32_t gmax, uint32_t n) {
+    const uint32_t *__restrict__ totals, Geo g, CallCtl *ctl, const DevState *st, uint64_t *WAGG, uint64_t *WINC,
+    int64_t *__restrict__ complete, int64_t *__restrict__ cfnew, uint32_t gmax, uint32_t n) {
   extern __shared__ __align__(16) unsigned char smem[];
   WinLds &S = *(WinLds *)smem;
   if (agent_load32(&ctl->err)) return;
   const uint32_t G = ctl->G, shift = ctl->shift, C = g.C;
-  if (!grid_bucketable<SL>(g, shift)) return;  // every cell is k_cell_rest's
+  if (G == 0 || !grid_bucketable<SL>(g, shift)) return;
   const int64_t cbase = ctl->cbase, xfer = g.xfer;
   const uint32_t t = threadIdx.x, w = t >> 6, lane = t & 63;
+  const uint32_t NG = (C + CH_GROUP - 1) / CH_GROUP;
+  const uint32_t U = G * NG;
   for (uint32_t q = t; q < WIN_SLOTS; q += WIN_THREADS) S.stage[q] = WIN_EMPTY;
   uint32_t errb = 0;
-  // windows by rounds of gridDim.x; within a round each XCD (workgroup
-  // b runs on XCD b mod NXCD) takes a contiguous run of windows, so the
-  // direct stores of neighbouring windows, which share cache lines, meet in
-  // one L2 (measured: 2.71 ms against 2.78 ms round robin)
-  const uint32_t nb = gridDim.x;
-  const uint32_t first = nb % NXCD == 0 ? (blockIdx.x % NXCD) * (nb / NXCD) + blockIdx.x / NXCD : blockIdx.x;
-  for (uint32_t j = first; j < G; j += nb) {
-    // the window's band start (smallest index of its bucket-path cells) and
-    // completion base (a lower bound of every completion in them)
-    uint32_t mn = CMIN_NONE;
-    int64_t bmin = INT64_MAX;
-    for (uint32_t c = t; c < C; c += WIN_THREADS) {
-      const size_t cell = (size_t)c * gmax + j;
-      const uint32_t h = CMIN[cell];
-      if (h != CMIN_NONE) {
-        mn = min(mn, h);
-        bmin = imin(bmin, (int64_t)(CR0[cell] + 1u) * xfer + GIN[cell]);
+  while (true) {
+    if (t == 0) S.unit = atomicAdd(&ctl->wctr, 1u);
+    __syncthreads();
+    const uint32_t u = S.unit;
+    if (u >= U) break;  // the same for the whole workgroup
+    const uint32_t j = u / NG, c0 = (u - j * NG) * CH_GROUP;
+    const int64_t cstart = cbase + ((int64_t)j << shift);
+    const uint32_t ca = c0 + w, cb = c0 + w + WIN_WAVES;
+    Merged<SL> A, B;
+    A.m = B.m = 0;
+    if (ca < C) {
+      const CellRuns cr = cell_runs(LB, seg_start, totals, g.Dk, gmax, ca, j);
+      uint64_t xv[SL];
+      load_runs<SL>(DD, cr, (int)g.Dk, xv);
+      cell_merge<SL>(S.tbl[w], cr, xv, g, cstart, A, &errb);
+    }
+    if (cb < C) {
+      const CellRuns cr = cell_runs(LB, seg_start, totals, g.Dk, gmax, cb, j);
+      uint64_t xv[SL];
+      load_runs<SL>(DD, cr, (int)g.Dk, xv);
+      cell_merge<SL>(S.tbl[w], cr, xv, g, cstart, B, &errb);
+    }
+    const int64_t ma = A.m ? wave_max(A.loc) : NEG, mb = B.m ? wave_max(B.loc) : NEG;
+    if (lane == 0) {
+      if (ca < C) agent_store64(&WAGG[(size_t)ca * gmax + j], enc_time(ma));
+      if (cb < C) agent_store64(&WAGG[(size_t)cb * gmax + j], enc_time(mb));
+    }
+    int64_t ga = NEG, gb = NEG;
+    look_back2(WAGG, WINC, C, gmax, j, ca, cb, ca < C ? st->chan_free[ca] : NEG, cb < C ? st->chan_free[cb] : NEG,
+               ga, gb, &errb);
+    const int64_t ia = imax(ga, ma), ib = imax(gb, mb);
+    if (lane == 0) {
+      if (ca < C) agent_store64(&WINC[(size_t)ca * gmax + j], enc_time(ia));
+      if (cb < C) agent_store64(&WINC[(size_t)cb * gmax + j], enc_time(ib));
+    }
+    if (j == G - 1) {  // the channels' clocks after the call
+      const uint32_t ta = ca < C ? chan_total(totals, g.Dk, ca) : 0u;
+      const uint32_t tb = cb < C ? chan_total(totals, g.Dk, cb) : 0u;
+      if (lane == 0) {
+        if (ca < C) {
+          cfnew[ca] = (int64_t)ta * xfer + ia;
+          if (ta) atomicMax((long long *)&ctl->max_cpl, (long long)((int64_t)ta * xfer + ia));
+        }
+        if (cb < C) {
+          cfnew[cb] = (int64_t)tb * xfer + ib;
+          if (tb) atomicMax((long long *)&ctl->max_cpl, (long long)((int64_t)tb * xfer + ib));
+        }
       }
     }
-    mn = wave_umin(mn);
-    bmin = wave_min(bmin);
+    // band start (smallest index of the unit's requests) and completion base
+    // (a lower bound of every completion of the unit)
+    uint32_t mn = min(A.m ? A.head : CMIN_NONE, B.m ? B.head : CMIN_NONE);
+    int64_t bmin = INT64_MAX;
+    if (A.m) bmin = imin(bmin, (A.rank0 + 1) * xfer + ga);
+    if (B.m) bmin = imin(bmin, (B.rank0 + 1) * xfer + gb);
     if (lane == 0) {
       S.rmin[w] = mn;
       S.rbase[w] = bmin;
@@ -1327,16 +1514,10 @@ __global__ __launch_bounds__(WIN_THREADS) void k_cell_win(
       lo = min(lo, S.rmin[k]);
       wbase = imin(wbase, S.rbase[k]);
     }
-    if (lo != CMIN_NONE) {
+    if (lo != CMIN_NONE) {  // the same for the whole workgroup
       uint32_t top = 0;
-      for (uint32_t c = w; c < C; c += WIN_WAVES) {
-        const CellRuns cr = cell_runs(LB, seg_start, totals, g.Dk, gmax, c, j);
-        uint64_t xv[SL];
-        load_runs<SL>(DD, cr, (int)g.Dk, xv);
-        cell_emit_win<SL>(S.tbl[w], cr, xv, g, shift, cbase, j, GIN[(size_t)c * gmax + j], lo, wbase, S.stage,
-                          complete, n, &errb, &top);
-        wave_sync();
-      }
+      cell_emit<SL>(A, g, cstart, ga, lo, wbase, S.stage, complete, n, &errb, top);
+      cell_emit<SL>(B, g, cstart, gb, lo, wbase, S.stage, complete, n, &errb, top);
       top = wave_umax(top);
       if (lane == 0 && top) atomicMax(&S.top, top);
       __syncthreads();
@@ -1355,8 +1536,9 @@ __global__ __launch_bounds__(WIN_THREADS) void k_cell_win(
   if (errb) atomicOr(&ctl->err, errb);
 }
 
-// The cells the window pass leaves (off the bucket path): one wave each,
-// streamed through the LDS, completions stored directly.
+// Grids off the bucket path: every cell k_cell_agg listed, one wave each,
+// streamed through the LDS with its entering term from k_cell_scan,
+// completions stored directly.
 template <int SL>
 __global__ __launch_bounds__(64) void k_cell_rest(
     const int64_t *__restrict__ DD, const uint32_t *__restrict__ IX, const uint32_t *__restrict__ LB,
@@ -1498,7 +1680,7 @@ __global__ __launch_bounds__(BLK) void k_fill(int64_t *__restrict__ p, int64_t n
 // ------------------------------------------------------------------ launchers
 
 const char *const kKernelNames[] = {"k_prologue",  "k_die_reduce", "k_tile_scan", "k_key_scan",
-                                    "k_die_scatter", "k_cell_agg",  "k_cell_scan", "k_cell_win",
+                                    "k_die_scatter", "k_cell_chan", "k_cell_agg",  "k_cell_scan",
                                     "k_cell_rest", "k_finalize"};
 const int kNumTimedKernels = 10;
 
@@ -1539,6 +1721,7 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   uint32_t *LB = (uint32_t *)(ws + Lo.off_lb);
   int64_t *AGG = (int64_t *)(ws + Lo.off_cagg);
   int64_t *GIN = (int64_t *)(ws + Lo.off_cgin);
+  uint64_t *WST = (uint64_t *)(ws + Lo.off_wst);
   const uint32_t kbits = bits_for(g.K);
   const bool p2 = g.pow2 != 0;
   int evi = 0;
@@ -1588,7 +1771,7 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     const size_t lds = lds_die_scatter(g.K);
     hipLaunchKernelGGL(refresh ? k_die_scatter<true> : k_die_scatter<false>, dim3(Lo.nt), dim3(DBLK), lds, s,
                        issue, KR, Lo.n, g, Lo.tile_elems, tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl,
-                       st);
+                       st, WST);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
@@ -1602,12 +1785,34 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     mark();
     mark();
   } else {
-    // channel stage: enough one-wave blocks to fill the chip, a multiple of
-    // the XCD count, and no more than there can be cells
+    // channel stage.  On the bucket path (every grid but those with very
+    // wide cells or more than 16 die queues per channel) k_cell_chan does
+    // all of it; otherwise k_cell_agg -> k_cell_scan -> k_cell_rest.  Each
+    // kernel reads the grid the die stage chose and returns at once when
+    // the stage is the other one's.
     int dev = 0, ncu = 256, per_cu = 0;
     hipGetDevice(&dev);
     hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
     const int sl = g.Dk <= 4 ? 4 : g.Dk <= 8 ? 8 : 16;
+    const uint32_t nn = (uint32_t)Lo.n;
+    uint64_t *WAGG = WST, *WINC = WST + (size_t)Lo.gmax * g.C;
+    {  // one 1,024-thread workgroup per CU (its LDS holds a unit's band)
+      const dim3 gw((uint32_t)ncu), bw(WIN_THREADS);
+      const size_t lw = sizeof(WinLds);
+      if (sl == 4)
+        hipLaunchKernelGGL(k_cell_chan<4>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, st, WAGG, WINC, complete,
+                           cfnew, Lo.gmax, nn);
+      else if (sl == 8)
+        hipLaunchKernelGGL(k_cell_chan<8>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, st, WAGG, WINC, complete,
+                           cfnew, Lo.gmax, nn);
+      else
+        hipLaunchKernelGGL(k_cell_chan<16>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, st, WAGG, WINC, complete,
+                           cfnew, Lo.gmax, nn);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    mark();
+    // off the bucket path: enough one-wave blocks to fill the chip, a
+    // multiple of the XCD count, and no more than there can be cells
     const void *kfn = sl == 4 ? (const void *)k_cell_agg<4>
                       : sl == 8 ? (const void *)k_cell_agg<8> : (const void *)k_cell_agg<16>;
     hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 64, sizeof(CellLds));
@@ -1624,39 +1829,19 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     const dim3 gr = grid_of(per_cu);
     const dim3 bl(64);
     const size_t lds = sizeof(CellLds);
-    const uint32_t nn = (uint32_t)Lo.n;
-    uint32_t *CMIN = (uint32_t *)(ws + Lo.off_cmin), *CR0 = (uint32_t *)(ws + Lo.off_cr0);
     uint32_t *NBL = (uint32_t *)(ws + Lo.off_nbl);
     if (sl == 4)
-      hipLaunchKernelGGL(k_cell_agg<4>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, CMIN, CR0, NBL,
-                         Lo.gmax, nn);
+      hipLaunchKernelGGL(k_cell_agg<4>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, NBL, Lo.gmax, nn);
     else if (sl == 8)
-      hipLaunchKernelGGL(k_cell_agg<8>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, CMIN, CR0, NBL,
-                         Lo.gmax, nn);
+      hipLaunchKernelGGL(k_cell_agg<8>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, NBL, Lo.gmax, nn);
     else
-      hipLaunchKernelGGL(k_cell_agg<16>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, CMIN, CR0, NBL,
-                         Lo.gmax, nn);
+      hipLaunchKernelGGL(k_cell_agg<16>, gr, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, AGG, NBL, Lo.gmax, nn);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     mark();
     hipLaunchKernelGGL(k_cell_scan, dim3(g.C), dim3(BLK), 0, s, AGG, GIN, totals, g, ctl, st, cfnew, Lo.gmax);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     mark();
-    // output: one workgroup per window (one per CU: its LDS holds the
-    // window's band), then the cells off the bucket path
     {
-      const dim3 gw((uint32_t)ncu), bw(WIN_THREADS);
-      const size_t lw = sizeof(WinLds);
-      if (sl == 4)
-        hipLaunchKernelGGL(k_cell_win<4>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, GIN, CMIN, CR0, complete,
-                           Lo.gmax, nn);
-      else if (sl == 8)
-        hipLaunchKernelGGL(k_cell_win<8>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, GIN, CMIN, CR0, complete,
-                           Lo.gmax, nn);
-      else
-        hipLaunchKernelGGL(k_cell_win<16>, gw, bw, lw, s, DD, LB, seg, totals, g, ctl, GIN, CMIN, CR0, complete,
-                           Lo.gmax, nn);
-      if ((e = hipGetLastError()) != hipSuccess) return e;
-      mark();
       const dim3 gx = grid_of(4);
       if (sl == 4)
         hipLaunchKernelGGL(k_cell_rest<4>, gx, bl, lds, s, DD, IX, LB, seg, totals, g, ctl, GIN, NBL, complete,
@@ -1772,7 +1957,7 @@ hipError_t set_lds_limits(uint32_t K) {
   const void *fc[] = {(const void *)k_die_count<true>, (const void *)k_die_count<false>};
   for (const void *f : fc)
     if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, c)) != hipSuccess) return e;
-  const void *fw[] = {(const void *)k_cell_win<4>, (const void *)k_cell_win<8>, (const void *)k_cell_win<16>};
+  const void *fw[] = {(const void *)k_cell_chan<4>, (const void *)k_cell_chan<8>, (const void *)k_cell_chan<16>};
   for (const void *f : fw)
     if ((e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)sizeof(WinLds))) != hipSuccess)
       return e;

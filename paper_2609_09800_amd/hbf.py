@@ -20,6 +20,7 @@ HBF_EUNSORTED = -5
 HBF_ERANGE_TIME = -6
 HBF_EHIP = -7
 HBF_ENOMEM = -8
+HBF_EINTERNAL = -9
 HBF_TIME_ERROR = -(1 << 63)
 HBF_FLAG_PLANE_PARALLEL = 1
 HBF_FLAG_REGISTER_BLOCKING = 2

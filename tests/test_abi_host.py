@@ -39,7 +39,7 @@ def test_status_codes_match_header(lib):
     from paper_2609_09800_amd import hbf
     src = open(HEADER).read()
     for name in ["HBF_OK", "HBF_EINVAL", "HBF_EALIGN", "HBF_EOVERLAP", "HBF_ENOWORKSPACE",
-                 "HBF_EUNSORTED", "HBF_ERANGE_TIME", "HBF_EHIP", "HBF_ENOMEM"]:
+                 "HBF_EUNSORTED", "HBF_ERANGE_TIME", "HBF_EHIP", "HBF_ENOMEM", "HBF_EINTERNAL"]:
         v = int(re.search(rf"#define {name}\s+(-?\d+)", src).group(1))
         assert getattr(hbf, name) == v
     assert lib.hbf_strerror(-5) == b"issue times decrease"
