@@ -142,6 +142,8 @@ DEVI int64_t dpp64(int64_t old, int64_t x) {
 }
 constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114, DPP_ROW_SHR8 = 0x118;
 constexpr int DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143;
+// whole-wave shift right by one lane (gfx9 DPP wave_shr:1): lane l gets lane l - 1
+constexpr int DPP_WAVE_SHR1 = 0x138;
 // Inclusive scans over the 64 lanes: within rows of 16 by shifts of 1, 2,
 // 4, 8, then row 0 -> 1 and 2 -> 3 (bcast15), then rows 0-1 -> 2-3 (bcast31).
 DEVI uint32_t wave_incl_sum(uint32_t x) {

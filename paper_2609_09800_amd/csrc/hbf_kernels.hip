@@ -51,26 +51,40 @@ namespace hbf {
 // ------------------------------------------------------------------ die stage, shared
 
 // Stable rank of each item among this wave's items with the same key, in
-// (item, lane) order; wcnt is the wave's private per-key counter row.
-// Match-any over the key bits: lanes whose keys agree on every bit are peers.
-DEVI void wave_rank(const uint32_t *key, uint32_t *rank, uint16_t *wcnt, uint32_t kbits) {
+// (item, lane) order; wcnt is the wave's private per-key counter row and tag
+// its private per-key scratch row.  Every lane writes its lane number into
+// tag[key] and reads it back: one write per key survives, so a lane that
+// reads another lane's number shares its key.  Only those groups (in a
+// stream of consecutive pages, none or a few per item) are resolved, one
+// ballot each; every other lane is alone with its key in this item.
+DEVI void wave_rank(const uint32_t *key, uint32_t *rank, uint16_t *wcnt, uint32_t *tag) {
+  const uint32_t lane = lane_id();
 #pragma unroll
   for (int e = 0; e < DITEMS; e++) {
     const uint32_t k = key[e];
     const bool valid = k != KEY_NONE;
-    uint64_t peers = __ballot(valid);
-    for (uint32_t b = 0; b < kbits; b++) {
-      const bool bit = (k >> b) & 1u;
-      const uint64_t bal = __ballot(bit);
-      peers &= bit ? bal : ~bal;
-    }
-    uint32_t below = mask_below(peers);
-    uint32_t prior = 0;
-    if (valid) prior = wcnt[k];
-    // all reads of this item happen before the leaders' writes
+    if (valid) tag[k] = lane;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    if (valid && below == 0) wcnt[k] = (uint16_t)(prior + __popcll(peers));
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint32_t lead = valid ? tag[k] : lane;
+    uint32_t below = 0, cnt = 1;
+    uint64_t dup = __ballot(lead != lane);
+    while (dup) {  // the same on every lane
+      const uint32_t g = (uint32_t)__builtin_amdgcn_readlane((int)lead, (int)__builtin_ctzll(dup));
+      const uint64_t gm = __ballot(lead == g);  // the group, its surviving writer included
+      if (lead == g) {
+        below = mask_below(gm);
+        cnt = (uint32_t)__popcll(gm);
+      }
+      dup &= ~gm;
+    }
+    uint32_t prior = 0;
+    if (valid) prior = wcnt[k];
+    // all reads of this item happen before the group writers' updates
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    if (valid && below == 0) wcnt[k] = (uint16_t)(prior + cnt);
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     rank[e] = prior + below;
@@ -122,7 +136,8 @@ DEVI int64_t svc_sum(uint32_t g, uint32_t R, int64_t tR, int64_t tQ) {
 // depends on its rank in the call, so the tile aggregate is kept in global
 // form, max over the tile of issue - svc_sum(global rank), with the global
 // ranks of the tile's first requests taken from a count pass (tin_base).
-// LDS: ranges | amax[K] i64 | cmax[K] i64 | cnt[K] u32 | wcnt[DWAVES][K] u16 | tot[K] u16 | refp[K] u32
+// LDS: ranges | amax[K] i64 | cmax[K] i64 | cnt[K] u32 | wcnt[DWAVES][K] u16 | tot[K] u16 | refp[K] u32 |
+//      tag[DWAVES][K] u32
 template <bool POW2, bool REF>
 __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict__ addr,
                                                     const int64_t *__restrict__ issue, int64_t n,
@@ -131,7 +146,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
                                                     uint32_t *__restrict__ agg_cnt,
                                                     int64_t *__restrict__ agg_A,
                                                     uint32_t *__restrict__ KR, CallCtl *ctl,
-                                                    uint32_t kbits, const uint32_t *__restrict__ tin_base,
+                                                    const uint32_t *__restrict__ tin_base,
                                                     const DevState *st) {
   extern __shared__ __align__(16) unsigned char smem[];
   LdsRanges *lr = (LdsRanges *)smem;
@@ -143,6 +158,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
   uint16_t *tot = wcnt + DWAVES * K;
   // REF: pending quanta per key, read once per block (4-byte aligned: K may be odd)
   uint32_t *refp = (uint32_t *)(((uintptr_t)(tot + K) + 3) & ~(uintptr_t)3);
+  uint32_t *tags = refp + K;
 
   // per-queue LDS state is indexed by the queue's LDS slot (lslot); global
   // per-queue arrays by the queue itself
@@ -201,7 +217,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
       const int64_t x = cx[e];
       const uint64_t a = ca[e];
       // previous request's issue time, for the order check
-      int64_t prev = __shfl_up(x, 1);
+      int64_t prev = dpp64<DPP_WAVE_SHR1, 0xF>(x, x);  // lane l - 1's issue time
       int64_t last_of_prev_item = carry_prev;
       carry_prev = __shfl(x, 63);
       if (lane == 0) prev = (e > 0) ? last_of_prev_item : ((i > 0 && v) ? before : x);
@@ -214,7 +230,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
       key[e] = k == KEY_NONE ? KEY_NONE : lslot(g, k);
       iss[e] = x;
     }
-    wave_rank(key, rank, mycnt, kbits);
+    wave_rank(key, rank, mycnt, tags + w * K);
     __syncthreads();
     cross_wave_offsets(wcnt, tot, K);
     __syncthreads();
@@ -1684,17 +1700,12 @@ const char *const kKernelNames[] = {"k_prologue",  "k_die_reduce", "k_tile_scan"
                                     "k_cell_rest", "k_finalize"};
 const int kNumTimedKernels = 10;
 
-static uint32_t bits_for(uint32_t K) {
-  uint32_t b = 0;
-  while ((1u << b) < K) b++;
-  return b ? b : 1;
-}
-
 static size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
 
-// LDS of pass 1: range table | amax[K], cmax[K] i64 | cnt[K] | wcnt[DWAVES][K] u16 | tot[K] u16
+// LDS of pass 1: range table | amax[K], cmax[K] i64 | cnt[K] | wcnt[DWAVES][K] u16 | tot[K] u16 |
+// refp[K] u32 | tag[DWAVES][K] u32
 size_t lds_die_reduce(uint32_t K) {
-  return align16(sizeof(LdsRanges)) + K * (8 + 8 + 4) + DWAVES * K * 2 + K * 2 + 4 + K * 4;
+  return align16(sizeof(LdsRanges)) + K * (8 + 8 + 4) + DWAVES * K * 2 + K * 2 + 4 + K * 4 + DWAVES * K * 4;
 }
 size_t lds_die_count(uint32_t K) { return align16(sizeof(LdsRanges)) + K * 4; }
 size_t lds_die_scatter(uint32_t K) {
@@ -1722,7 +1733,6 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
   int64_t *AGG = (int64_t *)(ws + Lo.off_cagg);
   int64_t *GIN = (int64_t *)(ws + Lo.off_cgin);
   uint64_t *WST = (uint64_t *)(ws + Lo.off_wst);
-  const uint32_t kbits = bits_for(g.K);
   const bool p2 = g.pow2 != 0;
   int evi = 0;
   auto mark = [&]() {
@@ -1752,7 +1762,7 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
     auto kfn = p2 ? (refresh ? k_die_reduce<true, true> : k_die_reduce<true, false>)
                   : (refresh ? k_die_reduce<false, true> : k_die_reduce<false, false>);
     hipLaunchKernelGGL(kfn, dim3(Lo.nt), dim3(DBLK), lds, s, addr, issue, Lo.n, complete, g, rt, Lo.tile_elems,
-                       agg_cnt, agg_A, KR, ctl, kbits, tin_base, st);
+                       agg_cnt, agg_A, KR, ctl, tin_base, st);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
