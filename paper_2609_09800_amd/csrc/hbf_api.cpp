@@ -105,6 +105,9 @@ struct hbf_model {
   bool ref_maybe = false;
   int64_t **ref_slot = nullptr;
   size_t ref_slot_cap = 0;
+  // closed-loop layers in one launch: library-owned scratch
+  void *lay_ws = nullptr;
+  size_t lay_cap = 0;
 };
 
 static bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
@@ -222,6 +225,7 @@ void hbf_model_destroy(hbf_model_t m) {
     hipFree(m->st);
   }
   if (m->ws && m->lib_ws) hipFree(m->ws);
+  if (m->lay_ws) hipFree(m->lay_ws);
   if (m->ref_slot) hipFree(m->ref_slot);
   for (auto &set : m->ev)
     for (auto &e : set)
@@ -378,9 +382,33 @@ int hbf_time_layers(hbf_model_t m, const uint64_t *addr, int64_t n, const int64_
   int rc = ensure_device(m);
   if (rc) return rc;
   if (L == 0) return HBF_OK;
-  if (most > 0 && (rc = ensure_ws(m, most))) return rc;
   const RangeTable rt = snapshot(m);
   const hipStream_t s = (hipStream_t)stream;
+  // One launch for all layers when nothing but the plain two-stage model is
+  // involved (no refresh quanta pending, no register blocking, not the vmem
+  // route), the library owns the scratch, and every channel's workgroup can
+  // be resident at once; otherwise one timing call per layer.
+  if (!m->ref_maybe && !m->g.reg_block && !m->g.vmem && !m->ws_caller && most <= LAYERS_MAX_LAYER &&
+      L <= LAYERS_MAX_COUNT && layers_fast_ok(m->g, m->ncu)) {
+    const size_t need = layers_ws_bytes(m->g, n, L);
+    if (m->lay_cap < need) {
+      if (m->lay_ws) {
+        hipDeviceSynchronize();
+        hipFree(m->lay_ws);
+        m->lay_ws = nullptr;
+        m->lay_cap = 0;
+      }
+      void *p = nullptr;
+      if (hipMalloc(&p, need) != hipSuccess) return HBF_ENOMEM;
+      m->lay_ws = p;
+      m->lay_cap = need;
+    }
+    if (launch_layers(m->g, rt, (char *)m->lay_ws, m->st, addr, n, ls, L, t_start, compute_ns, issue, complete,
+                      done, s) != hipSuccess)
+      return HBF_EHIP;
+    return HBF_OK;
+  }
+  if (most > 0 && (rc = ensure_ws(m, most))) return rc;
   for (int l = 0; l < L; l++) {
     const int64_t a = ls[l], cnt = ls[l + 1] - ls[l];
     const int64_t *prev = l > 0 ? done + (l - 1) : nullptr;

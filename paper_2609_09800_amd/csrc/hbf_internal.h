@@ -47,6 +47,10 @@ constexpr int MAX_BUCKETS = 64;
 // requests of one window, from every channel, complete in one L2.
 constexpr int NXCD = 8;
 constexpr int MAX_RUNS = 64;        // die queues per channel (D, or D*P)
+// Closed-loop layers in one launch: one workgroup per layer ranks each
+// layer's requests, so layers are bounded; larger ones take a call per layer.
+constexpr int64_t LAYERS_MAX_LAYER = int64_t(1) << 22;
+constexpr int LAYERS_MAX_COUNT = 1 << 20;
 
 // Snapshot of the registered ranges, sorted by base (passed by value).
 struct RangeTable {
@@ -159,6 +163,15 @@ constexpr int VM_ITEMS = 16;
 constexpr int64_t VM_TILE = VM_THREADS * VM_ITEMS;
 hipError_t launch_vmem(const Geo &g, const RangeTable &rt, const Layout &L, char *ws, DevState *st,
                        const uint64_t *addr, const int64_t *issue, int64_t *complete, hipStream_t s);
+// Closed-loop layers in one launch (hbf_layers.hip): whether a geometry can
+// take it on this GPU (every channel's workgroup resident at once), its
+// scratch for n requests in L layers, and the launch (host_ls: L + 1 layer
+// starts on the host).
+bool layers_fast_ok(const Geo &g, int ncu);
+size_t layers_ws_bytes(const Geo &g, int64_t n, int L);
+hipError_t launch_layers(const Geo &g, const RangeTable &rt, char *ws, DevState *st, const uint64_t *addr,
+                         int64_t n, const int64_t *host_ls, int L, int64_t t_start, int64_t compute_ns,
+                         int64_t *issue, int64_t *complete, int64_t *done, hipStream_t s);
 hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s);
 hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
 // Device address of this GPU's static scratch of hbf_time_requests_noalloc
