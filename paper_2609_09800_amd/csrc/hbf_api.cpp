@@ -105,9 +105,14 @@ struct hbf_model {
   bool ref_maybe = false;
   int64_t **ref_slot = nullptr;
   size_t ref_slot_cap = 0;
-  // closed-loop layers in one launch: library-owned scratch
+  // closed-loop layers in one launch: library-owned scratch, the host copy
+  // of each call's layer and tile lists and an event after its upload, and
+  // whether the geometry can take that path on this GPU (-1: not asked yet)
   void *lay_ws = nullptr;
   size_t lay_cap = 0;
+  std::vector<unsigned char> lay_up;
+  hipEvent_t lay_ev = nullptr;
+  int lay_ok = -1;
 };
 
 static bool is_pow2(uint64_t x) { return x && !(x & (x - 1)); }
@@ -226,6 +231,7 @@ void hbf_model_destroy(hbf_model_t m) {
   }
   if (m->ws && m->lib_ws) hipFree(m->ws);
   if (m->lay_ws) hipFree(m->lay_ws);
+  if (m->lay_ev) hipEventDestroy(m->lay_ev);
   if (m->ref_slot) hipFree(m->ref_slot);
   for (auto &set : m->ev)
     for (auto &e : set)
@@ -388,8 +394,13 @@ int hbf_time_layers(hbf_model_t m, const uint64_t *addr, int64_t n, const int64_
   // involved (no refresh quanta pending, no register blocking, not the vmem
   // route), the library owns the scratch, and every channel's workgroup can
   // be resident at once; otherwise one timing call per layer.
+  if (m->lay_ok < 0) m->lay_ok = layers_fast_ok(m->g, m->ncu) ? 1 : 0;
   if (!m->ref_maybe && !m->g.reg_block && !m->g.vmem && !m->ws_caller && most <= LAYERS_MAX_LAYER &&
-      L <= LAYERS_MAX_COUNT && layers_fast_ok(m->g, m->ncu)) {
+      L <= LAYERS_MAX_COUNT && m->lay_ok) {
+    if (!m->lay_ev) {
+      if (hipEventCreateWithFlags(&m->lay_ev, hipEventDisableTiming) != hipSuccess) return HBF_EHIP;
+      if (hipEventRecord(m->lay_ev, s) != hipSuccess) return HBF_EHIP;
+    }
     const size_t need = layers_ws_bytes(m->g, n, L);
     if (m->lay_cap < need) {
       if (m->lay_ws) {
@@ -404,7 +415,7 @@ int hbf_time_layers(hbf_model_t m, const uint64_t *addr, int64_t n, const int64_
       m->lay_cap = need;
     }
     if (launch_layers(m->g, rt, (char *)m->lay_ws, m->st, addr, n, ls, L, t_start, compute_ns, issue, complete,
-                      done, s) != hipSuccess)
+                      done, m->lay_up, m->lay_ev, s) != hipSuccess)
       return HBF_EHIP;
     return HBF_OK;
   }

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "hbf.h"
 
 namespace hbf {
@@ -171,7 +173,8 @@ bool layers_fast_ok(const Geo &g, int ncu);
 size_t layers_ws_bytes(const Geo &g, int64_t n, int L);
 hipError_t launch_layers(const Geo &g, const RangeTable &rt, char *ws, DevState *st, const uint64_t *addr,
                          int64_t n, const int64_t *host_ls, int L, int64_t t_start, int64_t compute_ns,
-                         int64_t *issue, int64_t *complete, int64_t *done, hipStream_t s);
+                         int64_t *issue, int64_t *complete, int64_t *done, std::vector<unsigned char> &up,
+                         hipEvent_t up_done, hipStream_t s);
 hipError_t launch_refresh_drain(const Geo &g, DevState *st, int64_t t_from, int64_t t_to, hipStream_t s);
 hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
 // Device address of this GPU's static scratch of hbf_time_requests_noalloc

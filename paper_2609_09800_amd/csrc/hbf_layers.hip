@@ -36,6 +36,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "hbf_device.h"
 #include "hbf_internal.h"
 
@@ -45,7 +47,7 @@ namespace {
 
 constexpr int LBLK = 512;
 constexpr int LWAVES = LBLK / 64;
-constexpr int LITEMS = 8;  // completions per thread per scan chunk
+constexpr int LITEMS = 4;  // completions per thread per scan chunk
 constexpr int RBLK = 1024; // k_lay_run: one workgroup per channel
 constexpr int RWAVES = RBLK / 64;
 constexpr uint32_t LAY_SPIN_ROUNDS = 1u << 24;
@@ -57,60 +59,77 @@ DEVI uint64_t lay_enc(int64_t x) { return (uint64_t)x + (uint64_t(1) << 62); }
 DEVI int64_t lay_dec(uint64_t w) { return (int64_t)(w - (uint64_t(1) << 62)); }
 constexpr uint64_t LAY_VALID = uint64_t(1) << 61;
 
+// Pre-passes work on tiles of at most LAY_TILE requests of one layer (the
+// host lists them: layer, first, end).
+struct LayTile {
+  int64_t a, b;
+  uint32_t layer, first_tile;  // first_tile: the layer's first tile
+};
+
 template <bool POW2>
-__global__ __launch_bounds__(LBLK) void k_lay_count(const uint64_t *__restrict__ addr, const int64_t *__restrict__ ls,
+__global__ __launch_bounds__(LBLK) void k_lay_count(const uint64_t *__restrict__ addr, const LayTile *__restrict__ tiles,
                                                     Geo g, RangeTable rt, uint16_t *__restrict__ KEY,
                                                     uint32_t *__restrict__ CNT) {
   extern __shared__ __align__(16) unsigned char smem[];
   LdsRanges *lr = (LdsRanges *)smem;
   uint32_t *cnt = (uint32_t *)(smem + ((sizeof(LdsRanges) + 15) & ~size_t(15)));
-  const uint32_t K = g.K, l = blockIdx.x;
+  const uint32_t K = g.K;
+  const LayTile tl = tiles[blockIdx.x];
   load_ranges(lr, rt);
   for (uint32_t k = threadIdx.x; k <= K; k += LBLK) cnt[k] = 0;
   __syncthreads();
-  const int64_t a = ls[l], b = ls[l + 1];
-  for (int64_t i = a + threadIdx.x; i < b; i += LBLK) {
+  for (int64_t i = tl.a + threadIdx.x; i < tl.b; i += LBLK) {
     const uint32_t k0 = key_of<POW2>(g, lr, addr[i]);
     const uint32_t k = k0 == KEY_NONE ? K : k0;
     KEY[i] = (uint16_t)k;
     atomicAdd(&cnt[k], 1u);
   }
   __syncthreads();
-  for (uint32_t k = threadIdx.x; k <= K; k += LBLK) CNT[(size_t)l * (K + 1) + k] = cnt[k];
+  for (uint32_t k = threadIdx.x; k <= K; k += LBLK) CNT[(size_t)blockIdx.x * (K + 1) + k] = cnt[k];
 }
 
-// Exclusive offsets of every (layer, bucket), layer-major (OFF has one more
-// entry, the total); the done words cleared.
-__global__ __launch_bounds__(1024) void k_lay_scan(const uint32_t *__restrict__ CNT, uint64_t nb,
-                                                   uint32_t *__restrict__ OFF, uint64_t *__restrict__ SLOT,
-                                                   uint64_t nslot) {
-  __shared__ uint32_t sh[16];
-  const uint64_t per = (nb + 1023) / 1024;
-  const uint64_t s0 = min(nb, (uint64_t)threadIdx.x * per), s1 = min(nb, s0 + per);
+// One block per layer: the layer's bucket offsets (from the layer's start;
+// OFF[l][K+1] is the layer's end) and each of its tiles' offset in every
+// bucket; the layer's done words cleared.
+__global__ __launch_bounds__(LBLK) void k_lay_scan(const uint32_t *__restrict__ CNT, const int64_t *__restrict__ ls,
+                                                   const uint32_t *__restrict__ tile0, uint32_t K,
+                                                   uint32_t *__restrict__ OFF, uint32_t *__restrict__ TOFF,
+                                                   uint64_t *__restrict__ SLOT, uint32_t C) {
+  __shared__ uint32_t sh[LWAVES];
+  const uint32_t l = blockIdx.x, KB = K + 1;
+  const uint32_t f = tile0[l], e = tile0[l + 1];
+  const uint32_t per = (KB + LBLK - 1) / LBLK;
+  const uint32_t k0 = min(KB, threadIdx.x * per), k1 = min(KB, k0 + per);
   uint32_t sum = 0;
-  for (uint64_t q = s0; q < s1; q++) sum += CNT[q];
+  for (uint32_t k = k0; k < k1; k++)
+    for (uint32_t q = f; q < e; q++) sum += CNT[(size_t)q * KB + k];
   uint32_t ex;
-  const uint32_t tot = block_excl_sum<16>(sum, &ex, sh);
-  for (uint64_t q = s0; q < s1; q++) {
-    OFF[q] = ex;
-    ex += CNT[q];
+  block_excl_sum<LWAVES>(sum, &ex, sh);
+  uint32_t o = (uint32_t)ls[l] + ex;
+  for (uint32_t k = k0; k < k1; k++) {
+    OFF[(size_t)l * (KB + 1) + k] = o;
+    for (uint32_t q = f; q < e; q++) {
+      TOFF[(size_t)q * KB + k] = o;
+      o += CNT[(size_t)q * KB + k];
+    }
   }
-  if (threadIdx.x == 0) OFF[nb] = tot;
-  for (uint64_t q = threadIdx.x; q < nslot; q += 1024) SLOT[q] = 0;
+  if (threadIdx.x == 0) OFF[(size_t)l * (KB + 1) + KB] = (uint32_t)ls[l + 1];
+  for (uint32_t c = threadIdx.x; c < C; c += LBLK) SLOT[(size_t)l * C + c] = 0;
 }
 
-// Each request's index at OFF[l][k] + its rank among the layer's requests of
-// bucket k (index order).  Chunks of LBLK requests, one per thread: the
-// lanes of a wave that share a bucket are found with an LDS tag word
-// (every lane writes its lane number into its bucket's word and reads it
-// back; one write survives per bucket), counted per wave, and offset by the
-// counts of the chunk's earlier waves and of the earlier chunks.
+// Each request's index at its tile's offset in its bucket + its rank among
+// the tile's requests of that bucket (index order).  Chunks of LBLK
+// requests, one per thread: the lanes of a wave that share a bucket are
+// found with an LDS tag word (every lane writes its lane number into its
+// bucket's word and reads it back; one write survives per bucket), counted
+// per wave, and offset by the counts of the chunk's earlier waves and of the
+// earlier chunks.
 // LDS: run[K+1] u32 | wcnt[LWAVES][K+1] u16 (zero between chunks) | tag[LWAVES][K+1] u32
-__global__ __launch_bounds__(LBLK) void k_lay_place(const int64_t *__restrict__ ls, const uint16_t *__restrict__ KEY,
-                                                    uint32_t K, const uint32_t *__restrict__ OFF,
+__global__ __launch_bounds__(LBLK) void k_lay_place(const LayTile *__restrict__ tiles, const uint16_t *__restrict__ KEY,
+                                                    uint32_t K, const uint32_t *__restrict__ TOFF,
                                                     uint32_t *__restrict__ LISTD) {
   extern __shared__ __align__(16) unsigned char smem[];
-  const uint32_t KB = K + 1, l = blockIdx.x;
+  const uint32_t KB = K + 1;
   uint32_t *run = (uint32_t *)smem;
   uint16_t *wcnt = (uint16_t *)(run + KB);
   uint32_t *tag = (uint32_t *)(((uintptr_t)(wcnt + LWAVES * KB) + 3) & ~(uintptr_t)3);
@@ -118,12 +137,12 @@ __global__ __launch_bounds__(LBLK) void k_lay_place(const int64_t *__restrict__ 
   for (uint32_t q = threadIdx.x; q < LWAVES * KB; q += LBLK) wcnt[q] = 0;
   __syncthreads();
   const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
-  const int64_t a = ls[l], b = ls[l + 1];
-  const uint32_t *off = OFF + (size_t)l * KB;
+  const LayTile tl = tiles[blockIdx.x];
+  const uint32_t *off = TOFF + (size_t)blockIdx.x * KB;
   uint32_t *mytag = tag + w * KB;
-  for (int64_t c0 = a; c0 < b; c0 += LBLK) {
+  for (int64_t c0 = tl.a; c0 < tl.b; c0 += LBLK) {
     const int64_t i = c0 + threadIdx.x;
-    const bool valid = i < b;
+    const bool valid = i < tl.b;
     const uint32_t k = valid ? KEY[i] : 0u;
     if (valid) mytag[k] = lane;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -187,8 +206,8 @@ struct LayArgs {
 // terms and indices by channel rank.  Inlined twice, on LDS arrays and on
 // device-memory arrays, so each copy addresses one memory directly.
 template <typename PL, typename PV, typename PI>
-DEVI void lay_rank_scan(PL LI, PV RV, PI RI, uint32_t Mc, uint32_t Dk, const uint32_t *boff, const uint32_t *m,
-                        const int64_t *base, const int64_t *alpha, const uint32_t *beta, int64_t tR, int64_t xfer,
+DEVI void lay_rank_scan(PL LI, PV RV, PI RI, uint32_t Mc, uint32_t Dk, const uint32_t *boff, const int64_t *base,
+                        const uint4 *pairs, int64_t tR, int64_t xfer,
                         int64_t cfree, int64_t *__restrict__ complete, int64_t *shm, int64_t *s_chunk,
                         int64_t *s_last, uint32_t *s_err) {
   const uint32_t t = threadIdx.x;
@@ -203,23 +222,24 @@ DEVI void lay_rank_scan(PL LI, PV RV, PI RI, uint32_t Mc, uint32_t Dk, const uin
     const uint32_t b = lo, j = p - boff[b];
     const uint32_t idx = LI[p];
     const int64_t dd = base[b] + (int64_t)(j + 1) * tR;
-    const int64_t *arow = alpha + b * Dk;
-    const uint32_t *brow = beta + b * Dk;
-    int64_t r = j;
-    // branch-free over the other die queues, so their LDS reads overlap
+    const uint4 *prow = pairs + b * Dk;
+    int32_t r = (int32_t)j;
+    // branch-free over the other die queues, one 16-byte record each, so
+    // their LDS reads overlap; 32-bit throughout (alpha is clamped to +-2^23,
+    // beyond any rank)
 #pragma unroll 4
     for (uint32_t b1 = 0; b1 < Dk; b1++) {
-      const int64_t mb = b1 == b ? 0 : (int64_t)m[b1];
-      const int64_t al = arow[b1] + (int64_t)j;
-      const uint32_t be = brow[b1];
-      int64_t k0 = be ? al + 1 : al;  // b1's requests that leave their die strictly earlier
-      k0 = k0 < 0 ? 0 : (k0 > mb ? mb : k0);
+      const uint4 pr = prow[b1];  // {alpha, beta, m (0 for b itself), first position}
+      const int32_t mb = (int32_t)pr.z;
+      const int32_t al = (int32_t)pr.x + (int32_t)j;
+      const uint32_t be = pr.y;
+      const int32_t k0 = min(max(be ? al + 1 : al, 0), mb);  // b1's requests leaving their die earlier
       // the one that leaves at the same time comes first if its index is smaller
-      const bool tie = !be && al >= 0 && al < mb;
-      const uint32_t other = LI[tie ? boff[b1] + (uint32_t)al : p];
+      const bool tie = !be && (uint32_t)al < (uint32_t)mb;
+      const uint32_t other = LI[tie ? pr.w + (uint32_t)al : p];
       r += k0 + ((tie && other < idx) ? 1 : 0);
     }
-    RV[r] = dd - r * xfer;
+    RV[r] = dd - (int64_t)r * xfer;
     RI[r] = idx;
   }
   __syncthreads();
@@ -256,63 +276,80 @@ DEVI void lay_rank_scan(PL LI, PV RV, PI RI, uint32_t Mc, uint32_t Dk, const uin
 // One workgroup per channel c; every layer in turn.  A layer's requests of
 // the channel (at most cap of them) are staged in LDS with their ranks and
 // Lindley terms; a larger share of a layer works in the device-memory copies.
-// LDS: dfree[Dk], base[Dk], alpha[Dk][Dk] i64 | m[Dk], boff[Dk+1], beta[Dk][Dk] u32 |
-//      sRV[cap] i64 | sL[cap], sRI[cap] u32
+// The next layer's offsets and request list are fetched into the other of
+// two buffers while wave 0 runs the current layer's exchange.
+// LDS: pairs[Dk][Dk] {alpha, beta, m, first position} | dfree[Dk], base[Dk], sRV[cap] i64 |
+//      m[Dk], boff[2][Dk+1], sL[2][cap], sRI[cap] u32
+struct LayHdr {
+  uint32_t oc, Mc, n0, nn, any;
+};
+
 __global__ __launch_bounds__(RBLK) void k_lay_run(LayArgs A, uint32_t cap) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ int64_t shm[RWAVES];
   __shared__ int64_t s_last, s_chunk, s_lmax;
   __shared__ uint32_t s_err, s_any;
+  __shared__ LayHdr hdr[2];
   const Geo &g = A.g;
   const uint32_t Dk = g.Dk, C = g.C, K = g.K, KB = K + 1, c = blockIdx.x;
   const int64_t tR = g.tR, xfer = g.xfer;
-  int64_t *dfree = (int64_t *)smem;
+  uint4 *pairs = (uint4 *)smem;
+  int64_t *dfree = (int64_t *)(pairs + Dk * Dk);
   int64_t *base = dfree + Dk;
-  int64_t *alpha = base + Dk;
-  int64_t *sRV = alpha + Dk * Dk;
+  int64_t *sRV = base + Dk;
   uint32_t *m = (uint32_t *)(sRV + cap);
-  uint32_t *boff = m + Dk;
-  uint32_t *beta = boff + Dk + 1;
-  uint32_t *sL = beta + Dk * Dk;
-  uint32_t *sRI = sL + cap;
+  uint32_t *boffb = m + Dk;  // [2][Dk + 1]
+  uint32_t *sLb = boffb + 2 * (Dk + 1);  // [2][cap]
+  uint32_t *sRI = sLb + 2 * cap;
   const uint32_t t = threadIdx.x, lane = lane_id();
+  // layer ll's offsets and (when it fits) its request list into buffer ll & 1,
+  // by threads [t0, RBLK)
+  auto fetch = [&](uint32_t ll, uint32_t t0) {
+    if (ll >= A.L || t < t0) return;
+    const uint32_t u = t - t0, nt = RBLK - t0, bi = ll & 1;
+    const uint32_t *off = A.OFF + (size_t)ll * (KB + 1);
+    const uint32_t oc = off[c * Dk], Mc = off[(c + 1) * Dk] - oc;
+    for (uint32_t d = u; d <= Dk; d += nt) boffb[bi * (Dk + 1) + d] = off[c * Dk + d] - oc;
+    if (Mc <= cap)
+      for (uint32_t p = u; p < Mc; p += nt) sLb[bi * cap + p] = A.LISTD[oc + p];
+    if (u == 0) hdr[bi] = LayHdr{oc, Mc, off[K], off[KB] - off[K], off[KB] > off[0] ? 1u : 0u};
+  };
   for (uint32_t d = t; d < Dk; d += RBLK) dfree[d] = A.st->die_free[c * Dk + d];
   int64_t cfree = A.st->chan_free[c];
   int64_t prev_done = 0;
+  fetch(0, 0);
+  __syncthreads();
   for (uint32_t l = 0; l < A.L; l++) {
     const int64_t tl = l == 0 ? A.t_start : prev_done + A.compute_ns;
-    const uint32_t *off = A.OFF + (size_t)l * KB;
-    const bool any_req = off[KB] > off[0];  // the layer is not empty
-    const uint32_t oc = off[c * Dk];
-    const uint32_t Mc = off[(c + 1) * Dk] - oc;
-    const uint32_t n0 = off[K], nn = off[KB] - n0;  // the layer's native requests
-    const bool staged = Mc <= cap;                   // the same for the whole workgroup
+    const uint32_t bi = l & 1;
+    const LayHdr h = hdr[bi];
+    const bool any_req = h.any != 0;  // the layer is not empty
+    const uint32_t oc = h.oc, Mc = h.Mc, n0 = h.n0, nn = h.nn;  // nn: the layer's native requests
+    const bool staged = Mc <= cap;  // the same for the whole workgroup
+    uint32_t *sL = sLb + bi * cap;
+    const uint32_t *boff = boffb + bi * (Dk + 1);
     const uint32_t *LI = staged ? sL : A.LISTD + oc;
-    int64_t *RV = staged ? sRV : A.RV + oc;
-    uint32_t *RI = staged ? sRI : A.RI + oc;
-    for (uint32_t d = t; d <= Dk; d += RBLK) boff[d] = off[c * Dk + d] - oc;
     if (t == 0) {
       // an issue time outside [0, 2^61) fails a layer that has requests; an
       // empty layer fails only behind a failed one (negative time)
       s_err = (tl < 0 || (any_req && tl >= ISSUE_LIMIT)) ? ERR_RANGE_TIME : 0u;
       s_last = NEG;
     }
-    // the channel's request indices (staged); the layer's issue times, a
-    // contiguous 1/C slice per workgroup; a 1/C share of the native requests
-    if (staged)
-      for (uint32_t p = t; p < Mc; p += RBLK) sL[p] = A.LISTD[oc + p];
+    // the layer's issue times, a contiguous 1/C slice per workgroup; a 1/C
+    // share of the native requests
     {
       const int64_t la = A.ls[l], lb = A.ls[l + 1];
       const int64_t sl = (lb - la + C - 1) / C, sa = la + (int64_t)c * sl, sb = sa + sl < lb ? sa + sl : lb;
       for (int64_t i = sa + t; i < sb; i += RBLK) A.issue[i] = tl;
     }
     for (uint32_t q = c + t * C; q < nn; q += RBLK * C) A.complete[A.LISTD[n0 + q]] = tl;
-    __syncthreads();
     for (uint32_t d = t; d < Dk; d += RBLK) {
       m[d] = boff[d + 1] - boff[d];
       base[d] = imax(tl, dfree[d]);
-      if (m[d] && base[d] >= TIME_LIMIT - (int64_t)m[d] * tR) atomicOr(&s_err, ERR_OVERFLOW);
     }
+    __syncthreads();
+    for (uint32_t d = t; d < Dk; d += RBLK)
+      if (m[d] && base[d] >= TIME_LIMIT - (int64_t)m[d] * tR) atomicOr(&s_err, ERR_OVERFLOW);
     __syncthreads();
     const bool go = s_err == 0;  // the same for the whole workgroup
     if (go) {
@@ -320,18 +357,20 @@ __global__ __launch_bounds__(RBLK) void k_lay_run(LayArgs A, uint32_t cap) {
         const uint32_t b0 = q / Dk, b1 = q - b0 * Dk;
         const int64_t delta = base[b0] - base[b1];
         const int64_t al = floor_div(delta, tR);
-        alpha[q] = al;
-        beta[q] = (uint32_t)(delta - al * tR);
+        const int64_t lim = int64_t(1) << 23;  // beyond any rank: clamping keeps every count
+        pairs[q] = make_uint4((uint32_t)(int32_t)(al < -lim ? -lim : (al > lim ? lim : al)),
+                              (uint32_t)(delta - al * tR), b0 == b1 ? 0u : m[b1], boff[b1]);
       }
       __syncthreads();
       if (staged)
-        lay_rank_scan(sL, sRV, sRI, Mc, Dk, boff, m, base, alpha, beta, tR, xfer, cfree, A.complete, shm, &s_chunk,
-                      &s_last, &s_err);
+        lay_rank_scan(sL, sRV, sRI, Mc, Dk, boff, base, pairs, tR, xfer, cfree, A.complete, shm, &s_chunk, &s_last,
+                      &s_err);
       else
-        lay_rank_scan(A.LISTD + oc, A.RV + oc, A.RI + oc, Mc, Dk, boff, m, base, alpha, beta, tR, xfer, cfree,
-                      A.complete, shm, &s_chunk, &s_last, &s_err);
+        lay_rank_scan(A.LISTD + oc, A.RV + oc, A.RI + oc, Mc, Dk, boff, base, pairs, tR, xfer, cfree, A.complete,
+                      shm, &s_chunk, &s_last, &s_err);
     }
     __syncthreads();
+    fetch(l + 1, 64);  // waves 1 and up, meanwhile wave 0 exchanges
     // the layer's exchange: the channel's latest completion, or its error
     if (t == 0) {
       const uint32_t e = s_err;
@@ -386,17 +425,18 @@ __global__ __launch_bounds__(RBLK) void k_lay_run(LayArgs A, uint32_t cap) {
 size_t lds_lay_count(uint32_t K) { return ((sizeof(LdsRanges) + 15) & ~size_t(15)) + (size_t)(K + 1) * 4; }
 size_t lds_lay_place(uint32_t K) { return (size_t)(K + 1) * 4 + LWAVES * (size_t)(K + 1) * 2 + 4 + LWAVES * (size_t)(K + 1) * 4; }
 size_t lds_lay_run_fixed(uint32_t Dk) {
-  return (size_t)Dk * 16 + (size_t)Dk * Dk * 8 + (size_t)Dk * 4 + (Dk + 1) * 4 + (size_t)Dk * Dk * 4;
+  return (size_t)Dk * Dk * 16 + (size_t)Dk * 16 + (size_t)Dk * 4 + 2 * (Dk + 1) * 4;
 }
 // Staged requests per layer and channel: what the LDS holds beside the
-// fixed part, at 16 bytes each (term, index, rank slot), up to 8,192.
+// fixed part, at 20 bytes each (term, index by rank, two request lists), up
+// to 8,192.
 constexpr size_t LAY_LDS_BUDGET = 152 * 1024;
 uint32_t lay_cap(uint32_t Dk) {
   const size_t f = lds_lay_run_fixed(Dk);
-  const size_t c = f < LAY_LDS_BUDGET ? (LAY_LDS_BUDGET - f) / 16 : 0;
+  const size_t c = f < LAY_LDS_BUDGET ? (LAY_LDS_BUDGET - f) / 20 : 0;
   return (uint32_t)(c > 8192 ? 8192 : c);
 }
-size_t lds_lay_run(uint32_t Dk) { return lds_lay_run_fixed(Dk) + (size_t)lay_cap(Dk) * 16; }
+size_t lds_lay_run(uint32_t Dk) { return lds_lay_run_fixed(Dk) + (size_t)lay_cap(Dk) * 20; }
 
 }  // namespace
 
@@ -409,7 +449,9 @@ bool layers_fast_ok(const Geo &g, int ncu) {
       hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess || !coop)
     return false;
   if (hipFuncSetAttribute((const void *)k_lay_run, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          (int)lds_lay_run(g.Dk)) != hipSuccess)
+                          (int)lds_lay_run(g.Dk)) != hipSuccess ||
+      hipFuncSetAttribute((const void *)k_lay_place, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)lds_lay_place(g.K)) != hipSuccess)
     return false;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void *)k_lay_run, RBLK, lds_lay_run(g.Dk)) !=
       hipSuccess)
@@ -417,43 +459,80 @@ bool layers_fast_ok(const Geo &g, int ncu) {
   return (int64_t)per_cu * ncu >= (int64_t)g.C;
 }
 
+// Tiles of the pre-passes: the layers cut into pieces of at most LAY_TILE
+// requests (an empty layer has none).
+constexpr int64_t LAY_TILE = 8192;
+static uint32_t n_tiles(const int64_t *ls, int L) {
+  uint64_t nt = 0;
+  for (int l = 0; l < L; l++) nt += (uint64_t)((ls[l + 1] - ls[l] + LAY_TILE - 1) / LAY_TILE);
+  return (uint32_t)nt;
+}
+
 size_t layers_ws_bytes(const Geo &g, int64_t n, int L) {
-  const size_t nb = (size_t)L * (g.K + 1);
-  return 256 * 8 + (size_t)n * (2 + 4 + 8 + 4) + (nb + 1) * 4 * 2 + (size_t)L * g.C * 8 + (size_t)(L + 1) * 8;
+  const size_t KB = g.K + 1, nt = (size_t)n / LAY_TILE + L + 1;
+  return 256 * 16 + (size_t)(L + 1) * 8 + (size_t)(L + 1) * 4 + nt * sizeof(LayTile) + (size_t)n * (2 + 4 + 8 + 4) +
+         nt * KB * 4 * 2 + (size_t)L * (KB + 1) * 4 + (size_t)L * g.C * 8;
 }
 
 hipError_t launch_layers(const Geo &g, const RangeTable &rt, char *ws, DevState *st, const uint64_t *addr,
                          int64_t n, const int64_t *host_ls, int L, int64_t t_start, int64_t compute_ns,
-                         int64_t *issue, int64_t *complete, int64_t *done, hipStream_t s) {
-  const size_t nb = (size_t)L * (g.K + 1);
+                         int64_t *issue, int64_t *complete, int64_t *done, std::vector<unsigned char> &up,
+                         hipEvent_t up_done, hipStream_t s) {
+  const size_t KB = g.K + 1;
+  const uint32_t NT = n_tiles(host_ls, L);
+  // host side: the layer starts, each layer's first tile, the tile list (one
+  // upload from a buffer the model keeps; an earlier call's upload must have
+  // left it first)
+  hipError_t e;
+  if ((e = hipEventSynchronize(up_done)) != hipSuccess) return e;
+  const size_t b_ls = (size_t)(L + 1) * 8, b_t0 = ((size_t)(L + 1) * 4 + 7) & ~size_t(7);
+  up.resize(b_ls + b_t0 + (size_t)(NT ? NT : 1) * sizeof(LayTile));
+  int64_t *h_ls = (int64_t *)up.data();
+  uint32_t *h_t0 = (uint32_t *)(up.data() + b_ls);
+  LayTile *h_tiles = (LayTile *)(up.data() + b_ls + b_t0);
+  uint32_t q = 0;
+  for (int l = 0; l < L; l++) {
+    h_ls[l] = host_ls[l];
+    h_t0[l] = q;
+    for (int64_t a = host_ls[l]; a < host_ls[l + 1]; a += LAY_TILE)
+      h_tiles[q++] = LayTile{a, a + LAY_TILE < host_ls[l + 1] ? a + LAY_TILE : host_ls[l + 1], (uint32_t)l, h_t0[l]};
+  }
+  h_ls[L] = host_ls[L];
+  h_t0[L] = q;
   size_t o = 0;
   auto take = [&](size_t bytes) {
     char *p = ws + o;
     o = (o + bytes + 255) & ~size_t(255);
     return p;
   };
-  int64_t *ls = (int64_t *)take((size_t)(L + 1) * 8);
+  unsigned char *d_up = (unsigned char *)take(up.size());
+  const int64_t *ls = (const int64_t *)d_up;
+  const uint32_t *tile0 = (const uint32_t *)(d_up + b_ls);
+  const LayTile *tiles = (const LayTile *)(d_up + b_ls + b_t0);
   uint16_t *KEY = (uint16_t *)take((size_t)n * 2);
-  uint32_t *CNT = (uint32_t *)take((nb + 1) * 4);
-  uint32_t *OFF = (uint32_t *)take((nb + 1) * 4);
+  uint32_t *CNT = (uint32_t *)take((size_t)(NT ? NT : 1) * KB * 4);
+  uint32_t *TOFF = (uint32_t *)take((size_t)(NT ? NT : 1) * KB * 4);
+  uint32_t *OFF = (uint32_t *)take((size_t)L * (KB + 1) * 4);
   uint32_t *LISTD = (uint32_t *)take((size_t)n * 4);
   int64_t *RV = (int64_t *)take((size_t)n * 8);
   uint32_t *RI = (uint32_t *)take((size_t)n * 4);
   uint64_t *SLOT = (uint64_t *)take((size_t)L * g.C * 8);
-  hipError_t e;
-  if ((e = hipMemcpyAsync(ls, host_ls, (size_t)(L + 1) * 8, hipMemcpyHostToDevice, s)) != hipSuccess) return e;
-  if ((e = hipFuncSetAttribute((const void *)k_lay_place, hipFuncAttributeMaxDynamicSharedMemorySize,
-                               (int)lds_lay_place(g.K))) != hipSuccess)
-    return e;
-  if (g.pow2)
-    hipLaunchKernelGGL(k_lay_count<true>, dim3(L), dim3(LBLK), lds_lay_count(g.K), s, addr, ls, g, rt, KEY, CNT);
-  else
-    hipLaunchKernelGGL(k_lay_count<false>, dim3(L), dim3(LBLK), lds_lay_count(g.K), s, addr, ls, g, rt, KEY, CNT);
+  if ((e = hipMemcpyAsync(d_up, up.data(), up.size(), hipMemcpyHostToDevice, s)) != hipSuccess) return e;
+  if ((e = hipEventRecord(up_done, s)) != hipSuccess) return e;
+  if (NT) {
+    if (g.pow2)
+      hipLaunchKernelGGL(k_lay_count<true>, dim3(NT), dim3(LBLK), lds_lay_count(g.K), s, addr, tiles, g, rt, KEY, CNT);
+    else
+      hipLaunchKernelGGL(k_lay_count<false>, dim3(NT), dim3(LBLK), lds_lay_count(g.K), s, addr, tiles, g, rt, KEY,
+                         CNT);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_lay_scan, dim3(L), dim3(LBLK), 0, s, CNT, ls, tile0, g.K, OFF, TOFF, SLOT, g.C);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_lay_scan, dim3(1), dim3(1024), 0, s, CNT, (uint64_t)nb, OFF, SLOT, (uint64_t)L * g.C);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(k_lay_place, dim3(L), dim3(LBLK), lds_lay_place(g.K), s, ls, KEY, g.K, OFF, LISTD);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (NT) {
+    hipLaunchKernelGGL(k_lay_place, dim3(NT), dim3(LBLK), lds_lay_place(g.K), s, tiles, KEY, g.K, TOFF, LISTD);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   LayArgs A;
   A.ls = ls;
   A.OFF = OFF;
