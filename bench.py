@@ -557,12 +557,58 @@ def vmem_leg(torch, hbf, wl, w, addr, issue, complete, reps=3):
                 parity_vs_reference_digest=parity)
 
 
+def time_calls(torch, calls, outs, reps):
+    """Per-call time of `calls` (closures launching on the stream they are
+    given, each writing its own output in `outs`), the fastest of two ways of
+    issuing them back to back: eagerly through the binding (host-bound when
+    a call is a few microseconds of GPU work) and replayed from one HIP
+    graph that captured them once (every replay is first checked equal to
+    the eager outputs).  Returns (ms per call, eager ms, graph ms)."""
+    s = torch.cuda.current_stream()
+    for c in calls:  # warm-up; reference outputs
+        assert c(s) == 0
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(s)
+    rc = 0
+    for _ in range(reps):
+        for c in calls:
+            rc |= c(s)
+    e1.record(s)
+    torch.cuda.synchronize()
+    assert rc == 0
+    eager = e0.elapsed_time(e1) / (reps * len(calls))
+    graph = torch.cuda.CUDAGraph()
+    gs = torch.cuda.Stream()
+    gs.wait_stream(s)
+    with torch.cuda.stream(gs):
+        with torch.cuda.graph(graph, stream=gs):
+            for c in calls:
+                assert c(gs) == 0
+    s.wait_stream(gs)
+    for _ in range(2):
+        for o in outs:
+            o.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert all(torch.equal(o, r) for o, r in zip(outs, ref)), "a graph replay differs from the eager calls"
+    e0.record(s)
+    for _ in range(reps * 4):
+        graph.replay()
+    e1.record(s)
+    torch.cuda.synchronize()
+    replayed = e0.elapsed_time(e1) / (reps * 4 * len(calls))
+    return min(eager, replayed), eager, replayed
+
+
 def gemv_leg(torch, hbf, wl, sets=16, reps=3):
     """Row a5's bandwidth with no delay injected: the 8-expert grouped GEMV
     (8 x [768 x 2048] bf16, 24 MiB) over `sets` distinct weight sets in turn
     (16 x 24 MiB = 384 MiB, more than the 256 MB MALL, so the weights come
     from HBM), at batch 1, 4 and 16.  Bytes = weights + activations +
-    outputs; peak 8 TB/s."""
+    outputs; peak 8 TB/s.  Calls are issued back to back, eagerly and from
+    a HIP graph (see time_calls); the faster is the rate."""
     page = 16384
     W, _ = wl.config4_operands(batch=1)
     E, N, K = W.shape
@@ -575,42 +621,33 @@ def gemv_leg(torch, hbf, wl, sets=16, reps=3):
         Wall[k].copy_(torch.from_numpy(Wk.view(np.int16)))
     gm = hbf.Model(**wl.geometry(16, 8, 4))
     assert gm.register_range(Wall.data_ptr(), sets * wbytes)[0] == 0
-    s = torch.cuda.current_stream()
+    zi = torch.zeros(E * N * K * 2 // page, dtype=torch.int64, device="cuda")
     out = {}
     for B in (1, 4, 16):
         _, X = wl.config4_operands(batch=B)
         Xd = torch.from_numpy(X.view(np.int16)).cuda()
-        Yd = torch.empty((E, B, N), dtype=torch.float32, device="cuda")
-        for k in range(sets):  # warm-up
-            assert gm.gemv_instrumented(Wall[k], Xd, Yd, stream=s) == 0
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(s)
-        for _ in range(reps):
-            for k in range(sets):
-                gm.gemv_instrumented(Wall[k], Xd, Yd, stream=s)
-        e1.record(s)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / (reps * sets)
+        Ys = torch.empty((sets, E, B, N), dtype=torch.float32, device="cuda")
+        plain = [lambda st, k=k: gm.gemv_instrumented(Wall[k], Xd, Ys[k], stream=st) for k in range(sets)]
+        ms, eager, replayed = time_calls(torch, plain, list(Ys), reps)
         # the same calls instrumented, every page's delay zero: the cost of
-        # the clock reads and the (immediately satisfied) wait
-        zi = torch.zeros(E * N * K * 2 // page, dtype=torch.int64, device="cuda")
-        e2, e3 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e2.record(s)
-        for _ in range(reps):
-            for k in range(sets):
-                gm.gemv_instrumented(Wall[k], Xd, Yd, zi, zi, None, stream=s)
-        e3.record(s)
-        torch.cuda.synchronize()
-        ms0 = e2.elapsed_time(e3) / (reps * sets)
+        # the clock reads, the time origin and the persistent schedule
+        zero = [lambda st, k=k: gm.gemv_instrumented(Wall[k], Xd, Ys[k], zi, zi, None, stream=st)
+                for k in range(sets)]
+        ms0, eager0, replayed0 = time_calls(torch, zero, list(Ys), reps)
         nbytes = wbytes + X.nbytes + E * B * N * 4
         gbps = nbytes / (ms / 1e3) / 1e9
         out[f"batch{B}"] = dict(us_per_call=ms * 1e3, GBps=gbps, frac_of_hbm_peak=gbps / HBM_PEAK_GBPS,
                                 TFLOPs=2 * E * B * N * K / (ms / 1e3) / 1e12,
-                                us_per_call_zero_delay=ms0 * 1e3)
+                                us_per_call_eager=eager * 1e3, us_per_call_graph=replayed * 1e3,
+                                us_per_call_zero_delay=ms0 * 1e3,
+                                us_per_call_zero_delay_eager=eager0 * 1e3,
+                                us_per_call_zero_delay_graph=replayed0 * 1e3)
     assert gm.get_status() == 0
     return dict(workload=f"8 experts x [768 x 2048] bf16 per call, {sets} weight sets rotated "
-                         f"({sets * wbytes >> 20} MiB), no instrumentation; us_per_call_zero_delay: "
-                         f"instrumented with every delay zero", **out)
+                         f"({sets * wbytes >> 20} MiB); us_per_call: no instrumentation, the faster of "
+                         f"back-to-back eager calls and a HIP graph of the {sets} calls replayed; "
+                         f"us_per_call_zero_delay: instrumented with every delay zero, timed the same way",
+                **out)
 
 
 def host_cpu():

@@ -20,8 +20,10 @@
 // release clocks into delays from the origin.
 //
 // Y[e][b][n] = sum_k X[e][b][k] * W[e][n][k], bf16 inputs, fp32 accumulate.
-// Bandwidth bound (B flop per weight byte): packed bf16 dot instructions
-// (two products per instruction, fp32 accumulate), no matrix cores.
+// Bandwidth bound (B flop per weight byte).  Delayed calls compute page by
+// page, each after its own wait, with packed bf16 dot instructions (two
+// products per instruction, fp32 accumulate); calls without delays have no
+// consumption point to honour and take the matrix cores on 16-row tiles.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -265,6 +267,113 @@ __device__ __forceinline__ void page_k2048(int q, const uint16_t *__restrict__ W
   __syncthreads();  // red is reused by the workgroup's next page
 }
 
+// ------------------------------------------------------------------ matrix cores
+
+// No delays, batch 9..16 (below that the per-page kernel, whose 1,536
+// small workgroups stream the weights faster, measured 6.0 against 8.2 us
+// per 24 MiB call at batch 1), N % 16 == 0, K % 512 == 0: one workgroup of
+// 4 waves per tile of 16 weight rows (one expert's), wave w taking the K/4
+// wide slice w.  Each 32-wide step of k is one v_mfma_f32_16x16x32_bf16
+// with A = the expert's activations (16 rows; rows >= B are zero) and B =
+// the tile's rows transposed: lane l holds 8 consecutive k of activation
+// row l % 16 and, for the same k, of tile row l % 16 (k group l / 16), and
+// accumulates outputs (batch 4 (l / 16) + j, tile row l % 16), j < 4.  A
+// round issues KS steps' loads (16 bytes of W and of X per lane each)
+// before its first product.  The slices' partial tiles meet in LDS.  At
+// B < 16 the unused rows cost matrix-core cycles only (no memory traffic),
+// which the instruction rate covers many times over.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4_t mfma_bf16(uint4 a, uint4 b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                 c, 0, 0, 0);
+}
+
+template <int KS>
+__global__ __launch_bounds__(256) void k_gemv_mfma(const uint16_t *__restrict__ W, int K, int N,
+                                                   const uint16_t *__restrict__ X, int B,
+                                                   float *__restrict__ Y) {
+  __shared__ f32x4_t red[3][64];
+  const int row0 = blockIdx.x * 16;
+  const int e = row0 / N, nb = row0 - e * N;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, kg = lane >> 4;
+  const int kq = K >> 2;
+  const uint16_t *wp = W + (size_t)(row0 + col) * K + (size_t)w * kq + kg * 8;
+  const bool xon = col < B;
+  const uint16_t *xp = X + ((size_t)e * B + (xon ? col : 0)) * K + (size_t)w * kq + kg * 8;
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < kq; k0 += 32 * KS) {
+    uint4 wv[KS], xv[KS];
+#pragma unroll
+    for (int s = 0; s < KS; s++) wv[s] = *(const uint4 *)(wp + k0 + 32 * s);
+#pragma unroll
+    for (int s = 0; s < KS; s++) xv[s] = xon ? *(const uint4 *)(xp + k0 + 32 * s) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int s = 0; s < KS; s++) acc = mfma_bf16(xv[s], wv[s], acc);
+  }
+  if (w) red[w - 1][lane] = acc;
+  __syncthreads();
+  if (w == 0) {
+    acc += red[0][lane];
+    acc += red[1][lane];
+    acc += red[2][lane];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int b = 4 * kg + j;
+      if (b < B) Y[((size_t)e * B + b) * N + nb + col] = acc[j];
+    }
+  }
+}
+
+// The expert shape (K = 2048, N % 32 == 0) at batch 9..16: two 16-row
+// tiles of one expert per workgroup of 8 waves, waves 4h .. 4h+3 on tile h
+// as above.  The activation slices, the same for both tiles, are loaded
+// once per workgroup into LDS (each wave fetching half of its slice's 16
+// steps) and read back in the operand layout: a quarter of the activation
+// traffic of one tile per 4 waves.  Measured 9.3 against 10.9 us per call
+// at batch 16 (one tile per workgroup), 12.0 for the per-page kernel.
+__global__ __launch_bounds__(512) void k_gemv_mfma_pair(const uint16_t *__restrict__ W, int N,
+                                                        const uint16_t *__restrict__ X, int B,
+                                                        float *__restrict__ Y) {
+  constexpr int K = 2048, KQ = K / 4, STEPS = KQ / 32;
+  __shared__ uint4 xs[4][STEPS][64];  // [slice][step][lane], 64 KiB
+  __shared__ f32x4_t red[2][3][64];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int h = w >> 2, wq = w & 3;
+  const int row0 = (blockIdx.x * 2 + h) * 16;
+  const int e = row0 / N, nb = row0 - e * N;  // both tiles lie in expert e (N % 32 == 0)
+  const int col = lane & 15, kg = lane >> 4;
+  const uint16_t *wp = W + (size_t)(row0 + col) * K + wq * KQ + kg * 8;
+  const bool xon = col < B;
+  const uint16_t *xp = X + ((size_t)e * B + (xon ? col : 0)) * K + wq * KQ + kg * 8;
+  uint4 wv[STEPS];
+#pragma unroll
+  for (int s = 0; s < STEPS; s++) wv[s] = *(const uint4 *)(wp + 32 * s);
+#pragma unroll
+  for (int i = 0; i < STEPS / 2; i++) {
+    const int s = h * (STEPS / 2) + i;
+    xs[wq][s][lane] = xon ? *(const uint4 *)(xp + 32 * s) : make_uint4(0, 0, 0, 0);
+  }
+  __syncthreads();
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < STEPS; s++) acc = mfma_bf16(xs[wq][s][lane], wv[s], acc);
+  if (wq) red[h][wq - 1][lane] = acc;
+  __syncthreads();
+  if (wq == 0) {
+    acc += red[h][0][lane];
+    acc += red[h][1][lane];
+    acc += red[h][2][lane];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int b = 4 * kg + j;
+      if (b < B) Y[((size_t)e * B + b) * N + nb + col] = acc[j];
+    }
+  }
+}
+
 // ------------------------------------------------------------------ schedulers
 
 // No delays: one workgroup per page, no clock reads.
@@ -375,6 +484,18 @@ hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, c
   const int R = page_bytes / (2 * K);
   const int64_t pages = (int64_t)E * N / R;
   const bool timed = pi != nullptr;
+  if (!timed && B >= 9 && B <= 16 && K == 2048 && N % 32 == 0) {
+    hipLaunchKernelGGL(k_gemv_mfma_pair, dim3((uint32_t)((int64_t)E * N / 32)), dim3(512), 0, s, W, N, X, B, Y);
+    return hipGetLastError();
+  }
+  if (!timed && B >= 9 && B <= 16 && N % 16 == 0 && K % 512 == 0) {
+    const uint32_t tiles = (uint32_t)((int64_t)E * N / 16);
+    if (K % 2048 == 0)
+      hipLaunchKernelGGL(k_gemv_mfma<16>, dim3(tiles), dim3(256), 0, s, W, K, N, X, B, Y);
+    else
+      hipLaunchKernelGGL(k_gemv_mfma<4>, dim3(tiles), dim3(256), 0, s, W, K, N, X, B, Y);
+    return hipGetLastError();
+  }
   if (K == 2048 && R == 4 && B >= 1 && B <= 16) {
     if (!timed) {
       auto kfn = B == 1 ? k_gemv_k2048<1, false> : B == 2 ? k_gemv_k2048<2, false>

@@ -136,6 +136,33 @@ def test_gemv_without_delays(torch):
     assert rel_l2(Y.cpu().numpy().astype(np.float64), oracle.gemv_bf16(W, X)) <= 1e-3
 
 
+@pytest.mark.parametrize("experts,K,N,batch", [
+    (8, 2048, 768, 1), (8, 2048, 768, 2), (8, 2048, 768, 3), (8, 2048, 768, 4), (8, 2048, 768, 8),
+    (8, 2048, 768, 12), (8, 2048, 768, 16), (8, 2048, 768, 17),
+    (8, 2048, 768, 9), (2, 512, 64, 3), (1, 4096, 32, 2), (3, 1024, 48, 16), (2, 4096, 80, 7),
+    (2, 4096, 80, 12), (2, 2048, 48, 16), (2, 2048, 40, 16), (1, 512, 16, 9)])
+def test_gemv_without_delays_shapes(torch, experts, K, N, batch):
+    """Calls without delays.  Batches 9..16 take the matrix cores: pairs of
+    16-row tiles sharing their activations at K = 2048, N % 32 == 0 (config
+    4 at batch 9, 12, 16), single tiles on the other N % 16 == 0 shapes
+    (N = 48; K = 512, 1024, 4096).  Batches up to 8, N = 40 and batch 17
+    take the per-page kernels."""
+    from oracle import oracle
+    from paper_2609_09800_amd import hbf
+    say(f"gemv no delays, {experts} experts, K {K}, N {N}, batch {batch}")
+    W, X = wl.config4_operands(seed=11 + batch, batch=batch, experts=experts, K=K, N=N)
+    buf, Wd = device_weights(torch, W)
+    Xd = torch.from_numpy(X.view(np.int16)).cuda()
+    Y = torch.full((experts, batch, N), float("nan"), dtype=torch.float32, device="cuda")
+    m = hbf.Model(**wl.geometry(16, 8, 4))
+    assert m.register_range(Wd.data_ptr(), W.nbytes)[0] == 0
+    assert m.gemv_instrumented(Wd, Xd, Y) == 0
+    assert m.get_status() == 0
+    got = Y.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all()
+    assert rel_l2(got, oracle.gemv_bf16(W, X)) <= 1e-3
+
+
 def test_gemv_delay_clamped_and_reported(torch):
     """A page delay above 1 s waits 1 s, still computes, and reports ERANGE_TIME."""
     from oracle import oracle
