@@ -11,13 +11,17 @@
 //
 // One time origin per call.  Every page of a call is issued at the call's
 // start, so page q is released at origin + (complete[q] - issue[q]), where
-// origin is one wall-clock reading taken by the call's first kernel (a
-// single thread, before any consumer starts).  With delays, the call runs
-// on persistent workgroups (at most as many as the GPU holds at once, so
-// none starts late behind a waiting one), each taking its pages in
-// ascending delay order.  No workgroup writes anything shared with another
-// (the origin is read-only to them); a last kernel turns the recorded
-// release clocks into delays from the origin.
+// origin is the wall clock at which the consuming kernel's earliest
+// workgroup began: a first one-thread kernel clears the origin record, and
+// each workgroup of the timed kernel, as its first act, folds its own start
+// clock into it by an atomic minimum and takes the smaller of the two.
+// Workgroups are dispatched in index order, so all of them see (within a
+// few clock reads) the first one's start; a separate kernel's clock would
+// also charge the gap until the host has queued the timed kernel.  With
+// delays, the call runs on persistent workgroups (at most as many as the
+// GPU holds at once, so none starts late behind a waiting one), each taking
+// its pages in ascending delay order; a last kernel turns the recorded
+// release clocks into delays from the final origin.
 //
 // Y[e][b][n] = sum_k X[e][b][k] * W[e][n][k], bf16 inputs, fp32 accumulate.
 // Bandwidth bound (B flop per weight byte).  Delayed calls compute page by
@@ -85,9 +89,10 @@ __device__ __forceinline__ uint64_t wait_release(uint64_t origin, uint64_t ticks
   return now;
 }
 
-// First kernel of a delayed call: its time origin.
+// First kernel of a delayed call: clears its origin record (the timed
+// kernel's workgroups fold their start clocks into it).
 __global__ void k_gemv_origin(DevState *st) {
-  if (threadIdx.x == 0) st->gemv_origin = __builtin_amdgcn_s_memrealtime();
+  if (threadIdx.x == 0) st->gemv_origin = ~uint64_t(0);
 }
 
 // Last kernel of a delayed call with measurements: release clock -> delay
@@ -400,9 +405,14 @@ __device__ __forceinline__ void timed_pages(int npages, const int64_t *__restric
                                             int64_t tick_ps, DevState *st, Page page) {
   __shared__ uint64_t s_ticks[GEMV_MAXP];
   __shared__ int s_order[GEMV_MAXP];
+  __shared__ uint64_t s_origin;
   const int t = threadIdx.x;
   const int G = gridDim.x, g = blockIdx.x;
-  const uint64_t origin = st->gemv_origin;
+  if (t == 0) {  // the call's origin: the earliest workgroup start folded in so far, or this one
+    const uint64_t now = __builtin_amdgcn_s_memrealtime();
+    const uint64_t old = atomicMin((unsigned long long *)&st->gemv_origin, (unsigned long long)now);
+    s_origin = old < now ? old : now;
+  }
   const int m = (npages - g + G - 1) / G;
   uint32_t errb = 0;
   uint64_t mine = 0;
@@ -420,6 +430,7 @@ __device__ __forceinline__ void timed_pages(int npages, const int64_t *__restric
     s_order[r] = t;
   }
   __syncthreads();
+  const uint64_t origin = s_origin;
   for (int i = 0; i < m; i++) {
     const int li = s_order[i];
     const int q = g + li * G;
