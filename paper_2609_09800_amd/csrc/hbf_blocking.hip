@@ -8,11 +8,13 @@
 // The die and channel stages are now coupled: a die's next read waits on the
 // channel, whose order depends on every die's reads.  A channel and its die
 // queues form an independent system, so one wave runs each channel, one lane
-// per die queue.  Every die queue has at most one page pending at a time;
-// each step transfers the pending page with the smallest (die-done, index)
-// (a wave-wide minimum) and lets its die read its next request.  The
-// die-order request lists come from the unblocked path's die stage (same
-// ranks, same segments).
+// per die queue.  Every die queue has at most one page pending at a time.
+// The channel takes pending pages in (die-done, index) order, and a die
+// reads its next request when its page has been transferred; each round of
+// the loop serves the whole prefix of the ranked pending pages that no
+// re-admitted page can overtake (all of them when the channel is
+// saturated).  The die-order request lists come from the unblocked path's
+// die stage (same ranks, same segments).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -23,9 +25,8 @@ namespace hbf {
 namespace {
 
 __device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
-__device__ __forceinline__ int64_t min64(int64_t a, int64_t b) { return a < b ? a : b; }
 
-// Wave-wide minima with DPP row shifts (within rows of 16 by 1, 2, 4, 8,
+// Wave-wide minimum with DPP row shifts (within rows of 16 by 1, 2, 4, 8,
 // then row 0 -> 1, 2 -> 3 and rows 0-1 -> 2-3): lane 63 ends with the
 // minimum of all 64 lanes, which readlane broadcasts.  Lanes without a
 // source keep the identity.
@@ -33,23 +34,11 @@ template <int CTRL, int ROWMASK>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t x) {
   return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)x, CTRL, ROWMASK, 0xF, false);
 }
-template <int CTRL, int ROWMASK>
-__device__ __forceinline__ int64_t dpp_i64(int64_t old, int64_t x) {
-  const uint32_t lo = dpp_u32<CTRL, ROWMASK>((uint32_t)old, (uint32_t)x);
-  const uint32_t hi = dpp_u32<CTRL, ROWMASK>((uint32_t)((uint64_t)old >> 32), (uint32_t)((uint64_t)x >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
 constexpr int SHR1 = 0x111, SHR2 = 0x112, SHR4 = 0x114, SHR8 = 0x118, BC15 = 0x142, BC31 = 0x143;
 
-__device__ __forceinline__ int64_t wave_min64(int64_t x) {
-  x = min64(x, dpp_i64<SHR1, 0xF>(INT64_MAX, x));
-  x = min64(x, dpp_i64<SHR2, 0xF>(INT64_MAX, x));
-  x = min64(x, dpp_i64<SHR4, 0xF>(INT64_MAX, x));
-  x = min64(x, dpp_i64<SHR8, 0xF>(INT64_MAX, x));
-  x = min64(x, dpp_i64<BC15, 0xA>(INT64_MAX, x));
-  x = min64(x, dpp_i64<BC31, 0xC>(INT64_MAX, x));
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, 63);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), 63);
+__device__ __forceinline__ int64_t lane_i64(int64_t x, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), l);
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 __device__ __forceinline__ uint32_t wave_min32(uint32_t x) {
@@ -91,7 +80,7 @@ constexpr int RING = 64;
 constexpr int CHUNK_R = 32;
 constexpr int RSTRIDE = RING + 1;   // padded: lanes' rings start in different banks
 constexpr int OUTB = 256;           // staged completions per write-out
-constexpr int QB = 64;              // staged quantum completions per write-out
+constexpr int QB = 128;             // staged quantum completions per write-out
 
 // One wave per channel (blockIdx.x); lane j = die queue c*Dk + j.
 //   DDw / IX: die-ordered request indices (packed word's low half when the
@@ -211,43 +200,98 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
   }
   top_up();   // second chunk into the ring, third in flight
 
+  // Rounds.  Every die queue with a page pending is ranked by (die-done,
+  // index).  If the channel takes the pending pages in that order, the page
+  // of rank r completes at (r+1)*xfer + max(cfree, max over ranks i <= r of
+  // die_done_i - i*xfer), and its die can then read its next request.  The
+  // channel really does take them in that order up to the first rank that
+  // some die's next page (read after an earlier rank's transfer) would
+  // precede; that prefix is served at once, its dies are re-admitted, and
+  // the next round ranks again.  A saturated channel serves every pending
+  // page per round; an idle one at least the first.
   uint32_t left = total;             // not yet transferred
   bool any = false;
   for (;;) {
-    const int64_t key = left ? dd : INT64_MAX;
-    const int64_t m = wave_min64(key);
-    if (m == INT64_MAX) break;
-    const bool tie = left && dd == m;
-    const uint64_t tied = __ballot(tie);
-    // several pages reached the channel at the same time: the lowest request
-    // index goes first.  The reduction runs on every lane (a collective must
-    // not sit behind a per-lane condition); the branch on `tied` is uniform.
-    const bool several = __popcll(tied) > 1;
-    const uint32_t first = several ? wave_min32(tie ? pidx : UINT32_MAX) : 0u;
-    const bool win = tie && (!several || pidx == first);
-    const int64_t cpl = max64(m, cfree) + xfer;
-    cfree = cpl;
-    any = true;
-    if (win) {
-      out_idx[nout] = pidx;
-      out_cpl[nout] = cpl;
+    const bool pend = left != 0;
+    const uint64_t pm = __ballot(pend);
+    if (pm == 0) break;
+    const uint32_t P = (uint32_t)__popcll(pm);
+    // rank among the pending pages
+    uint32_t r = 0;
+    for (uint64_t mm = pm; mm; mm &= mm - 1) {
+      const int j = (int)__builtin_ctzll(mm);
+      const int64_t dj = lane_i64(dd, j);
+      const uint32_t ij = (uint32_t)__builtin_amdgcn_readlane((int)pidx, j);
+      r += (dj < dd || (dj == dd && ij < pidx)) ? 1u : 0u;
+    }
+    // completion if every lower rank is served first
+    const int64_t val = dd - (int64_t)r * xfer;
+    int64_t M = cfree;
+    for (uint64_t mm = pm; mm; mm &= mm - 1) {
+      const int j = (int)__builtin_ctzll(mm);
+      const int64_t vj = lane_i64(val, j);
+      const uint32_t rj = (uint32_t)__builtin_amdgcn_readlane((int)r, j);
+      if (rj <= r) M = max64(M, vj);
+    }
+    const int64_t cpl = (int64_t)(r + 1) * xfer + M;
+    // the die's next read once this page has left its register
+    bool claim = false;
+    int64_t ndd = INT64_MAX;
+    uint32_t nidx = UINT32_MAX;
+    if (pend && admitted < total) {
+      const uint32_t sl = lane * RSTRIDE + admitted % RING;
+      claim = admitted < R;
+      int64_t s0 = max64(ring_iss[sl], cpl);
+      if (claim) s0 += tQ;
+      ndd = s0 + tR;
+      nidx = ring_idx[sl];
+    }
+    // first rank that this next page would precede
+    uint32_t cut = P;
+    if (ndd != INT64_MAX) {
+      cut = 0;
+      for (uint64_t mm = pm; mm; mm &= mm - 1) {
+        const int j = (int)__builtin_ctzll(mm);
+        const int64_t dj = lane_i64(dd, j);
+        const uint32_t ij = (uint32_t)__builtin_amdgcn_readlane((int)pidx, j);
+        cut += (dj < ndd || (dj == ndd && ij < nidx)) ? 1u : 0u;
+      }
+    }
+    const uint32_t v = wave_min32(pend ? cut : UINT32_MAX);  // >= 1: a next page follows its own
+    const bool served = pend && r < v;
+    if (served) {
+      out_idx[nout + r] = pidx;
+      out_cpl[nout + r] = cpl;
       left--;
       free_at = cpl;  // the page has left the register
+      if (cpl >= TIME_LIMIT) err |= ERR_OVERFLOW;
     }
-    if (cpl >= TIME_LIMIT) err |= on ? ERR_OVERFLOW : 0u;
-    if (++nout == OUTB) flush_out();
-    // the winner's next request must be in its ring
-    if (__ballot(win && left && loaded - admitted < 8)) top_up();
-    bool cl = false;
-    if (win && left) cl = admit();
-    if (__ballot(cl)) {   // at most the winner
+    const uint64_t last = __ballot(served && r == v - 1);
+    cfree = lane_i64(cpl, (int)__builtin_ctzll(last));
+    any = true;
+    nout += v;
+    const bool adm = served && left != 0;
+    if (adm) {
+      dd = ndd;
+      pidx = nidx;
+      admitted++;
+      if (dd >= TIME_LIMIT) err |= ERR_OVERFLOW;
+    }
+    const bool cl = adm && claim;
+    const uint64_t cm = __ballot(cl);
+    if (cm) {
       if (cl) {
-        q_die[nq] = k;
-        q_rank[nq] = admitted - 1;
-        q_val[nq] = dd - tR;
+        const uint32_t slot = nq + (uint32_t)__popcll(cm & ((1ull << lane) - 1));
+        q_die[slot] = k;
+        q_rank[slot] = admitted - 1;
+        q_val[slot] = dd - tR;
       }
-      if (++nq == QB) flush_q();
+      nq += (uint32_t)__popcll(cm);
+      if (nq > QB - 64) flush_q();
     }
+    if (nout > OUTB - 64) flush_out();
+    // each die's next request must be in its ring before the next round
+    if (__ballot(on && admitted < total && loaded - admitted < 2)) top_up();
   }
   if (nout) flush_out();
   if (nq) flush_q();
