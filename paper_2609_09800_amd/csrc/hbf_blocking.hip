@@ -36,6 +36,40 @@ __device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t x) {
 }
 constexpr int SHR1 = 0x111, SHR2 = 0x112, SHR4 = 0x114, SHR8 = 0x118, BC15 = 0x142, BC31 = 0x143;
 
+// Within each row of 16 lanes, rotated right by S: lane l receives lane
+// (l - S) mod 16's value, so S = 1..15 visit every other lane of the row once.
+template <int S>
+__device__ __forceinline__ uint32_t ror32(uint32_t x) {
+  return dpp_u32<0x120 | S, 0xF>(x, x);
+}
+template <int S>
+__device__ __forceinline__ int64_t ror64(int64_t x) {
+  const uint32_t lo = ror32<S>((uint32_t)x), hi = ror32<S>((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+template <int S = 1>
+__device__ __forceinline__ void row_rotations(int64_t key, uint32_t kix, int64_t (&kd)[15], uint32_t (&ki)[15]) {
+  kd[S - 1] = ror64<S>(key);
+  ki[S - 1] = ror32<S>(kix);
+  if constexpr (S < 15) row_rotations<S + 1>(key, kix, kd, ki);
+}
+template <int S = 1>
+__device__ __forceinline__ int64_t row_prefix_max(int64_t val, uint32_t rr, uint32_t r, int64_t M) {
+  const int64_t vj = ror64<S>(val);
+  const uint32_t rj = ror32<S>(rr);
+  if (rj <= r) M = vj > M ? vj : M;
+  if constexpr (S < 15) return row_prefix_max<S + 1>(val, rr, r, M);
+  return M;
+}
+// minimum over the 16 lanes of row 0, broadcast
+__device__ __forceinline__ uint32_t row0_min32(uint32_t x) {
+  x = min(x, dpp_u32<SHR1, 0xF>(UINT32_MAX, x));
+  x = min(x, dpp_u32<SHR2, 0xF>(UINT32_MAX, x));
+  x = min(x, dpp_u32<SHR4, 0xF>(UINT32_MAX, x));
+  x = min(x, dpp_u32<SHR8, 0xF>(UINT32_MAX, x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 15);
+}
+
 __device__ __forceinline__ int64_t lane_i64(int64_t x, int l) {
   const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
   const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)x >> 32), l);
@@ -88,6 +122,9 @@ constexpr int QB = 128;             // staged quantum completions per write-out
 //   totals: each die queue's run.  ref: refresh quanta pending (each die
 //   queue's first ref_pend admissions claim one, tQ before the read; the
 //   quantum's completion is written).
+// ROW: at most 16 die queues per channel, all in lanes 0-15 (one DPP row),
+// so the all-pairs comparisons of a round run on row rotations.
+template <bool ROW>
 __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DDw, const uint32_t *__restrict__ IX,
                                                  const int64_t *__restrict__ issue_do,
                                                  const uint32_t *__restrict__ seg_start,
@@ -199,6 +236,15 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     if (nq) flush_q();
   }
   top_up();   // second chunk into the ring, third in flight
+  // each die queue's next request (after the pending one), read from its
+  // ring a round ahead of its use
+  int64_t nx_iss = 0;
+  uint32_t nx_idx = UINT32_MAX;
+  if (on && admitted < total) {
+    const uint32_t sl = lane * RSTRIDE + admitted % RING;
+    nx_iss = ring_iss[sl];
+    nx_idx = ring_idx[sl];
+  }
 
   // Rounds.  Every die queue with a page pending is ranked by (die-done,
   // index).  If the channel takes the pending pages in that order, the page
@@ -216,22 +262,36 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     const uint64_t pm = __ballot(pend);
     if (pm == 0) break;
     const uint32_t P = (uint32_t)__popcll(pm);
-    // rank among the pending pages
+    // rank among the pending pages (other lanes' pages: key INT64_MAX)
+    const int64_t key = pend ? dd : INT64_MAX;
+    const uint32_t kix = pend ? pidx : UINT32_MAX;
+    int64_t kd[15];
+    uint32_t ki[15];
     uint32_t r = 0;
-    for (uint64_t mm = pm; mm; mm &= mm - 1) {
-      const int j = (int)__builtin_ctzll(mm);
-      const int64_t dj = lane_i64(dd, j);
-      const uint32_t ij = (uint32_t)__builtin_amdgcn_readlane((int)pidx, j);
-      r += (dj < dd || (dj == dd && ij < pidx)) ? 1u : 0u;
+    if (ROW) {
+      row_rotations(key, kix, kd, ki);
+#pragma unroll
+      for (int q = 0; q < 15; q++) r += (kd[q] < key || (kd[q] == key && ki[q] < kix)) ? 1u : 0u;
+    } else {
+      for (uint64_t mm = pm; mm; mm &= mm - 1) {
+        const int j = (int)__builtin_ctzll(mm);
+        const int64_t dj = lane_i64(dd, j);
+        const uint32_t ij = (uint32_t)__builtin_amdgcn_readlane((int)pidx, j);
+        r += (dj < dd || (dj == dd && ij < pidx)) ? 1u : 0u;
+      }
     }
     // completion if every lower rank is served first
     const int64_t val = dd - (int64_t)r * xfer;
-    int64_t M = cfree;
-    for (uint64_t mm = pm; mm; mm &= mm - 1) {
-      const int j = (int)__builtin_ctzll(mm);
-      const int64_t vj = lane_i64(val, j);
-      const uint32_t rj = (uint32_t)__builtin_amdgcn_readlane((int)r, j);
-      if (rj <= r) M = max64(M, vj);
+    int64_t M = max64(cfree, val);
+    if (ROW) {
+      M = row_prefix_max(val, pend ? r : 0xFFFFu, r, M);
+    } else {
+      for (uint64_t mm = pm; mm; mm &= mm - 1) {
+        const int j = (int)__builtin_ctzll(mm);
+        const int64_t vj = lane_i64(val, j);
+        const uint32_t rj = (uint32_t)__builtin_amdgcn_readlane((int)r, j);
+        if (rj <= r) M = max64(M, vj);
+      }
     }
     const int64_t cpl = (int64_t)(r + 1) * xfer + M;
     // the die's next read once this page has left its register
@@ -239,16 +299,20 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     int64_t ndd = INT64_MAX;
     uint32_t nidx = UINT32_MAX;
     if (pend && admitted < total) {
-      const uint32_t sl = lane * RSTRIDE + admitted % RING;
       claim = admitted < R;
-      int64_t s0 = max64(ring_iss[sl], cpl);
+      int64_t s0 = max64(nx_iss, cpl);
       if (claim) s0 += tQ;
       ndd = s0 + tR;
-      nidx = ring_idx[sl];
+      nidx = nx_idx;
     }
     // first rank that this next page would precede
     uint32_t cut = P;
-    if (ndd != INT64_MAX) {
+    if (ROW) {
+      uint32_t c2 = 1;  // its own pending page precedes it
+#pragma unroll
+      for (int q = 0; q < 15; q++) c2 += (kd[q] < ndd || (kd[q] == ndd && ki[q] < nidx)) ? 1u : 0u;
+      if (ndd != INT64_MAX) cut = c2;
+    } else if (ndd != INT64_MAX) {
       cut = 0;
       for (uint64_t mm = pm; mm; mm &= mm - 1) {
         const int j = (int)__builtin_ctzll(mm);
@@ -257,7 +321,8 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
         cut += (dj < ndd || (dj == ndd && ij < nidx)) ? 1u : 0u;
       }
     }
-    const uint32_t v = wave_min32(pend ? cut : UINT32_MAX);  // >= 1: a next page follows its own
+    // >= 1: a next page follows its own
+    const uint32_t v = ROW ? row0_min32(pend ? cut : UINT32_MAX) : wave_min32(pend ? cut : UINT32_MAX);
     const bool served = pend && r < v;
     if (served) {
       out_idx[nout + r] = pidx;
@@ -292,6 +357,11 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     if (nout > OUTB - 64) flush_out();
     // each die's next request must be in its ring before the next round
     if (__ballot(on && admitted < total && loaded - admitted < 2)) top_up();
+    if (adm && admitted < total) {
+      const uint32_t sl = lane * RSTRIDE + admitted % RING;
+      nx_iss = ring_iss[sl];
+      nx_idx = ring_idx[sl];
+    }
   }
   if (nout) flush_out();
   if (nq) flush_q();
@@ -317,8 +387,8 @@ hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX
   hipLaunchKernelGGL(k_regblock_gather, dim3((uint32_t)blocks), dim3(256), 0, s, DDw, IX, issue, issue_do, n, ctl);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_regblock, dim3(g.C), dim3(64), 0, s, DDw, IX, issue_do, seg_start, totals, g, st, ctl,
-                     complete, dfnew, cfnew, ref ? 1 : 0);
+  hipLaunchKernelGGL(g.Dk <= 16 ? k_regblock<true> : k_regblock<false>, dim3(g.C), dim3(64), 0, s, DDw, IX,
+                     issue_do, seg_start, totals, g, st, ctl, complete, dfnew, cfnew, ref ? 1 : 0);
   return hipGetLastError();
 }
 
