@@ -273,12 +273,31 @@ DEVI uint32_t lkey(const Geo &g, uint32_t li) {
   return (li - d * g.C) * g.Dk + d;
 }
 
+// The range snapshot's count and its first range, held in registers (read
+// once after load_ranges): with a single range the test is one subtraction
+// and compare instead of a search through the LDS table.
+struct RangeReg {
+  int32_t n;
+  uint64_t base, bytes, pbase;
+};
+DEVI RangeReg range_reg(const LdsRanges *lr) {
+  return RangeReg{lr->n, lr->base[0], lr->bytes[0], lr->pbase[0]};
+}
+
 // Die-queue key of an address, or KEY_NONE for the native path.
 template <bool POW2>
-DEVI uint32_t key_of(const Geo &g, const LdsRanges *lr, uint64_t a) {
-  int r = find_range(lr, a);
-  if (r < 0) return KEY_NONE;
-  Loc L = map_page<POW2>(g, dev_page<POW2>(g, lr, r, a));
+DEVI uint32_t key_of(const Geo &g, const LdsRanges *lr, const RangeReg &rr, uint64_t a) {
+  uint64_t dp;
+  if (rr.n == 1) {
+    const uint64_t off = a - rr.base;  // wraps above bytes when a < base
+    if (off >= rr.bytes) return KEY_NONE;
+    dp = rr.pbase + (POW2 ? (off >> g.lg_page) : off / g.page_bytes);
+  } else {
+    const int r = find_range(lr, a);
+    if (r < 0) return KEY_NONE;
+    dp = dev_page<POW2>(g, lr, r, a);
+  }
+  Loc L = map_page<POW2>(g, dp);
   uint32_t k = L.ch * g.D + L.die;
   if (g.plane_parallel) k = k * g.P + L.plane;
   return k;

@@ -172,6 +172,7 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
     if (REF) refp[li] = st->ref_pend[k];
   }
   __syncthreads();
+  const RangeReg rr = range_reg(lr);
 
   const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
   const int64_t t0 = (int64_t)blockIdx.x * tile_elems;
@@ -219,13 +220,13 @@ __global__ __launch_bounds__(DBLK) void k_die_reduce(const uint64_t *__restrict_
       // previous request's issue time, for the order check
       int64_t prev = dpp64<DPP_WAVE_SHR1, 0xF>(x, x);  // lane l - 1's issue time
       int64_t last_of_prev_item = carry_prev;
-      carry_prev = __shfl(x, 63);
+      carry_prev = lane63(x);
       if (lane == 0) prev = (e > 0) ? last_of_prev_item : ((i > 0 && v) ? before : x);
       if (v) {
         if (x < 0 || x >= ISSUE_LIMIT) errb |= ERR_RANGE_TIME;
         if (i > 0 && x < prev) errb |= ERR_UNSORTED;
       }
-      uint32_t k = v ? key_of<POW2>(g, lr, a) : KEY_NONE;
+      uint32_t k = v ? key_of<POW2>(g, lr, rr, a) : KEY_NONE;
       if (v && k == KEY_NONE) complete[i] = x;  // native path: no modeled delay
       key[e] = k == KEY_NONE ? KEY_NONE : lslot(g, k);
       iss[e] = x;
@@ -293,8 +294,9 @@ __global__ __launch_bounds__(DBLK) void k_die_count(const uint64_t *__restrict__
   __syncthreads();
   const int64_t t0 = (int64_t)blockIdx.x * tile_elems;
   const int64_t t1 = imin(n, t0 + tile_elems);
+  const RangeReg rr = range_reg(lr);
   for (int64_t i = t0 + threadIdx.x; i < t1; i += DBLK) {
-    const uint32_t k = key_of<POW2>(g, lr, addr[i]);
+    const uint32_t k = key_of<POW2>(g, lr, rr, addr[i]);
     if (k != KEY_NONE) atomicAdd(&cnt[lslot(g, k)], 1u);
   }
   __syncthreads();

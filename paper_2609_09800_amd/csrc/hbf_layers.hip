@@ -78,8 +78,9 @@ __global__ __launch_bounds__(LBLK) void k_lay_count(const uint64_t *__restrict__
   load_ranges(lr, rt);
   for (uint32_t k = threadIdx.x; k <= K; k += LBLK) cnt[k] = 0;
   __syncthreads();
+  const RangeReg rr = range_reg(lr);
   for (int64_t i = tl.a + threadIdx.x; i < tl.b; i += LBLK) {
-    const uint32_t k0 = key_of<POW2>(g, lr, addr[i]);
+    const uint32_t k0 = key_of<POW2>(g, lr, rr, addr[i]);
     const uint32_t k = k0 == KEY_NONE ? K : k0;
     KEY[i] = (uint16_t)k;
     atomicAdd(&cnt[k], 1u);
