@@ -479,7 +479,7 @@ __global__ __launch_bounds__(BLK) void k_key_scan(const uint32_t *__restrict__ t
 //            chunk, pbase: its die-order position, lbo: k's column in the
 //            cell table, tot: k's requests in the call}
 // LDS: sval[CP] i64 | KA[K] | KW[K] | hist[K] u32 | (SC = 2) histA[K] u32 | refp[K] u32 |
-//      skey, srank, sloc [CP] u16, with CP = SC*CHUNK + SC*CHUNK/16
+//      skr [CP] u32 (key << 16 | rank in the step) | sloc [CP] u16, with CP = SC*CHUNK + SC*CHUNK/16
 //
 // SC pass-1 chunks are staged together (SC = 2 wherever its LDS fits: up to
 // 954 die queues). A queue's run in die order then grows from one chunk's
@@ -530,9 +530,8 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
   uint32_t *hist = (uint32_t *)(KW + K);
   uint32_t *histA = hist + K;  // SC = 2: requests of each key in the first of the two chunks
   uint32_t *refp = histA + (SC == 2 ? K : 0);  // REF: pending quanta per key, read once per block
-  uint16_t *skey = (uint16_t *)(refp + K);
-  uint16_t *srank = skey + CP;
-  uint16_t *sloc = srank + CP;
+  uint32_t *skr = refp + K;
+  uint16_t *sloc = (uint16_t *)(skr + CP);
 
   const uint32_t Dk = g.Dk;
   const size_t row = (size_t)blockIdx.x * K;
@@ -635,8 +634,7 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
           if (rc == 0) v = imax(v, ka.L - (int64_t)mul32(ka.cnt, tR));
         }
         sval[P] = v;
-        skey[P] = (uint16_t)k;
-        srank[P] = (uint16_t)rc;
+        skr[P] = k << 16 | rc;
         sloc[P] = (uint16_t)(e * SBLK + threadIdx.x);
       }
     }
@@ -677,7 +675,7 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
         if (p < nv) {
           const int64_t v = sval[pad16(p)];
           vals[q] = v;
-          agg = seg_comb(agg, SegMax{srank[pad16(p)] == 0, v});
+          agg = seg_comb(agg, SegMax{(skr[pad16(p)] & 0xFFFFu) == 0, v});
         }
       }
       SegMax ex = block_excl_segmax<SWAVES>(agg, shseg);
@@ -686,9 +684,10 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
       for (int q = 0; q < SITEMS; q++) {
         const uint32_t p = p0 + q;
         if (p < nv) {
-          const uint32_t rc = srank[pad16(p)];
+          const uint32_t kr2 = skr[pad16(p)];
+          const uint32_t rc = kr2 & 0xFFFFu;
           run = (rc == 0) ? vals[q] : imax(run, vals[q]);
-          const uint32_t kk = skey[pad16(p)];
+          const uint32_t kk = kr2 >> 16;
           if (REF)
             sval[pad16(p)] = svc_sum(KW[kk].rbase + rc + 1, refp[kk], g.tR, g.tQ) + run;
           else
@@ -700,8 +699,9 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
     // write die-ordered (die_done, index); fill the cell table
     for (uint32_t p = threadIdx.x; p < nv; p += SBLK) {
       const uint32_t P = pad16(p);
-      const uint32_t k = skey[P];
-      const uint32_t rc = srank[P];
+      const uint32_t kr2 = skr[P];
+      const uint32_t k = kr2 >> 16;
+      const uint32_t rc = kr2 & 0xFFFFu;
       const KeyW kw = KW[k];
       const uint32_t r = kw.rbase + rc;  // die rank within this call
       const int64_t dd = sval[P];
@@ -719,7 +719,11 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
         const uint32_t kq = lkey(g, k);
         *st->ref_slot[st->ref_off[kq] + st->ref_head[kq] + r] = dd - g.tR;
       }
-      const int64_t prev = (rc > 0) ? sval[pad16(p - 1)] : KA[k].L;
+      // die-done of slot p - 1 (the same queue's previous request when rc > 0):
+      // lane l - 1's value, or read back by lane 0
+      int64_t pdd = dpp64<DPP_WAVE_SHR1, 0xF>(dd, dd);
+      if (lane_id() == 0 && p > 0) pdd = sval[pad16(p - 1)];
+      const int64_t prev = (rc > 0) ? pdd : KA[k].L;
       const int64_t cell = imin((dd - cbase) >> shift, (int64_t)G);
       const int64_t pcell = (r == 0) ? -1 : imin((prev - cbase) >> shift, (int64_t)G);
       uint32_t *lbrow = LB + kw.lbo;
