@@ -240,7 +240,7 @@ int hbf_time_layers(hbf_model_t model, const uint64_t *dev_addr, int64_t n,
  *   (E*N*K*2 / page_bytes entries, page order of W), e.g. from
  *   hbf_time_requests.  Every page of the call is issued at the call's
  *   start: its time origin is the GPU wall clock (constant rate, see
- *   hbf_wall_clock_tick_ps) at which the call's earliest workgroup began.
+ *   hbf_wall_clock_tick_ps) at which the consuming kernel's first workgroup began.
  *   Page q's loads are issued before its first use, and that use waits
  *   until origin + (complete[q] - issue[q]) ns.  The call runs on at most
  *   as many workgroups as the GPU holds at once, each taking its pages in

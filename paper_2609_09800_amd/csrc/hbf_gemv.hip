@@ -11,13 +11,14 @@
 //
 // One time origin per call.  Every page of a call is issued at the call's
 // start, so page q is released at origin + (complete[q] - issue[q]), where
-// origin is the wall clock at which the consuming kernel's earliest
-// workgroup began: a first one-thread kernel clears the origin record, and
-// each workgroup of the timed kernel, as its first act, folds its own start
-// clock into it by an atomic minimum and takes the smaller of the two.
-// Workgroups are dispatched in index order, so all of them see (within a
-// few clock reads) the first one's start; a separate kernel's clock would
-// also charge the gap until the host has queued the timed kernel.  With
+// origin is the wall clock at which the consuming kernel began: a first
+// one-thread kernel clears the origin record, the timed kernel's workgroup
+// 0 (dispatched first) writes its start clock there as its first act, and
+// every other workgroup reads it once, at its first consumption point
+// (waiting, boundedly, in the rare case it is not there yet).
+// A clock taken by a separate earlier kernel would also charge the gap
+// until the host has queued the timed kernel; an atomic minimum taken by
+// every workgroup serializes them on one address for microseconds.  With
 // delays, the call runs on persistent workgroups (at most as many as the
 // GPU holds at once, so none starts late behind a waiting one), each taking
 // its pages in ascending delay order; a last kernel turns the recorded
@@ -36,6 +37,9 @@
 namespace hbf {
 
 constexpr int GEMV_MAXV = 8;  // 16-byte weight vectors held per lane
+// Longest wait of a workgroup for the call's origin (never reached: workgroup
+// 0 publishes it as soon as it starts); past it the call fails.
+constexpr int64_t ORIGIN_WAIT_PS = 100000000000;  // 100 ms
 // Longest delay one page may inject; longer requests are clamped to it and
 // reported (HBF_ERANGE_TIME) so that a bad time array can never stall the GPU.
 constexpr int64_t MAX_PAGE_DELAY_NS = 1000000000;
@@ -78,6 +82,24 @@ __device__ __forceinline__ uint64_t page_ticks(const int64_t *pi, const int64_t 
   return (uint64_t)((d * 1000 + tick_ps - 1) / tick_ps);
 }
 
+// The call's origin as published by the timed kernel's workgroup 0, waiting
+// (boundedly) until it is there; past the bound the caller's own clock
+// stands in and the call fails with ERR_INTERNAL.
+__device__ __forceinline__ uint64_t read_origin(DevState *st, int64_t tick_ps, uint32_t *errb) {
+  const uint64_t start = __builtin_amdgcn_s_memrealtime();
+  const uint64_t limit = (uint64_t)(ORIGIN_WAIT_PS / tick_ps);
+  uint64_t o = __hip_atomic_load(&st->gemv_origin, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+  while (o == ~uint64_t(0)) {
+    if (__builtin_amdgcn_s_memrealtime() - start > limit) {
+      *errb |= ERR_INTERNAL;
+      return start;
+    }
+    __builtin_amdgcn_s_sleep(2);
+    o = __hip_atomic_load(&st->gemv_origin, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  return o;
+}
+
 // Consumption point of a delayed page: spin until `ticks` have passed since
 // the call's origin.  Returns the release clock.
 __device__ __forceinline__ uint64_t wait_release(uint64_t origin, uint64_t ticks) {
@@ -90,7 +112,7 @@ __device__ __forceinline__ uint64_t wait_release(uint64_t origin, uint64_t ticks
 }
 
 // First kernel of a delayed call: clears its origin record (the timed
-// kernel's workgroups fold their start clocks into it).
+// kernel's workgroup 0 writes its start clock there).
 __global__ void k_gemv_origin(DevState *st) {
   if (threadIdx.x == 0) st->gemv_origin = ~uint64_t(0);
 }
@@ -408,13 +430,13 @@ __device__ __forceinline__ void timed_pages(int npages, const int64_t *__restric
   __shared__ uint64_t s_origin;
   const int t = threadIdx.x;
   const int G = gridDim.x, g = blockIdx.x;
-  if (t == 0) {  // the call's origin: the earliest workgroup start folded in so far, or this one
-    const uint64_t now = __builtin_amdgcn_s_memrealtime();
-    const uint64_t old = atomicMin((unsigned long long *)&st->gemv_origin, (unsigned long long)now);
-    s_origin = old < now ? old : now;
-  }
   const int m = (npages - g + G - 1) / G;
   uint32_t errb = 0;
+  if (g == 0 && t == 0) {  // the call's origin: workgroup 0's start, published for the others
+    const uint64_t now = __builtin_amdgcn_s_memrealtime();
+    __hip_atomic_store(&st->gemv_origin, now, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    s_origin = now;
+  }
   uint64_t mine = 0;
   if (t < m) {
     mine = page_ticks(pi, pc, g + t * G, tick_ps, &errb);
@@ -430,12 +452,15 @@ __device__ __forceinline__ void timed_pages(int npages, const int64_t *__restric
     s_order[r] = t;
   }
   __syncthreads();
-  const uint64_t origin = s_origin;
+  // other workgroups read the origin at their first consumption point, by
+  // when workgroup 0 has long published it (they wait for it otherwise)
+  uint64_t origin = g == 0 ? s_origin : ~uint64_t(0);
   for (int i = 0; i < m; i++) {
     const int li = s_order[i];
     const int q = g + li * G;
     const uint64_t ticks = s_ticks[li];
     page(q, [&] {
+      if (origin == ~uint64_t(0)) origin = read_origin(st, tick_ps, &errb);
       const uint64_t rel = wait_release(origin, ticks);
       if (meas && t == 0) meas[q] = (int64_t)rel;  // release clock; a delay after k_gemv_measured
     });
