@@ -828,7 +828,7 @@ def main():
             e1.record(stream)
             e1.synchronize()
             gd.append(e0.elapsed_time(e1) * 1e3)
-        delay = dict(pages=int(req.size), origin="one wall-clock reading per call: the start of the timed kernel's workgroup 0, read by the others at their first consumption point",
+        delay = dict(pages=int(req.size), origin="one wall-clock reading per call: the start of the timed kernel's workgroup 0, read by the others at their first delayed page",
                      mean_requested_ns=float(req.mean()), mean_measured_ns=float(got.mean()),
                      error_pct=float(abs(got.mean() - req.mean()) / req.mean() * 100),
                      mean_lateness_ns=float(late.mean()), p99_lateness_ns=float(np.percentile(late, 99)),

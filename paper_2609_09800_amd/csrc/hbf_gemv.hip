@@ -452,16 +452,18 @@ __device__ __forceinline__ void timed_pages(int npages, const int64_t *__restric
     s_order[r] = t;
   }
   __syncthreads();
-  // other workgroups read the origin at their first consumption point, by
-  // when workgroup 0 has long published it (they wait for it otherwise)
+  // other workgroups read the origin at their first delayed page's
+  // consumption point, by when workgroup 0 has long published it (they wait
+  // for it otherwise)
   uint64_t origin = g == 0 ? s_origin : ~uint64_t(0);
   for (int i = 0; i < m; i++) {
     const int li = s_order[i];
     const int q = g + li * G;
     const uint64_t ticks = s_ticks[li];
     page(q, [&] {
-      if (origin == ~uint64_t(0)) origin = read_origin(st, tick_ps, &errb);
-      const uint64_t rel = wait_release(origin, ticks);
+      // a page without delay is released at once and needs no origin
+      if (ticks != 0 && origin == ~uint64_t(0)) origin = read_origin(st, tick_ps, &errb);
+      const uint64_t rel = ticks == 0 ? __builtin_amdgcn_s_memrealtime() : wait_release(origin, ticks);
       if (meas && t == 0) meas[q] = (int64_t)rel;  // release clock; a delay after k_gemv_measured
     });
   }
