@@ -242,7 +242,9 @@ def small_configs_leg(torch, hbf, wl, reps=20):
     """The two small streams (4,096 and 1,048,576 requests): their inputs and
     outputs (at most 48 MB) stay in the 256 MB MALL, so these rates are
     cache-resident, not HBM-bound.  Median of `reps` timed calls of reset +
-    hbf_time_requests each, checked against the reference digests."""
+    hbf_time_requests each (HIP events around the call: the Python binding's
+    own time before the launch counts), checked against the reference
+    digests; also the call's kernels alone, and calls issued back to back."""
     gold_p = os.path.join(ROOT, "tests", "golden", "oracle_digests.json")
     gold = json.load(open(gold_p)) if os.path.exists(gold_p) else {}
     out = {}
@@ -267,9 +269,29 @@ def small_configs_leg(torch, hbf, wl, reps=20):
         assert m.get_status() == 0
         ms = float(np.median(times))
         g = gold.get(name)
+        digest_ok = (sha(c.cpu().numpy()) == g["complete_sha256"]) if g else None
+        # the call's kernels alone (HIP events between them, on the call's stream)
+        m.profile(True)
+        kts = []
+        for r in range(reps + 1):
+            m.reset(s)
+            assert m.time_requests(a, i, c, s) == 0
+            torch.cuda.synchronize()
+            if r:
+                kts.append(sum(t for _, t in m.kernel_times()))
+        m.profile(False)
+        # calls issued back to back from Python without waiting (clocks carry
+        # over from call to call; timing only): the rate a host loop reaches
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for r in range(reps):
+            assert m.time_requests(a, i, c, s) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+        b2b = e0.elapsed_time(e1) / reps
         out[name] = dict(requests=int(w.n), ms_per_call=ms, requests_per_s=w.n / (ms / 1e3),
-                         residency="cache-resident (MALL)",
-                         parity_vs_reference_digest=(sha(c.cpu().numpy()) == g["complete_sha256"]) if g else None)
+                         kernel_ms_per_call=float(np.median(kts)), back_to_back_ms_per_call=b2b,
+                         residency="cache-resident (MALL)", parity_vs_reference_digest=digest_ok)
     return out
 
 

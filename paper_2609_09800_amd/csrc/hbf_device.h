@@ -184,6 +184,64 @@ DEVI uint32_t wave_excl_sum(uint32_t v) { return wave_incl_sum(v) - v; }
 DEVI int64_t wave_max(int64_t x) { return lane63(wave_incl_max(x)); }
 DEVI uint32_t wave_umax(uint32_t x) { return lane63(wave_incl_umax(x)); }
 
+// ------------------------------------------------------------------ die-stage ranks
+
+// Stable rank of each item among this wave's items with the same key, in
+// (item, lane) order; wcnt is the wave's private per-key counter row and tag
+// its private per-key scratch row.  Every lane writes its lane number into
+// tag[key] and reads it back: one write per key survives, so a lane that
+// reads another lane's number shares its key.  Only those groups (in a
+// stream of consecutive pages, none or a few per item) are resolved, one
+// ballot each; every other lane is alone with its key in this item.
+DEVI void wave_rank(const uint32_t *key, uint32_t *rank, uint16_t *wcnt, uint32_t *tag) {
+  const uint32_t lane = lane_id();
+#pragma unroll
+  for (int e = 0; e < DITEMS; e++) {
+    const uint32_t k = key[e];
+    const bool valid = k != KEY_NONE;
+    if (valid) tag[k] = lane;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint32_t lead = valid ? tag[k] : lane;
+    uint32_t below = 0, cnt = 1;
+    uint64_t dup = __ballot(lead != lane);
+    while (dup) {  // the same on every lane
+      const uint32_t g = (uint32_t)__builtin_amdgcn_readlane((int)lead, (int)__builtin_ctzll(dup));
+      const uint64_t gm = __ballot(lead == g);  // the group, its surviving writer included
+      if (lead == g) {
+        below = mask_below(gm);
+        cnt = (uint32_t)__popcll(gm);
+      }
+      dup &= ~gm;
+    }
+    uint32_t prior = 0;
+    if (valid) prior = wcnt[k];
+    // all reads of this item happen before the group writers' updates
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    if (valid && below == 0) wcnt[k] = (uint16_t)(prior + cnt);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    rank[e] = prior + below;
+  }
+}
+
+// After wave_rank: turn wcnt[w][k] into the wave's exclusive offset among
+// the block's waves and write the chunk total of key k to tot[k].
+DEVI void cross_wave_offsets(uint16_t *wcnt, uint16_t *tot, uint32_t K) {
+  for (uint32_t k = threadIdx.x; k < K; k += DBLK) {
+    uint32_t run = 0;
+#pragma unroll
+    for (int w = 0; w < DWAVES; w++) {
+      uint32_t c = wcnt[w * K + k];
+      wcnt[w * K + k] = (uint16_t)run;
+      run += c;
+    }
+    tot[k] = (uint16_t)run;
+  }
+}
+
 // ------------------------------------------------------------------ classification
 
 // Copy the range table into LDS (dynamic indexing then stays in LDS).

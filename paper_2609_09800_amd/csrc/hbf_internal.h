@@ -180,6 +180,16 @@ hipError_t launch_fill(int64_t *p, int64_t n, int64_t v, hipStream_t s);
 // Device address of this GPU's static scratch of hbf_time_requests_noalloc
 // (HBF_NOALLOC_SCRATCH_BYTES); `dev` must be the current device.
 hipError_t noalloc_scratch(int dev, char **ptr);
+// Small calls (hbf_small.hip): a whole timing call of at most CHUNK
+// requests by one workgroup, for the plain two-stage model with at most
+// SMALL_K die queues, at most SMALL_DK per channel.
+constexpr uint32_t SMALL_K = 512;
+constexpr uint32_t SMALL_DK = 16;
+constexpr int SMALL_LDS_MAX = 156 * 1024;  // dynamic LDS; the kernel's static LDS fits beside it in 160 KB
+bool small_path_ok(const Geo &g, int64_t n, bool refresh);
+hipError_t launch_small(const Geo &g, const RangeTable &rt, DevState *st, CallCtl *ctl, const uint64_t *addr,
+                        const int64_t *issue, int64_t n, int64_t *complete, hipStream_t s);
+hipError_t set_lds_small();
 hipError_t launch_classify(const Geo &g, const RangeTable &rt, DevState *st, const uint64_t *addr,
                            int64_t n, uint64_t *map, hipStream_t s);
 hipError_t launch_reset(DevState *st, hipStream_t s);
