@@ -244,7 +244,8 @@ def small_configs_leg(torch, hbf, wl, reps=20):
     cache-resident, not HBM-bound.  Median of `reps` timed calls of reset +
     hbf_time_requests each (HIP events around the call: the Python binding's
     own time before the launch counts), checked against the reference
-    digests; also the call's kernels alone, and calls issued back to back."""
+    digests; also reset + call issued back to back (the host side of a call
+    takes a few microseconds, less than its kernels)."""
     gold_p = os.path.join(ROOT, "tests", "golden", "oracle_digests.json")
     gold = json.load(open(gold_p)) if os.path.exists(gold_p) else {}
     out = {}
@@ -270,27 +271,18 @@ def small_configs_leg(torch, hbf, wl, reps=20):
         ms = float(np.median(times))
         g = gold.get(name)
         digest_ok = (sha(c.cpu().numpy()) == g["complete_sha256"]) if g else None
-        # the call's kernels alone (HIP events between them, on the call's stream)
-        m.profile(True)
-        kts = []
-        for r in range(reps + 1):
-            m.reset(s)
-            assert m.time_requests(a, i, c, s) == 0
-            torch.cuda.synchronize()
-            if r:
-                kts.append(sum(t for _, t in m.kernel_times()))
-        m.profile(False)
-        # calls issued back to back from Python without waiting (clocks carry
-        # over from call to call; timing only): the rate a host loop reaches
+        # reset + call issued back to back from Python without waiting: the
+        # rate a host loop reaches on this workload
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(s)
         for r in range(reps):
+            m.reset(s)
             assert m.time_requests(a, i, c, s) == 0
         e1.record(s)
         torch.cuda.synchronize()
         b2b = e0.elapsed_time(e1) / reps
         out[name] = dict(requests=int(w.n), ms_per_call=ms, requests_per_s=w.n / (ms / 1e3),
-                         kernel_ms_per_call=float(np.median(kts)), back_to_back_ms_per_call=b2b,
+                         back_to_back_ms_per_call=b2b,
                          residency="cache-resident (MALL)", parity_vs_reference_digest=digest_ok)
     return out
 
