@@ -362,7 +362,10 @@ int hbf_refresh_pending(hbf_model_t model, uint32_t *host_pending, void *stream)
 typedef struct hbf_cache *hbf_cache_t;  /* opaque, owned by the library */
 
 /* Create an empty cache (allocates frames*12 bytes of device memory for up
- * to 63 frames, range_pages*8 + frames*2 bytes above; synchronous). */
+ * to 63 frames, range_pages*8 + frames*2 bytes above; caches of 64 frames
+ * or more over at most 2^26 range pages also hold the chunk state below,
+ * range_pages*24 bytes and about 1 MiB;
+ * synchronous). */
 int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pages, hbf_cache_t *out);
 void hbf_cache_destroy(hbf_cache_t cache);
 /* Empty every frame and zero the counters (asynchronous on `stream`). */
@@ -381,13 +384,30 @@ int hbf_cache_access(hbf_cache_t cache, const uint64_t *dev_pages, int64_t n, ui
                      uint64_t *dev_pf_page, int64_t *dev_pf_src, int64_t pf_cap, int64_t *dev_counts,
                      void *stream);
 
+/* Accesses served together (default: frames/16 clamped to [1024, 65536]
+ * for caches of 8,192 frames or more with chunk state, else 0).  A call is
+ * cut into chunks of that many accesses.  Each chunk is first solved in
+ * parallel as if nothing were evicted: an access faults only as the first
+ * access of a page not resident when the chunk began, unless an earlier
+ * fault at most prefetch_pages below it inserted the page.  That answer
+ * is kept only if every hit and every prefetch candidate it found resident
+ * is still within the last `frames` insertions at that moment, which makes
+ * it exactly the FIFO answer.  Otherwise the chunk is served one access
+ * after another.  The results do not depend on the chunk length.
+ * 0 <= accesses <= 65536; a nonzero value needs chunk state (HBF_EINVAL
+ * otherwise).  Host only. */
+int hbf_cache_set_chunk(hbf_cache_t cache, uint32_t accesses);
+int hbf_cache_get_chunk(hbf_cache_t cache, uint32_t *accesses);
+
 /* Many caches over one stream at once (a sweep of frame budgets and
  * prefetch depths): configuration b has host_frames[b] frames and
  * host_prefetch[b] prefetch pages, starts empty, and serves all of
  * dev_pages[0..n).  dev_counts: int64[n_cfg][5], the five counters of
- * each.  1 <= n_cfg <= 65535.  Allocates the caches' state for the call
- * and synchronises `stream` before returning; returns HBF_EINVAL if some
- * page was >= range_pages (counts then all zero). */
+ * each.  1 <= n_cfg <= 65535.  Caches that have a default chunk length
+ * (see hbf_cache_set_chunk) are served chunk by chunk with the smallest of
+ * those lengths.  Allocates the caches' state for the call and
+ * synchronises `stream` before returning; returns HBF_EINVAL if some page
+ * was >= range_pages (counts then all zero). */
 int hbf_cache_sweep(const uint32_t *host_frames, const uint32_t *host_prefetch, int n_cfg, uint64_t range_pages,
                     const uint64_t *dev_pages, int64_t n, int64_t *dev_counts, void *stream);
 

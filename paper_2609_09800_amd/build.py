@@ -11,7 +11,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libhbf.so")
 SOURCES = ["hbf_api.cpp", "hbf_kernels.hip", "hbf_gemv.hip", "hbf_cache.hip", "hbf_blocking.hip", "hbf_vmem.hip",
-           "hbf_layers.hip", "hbf_small.hip"]
+           "hbf_layers.hip", "hbf_small.hip", "hbf_cache_chunk.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

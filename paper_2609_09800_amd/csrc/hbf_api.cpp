@@ -614,21 +614,36 @@ int hbf_refresh_pending(hbf_model_t m, uint32_t *host_pending, void *stream) {
 struct hbf_cache {
   uint32_t F = 0, d = 0;
   uint64_t R = 0;
-  void *mem = nullptr;         // frames | flags | slots | ctl | cfg | status, n_pf
+  void *mem = nullptr;         // frames | flags | slots | ctl | chunk state | cfg | status, n_pf
   CacheCfg *dcfg = nullptr;
+  ChunkCfg *dccfg = nullptr;   // null when the cache has no chunk state
   int64_t *status = nullptr;   // [0] status, [1] prefetch reads of the call
   int *dids = nullptr;
+  uint32_t lmax = 0;           // chunk state allocated for chunks of up to lmax accesses
+  uint32_t chunk = 0;          // accesses per chunk; 0 = the sequential run alone
+  uint32_t epoch = 0;          // last chunk tag used
 };
 
 static bool cache_params_ok(uint32_t F, uint32_t d, uint64_t R) {
   return F >= 1 && F < (1u << 31) && d < F && d <= CACHE_MAX_PREFETCH && R >= 1 && R <= (uint64_t)N_LIMIT;
 }
 
-// Device state of n caches in one allocation; returns the config array.
-static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, void **mem, CacheCfg **dcfg,
-                       int64_t **status, int **dids) {
+struct CacheAlloc {
+  void *mem = nullptr;
+  CacheCfg *dcfg = nullptr;
+  ChunkCfg *dccfg = nullptr;
+  int64_t *status = nullptr;
+  int *dids = nullptr;   // LDS caches, then sequential device-memory caches, then chunked ones
+  int n_lds = 0, n_seq = 0, n_chunk = 0;
+};
+
+// Device state of n caches in one allocation.  lmax[b] > 0: cache b (a
+// device-memory cache) also gets chunk state for chunks of up to lmax[b]
+// accesses.
+static int cache_alloc(const uint32_t *F, const uint32_t *d, const uint32_t *lmax, int n, uint64_t R,
+                       CacheAlloc *out) {
   size_t o = 0;
-  std::vector<size_t> off(n);
+  std::vector<size_t> off(n), coff(n);
   for (int b = 0; b < n; b++) {
     off[b] = o;
     if (F[b] <= CACHE_LDS_MAX) {  // frame pages and flags
@@ -640,17 +655,29 @@ static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, 
       o = up256(o + (size_t)F[b]);
     }
     o = up256(o + sizeof(CacheCtl));
+    coff[b] = o;
+    if (lmax[b]) {
+      const size_t L = lmax[b];
+      o = up256(o + R * 8 * 3);           // at, lt, tt
+      o = up256(o + (L + 1) * 8);         // S
+      o = up256(o + (L / 1024 + 1) * 8);  // bs
+      o = up256(o + L * 4);               // seg
+      o = up256(o + sizeof(ChunkCtl));
+    }
   }
   const size_t oids = o;
   o = up256(o + sizeof(int) * n);
   const size_t ocfg = o;
   o = up256(o + sizeof(CacheCfg) * n);
+  const size_t occfg = o;
+  o = up256(o + sizeof(ChunkCfg) * n);
   const size_t ost = o;
   o = up256(o + 16);
   void *p = nullptr;
   if (hipMalloc(&p, o) != hipSuccess) return HBF_ENOMEM;
   char *base = (char *)p;
   std::vector<CacheCfg> cfg(n);
+  std::vector<ChunkCfg> ccfg(n);
   for (int b = 0; b < n; b++) {
     size_t q = off[b];
     cfg[b] = CacheCfg{};
@@ -670,24 +697,68 @@ static int cache_alloc(const uint32_t *F, const uint32_t *d, int n, uint64_t R, 
     cfg[b].ctl = (CacheCtl *)(base + q);
     cfg[b].F = F[b];
     cfg[b].d = d[b];
+    ccfg[b] = ChunkCfg{};
+    if (lmax[b]) {
+      const size_t L = lmax[b];
+      q = coff[b];
+      ccfg[b].at = (uint64_t *)(base + q);
+      ccfg[b].lt = ccfg[b].at + R;
+      ccfg[b].tt = ccfg[b].lt + R;
+      q = up256(q + R * 8 * 3);
+      ccfg[b].S = (uint64_t *)(base + q);
+      q = up256(q + (L + 1) * 8);
+      ccfg[b].bs = (uint64_t *)(base + q);
+      q = up256(q + (L / 1024 + 1) * 8);
+      ccfg[b].seg = (uint32_t *)(base + q);
+      q = up256(q + L * 4);
+      ccfg[b].ctl = (ChunkCtl *)(base + q);
+      ccfg[b].Lmax = lmax[b];
+    }
   }
-  // cache ids grouped: the LDS-resident ones first, then the others
   std::vector<int> ids;
   for (int b = 0; b < n; b++)
     if (F[b] <= CACHE_LDS_MAX) ids.push_back(b);
+  out->n_lds = (int)ids.size();
   for (int b = 0; b < n; b++)
-    if (F[b] > CACHE_LDS_MAX) ids.push_back(b);
+    if (F[b] > CACHE_LDS_MAX && !lmax[b]) ids.push_back(b);
+  out->n_seq = (int)ids.size() - out->n_lds;
+  for (int b = 0; b < n; b++)
+    if (F[b] > CACHE_LDS_MAX && lmax[b]) ids.push_back(b);
+  out->n_chunk = n - out->n_lds - out->n_seq;
   if (hipMemcpy(base + ocfg, cfg.data(), sizeof(CacheCfg) * n, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(base + occfg, ccfg.data(), sizeof(ChunkCfg) * n, hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(base + oids, ids.data(), sizeof(int) * n, hipMemcpyHostToDevice) != hipSuccess ||
       cache_set_lds_limit() != hipSuccess) {
     hipFree(p);
     return HBF_EHIP;
   }
-  *mem = p;
-  *dcfg = (CacheCfg *)(base + ocfg);
-  *status = (int64_t *)(base + ost);
-  *dids = (int *)(base + oids);
+  out->mem = p;
+  out->dcfg = (CacheCfg *)(base + ocfg);
+  out->dccfg = (ChunkCfg *)(base + occfg);
+  out->status = (int64_t *)(base + ost);
+  out->dids = (int *)(base + oids);
   return HBF_OK;
+}
+
+// Serve pages[0..n) on the chunked caches ids[0..n_chunk): chunk after chunk,
+// each solved in parallel and checked, the sequential run for those that
+// fail; then the prefetched pages still pending.  *epoch: the last tag used.
+static bool run_chunks(const CacheCfg *dcfg, const ChunkCfg *dccfg, const int *ids, int n_chunk, uint32_t max_f,
+                       uint32_t max_d, uint64_t R, const uint64_t *pages, int64_t n, uint32_t chunk,
+                       uint32_t *epoch, uint8_t *hit, uint64_t *pf_page, int64_t *pf_src, int64_t pf_cap,
+                       int64_t *status, int64_t *n_pf, hipStream_t s) {
+  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
+    if (*epoch >= 0xFFFFFF00u) {  // tags about to repeat: clear them
+      if (launch_chunk_clear(dccfg, ids, n_chunk, R, s) != hipSuccess) return false;
+      *epoch = 0;
+    }
+    ++*epoch;
+    const int64_t L = n - c0 < (int64_t)chunk ? n - c0 : (int64_t)chunk;
+    if (launch_cache_chunk(dcfg, dccfg, ids, n_chunk, max_f, max_d, R, pages, c0, L, *epoch, hit, pf_page, pf_src,
+                           pf_cap, status, n_pf, s) != hipSuccess)
+      return false;
+  }
+  return launch_cache_pending(dcfg, ids, n_chunk, max_f, status, s) == hipSuccess;
 }
 
 extern "C" {
@@ -699,12 +770,22 @@ int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pa
   c->F = frames;
   c->d = prefetch_pages;
   c->R = range_pages;
-  int rc = cache_alloc(&c->F, &c->d, 1, c->R, &c->mem, &c->dcfg, &c->status, &c->dids);
+  c->lmax = frames > CACHE_LDS_MAX && range_pages <= CHUNK_MAX_R ? CHUNK_MAX : 0;
+  c->chunk = chunk_default(frames, range_pages);
+  CacheAlloc al;
+  int rc = cache_alloc(&c->F, &c->d, &c->lmax, 1, c->R, &al);
   if (rc) {
     delete c;
     return rc;
   }
-  if (launch_cache_clear(c->dcfg, 1, c->R, c->F, nullptr) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+  c->mem = al.mem;
+  c->dcfg = al.dcfg;
+  c->dccfg = c->lmax ? al.dccfg : nullptr;
+  c->status = al.status;
+  c->dids = al.dids;
+  bool ok = launch_cache_clear(c->dcfg, 1, c->R, c->F, nullptr) == hipSuccess;
+  if (ok && c->dccfg) ok = launch_chunk_clear(c->dccfg, c->dids, 1, c->R, nullptr) == hipSuccess;
+  if (!ok || hipDeviceSynchronize() != hipSuccess) {
     hipFree(c->mem);
     delete c;
     return HBF_EHIP;
@@ -725,15 +806,34 @@ int hbf_cache_reset(hbf_cache_t c, void *stream) {
   return launch_cache_clear(c->dcfg, 1, c->R, c->F, (hipStream_t)stream) == hipSuccess ? HBF_OK : HBF_EHIP;
 }
 
+int hbf_cache_set_chunk(hbf_cache_t c, uint32_t accesses) {
+  if (!c || (accesses && (!c->dccfg || accesses > c->lmax))) return HBF_EINVAL;
+  c->chunk = accesses;
+  return HBF_OK;
+}
+
+int hbf_cache_get_chunk(hbf_cache_t c, uint32_t *accesses) {
+  if (!c || !accesses) return HBF_EINVAL;
+  *accesses = c->chunk;
+  return HBF_OK;
+}
+
 int hbf_cache_access(hbf_cache_t c, const uint64_t *pages, int64_t n, uint8_t *hit, uint64_t *pf_page,
                      int64_t *pf_src, int64_t pf_cap, int64_t *counts, void *stream) {
   if (!c || !counts || n < 0 || n > N_LIMIT || (n > 0 && (!pages || !hit))) return HBF_EINVAL;
   if ((pf_page == nullptr) != (pf_src == nullptr) || pf_cap < 0) return HBF_EINVAL;
   const hipStream_t s = (hipStream_t)stream;
   if (launch_fill(c->status, 2, 0, s) != hipSuccess) return HBF_EHIP;
-  if (n > 0 && launch_cache_run(c->dcfg, c->dids, 1, c->F <= CACHE_LDS_MAX, c->F, c->R, pages, n, hit, pf_page,
-                                pf_src, pf_page ? pf_cap : 0, c->status, c->status + 1, s) != hipSuccess)
+  if (n > 0 && c->chunk) {
+    if (launch_cache_check(pages, n, c->R, c->status, s) != hipSuccess ||
+        !run_chunks(c->dcfg, c->dccfg, c->dids, 1, c->F, c->d, c->R, pages, n, c->chunk, &c->epoch, hit, pf_page,
+                    pf_src, pf_page ? pf_cap : 0, c->status, c->status + 1, s))
+      return HBF_EHIP;
+  } else if (n > 0 && launch_cache_run(c->dcfg, c->dids, 1, c->F <= CACHE_LDS_MAX, c->F, c->R, pages, n, hit,
+                                       pf_page, pf_src, pf_page ? pf_cap : 0, c->status, c->status + 1,
+                                       s) != hipSuccess) {
     return HBF_EHIP;
+  }
   return launch_cache_report(c->dcfg, 1, c->status + 1, c->status, counts, 8, s) == hipSuccess ? HBF_OK
                                                                                               : HBF_EHIP;
 }
@@ -742,43 +842,54 @@ int hbf_cache_sweep(const uint32_t *frames, const uint32_t *prefetch, int n_cfg,
                     const uint64_t *pages, int64_t n, int64_t *counts, void *stream) {
   if (!frames || !prefetch || n_cfg < 1 || n_cfg > 65535 || !counts || n < 0 || n > N_LIMIT || (n > 0 && !pages))
     return HBF_EINVAL;
-  uint32_t max_f = 0;
+  uint32_t max_f = 0, chunk = 0;
+  std::vector<uint32_t> lmax(n_cfg, 0);
   for (int b = 0; b < n_cfg; b++) {
     if (!cache_params_ok(frames[b], prefetch[b], range_pages)) return HBF_EINVAL;
     max_f = std::max(max_f, frames[b]);
+    const uint32_t cd = chunk_default(frames[b], range_pages);
+    if (cd) chunk = chunk ? std::min(chunk, cd) : cd;
   }
-  void *mem = nullptr;
-  CacheCfg *dcfg = nullptr;
-  int64_t *status = nullptr;
-  int *dids = nullptr;
-  int rc = cache_alloc(frames, prefetch, n_cfg, range_pages, &mem, &dcfg, &status, &dids);
+  // the chunked caches share one chunk length: the smallest of their defaults
+  for (int b = 0; b < n_cfg; b++)
+    if (chunk_default(frames[b], range_pages)) lmax[b] = chunk;
+  CacheAlloc al;
+  int rc = cache_alloc(frames, prefetch, lmax.data(), n_cfg, range_pages, &al);
   if (rc) return rc;
   const hipStream_t s = (hipStream_t)stream;
-  int n_lds = 0;
-  uint32_t max_lds = 0, max_big = 0;
+  uint32_t max_lds = 0, max_seq = 0, max_chunk = 0, max_dchunk = 0;
   for (int b = 0; b < n_cfg; b++) {
-    if (frames[b] <= CACHE_LDS_MAX) {
-      n_lds++;
-      max_lds = std::max(max_lds, frames[b]);
-    } else {
-      max_big = std::max(max_big, frames[b]);
+    if (frames[b] <= CACHE_LDS_MAX) max_lds = std::max(max_lds, frames[b]);
+    else if (!lmax[b]) max_seq = std::max(max_seq, frames[b]);
+    else {
+      max_chunk = std::max(max_chunk, frames[b]);
+      max_dchunk = std::max(max_dchunk, prefetch[b]);
     }
   }
-  bool ok = launch_fill(status, 2, 0, s) == hipSuccess &&
-            launch_cache_clear(dcfg, n_cfg, range_pages, max_f, s) == hipSuccess;
-  // one launch for the LDS-resident caches, one for the others (both queued)
-  if (ok && n > 0 && n_lds > 0)
-    ok = launch_cache_run(dcfg, dids, n_lds, true, max_lds, range_pages, pages, n, nullptr, nullptr, nullptr, 0,
-                          status, nullptr, s) == hipSuccess;
-  if (ok && n > 0 && n_lds < n_cfg)
-    ok = launch_cache_run(dcfg, dids + n_lds, n_cfg - n_lds, false, max_big, range_pages, pages, n, nullptr, nullptr,
-                          nullptr, 0, status, nullptr, s) == hipSuccess;
-  ok = ok && launch_cache_report(dcfg, n_cfg, nullptr, status, counts, 5, s) == hipSuccess;
+  const int *ids_seq = al.dids + al.n_lds, *ids_chunk = al.dids + al.n_lds + al.n_seq;
+  bool ok = launch_fill(al.status, 2, 0, s) == hipSuccess &&
+            launch_cache_clear(al.dcfg, n_cfg, range_pages, max_f, s) == hipSuccess;
+  if (ok && al.n_chunk) ok = launch_chunk_clear(al.dccfg, ids_chunk, al.n_chunk, range_pages, s) == hipSuccess;
+  // the LDS-resident caches, the sequential device-memory ones, then the
+  // chunked ones (all queued on the stream)
+  if (ok && n > 0 && al.n_lds > 0)
+    ok = launch_cache_run(al.dcfg, al.dids, al.n_lds, true, max_lds, range_pages, pages, n, nullptr, nullptr,
+                          nullptr, 0, al.status, nullptr, s) == hipSuccess;
+  if (ok && n > 0 && al.n_seq > 0)
+    ok = launch_cache_run(al.dcfg, ids_seq, al.n_seq, false, max_seq, range_pages, pages, n, nullptr, nullptr,
+                          nullptr, 0, al.status, nullptr, s) == hipSuccess;
+  if (ok && n > 0 && al.n_chunk > 0) {
+    uint32_t epoch = 0;
+    ok = (al.n_lds + al.n_seq > 0 || launch_cache_check(pages, n, range_pages, al.status, s) == hipSuccess) &&
+         run_chunks(al.dcfg, al.dccfg, ids_chunk, al.n_chunk, max_chunk, max_dchunk, range_pages, pages, n, chunk,
+                    &epoch, nullptr, nullptr, nullptr, 0, al.status, nullptr, s);
+  }
+  ok = ok && launch_cache_report(al.dcfg, n_cfg, nullptr, al.status, counts, 5, s) == hipSuccess;
   // the temporary state is freed once the sweep has run
   ok = hipStreamSynchronize(s) == hipSuccess && ok;
   int64_t st = 0;
-  ok = ok && hipMemcpy(&st, status, 8, hipMemcpyDeviceToHost) == hipSuccess;
-  hipFree(mem);
+  ok = ok && hipMemcpy(&st, al.status, 8, hipMemcpyDeviceToHost) == hipSuccess;
+  hipFree(al.mem);
   if (!ok) return HBF_EHIP;
   return st ? (int)st : HBF_OK;
 }

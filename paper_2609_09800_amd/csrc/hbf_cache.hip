@@ -125,7 +125,8 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
                                                   const uint64_t *__restrict__ pages, int64_t n,
                                                   uint8_t *__restrict__ hit, uint64_t *__restrict__ pf_page,
                                                   int64_t *__restrict__ pf_src, int64_t pf_cap,
-                                                  const int64_t *status, int64_t *n_pf_out) {
+                                                  const int64_t *status, int64_t *n_pf_out,
+                                                  const ChunkCfg *__restrict__ ccfgs, int64_t i_base) {
   __shared__ int64_t s_cand[64 * 64];   // [slot][k]: latest insertion of candidate k of the slot-th start miss
   __shared__ int64_t s_page[64], s_cod[64];
   __shared__ uint32_t s_mlane[64];
@@ -135,14 +136,17 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
   __shared__ uint8_t s_ipf[SNAP_MAX], s_ihit[SNAP_MAX];  // the round's own insertions I_rs + u
   if (ld(status)) return;  // a page outside the range: nothing changes
   const int id = cfg_ids ? cfg_ids[blockIdx.x] : (int)blockIdx.x;
+  if (ccfgs && ld(&ccfgs[id].ctl->valid)) return;  // this chunk was solved in parallel
   const CacheCfg c = cfgs[id];
   const uint32_t lane = lane_no(), d = c.d;
   const int64_t F = c.F;  // >= 64: an insertion offset within one fault (<= 63) is below F
   uint8_t *myhit = hit ? hit + (size_t)id * n : nullptr;
   const bool keep_pf = pf_page && id == 0;
-  int64_t I = c.ctl->ins;
+  // state left by earlier launches: coherent loads, never the scalar cache
+  int64_t I = ld(&c.ctl->ins);
   int64_t Imod = (int64_t)((uint64_t)I % (uint64_t)F);
-  int64_t hits = 0, faults = 0, pfr = 0, npf = 0, unused_l = 0;
+  int64_t hits = 0, faults = 0, pfr = 0, unused_l = 0;
+  int64_t npf = (id == 0 && n_pf_out) ? ld(n_pf_out) : 0;  // prefetch outputs of earlier chunks
 
   if (d == 0) {
     // No prefetch: a fault inserts only its own page, no frame is ever
@@ -191,7 +195,6 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
       c.ctl->count[0] += hits;
       c.ctl->count[1] += faults;
       c.ctl->pend = 0;
-      if (id == 0 && n_pf_out) *n_pf_out = 0;
     }
     return;
   }
@@ -338,7 +341,7 @@ __global__ __launch_bounds__(64) void k_cache_run(const CacheCfg *__restrict__ c
           const int64_t j = npf + (int64_t)off - 1;
           if (j < pf_cap) {
             pf_page[j] = (uint64_t)q;
-            pf_src[j] = im;
+            pf_src[j] = i_base + im;
           }
         }
       }
@@ -733,13 +736,36 @@ hipError_t launch_cache_run(const CacheCfg *dev_cfgs, const int *cfg_ids, int n_
                        cfg_ids, R, pages, n, hit, pf_page, pf_src, pf_cap, status, n_pf_out);
   else {
     hipLaunchKernelGGL(k_cache_run, dim3((uint32_t)n_cfg), dim3(64), 0, s, dev_cfgs, cfg_ids, R, pages, n, hit,
-                       pf_page, pf_src, pf_cap, status, n_pf_out);
+                       pf_page, pf_src, pf_cap, status, n_pf_out, (const ChunkCfg *)nullptr, (int64_t)0);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    uint64_t pb = ((uint64_t)max_f + 255) / 256;
-    if (pb > 256) pb = 256;
-    hipLaunchKernelGGL(k_cache_pending, dim3((uint32_t)pb, (uint32_t)n_cfg), dim3(256), 0, s, dev_cfgs, cfg_ids, status);
+    return launch_cache_pending(dev_cfgs, cfg_ids, n_cfg, max_f, status, s);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_check(const uint64_t *pages, int64_t n, uint64_t R, int64_t *status, hipStream_t s) {
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_cache_check, dim3((uint32_t)blocks), dim3(256), 0, s, pages, n, R, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_pending(const CacheCfg *dev_cfgs, const int *cfg_ids, int n_cfg, uint32_t max_f,
+                                const int64_t *status, hipStream_t s) {
+  uint64_t pb = ((uint64_t)max_f + 255) / 256;
+  if (pb > 256) pb = 256;
+  hipLaunchKernelGGL(k_cache_pending, dim3((uint32_t)pb, (uint32_t)n_cfg), dim3(256), 0, s, dev_cfgs, cfg_ids, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache_seq(const CacheCfg *dev_cfgs, const ChunkCfg *dev_ccfgs, const int *cfg_ids, int n_cfg,
+                            uint64_t R, const uint64_t *pages, int64_t n, int64_t i_base, uint8_t *hit,
+                            uint64_t *pf_page, int64_t *pf_src, int64_t pf_cap, const int64_t *status,
+                            int64_t *n_pf_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_cache_run, dim3((uint32_t)n_cfg), dim3(64), 0, s, dev_cfgs, cfg_ids, R, pages, n, hit,
+                     pf_page, pf_src, pf_cap, status, n_pf_out, dev_ccfgs, i_base);
   return hipGetLastError();
 }
 

@@ -225,6 +225,35 @@ struct CacheCfg {
   uint32_t F, d;
 };
 constexpr int64_t PINS_NEVER = INT64_MIN / 4;
+// Chunked solve of a device-memory cache (hbf_cache_chunk.hip).  Per page
+// (R entries each, tagged with the chunk's epoch in the high 32 bits): the
+// chunk's first access (tag ~epoch, kept by atomicMin), its last access,
+// and, for a page inserted by the chunk, the time of the fault that
+// inserted it (bits 0-23) and its rank among that fault's insertions (bits
+// 24-29).  Per chunk: the per-access insertion/fault counts and their
+// exclusive scan (S, Lmax + 1 entries), the sums per 1,024 accesses and
+// the segment starts.
+struct ChunkCtl {
+  uint32_t nseg, valid;
+  int64_t I0, npf0;  // insertions and prefetch outputs before the chunk
+};
+struct ChunkCfg {
+  uint64_t *at, *lt, *tt;
+  uint64_t *S;
+  uint64_t *bs;
+  uint32_t *seg;
+  ChunkCtl *ctl;
+  uint32_t Lmax;
+};
+constexpr uint32_t CHUNK_MAX = 65536;            // accesses per chunk
+constexpr uint64_t CHUNK_MAX_R = uint64_t(1) << 26;  // range pages with per-page chunk state
+constexpr uint32_t CHUNK_MIN_F = 8192;           // frames from which chunks are the default
+// Default accesses per chunk for F frames (0: sequential only).
+inline uint32_t chunk_default(uint32_t F, uint64_t R) {
+  if (F < CHUNK_MIN_F || R > CHUNK_MAX_R) return 0;
+  uint32_t c = F / 16;
+  return c < 1024 ? 1024 : (c > CHUNK_MAX ? CHUNK_MAX : c);
+}
 constexpr uint32_t CACHE_MAX_PREFETCH = 63;  // one fault's candidates fit one wave
 // Caches of up to this many frames run with their whole state in LDS (a
 // hash of the resident pages); larger ones keep each page's latest
@@ -239,7 +268,26 @@ hipError_t launch_cache_clear(CacheCfg *dev_cfgs, int n_cfg, uint64_t R, uint32_
 hipError_t launch_cache_run(const CacheCfg *dev_cfgs, const int *cfg_ids, int n_cfg, bool lds, uint32_t max_f,
                             uint64_t R, const uint64_t *pages, int64_t n, uint8_t *hit, uint64_t *pf_page,
                             int64_t *pf_src, int64_t pf_cap, int64_t *status, int64_t *n_pf_out, hipStream_t s);
+// The sequential device-memory run alone (no page check, no pending count):
+// caches whose chunk check passed (ccfgs[id].ctl->valid) are skipped; the
+// prefetch outputs continue from *n_pf_out and name access i_base + i.
+hipError_t launch_cache_seq(const CacheCfg *dev_cfgs, const ChunkCfg *dev_ccfgs, const int *cfg_ids, int n_cfg,
+                            uint64_t R, const uint64_t *pages, int64_t n, int64_t i_base, uint8_t *hit,
+                            uint64_t *pf_page, int64_t *pf_src, int64_t pf_cap, const int64_t *status,
+                            int64_t *n_pf_out, hipStream_t s);
 hipError_t cache_set_lds_limit();
+// One chunk pages[c0 .. c0 + L) of the caches ids[0..n_cfg) (all with chunk
+// state, L <= their Lmax): parallel solve, check, commit or undo, then the
+// sequential run for the caches whose check failed.  epoch: nonzero, new
+// for every chunk since the tags were cleared.
+hipError_t launch_cache_chunk(const CacheCfg *dev_cfgs, const ChunkCfg *dev_ccfgs, const int *cfg_ids, int n_cfg,
+                              uint32_t max_f, uint32_t max_d, uint64_t R, const uint64_t *pages, int64_t c0,
+                              int64_t L, uint32_t epoch, uint8_t *hit, uint64_t *pf_page, int64_t *pf_src,
+                              int64_t pf_cap, int64_t *status, int64_t *n_pf, hipStream_t s);
+hipError_t launch_cache_check(const uint64_t *pages, int64_t n, uint64_t R, int64_t *status, hipStream_t s);
+hipError_t launch_cache_pending(const CacheCfg *dev_cfgs, const int *cfg_ids, int n_cfg, uint32_t max_f,
+                                const int64_t *status, hipStream_t s);
+hipError_t launch_chunk_clear(const ChunkCfg *dev_ccfgs, const int *cfg_ids, int n_cfg, uint64_t R, hipStream_t s);
 hipError_t launch_cache_report(const CacheCfg *dev_cfgs, int n_cfg, const int64_t *n_pf, const int64_t *status,
                                int64_t *out, int per_cfg, hipStream_t s);
 

@@ -33,6 +33,7 @@ EXPORTED = [
     "hbf_get_state", "hbf_set_state", "hbf_profile", "hbf_kernel_times", "hbf_strerror",
     "hbf_refresh_plan", "hbf_refresh_configure", "hbf_refresh_submit", "hbf_refresh_drain", "hbf_refresh_pending",
     "hbf_cache_create", "hbf_cache_destroy", "hbf_cache_reset", "hbf_cache_access", "hbf_cache_sweep",
+    "hbf_cache_set_chunk", "hbf_cache_get_chunk",
     "hbf_time_requests_noalloc", "hbf_vmem_configure",
 ]
 HBF_NOALLOC_SCRATCH_BYTES = 64 << 20
@@ -95,6 +96,8 @@ def load_library(path=LIB_PATH):
         "hbf_cache_reset": ([vp, vp], i32),
         "hbf_cache_access": ([vp, vp, i64, vp, vp, vp, i64, vp, vp], i32),
         "hbf_cache_sweep": ([vp, vp, i32, u64, vp, i64, vp, vp], i32),
+        "hbf_cache_set_chunk": ([vp, u32], i32),
+        "hbf_cache_get_chunk": ([vp, ctypes.POINTER(u32)], i32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -378,6 +381,15 @@ class Cache:
 
     def reset(self, stream=None):
         return self._lib.hbf_cache_reset(self._h, _sp(stream))
+
+    def set_chunk(self, accesses):
+        """Accesses served together (0 = one after another); see include/hbf.h."""
+        _check(self._lib.hbf_cache_set_chunk(self._h, int(accesses)), "hbf_cache_set_chunk")
+
+    def chunk(self):
+        x = ctypes.c_uint32()
+        _check(self._lib.hbf_cache_get_chunk(self._h, ctypes.byref(x)), "hbf_cache_get_chunk")
+        return x.value
 
     def access(self, pages, hit, counts, pf_page=None, pf_src=None, stream=None):
         """pages: int64 device tensor [n] (page numbers); hit: uint8 [n];
