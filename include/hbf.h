@@ -364,7 +364,7 @@ typedef struct hbf_cache *hbf_cache_t;  /* opaque, owned by the library */
 /* Create an empty cache (allocates frames*12 bytes of device memory for up
  * to 63 frames, range_pages*8 + frames*2 bytes above; caches of 64 frames
  * or more over at most 2^26 range pages also hold the chunk state below,
- * range_pages*24 bytes and about 1 MiB;
+ * range_pages*24 bytes and about 3.1 MiB;
  * synchronous). */
 int hbf_cache_create(uint32_t frames, uint32_t prefetch_pages, uint64_t range_pages, hbf_cache_t *out);
 void hbf_cache_destroy(hbf_cache_t cache);
@@ -384,7 +384,7 @@ int hbf_cache_access(hbf_cache_t cache, const uint64_t *dev_pages, int64_t n, ui
                      uint64_t *dev_pf_page, int64_t *dev_pf_src, int64_t pf_cap, int64_t *dev_counts,
                      void *stream);
 
-/* Accesses served together (default: frames/16 clamped to [1024, 65536]
+/* Accesses served together (default: frames/16 clamped to [1024, 262144]
  * for caches of 8,192 frames or more with chunk state, else 0).  A call is
  * cut into chunks of that many accesses.  Each chunk is first solved in
  * parallel as if nothing were evicted: an access faults only as the first
@@ -394,7 +394,7 @@ int hbf_cache_access(hbf_cache_t cache, const uint64_t *dev_pages, int64_t n, ui
  * is still within the last `frames` insertions at that moment, which makes
  * it exactly the FIFO answer.  Otherwise the chunk is served one access
  * after another.  The results do not depend on the chunk length.
- * 0 <= accesses <= 65536; a nonzero value needs chunk state (HBF_EINVAL
+ * 0 <= accesses <= 262144; a nonzero value needs chunk state (HBF_EINVAL
  * otherwise).  Host only. */
 int hbf_cache_set_chunk(hbf_cache_t cache, uint32_t accesses);
 int hbf_cache_get_chunk(hbf_cache_t cache, uint32_t *accesses);

@@ -88,6 +88,7 @@ __global__ __launch_bounds__(256) void k_chunk_tag(const CacheCfg *__restrict__ 
     cc.S[L] = 0;
     cc.ctl->nseg = 0;
     cc.ctl->valid = 1;
+    cc.ctl->lost_old = 0;
     cc.ctl->I0 = ldr(&cfgs[id].ctl->ins);
     cfgs[id].ctl->pend = 0;  // recounted once the call's chunks have run
     cc.ctl->npf0 = (id == ids[0] && n_pf) ? ldr(n_pf) : 0;
@@ -139,13 +140,24 @@ struct Walk {
   uint32_t pa;      // previous group: this lane's first-access time
   uint64_t open;    // previous group: faults whose windows reach this group
   uint32_t pcnt;    // previous group: insertions so far of this lane's open fault
+  uint32_t lastA;   // the largest first-access time among the segment's candidates so far
+  bool hasA;
 };
 
 // Resolve the 64 pages at `base`; returns true once the segment has ended.
+//
+// Where the candidates' first-access times increase along the pages (a
+// scan) and at most one fault reaches in from the previous group, every
+// earlier fault within d pages blocks a candidate, so the faults are the
+// greedy choice of candidates more than d pages apart, each page lies in
+// at most one fault's window, and insertion time, rank and per-fault
+// counts follow per lane.  Other groups take the general path: the lowest
+// candidate not blocked by an earlier fault of smaller time is a fault.
 __device__ __forceinline__ bool walk_group(Walk &w, uint64_t base, uint64_t at_c, int64_t pin_c, uint64_t R,
                                            uint32_t d, int64_t lim, const Tags &tg, const ChunkCfg &cc) {
   const uint32_t lane = lane_id();
   const uint64_t lt = (1ull << lane) - 1;
+  const uint64_t le = lane == 63 ? ~0ull : (2ull << lane) - 1;
   const uint64_t r = base + lane;
   const bool inR = r < R;
   const uint32_t a = inR && (at_c & HI) == tg.a ? (uint32_t)at_c : NONE32;
@@ -160,61 +172,112 @@ __device__ __forceinline__ bool walk_group(Walk &w, uint64_t base, uint64_t at_c
   if (segc) w.lastc = base + 63 - (uint64_t)__builtin_clzll(segc);
   const bool in_ext = inR && r <= w.lastc + d;
   const bool last = !(w.lastc + d >= base + 64 && base + 64 < R);
-  // faults: the lowest candidate not blocked by an earlier fault is one
-  uint64_t rem = segc;
-  for (uint64_t m = w.open; m; m &= m - 1) {
-    const uint32_t g = ctz64(m);
-    const uint32_t ag = rdl(w.pa, g);
-    rem &= ~__ballot(lane + 64 - g <= d && ag < a);
-  }
-  uint64_t fm = 0;
-  while (rem) {
-    const uint32_t f = ctz64(rem);
-    fm |= 1ull << f;
-    const uint32_t af = rdl(a, f);
-    rem &= ~(1ull << f);
-    rem &= ~__ballot(lane > f && lane - f <= d && af < a);
-  }
-  // insertion time: the earliest fault whose window holds this page
-  uint32_t tau = NONE32;
-  for (uint64_t m = w.open; m; m &= m - 1) {
-    const uint32_t g = ctz64(m);
-    const uint32_t ag = rdl(w.pa, g);
-    if (lane + 64 - g <= d) tau = ag < tau ? ag : tau;
-  }
-  for (uint64_t m = fm; m; m &= m - 1) {
-    const uint32_t f = ctz64(m);
-    const uint32_t af = rdl(a, f);
-    if (lane >= f && lane - f <= d) tau = af < tau ? af : tau;
-  }
-  const bool ins = in_ext && tau != NONE32 && nonres;
-  uint32_t rank = 0, cnt = 0, ncnt = 0;
-  bool fin_prev = false, fin_cur = false;
-  uint64_t nopen = 0;
-  for (uint64_t m = w.open; m; m &= m - 1) {  // windows that end in this group
-    const uint32_t g = ctz64(m);
-    const uint32_t ag = rdl(w.pa, g);
-    const bool mine = ins && tau == ag;
-    const uint64_t mm = __ballot(mine);
-    const uint32_t c0 = rdl(w.pcnt, g);
-    if (mine) rank = c0 + popc(mm & lt);
-    if (lane == g) {
+  // do the segment's candidates so far have increasing first-access times?
+  const bool sc = (segc >> lane) & 1;
+  const uint64_t sbelow = segc & lt;
+  const uint32_t apl = (uint32_t)__shfl((int)a, sbelow ? 63 - __builtin_clzll(sbelow) : lane);
+  const bool viol = sc && (sbelow ? apl >= a : (w.hasA && w.lastA >= a));
+  const bool mono = !__ballot(viol) && popc(w.open) <= 1;
+
+  uint64_t fm = 0, nopen = 0;
+  uint32_t tau = NONE32, rank = 0, cnt = 0, ncnt = 0;
+  bool fin_prev = false, fin_cur = false, ins = false;
+  if (mono) {
+    uint64_t rem = segc;
+    const uint32_t g = w.open ? ctz64(w.open) : 0;
+    if (w.open) rem &= ~((2ull << (g + d - 64)) - 1);  // lanes within the open fault's window
+    while (rem) {
+      const uint32_t f = ctz64(rem);
+      fm |= 1ull << f;
+      rem = f + d >= 63 ? 0 : rem & ~((2ull << (f + d)) - 1);
+    }
+    const uint64_t fb = fm & le;
+    const uint32_t fs = fb ? 63 - __builtin_clzll(fb) : lane;
+    const uint32_t af = (uint32_t)__shfl((int)a, fs);
+    const bool cov = fb && lane - fs <= d;
+    const uint32_t ag = w.open ? rdl(w.pa, g) : NONE32;
+    const uint32_t c0 = w.open ? rdl(w.pcnt, g) : 0;
+    const bool cov_prev = !cov && w.open && lane + 64 - g <= d;
+    tau = cov ? af : (cov_prev ? ag : NONE32);
+    ins = in_ext && tau != NONE32 && nonres;
+    const uint64_t im = __ballot(ins);
+    rank = cov ? popc(im & lt & ~((1ull << fs) - 1)) : c0 + popc(im & lt);
+    if (w.open && lane == g) {
       fin_prev = true;
-      ncnt = c0 + popc(mm);  // the count of the previous group's fault in this lane
+      ncnt = c0 + popc(im & ((2ull << (g + d - 64)) - 1));
+    }
+    if ((fm >> lane) & 1) {
+      const uint64_t win = (lane + d >= 63 ? ~0ull : (2ull << (lane + d)) - 1) & ~lt;
+      cnt = popc(im & win);
+      fin_cur = lane + d < 64 || last;
+    }
+    nopen = __ballot(((fm >> lane) & 1) && !fin_cur);
+  } else {
+    uint64_t rem = segc;
+    for (uint64_t m = w.open; m; m &= m - 1) {
+      const uint32_t g = ctz64(m);
+      const uint32_t ag = rdl(w.pa, g);
+      rem &= ~__ballot(lane + 64 - g <= d && ag < a);
+    }
+    while (rem) {
+      const uint32_t f = ctz64(rem);
+      fm |= 1ull << f;
+      const uint32_t af = rdl(a, f);
+      rem &= ~(1ull << f);
+      rem &= ~__ballot(lane > f && lane - f <= d && af < a);
+    }
+    // insertion time: the earliest fault whose window holds this page
+    for (uint64_t m = w.open; m; m &= m - 1) {
+      const uint32_t g = ctz64(m);
+      const uint32_t ag = rdl(w.pa, g);
+      if (lane + 64 - g <= d) tau = ag < tau ? ag : tau;
+    }
+    for (uint64_t m = fm; m; m &= m - 1) {
+      const uint32_t f = ctz64(m);
+      const uint32_t af = rdl(a, f);
+      if (lane >= f && lane - f <= d) tau = af < tau ? af : tau;
+    }
+    ins = in_ext && tau != NONE32 && nonres;
+    for (uint64_t m = w.open; m; m &= m - 1) {  // windows that end in this group
+      const uint32_t g = ctz64(m);
+      const uint32_t ag = rdl(w.pa, g);
+      const bool mine = ins && tau == ag;
+      const uint64_t mm = __ballot(mine);
+      const uint32_t c0 = rdl(w.pcnt, g);
+      if (mine) rank = c0 + popc(mm & lt);
+      if (lane == g) {
+        fin_prev = true;
+        ncnt = c0 + popc(mm);  // the count of the previous group's fault in this lane
+      }
+    }
+    for (uint64_t m = fm; m; m &= m - 1) {
+      const uint32_t f = ctz64(m);
+      const uint32_t af = rdl(a, f);
+      const bool mine = ins && tau == af;
+      const uint64_t mm = __ballot(mine);
+      if (mine) rank = popc(mm & lt);
+      if (lane == f) cnt = popc(mm);
+      if (f + d < 64 || last) {
+        if (lane == f) fin_cur = true;
+      } else {
+        nopen |= 1ull << f;
+      }
     }
   }
-  for (uint64_t m = fm; m; m &= m - 1) {
-    const uint32_t f = ctz64(m);
-    const uint32_t af = rdl(a, f);
-    const bool mine = ins && tau == af;
-    const uint64_t mm = __ballot(mine);
-    if (mine) rank = popc(mm & lt);
-    if (lane == f) cnt = popc(mm);
-    if (f + d < 64 || last) {
-      if (lane == f) fin_cur = true;
+  // the largest first-access time among the segment's candidates
+  if (segc) {
+    uint32_t mx = sc ? a : 0;
+    if (mono) {
+      mx = rdl(a, 63 - __builtin_clzll(segc));
     } else {
-      nopen |= 1ull << f;
+      for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t y = (uint32_t)__shfl_xor((int)mx, o);
+        mx = y > mx ? y : mx;
+      }
+      mx = rdl(mx, 0);
     }
+    w.lastA = w.hasA && w.lastA > mx ? w.lastA : mx;
+    w.hasA = true;
   }
   // per-fault counts (packed: insertions << 32 | 1) and the page words
   if (fin_prev) cc.S[w.pa] = ((uint64_t)ncnt << 32) | 1u;
@@ -247,7 +310,7 @@ __global__ __launch_bounds__(256) void k_chunk_walk(const CacheCfg *__restrict__
   auto pin_of = [&](uint64_t base) { return ping[base + lane < R ? base + lane : R - 1]; };
   for (uint32_t si = blockIdx.x * 4 + threadIdx.x / 64; si < nseg; si += gridDim.x * 4) {
     const uint64_t s = ldr(&cc.seg[si]);
-    Walk w{s, NONE32, 0, 0};
+    Walk w{s, NONE32, 0, 0, 0, false};
     // the next four groups in flight
     uint64_t a0 = at_of(s), a1 = at_of(s + 64), a2 = at_of(s + 128), a3 = at_of(s + 192);
     int64_t p0 = pin_of(s), p1 = pin_of(s + 64), p2 = pin_of(s + 128), p3 = pin_of(s + 192);
@@ -290,12 +353,27 @@ __global__ __launch_bounds__(1024) void k_chunk_bsum(const ChunkCfg *__restrict_
   if (threadIdx.x == 0) cc.bs[blockIdx.x] = t;
 }
 
-__global__ __launch_bounds__(1024) void k_chunk_scan(const ChunkCfg *__restrict__ ccs, const int *ids, int64_t L,
-                                                     const int64_t *status) {
+namespace {
+// The page word of r, if the fault at access A inserted it: its rank, else -1.
+__device__ __forceinline__ int owned_rank(uint64_t v, const Tags &tg, uint32_t A) {
+  return (v & (HI | 0xFFFFFFull)) == (tg.t | A) ? (int)((v >> 24) & 63u) : -1;
+}
+}  // namespace
+
+// Second scan pass: each block's exclusive scan offset by the sums before
+// it; then each fault in the block (an access j whose page word names j
+// itself, rank 0) numbers its insertions: I0 + insertions before j + rank.
+__global__ __launch_bounds__(1024) void k_chunk_scan(const CacheCfg *__restrict__ cfgs,
+                                                     const ChunkCfg *__restrict__ ccs, const int *ids,
+                                                     const uint64_t *__restrict__ pages, int64_t L, uint64_t R,
+                                                     uint32_t epoch, const int64_t *status) {
   __shared__ uint64_t part[16];
   __shared__ uint64_t s_pre;
   if (ldr(status)) return;
-  const ChunkCfg cc = ccs[ids[blockIdx.y]];
+  const int id = ids[blockIdx.y];
+  const CacheCfg c = cfgs[id];
+  const ChunkCfg cc = ccs[id];
+  const Tags tg(epoch);
   const uint32_t lane = lane_id(), w = threadIdx.x >> 6;
   if (w == 0) {  // the sums of the blocks before this one
     uint64_t p = 0;
@@ -314,33 +392,13 @@ __global__ __launch_bounds__(1024) void k_chunk_scan(const ChunkCfg *__restrict_
   __syncthreads();
   uint64_t off = s_pre;
   for (uint32_t i = 0; i < w; i++) off += part[i];
-  if (j < L) cc.S[j] = off + x - v;
-  if (j == L - 1) cc.S[L] = off + x;
-}
-
-namespace {
-// The page word of r, if the fault at access A inserted it: its rank, else -1.
-__device__ __forceinline__ int owned_rank(uint64_t v, const Tags &tg, uint32_t A) {
-  return (v & (HI | 0xFFFFFFull)) == (tg.t | A) ? (int)((v >> 24) & 63u) : -1;
-}
-}  // namespace
-
-// Insertion numbers: I0 + insertions before the fault + rank.  A fault is
-// an access j whose page word names j itself (rank 0).
-__global__ __launch_bounds__(256) void k_chunk_assign(const CacheCfg *__restrict__ cfgs,
-                                                      const ChunkCfg *__restrict__ ccs, const int *ids,
-                                                      const uint64_t *__restrict__ pages, int64_t L, uint64_t R,
-                                                      uint32_t epoch, const int64_t *status) {
-  if (ldr(status)) return;
-  const int id = ids[blockIdx.y];
-  const CacheCfg c = cfgs[id];
-  const ChunkCfg cc = ccs[id];
-  const Tags tg(epoch);
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (j >= L) return;
+  const uint64_t sj = off + x - v;
+  cc.S[j] = sj;
+  if (j == L - 1) cc.S[L] = off + x;
+  if (v == 0) return;  // not a fault
   const uint64_t p = pages[j];
-  if (cc.tt[p] != (tg.t | (uint64_t)j)) return;
-  const int64_t x0 = ldr(&cc.ctl->I0) + (int64_t)(cc.S[j] >> 32);
+  const int64_t x0 = ldr(&cc.ctl->I0) + (int64_t)(sj >> 32);
   for (uint32_t k = 0; k <= c.d && p + k < R; k++) {
     const int rk = owned_rank(cc.tt[p + k], tg, (uint32_t)j);
     if (rk >= 0) c.pins[p + k] = x0 + rk;
@@ -348,7 +406,10 @@ __global__ __launch_bounds__(256) void k_chunk_assign(const CacheCfg *__restrict
 }
 
 // The check: every page's last hit, and every prefetch candidate found
-// resident, lies within the last F insertions at that moment.
+// resident, lies within the last F insertions at that moment.  Also, read
+// before anything changes: frames filled before the chunk and evicted
+// within it that hold a prefetched page never hit (a page resident at the
+// start and accessed in the chunk was hit before its eviction).
 __global__ __launch_bounds__(256) void k_chunk_check(const CacheCfg *__restrict__ cfgs,
                                                      const ChunkCfg *__restrict__ ccs, const int *ids,
                                                      const uint64_t *__restrict__ pages, int64_t L, uint64_t R,
@@ -359,59 +420,34 @@ __global__ __launch_bounds__(256) void k_chunk_check(const CacheCfg *__restrict_
   const ChunkCfg cc = ccs[id];
   const Tags tg(epoch);
   const int64_t I0 = ldr(&cc.ctl->I0), F = c.F;
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  bool bad = false;
-  if (j < L) {
-    const uint64_t p = pages[j];
-    const bool fault = cc.tt[p] == (tg.t | (uint64_t)j);
-    if (cc.lt[p] == (tg.t | (uint64_t)j) && !fault)  // the page's last access, a hit
-      bad = c.pins[p] < I0 + (int64_t)(cc.S[j] >> 32) - F;
-    if (fault) {  // the candidates this fault found resident
-      const int64_t at_fault = I0 + (int64_t)(cc.S[j] >> 32) - F;
-      int64_t before = 1;
-      for (uint32_t k = 1; k <= c.d && p + k < R; k++) {
-        const uint64_t q = p + k;
-        if (owned_rank(cc.tt[q], tg, (uint32_t)j) >= 0) {
-          before++;
-        } else if (c.pins[q] < at_fault + before) {
-          bad = true;
-          break;
-        }
-      }
-    }
-  }
-  if (__ballot(bad) && lane_id() == 0) cc.ctl->valid = 0;
-}
-
-// Commit, part 1 (checked chunks only): hit flags; hits on pages resident
-// at the start mark their frame, or, for a frame evicted within the chunk,
-// cancel its count as unused; evictions of frames filled before the chunk
-// that hold a prefetched page never hit.
-__global__ __launch_bounds__(256) void k_chunk_commit1(const CacheCfg *__restrict__ cfgs,
-                                                       const ChunkCfg *__restrict__ ccs, const int *ids,
-                                                       const uint64_t *__restrict__ pages, int64_t L, uint32_t epoch,
-                                                       uint8_t *hit, const int64_t *status) {
-  if (ldr(status)) return;
-  const int id = ids[blockIdx.y];
-  const CacheCfg c = cfgs[id];
-  const ChunkCfg cc = ccs[id];
-  if (!ldr(&cc.ctl->valid)) return;
-  const Tags tg(epoch);
-  const int64_t I0 = ldr(&cc.ctl->I0), F = c.F;
   const int64_t I1 = I0 + (int64_t)(ldr(&cc.S[L]) >> 32);
   const uint32_t nblk_a = (uint32_t)((L + 255) / 256);
+  bool bad = false;
   int64_t lost = 0;
   if (blockIdx.x < nblk_a) {
     const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (j < L) {
       const uint64_t p = pages[j];
-      if (hit) hit[j] = cc.tt[p] == (tg.t | (uint64_t)j) ? 0 : 1;
-      if (cc.at[p] == (tg.a | (uint64_t)j)) {
+      const bool fault = cc.tt[p] == (tg.t | (uint64_t)j);
+      if (cc.lt[p] == (tg.t | (uint64_t)j) && !fault)  // the page's last access, a hit
+        bad = c.pins[p] < I0 + (int64_t)(cc.S[j] >> 32) - F;
+      if (fault) {  // the candidates this fault found resident
+        const int64_t at_fault = I0 + (int64_t)(cc.S[j] >> 32) - F;
+        int64_t before = 1;
+        for (uint32_t k = 1; k <= c.d && p + k < R; k++) {
+          const uint64_t q = p + k;
+          if (owned_rank(cc.tt[q], tg, (uint32_t)j) >= 0) {
+            before++;
+          } else if (c.pins[q] < at_fault + before) {
+            bad = true;
+            break;
+          }
+        }
+      } else if (cc.at[p] == (tg.a | (uint64_t)j)) {
         const int64_t x = c.pins[p];
-        if (x >= I0 - F && x < I0) {
+        if (x >= I0 - F && x < I0 && x < I1 - F) {
           const uint64_t fr = (uint64_t)x % (uint64_t)F;
-          if (x >= I1 - F) c.fhit[fr] = 1;
-          else lost -= (c.fpf[fr] && !c.fhit[fr]) ? 1 : 0;
+          lost -= (c.fpf[fr] && !c.fhit[fr]) ? 1 : 0;
         }
       }
     }
@@ -423,21 +459,25 @@ __global__ __launch_bounds__(256) void k_chunk_commit1(const CacheCfg *__restric
       lost += (c.fpf[fr] && !c.fhit[fr]) ? 1 : 0;
     }
   }
+  if (__ballot(bad) && lane_id() == 0) cc.ctl->valid = 0;
   lost = wave_sum(lost);
-  if (lane_id() == 0 && lost) atomicAdd((unsigned long long *)&c.ctl->count[4], (unsigned long long)lost);
+  if (lane_id() == 0 && lost) atomicAdd((unsigned long long *)&cc.ctl->lost_old, (unsigned long long)lost);
 }
 
-// Commit, part 2, per fault and its pages: frame flags of the insertions
-// still resident, evictions within the chunk of prefetched pages never hit,
-// prefetch outputs and counters -- or, for a chunk that failed its check,
-// undo the insertion numbers so that the sequential run starts from the
-// chunk's initial state (a page not resident at the start stays so).
-__global__ __launch_bounds__(256) void k_chunk_commit2(const CacheCfg *__restrict__ cfgs,
-                                                       const ChunkCfg *__restrict__ ccs, const int *ids,
-                                                       const uint64_t *__restrict__ pages, int64_t c0, int64_t L,
-                                                       uint64_t R, uint32_t epoch, uint64_t *pf_page,
-                                                       int64_t *pf_src, int64_t pf_cap, const int64_t *status,
-                                                       int64_t *n_pf) {
+// Commit, per access (checked chunks): hit flags; a hit on a page resident
+// at the start marks its frame; each fault's insertions still resident set
+// their frame flags, those evicted within the chunk count as unused when
+// prefetched and never hit, prefetch outputs; then the counters.  A chunk
+// that failed its check is undone instead, so that the sequential run
+// starts from the chunk's initial state (a page not resident at the start
+// stays so).  The frames written here are distinct: they hold the last F
+// insertions.
+__global__ __launch_bounds__(256) void k_chunk_commit(const CacheCfg *__restrict__ cfgs,
+                                                      const ChunkCfg *__restrict__ ccs, const int *ids,
+                                                      const uint64_t *__restrict__ pages, int64_t c0, int64_t L,
+                                                      uint64_t R, uint32_t epoch, uint8_t *hit, uint64_t *pf_page,
+                                                      int64_t *pf_src, int64_t pf_cap, const int64_t *status,
+                                                      int64_t *n_pf) {
   if (ldr(status)) return;
   const int id = ids[blockIdx.y];
   const CacheCfg c = cfgs[id];
@@ -451,7 +491,13 @@ __global__ __launch_bounds__(256) void k_chunk_commit2(const CacheCfg *__restric
   int64_t lost = 0;
   if (j < L) {
     const uint64_t p = pages[j];
-    if (cc.tt[p] == (tg.t | (uint64_t)j)) {
+    const bool fault = cc.tt[p] == (tg.t | (uint64_t)j);
+    if (ok && hit) hit[c0 + j] = fault ? 0 : 1;
+    if (ok && !fault && cc.at[p] == (tg.a | (uint64_t)j)) {
+      const int64_t x = c.pins[p];
+      if (x >= I1 - F && x < I0) c.fhit[(uint64_t)x % (uint64_t)F] = 1;
+    }
+    if (fault) {
       const uint64_t sj = cc.S[j];
       const int64_t pf_before = ldr(&cc.ctl->npf0) + (int64_t)(sj >> 32) - (int64_t)(uint32_t)sj;
       for (uint32_t k = 0; k <= c.d && p + k < R; k++) {
@@ -488,6 +534,7 @@ __global__ __launch_bounds__(256) void k_chunk_commit2(const CacheCfg *__restric
     c.ctl->count[0] += L - nf;
     c.ctl->count[1] += nf;
     c.ctl->count[2] += M - nf;
+    atomicAdd((unsigned long long *)&c.ctl->count[4], (unsigned long long)ldr(&cc.ctl->lost_old));
     c.ctl->ins = I1;
     c.ctl->head = (uint32_t)((uint64_t)I1 % (uint64_t)F);
     if (keep_pf && n_pf) *n_pf = ldr(&cc.ctl->npf0) + M - nf;
@@ -525,12 +572,10 @@ hipError_t launch_cache_chunk(const CacheCfg *cfgs, const ChunkCfg *ccs, const i
   hipLaunchKernelGGL(k_chunk_starts, dim3(nb, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, pg, L, epoch, status);
   hipLaunchKernelGGL(k_chunk_walk, dim3(walk, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, R, epoch, status);
   hipLaunchKernelGGL(k_chunk_bsum, dim3(nsb, n_cfg), dim3(1024), 0, s, ccs, ids, L, status);
-  hipLaunchKernelGGL(k_chunk_scan, dim3(nsb, n_cfg), dim3(1024), 0, s, ccs, ids, L, status);
-  hipLaunchKernelGGL(k_chunk_assign, dim3(nb, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, pg, L, R, epoch, status);
-  hipLaunchKernelGGL(k_chunk_check, dim3(nb, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, pg, L, R, epoch, status);
-  hipLaunchKernelGGL(k_chunk_commit1, dim3(nb + nev, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, pg, L, epoch,
-                     hit ? hit + c0 : nullptr, status);
-  hipLaunchKernelGGL(k_chunk_commit2, dim3(nb, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, pg, c0, L, R, epoch,
+  hipLaunchKernelGGL(k_chunk_scan, dim3(nsb, n_cfg), dim3(1024), 0, s, cfgs, ccs, ids, pg, L, R, epoch, status);
+  hipLaunchKernelGGL(k_chunk_check, dim3(nb + nev, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, pg, L, R, epoch,
+                     status);
+  hipLaunchKernelGGL(k_chunk_commit, dim3(nb, n_cfg), dim3(256), 0, s, cfgs, ccs, ids, pg, c0, L, R, epoch, hit,
                      pf_page, pf_src, pf_cap, status, n_pf);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

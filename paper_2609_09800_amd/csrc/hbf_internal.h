@@ -236,6 +236,7 @@ constexpr int64_t PINS_NEVER = INT64_MIN / 4;
 struct ChunkCtl {
   uint32_t nseg, valid;
   int64_t I0, npf0;  // insertions and prefetch outputs before the chunk
+  int64_t lost_old;  // frames filled before the chunk, evicted within it holding a prefetched page never hit
 };
 struct ChunkCfg {
   uint64_t *at, *lt, *tt;
@@ -245,7 +246,7 @@ struct ChunkCfg {
   ChunkCtl *ctl;
   uint32_t Lmax;
 };
-constexpr uint32_t CHUNK_MAX = 65536;            // accesses per chunk
+constexpr uint32_t CHUNK_MAX = 1u << 18;          // accesses per chunk
 constexpr uint64_t CHUNK_MAX_R = uint64_t(1) << 26;  // range pages with per-page chunk state
 constexpr uint32_t CHUNK_MIN_F = 8192;           // frames from which chunks are the default
 // Default accesses per chunk for F frames (0: sequential only).

@@ -110,7 +110,7 @@ def test_chunked_calls_continue(torch):
     run_both(torch, 500, 7, 3000, [s[:10], s[10:11], [], s[11:5000], s[5000:17001], s[17001:]], 999, "continue")
 
 
-@pytest.mark.parametrize("chunk", [0, 1, 50, 4096, 65536])
+@pytest.mark.parametrize("chunk", [0, 1, 50, 4096, 262144])
 def test_chunk_length_does_not_change_results(torch, chunk):
     """One stream, one cache shape, every chunk length: identical hit flags,
     prefetch outputs and counters (the reference model checks each)."""
@@ -182,11 +182,11 @@ def test_chunk_setting_errors(torch):
     big = hbf.Cache(10000, 7, 20000)
     assert big.chunk() == 1024        # frames / 16, at least 1,024
     with pytest.raises(hbf.HbfError):
-        big.set_chunk(65537)
-    big.set_chunk(65536)
+        big.set_chunk(262145)
+    big.set_chunk(262144)
     big.close()
-    huge = hbf.Cache(1 << 20, 7, 1 << 20)
-    assert huge.chunk() == 65536
+    huge = hbf.Cache(1 << 23, 7, 1 << 23)
+    assert huge.chunk() == 262144     # frames / 16, at most 262,144
     huge.close()
 
 
