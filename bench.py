@@ -292,9 +292,11 @@ def capacity_leg(torch, hbf, wl, reps=2):
     8 as a capacity-mode stream through one frame cache holding half of the
     expert set (a step's working set fits, so the second step reuses the
     first), prefetching 7 pages per fault; then a sweep of 42 caches (frame
-    budgets x prefetch depths) over the same stream, one wave each.  The
-    reference model serves the same stream on the host for parity and for
-    comparison."""
+    budgets x prefetch depths) over the same stream.  Caches of 8,192 frames
+    or more are served in chunks solved in parallel and checked on the
+    device (sequential waves for chunks that fail the check); smaller ones,
+    one wave each.  The reference model serves the same stream on the host
+    for parity and for comparison."""
     from oracle import oracle
     pages, R = wl.capacity_stream(steps=2, tokens=8)
     n = int(pages.size)
@@ -303,6 +305,7 @@ def capacity_leg(torch, hbf, wl, reps=2):
     hit = torch.empty(n, dtype=torch.uint8, device="cuda")
     cnt = torch.zeros(8, dtype=torch.int64, device="cuda")
     c = hbf.Cache(F, d, R)
+    chunk = c.chunk()
     s = torch.cuda.current_stream()
     times = []
     for r in range(reps + 1):
@@ -363,7 +366,8 @@ def capacity_leg(torch, hbf, wl, reps=2):
     h, m, pr, used, unused = (int(x) for x in got[:5])
     return dict(workload=f"two config-3 decode steps at batch 8 as a capacity stream: {n} accesses over {R} "
                          f"expert pages, {F} frames (half), prefetch {d} pages per fault",
-                accesses=n, ms_per_call=ms, accesses_per_s=n / (ms / 1e3), hit_share=h / n, faults=m,
+                accesses=n, chunk_accesses=chunk, ms_per_call=ms, accesses_per_s=n / (ms / 1e3),
+                hit_share=h / n, faults=m,
                 prefetch_reads=pr, prefetch_used=used, prefetch_evicted_unused=unused,
                 parity_vs_reference=parity, reference_cpu_s=cpu_s, reference_cores=1,
                 sweep=dict(caches=len(frames), seconds=sweep_s,
