@@ -292,11 +292,11 @@ def capacity_leg(torch, hbf, wl, reps=2):
     8 as a capacity-mode stream through one frame cache holding half of the
     expert set (a step's working set fits, so the second step reuses the
     first), prefetching 7 pages per fault; then a sweep of 42 caches (frame
-    budgets x prefetch depths) over the same stream.  Caches of 8,192 frames
-    or more are served in chunks solved in parallel and checked on the
-    device (sequential waves for chunks that fail the check); smaller ones,
-    one wave each.  The reference model serves the same stream on the host
-    for parity and for comparison."""
+    budgets x prefetch depths) over the same stream, and one of 84 small
+    caches.  Caches of 64 frames or more are served in chunks solved in
+    parallel and checked on the device (sequential waves for chunks that
+    fail the check); smaller ones, one wave each.  The reference model
+    serves the same stream on the host for parity and for comparison."""
     from oracle import oracle
     pages, R = wl.capacity_stream(steps=2, tokens=8)
     n = int(pages.size)

@@ -384,8 +384,8 @@ int hbf_cache_access(hbf_cache_t cache, const uint64_t *dev_pages, int64_t n, ui
                      uint64_t *dev_pf_page, int64_t *dev_pf_src, int64_t pf_cap, int64_t *dev_counts,
                      void *stream);
 
-/* Accesses served together (default: frames/16 clamped to [1024, 262144]
- * for caches of 8,192 frames or more with chunk state, else 0).  A call is
+/* Accesses served together (default: frames/16 clamped to [16384, 262144]
+ * for caches with chunk state, else 0).  A call is
  * cut into chunks of that many accesses.  Each chunk is first solved in
  * parallel as if nothing were evicted: an access faults only as the first
  * access of a page not resident when the chunk began, unless an earlier

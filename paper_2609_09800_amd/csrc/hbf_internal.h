@@ -248,13 +248,8 @@ struct ChunkCfg {
 };
 constexpr uint32_t CHUNK_MAX = 1u << 18;          // accesses per chunk
 constexpr uint64_t CHUNK_MAX_R = uint64_t(1) << 26;  // range pages with per-page chunk state
-constexpr uint32_t CHUNK_MIN_F = 8192;           // frames from which chunks are the default
-// Default accesses per chunk for F frames (0: sequential only).
-inline uint32_t chunk_default(uint32_t F, uint64_t R) {
-  if (F < CHUNK_MIN_F || R > CHUNK_MAX_R) return 0;
-  uint32_t c = F / 16;
-  return c < 1024 ? 1024 : (c > CHUNK_MAX ? CHUNK_MAX : c);
-}
+constexpr uint32_t CHUNK_MIN = 16384;            // default accesses per chunk, at least
+
 constexpr uint32_t CACHE_MAX_PREFETCH = 63;  // one fault's candidates fit one wave
 // Caches of up to this many frames run with their whole state in LDS (a
 // hash of the resident pages); larger ones keep each page's latest
@@ -262,6 +257,15 @@ constexpr uint32_t CACHE_MAX_PREFETCH = 63;  // one fault's candidates fit one w
 // round of 64 accesses without prefetch then never evicts a page it
 // inserted, and one fault's insertion offsets, at most 63, stay below F).
 constexpr uint32_t CACHE_LDS_MAX = 63;
+// Default accesses per chunk for F frames (0: sequential only).  A chunk
+// whose check fails costs its sequential run plus a few launches, so the
+// default is long; F/16 above the minimum keeps a large cache's chunks from
+// turning over its whole window.
+inline uint32_t chunk_default(uint32_t F, uint64_t R) {
+  if (F <= CACHE_LDS_MAX || R > CHUNK_MAX_R) return 0;
+  uint32_t c = F / 16;
+  return c < CHUNK_MIN ? CHUNK_MIN : (c > CHUNK_MAX ? CHUNK_MAX : c);
+}
 hipError_t launch_cache_clear(CacheCfg *dev_cfgs, int n_cfg, uint64_t R, uint32_t max_f, hipStream_t s);
 // cfg_ids: the caches to run (device, n_cfg entries); every one of them has
 // F <= CACHE_LDS_MAX when lds is set, else F > CACHE_LDS_MAX.  max_f: their

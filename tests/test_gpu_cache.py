@@ -6,7 +6,8 @@ prefetch depth + 1) where a fault often evicts one of its own later
 candidates (the in-order replay), the widest prefetch (63 pages), long
 streams spanning many 64-access batches, calls that continue one cache, an
 out-of-range page, and both homes of the cache state (LDS up to 63 frames,
-device memory above).
+device memory above; a device-memory cache runs both its default chunked
+solve and the sequential wave alone).
 """
 import sys
 
@@ -31,9 +32,21 @@ def torch():
 
 
 def run_both(torch, F, d, R, calls, what):
+    """Both device paths of a device-memory cache -- the default (chunks
+    solved in parallel and checked) and the sequential wave alone -- against
+    the reference model; LDS caches have one path."""
+    from paper_2609_09800_amd import hbf
+    run_one(torch, F, d, R, calls, what, None)
+    if F > 63 and R <= (1 << 26):
+        run_one(torch, F, d, R, calls, what + "-sequential", 0)
+
+
+def run_one(torch, F, d, R, calls, what, chunk):
     from oracle import oracle
     from paper_2609_09800_amd import hbf
     g = hbf.Cache(F, d, R)
+    if chunk is not None:
+        g.set_chunk(chunk)
     o = oracle.OracleCache(F, d, R)
     for ci, pages in enumerate(calls):
         pages = np.asarray(pages, dtype=np.int64)

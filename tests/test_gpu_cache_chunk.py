@@ -180,7 +180,7 @@ def test_chunk_setting_errors(torch):
     small.set_chunk(0)
     small.close()
     big = hbf.Cache(10000, 7, 20000)
-    assert big.chunk() == 1024        # frames / 16, at least 1,024
+    assert big.chunk() == 16384       # frames / 16, at least 16,384
     with pytest.raises(hbf.HbfError):
         big.set_chunk(262145)
     big.set_chunk(262144)
