@@ -405,9 +405,12 @@ int hbf_cache_get_chunk(hbf_cache_t cache, uint32_t *accesses);
  * dev_pages[0..n).  dev_counts: int64[n_cfg][5], the five counters of
  * each.  1 <= n_cfg <= 65535.  Caches that have a default chunk length
  * (see hbf_cache_set_chunk) are served chunk by chunk with the smallest of
- * those lengths.  Allocates the caches' state for the call and
- * synchronises `stream` before returning; returns HBF_EINVAL if some page
- * was >= range_pages (counts then all zero). */
+ * those lengths.  Allocates the caches' state for the call (about
+ * range_pages*32 bytes per cache of 64 frames or more over at most 2^26
+ * range pages, range_pages*8 for larger ranges, frames*12 below 64 frames;
+ * HBF_ENOMEM if that does not fit) and synchronises `stream` before
+ * returning; returns HBF_EINVAL if some page was >= range_pages (counts
+ * then all zero). */
 int hbf_cache_sweep(const uint32_t *host_frames, const uint32_t *host_prefetch, int n_cfg, uint64_t range_pages,
                     const uint64_t *dev_pages, int64_t n, int64_t *dev_counts, void *stream);
 
