@@ -354,35 +354,45 @@ __global__ __launch_bounds__(256) void k_gemv_mfma(const uint16_t *__restrict__ 
   }
 }
 
-// The expert shape (K = 2048, N % 32 == 0) at batch 9..16: two 16-row
-// tiles of one expert per workgroup of 8 waves, waves 4h .. 4h+3 on tile h
-// as above.  The activation slices, the same for both tiles, are loaded
-// once per workgroup into LDS (each wave fetching half of its slice's 16
-// steps) and read back in the operand layout: a quarter of the activation
-// traffic of one tile per 4 waves.  Measured 9.3 against 10.9 us per call
-// at batch 16 (one tile per workgroup), 12.0 for the per-page kernel.
-__global__ __launch_bounds__(512) void k_gemv_mfma_pair(const uint16_t *__restrict__ W, int N,
-                                                        const uint16_t *__restrict__ X, int B,
-                                                        float *__restrict__ Y) {
-  constexpr int K = 2048, KQ = K / 4, STEPS = KQ / 32;
+// The expert shape (K = 2048) at batch 9..16: two tiles of one expert per
+// workgroup of 8 waves, waves 4h .. 4h+3 on tile h as above; the second
+// tile holds T1 rows (16, or 8 with its other lanes' weights zero, so that
+// E*N/24 workgroups fill every CU where E*N/32 would leave some idle).
+// The activation slices, the same for both tiles, are loaded once per
+// workgroup into LDS (each wave fetching half of its slice's 16 steps) and
+// read back in the operand layout: a quarter of the activation traffic of
+// one tile per 4 waves.  Measured at batch 16 on 8 x [768 x 2048]: 9.05 us
+// per call with 24 rows per workgroup (256 workgroups), 9.3 with 32 rows
+// (192, before the loads were reordered), 10.9 with one tile per
+// workgroup, 12.0 for the per-page kernel.
+template <int T1>
+__global__ __launch_bounds__(512) void k_gemv_mfma_2t(const uint16_t *__restrict__ W, int N,
+                                                      const uint16_t *__restrict__ X, int B,
+                                                      float *__restrict__ Y) {
+  constexpr int K = 2048, KQ = K / 4, STEPS = KQ / 32, ROWS = 16 + T1;
   __shared__ uint4 xs[4][STEPS][64];  // [slice][step][lane], 64 KiB
   __shared__ f32x4_t red[2][3][64];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int h = w >> 2, wq = w & 3;
-  const int row0 = (blockIdx.x * 2 + h) * 16;
-  const int e = row0 / N, nb = row0 - e * N;  // both tiles lie in expert e (N % 32 == 0)
+  const int base = blockIdx.x * ROWS;
+  const int e = base / N, nb = base - e * N;  // every row lies in expert e (N % ROWS == 0)
   const int col = lane & 15, kg = lane >> 4;
-  const uint16_t *wp = W + (size_t)(row0 + col) * K + wq * KQ + kg * 8;
-  const bool xon = col < B;
-  const uint16_t *xp = X + ((size_t)e * B + (xon ? col : 0)) * K + wq * KQ + kg * 8;
-  uint4 wv[STEPS];
+  const bool won = h == 0 || col < T1;        // a row of this workgroup
+  // Lanes past the tile's rows or the batch load a duplicate row (the same
+  // lines as a neighbouring lane) instead of selecting zeros, so that no
+  // load is waited for before the activations go to LDS; their outputs
+  // (batch b depends on activation row b only) are not stored.
+  const uint16_t *wp = W + (size_t)(base + h * 16 + (won ? col : col - T1)) * K + wq * KQ + kg * 8;
+  const uint16_t *xp = X + ((size_t)e * B + (col < B ? col : B - 1)) * K + wq * KQ + kg * 8;
+  // activation loads first, then the weights, so that both are in flight
+  // when the activations are written to LDS
+  uint4 xv[STEPS / 2], wv[STEPS];
+#pragma unroll
+  for (int i = 0; i < STEPS / 2; i++) xv[i] = *(const uint4 *)(xp + 32 * (h * (STEPS / 2) + i));
 #pragma unroll
   for (int s = 0; s < STEPS; s++) wv[s] = *(const uint4 *)(wp + 32 * s);
 #pragma unroll
-  for (int i = 0; i < STEPS / 2; i++) {
-    const int s = h * (STEPS / 2) + i;
-    xs[wq][s][lane] = xon ? *(const uint4 *)(xp + 32 * s) : make_uint4(0, 0, 0, 0);
-  }
+  for (int i = 0; i < STEPS / 2; i++) xs[wq][h * (STEPS / 2) + i][lane] = xv[i];
   __syncthreads();
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -396,7 +406,7 @@ __global__ __launch_bounds__(512) void k_gemv_mfma_pair(const uint16_t *__restri
 #pragma unroll
     for (int j = 0; j < 4; j++) {
       const int b = 4 * kg + j;
-      if (b < B) Y[((size_t)e * B + b) * N + nb + col] = acc[j];
+      if (b < B && won) Y[((size_t)e * B + b) * N + nb + h * 16 + col] = acc[j];
     }
   }
 }
@@ -522,8 +532,12 @@ hipError_t launch_gemv(const uint16_t *W, int E, int K, int N, int page_bytes, c
   const int R = page_bytes / (2 * K);
   const int64_t pages = (int64_t)E * N / R;
   const bool timed = pi != nullptr;
-  if (!timed && B >= 9 && B <= 16 && K == 2048 && N % 32 == 0) {
-    hipLaunchKernelGGL(k_gemv_mfma_pair, dim3((uint32_t)((int64_t)E * N / 32)), dim3(512), 0, s, W, N, X, B, Y);
+  if (!timed && B >= 9 && B <= 16 && K == 2048 && (N % 32 == 0 || N % 24 == 0)) {
+    // 24 rows per workgroup where 32 would leave CUs idle
+    if (N % 24 == 0 && ((int64_t)E * N / 32 < ncu || N % 32 != 0))
+      hipLaunchKernelGGL(k_gemv_mfma_2t<8>, dim3((uint32_t)((int64_t)E * N / 24)), dim3(512), 0, s, W, N, X, B, Y);
+    else
+      hipLaunchKernelGGL(k_gemv_mfma_2t<16>, dim3((uint32_t)((int64_t)E * N / 32)), dim3(512), 0, s, W, N, X, B, Y);
     return hipGetLastError();
   }
   if (!timed && B >= 9 && B <= 16 && N % 16 == 0 && K % 512 == 0) {

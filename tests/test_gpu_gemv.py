@@ -140,6 +140,7 @@ def test_gemv_without_delays(torch):
     (8, 2048, 768, 1), (8, 2048, 768, 2), (8, 2048, 768, 3), (8, 2048, 768, 4), (8, 2048, 768, 8),
     (8, 2048, 768, 12), (8, 2048, 768, 16), (8, 2048, 768, 17),
     (8, 2048, 768, 9), (2, 512, 64, 3), (1, 4096, 32, 2), (3, 1024, 48, 16), (2, 4096, 80, 7),
+    (2, 2048, 72, 16), (16, 2048, 768, 13),
     (2, 4096, 80, 12), (2, 2048, 48, 16), (2, 2048, 40, 16), (1, 512, 16, 9)])
 def test_gemv_without_delays_shapes(torch, experts, K, N, batch):
     """Calls without delays.  Batches 9..16 take the matrix cores: pairs of
