@@ -355,6 +355,100 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
       if (nq > QB - 64) flush_q();
     }
     if (nout > OUTB - 64) flush_out();
+    // Steady rounds.  If this round served every pending page back to back
+    // and every die re-read at once (its next request issued by then, no
+    // quantum claimed), the next round ranks the dies in the same order:
+    // each next page is ready tR after its predecessor left, and with
+    // P*xfer >= tR + xfer it is ready before the channel reaches it.  So
+    // in round j = 1, 2, ... the page of rank r completes at
+    // cf + ((j-1)*P + r + 1)*xfer, as long as every die's page of that round
+    // was issued by its predecessor's completion and claims nothing.  Each
+    // lane checks its own queue ahead, the shortest run decides, and those
+    // rounds are written at once; the round after them is admitted as usual.
+    const bool steady = v == P && cm == 0 && (int64_t)P * xfer >= tR + xfer && !__ballot(pend && !adm) &&
+                        !__ballot(pend && (cpl != cfree - (int64_t)(P - 1 - r) * xfer || dd != cpl + tR));
+    if (steady) {
+      constexpr uint32_t FB = 16, FMAX = 1024;  // rounds checked per batch, rounds per step
+      const int64_t cf0 = cfree;
+      const uint32_t a0 = admitted;             // the pending page is request a0 - 1 of the queue
+      uint32_t m = FMAX;                        // rounds served now (round 1: the pending pages)
+      for (uint32_t j0 = 2; j0 <= FMAX; j0 += FB) {
+        uint32_t bad = UINT32_MAX;
+        if (pend) {
+          int64_t is[FB];
+#pragma unroll
+          for (uint32_t u = 0; u < FB; u++) {
+            const uint32_t pos = a0 + j0 + u - 2;
+            is[u] = issue_do[pos < total ? base + pos : base];
+          }
+#pragma unroll
+          for (int u = (int)FB - 1; u >= 0; u--) {
+            const uint32_t j = j0 + (uint32_t)u, pos = a0 + j - 2;
+            const bool ok = pos < total && pos >= R && is[u] <= cf0 + ((int64_t)(j - 2) * P + r + 1) * xfer;
+            if (!ok) bad = j;
+          }
+        }
+        const uint32_t fb = ROW ? row0_min32(bad) : wave_min32(bad);
+        if (fb != UINT32_MAX) {
+          m = fb - 1;
+          break;
+        }
+      }
+      if (pend) {
+        for (uint32_t j0 = 1; j0 <= m; j0 += FB) {
+          uint32_t ix[FB];
+#pragma unroll
+          for (uint32_t u = 0; u < FB; u++) {
+            const uint32_t pos = a0 + j0 + u - 2;
+            ix[u] = j0 + u <= m ? ixs[(size_t)(base + pos) * ixstride] : 0;
+          }
+#pragma unroll
+          for (uint32_t u = 0; u < FB; u++)
+            if (j0 + u <= m) complete[ix[u]] = cf0 + ((int64_t)(j0 + u - 1) * P + r + 1) * xfer;
+        }
+      }
+      const int64_t clm = cf0 + ((int64_t)(m - 1) * P + r + 1) * xfer;  // this lane's last completion
+      cfree = cf0 + (int64_t)m * P * xfer;
+      bool cl2 = false;
+      if (pend) {
+        if (clm >= TIME_LIMIT) err |= ERR_OVERFLOW;
+        left -= m;
+        free_at = clm;
+        if (left != 0) {  // admit the page of round m + 1
+          const uint32_t pos = a0 + m - 1;
+          cl2 = pos < R;
+          int64_t s0 = max64(issue_do[base + pos], clm);
+          if (cl2) s0 += tQ;
+          dd = s0 + tR;
+          pidx = ixs[(size_t)(base + pos) * ixstride];
+          admitted = pos + 1;
+          if (dd >= TIME_LIMIT) err |= ERR_OVERFLOW;
+        }
+      }
+      const uint64_t cm2 = __ballot(cl2);
+      if (cm2) {
+        if (cl2) {
+          const uint32_t slot = nq + (uint32_t)__popcll(cm2 & ((1ull << lane) - 1));
+          q_die[slot] = k;
+          q_rank[slot] = admitted - 1;
+          q_val[slot] = dd - tR;
+        }
+        nq += (uint32_t)__popcll(cm2);
+        if (nq > QB - 64) flush_q();
+      }
+      // the ring restarts after the requests admitted here
+      if (pend && loaded < admitted) {
+        loaded = admitted;
+        fetch();
+      }
+      top_up();
+      if (pend && left != 0 && admitted < total) {
+        const uint32_t sl = lane * RSTRIDE + admitted % RING;
+        nx_iss = ring_iss[sl];
+        nx_idx = ring_idx[sl];
+      }
+      continue;
+    }
     // each die's next request must be in its ring before the next round
     if (__ballot(on && admitted < total && loaded - admitted < 2)) top_up();
     if (adm && admitted < total) {
