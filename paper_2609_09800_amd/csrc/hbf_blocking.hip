@@ -368,44 +368,51 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
     const bool steady = v == P && cm == 0 && (int64_t)P * xfer >= tR + xfer && !__ballot(pend && !adm) &&
                         !__ballot(pend && (cpl != cfree - (int64_t)(P - 1 - r) * xfer || dd != cpl + tR));
     if (steady) {
-      constexpr uint32_t FB = 16, FMAX = 1024;  // rounds checked per batch, rounds per step
+      constexpr uint32_t FL = 16, FMAX = 4096;  // rounds per lane per batch, rounds per step
       const int64_t cf0 = cfree;
       const uint32_t a0 = admitted;             // the pending page is request a0 - 1 of the queue
-      uint32_t m = FMAX;                        // rounds served now (round 1: the pending pages)
-      for (uint32_t j0 = 2; j0 <= FMAX; j0 += FB) {
+      // Every lane works here: lane l takes die queue l mod Dp (Dp: Dk
+      // rounded up to a power of two) and every S-th round (S = 64 / Dp),
+      // so a batch covers S*FL rounds.  Per batch: load each round's request
+      // (issue time, index), find the first round some die cannot keep,
+      // write the rounds before it.
+      const uint32_t lgD = Dk <= 16 ? 4u : Dk <= 32 ? 5u : 6u, S = 64u >> lgD;
+      const uint32_t dl = lane & ((1u << lgD) - 1), sub = lane >> lgD;
+      const bool pd = __shfl((int)(pend ? 1 : 0), (int)dl) != 0;
+      const uint32_t a0d = (uint32_t)__shfl((int)a0, (int)dl), rd = (uint32_t)__shfl((int)r, (int)dl);
+      const uint32_t td = (uint32_t)__shfl((int)total, (int)dl), Rd = (uint32_t)__shfl((int)R, (int)dl);
+      const uint32_t bd = (uint32_t)__shfl((int)base, (int)dl);
+      uint32_t m = 0;                           // rounds written (round 1: the pending pages)
+      for (uint32_t j0 = 1;; j0 += S * FL) {
         uint32_t bad = UINT32_MAX;
-        if (pend) {
-          int64_t is[FB];
+        int64_t is[FL];
+        uint32_t ix[FL];
+        if (pd) {
 #pragma unroll
-          for (uint32_t u = 0; u < FB; u++) {
-            const uint32_t pos = a0 + j0 + u - 2;
-            is[u] = issue_do[pos < total ? base + pos : base];
+          for (uint32_t u = 0; u < FL; u++) {
+            const uint32_t pos = a0d + j0 + sub + S * u - 2, at = pos < td ? bd + pos : bd;
+            is[u] = issue_do[at];
+            ix[u] = ixs[(size_t)at * ixstride];
           }
 #pragma unroll
-          for (int u = (int)FB - 1; u >= 0; u--) {
-            const uint32_t j = j0 + (uint32_t)u, pos = a0 + j - 2;
-            const bool ok = pos < total && pos >= R && is[u] <= cf0 + ((int64_t)(j - 2) * P + r + 1) * xfer;
+          for (int u = (int)FL - 1; u >= 0; u--) {
+            const uint32_t j = j0 + sub + S * (uint32_t)u, pos = a0d + j - 2;
+            const bool ok = j == 1 || (pos < td && pos >= Rd &&
+                                       is[u] <= cf0 + ((int64_t)(j - 2) * P + rd + 1) * xfer);
             if (!ok) bad = j;
           }
         }
-        const uint32_t fb = ROW ? row0_min32(bad) : wave_min32(bad);
-        if (fb != UINT32_MAX) {
-          m = fb - 1;
-          break;
-        }
-      }
-      if (pend) {
-        for (uint32_t j0 = 1; j0 <= m; j0 += FB) {
-          uint32_t ix[FB];
+        const uint32_t fb = wave_min32(bad);
+        const uint32_t upto = fb == UINT32_MAX ? j0 + S * FL - 1 : fb - 1;
+        if (pd) {
 #pragma unroll
-          for (uint32_t u = 0; u < FB; u++) {
-            const uint32_t pos = a0 + j0 + u - 2;
-            ix[u] = j0 + u <= m ? ixs[(size_t)(base + pos) * ixstride] : 0;
+          for (uint32_t u = 0; u < FL; u++) {
+            const uint32_t j = j0 + sub + S * u;
+            if (j <= upto) complete[ix[u]] = cf0 + ((int64_t)(j - 1) * P + rd + 1) * xfer;
           }
-#pragma unroll
-          for (uint32_t u = 0; u < FB; u++)
-            if (j0 + u <= m) complete[ix[u]] = cf0 + ((int64_t)(j0 + u - 1) * P + r + 1) * xfer;
         }
+        m = upto;
+        if (fb != UINT32_MAX || m >= FMAX) break;
       }
       const int64_t clm = cf0 + ((int64_t)(m - 1) * P + r + 1) * xfer;  // this lane's last completion
       cfree = cf0 + (int64_t)m * P * xfer;
