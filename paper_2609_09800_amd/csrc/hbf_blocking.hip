@@ -87,22 +87,6 @@ __device__ __forceinline__ uint32_t wave_min32(uint32_t x) {
 
 }  // namespace
 
-// Issue times in die order, so that each die queue's requests are two
-// contiguous runs (indices, issue times) for the sequential stage.
-__global__ __launch_bounds__(256) void k_regblock_gather(const uint64_t *__restrict__ DDw,
-                                                         const uint32_t *__restrict__ IX,
-                                                         const int64_t *__restrict__ issue,
-                                                         int64_t *__restrict__ issue_do, int64_t n,
-                                                         const CallCtl *ctl) {
-  if (__hip_atomic_load(&ctl->err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
-  const bool narrow = ctl->shift <= 32;
-  const int64_t m = ctl->n_in;
-  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < m && p < n; p += (int64_t)gridDim.x * 256) {
-    const uint32_t ix = narrow ? (uint32_t)DDw[p] : IX[p];
-    issue_do[p] = issue[ix];
-  }
-}
-
 // Per lane, the die queue's upcoming requests (index, issue time) wait in an
 // LDS ring of RING entries.  The next CHUNK_R of them are always in flight
 // in registers: a top-up writes them to the ring and starts loading the
@@ -478,16 +462,9 @@ __global__ __launch_bounds__(64) void k_regblock(const uint64_t *__restrict__ DD
   }
 }
 
-hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue,
-                           int64_t *issue_do, int64_t n, const uint32_t *seg_start, const uint32_t *totals,
-                           DevState *st, CallCtl *ctl, int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref,
-                           hipStream_t s) {
-  int64_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_regblock_gather, dim3((uint32_t)blocks), dim3(256), 0, s, DDw, IX, issue, issue_do, n, ctl);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue_do,
+                           const uint32_t *seg_start, const uint32_t *totals, DevState *st, CallCtl *ctl,
+                           int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref, hipStream_t s) {
   hipLaunchKernelGGL(g.Dk <= 16 ? k_regblock<true> : k_regblock<false>, dim3(g.C), dim3(64), 0, s, DDw, IX,
                      issue_do, seg_start, totals, g, st, ctl, complete, dfnew, cfnew, ref ? 1 : 0);
   return hipGetLastError();

@@ -154,10 +154,9 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
                                 int64_t *complete, hipStream_t s, hipEvent_t *ev, int n_ev,
                                 bool refresh);
 // Register-blocking channel stage (hbf_blocking.hip): one wave per channel.
-hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue,
-                           int64_t *issue_do, int64_t n, const uint32_t *seg_start, const uint32_t *totals,
-                           DevState *st, CallCtl *ctl, int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref,
-                           hipStream_t s);
+hipError_t launch_regblock(const Geo &g, const uint64_t *DDw, const uint32_t *IX, const int64_t *issue_do,
+                           const uint32_t *seg_start, const uint32_t *totals, DevState *st, CallCtl *ctl,
+                           int64_t *complete, int64_t *dfnew, int64_t *cfnew, bool ref, hipStream_t s);
 // Calibrated vmem curve (hbf_vmem.hip): the whole timing call on the vmem
 // route (classification, burst lengths, route clock, complete[]).
 constexpr int VM_THREADS = 256;

@@ -456,7 +456,7 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
     int64_t tile_elems, const int64_t *__restrict__ tin_L, const uint32_t *__restrict__ tin_base,
     const uint32_t *__restrict__ seg_start, const uint32_t *__restrict__ totals,
     int64_t *__restrict__ DD, uint32_t *__restrict__ IX, uint32_t *__restrict__ LB, uint32_t gmax,
-    CallCtl *ctl, const DevState *st, uint64_t *__restrict__ WST) {
+    CallCtl *ctl, const DevState *st, uint64_t *__restrict__ WST, int64_t *__restrict__ ISS) {
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ SegMax shseg[SWAVES];
   __shared__ uint32_t shsum[SWAVES];
@@ -578,6 +578,10 @@ __global__ __launch_bounds__(SBLK) void k_die_scatter(
         sval[P] = v;
         skr[P] = k << 16 | rc;
         sloc[P] = (uint16_t)(e * SBLK + threadIdx.x);
+        if (ISS) {  // register blocking: the issue times in die order as well
+          const uint32_t gp = KW[k].pbase + rc;
+          if (gp < n) ISS[gp] = iss[e];
+        }
       }
     }
     __syncthreads();
@@ -1767,15 +1771,15 @@ hipError_t launch_time_requests(const Geo &g, const RangeTable &rt, const Layout
                                : (two ? k_die_scatter<false, 2> : k_die_scatter<false, 1>),
                        dim3(Lo.nt), dim3(SBLK), lds, s,
                        issue, KR, Lo.n, g, Lo.tile_elems, tin_L, tin_base, seg, totals, DD, IX, LB, Lo.gmax, ctl,
-                       st, WST);
+                       st, WST, g.reg_block ? (int64_t *)(ws + Lo.off_iss) : (int64_t *)nullptr);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   mark();
   if (g.reg_block) {
     // media variant: the channel stage simulated per channel in service
     // order (timed in the first channel-stage slot)
-    if ((e = launch_regblock(g, (const uint64_t *)DD, IX, issue, (int64_t *)(ws + Lo.off_iss), Lo.n, seg, totals,
-                             st, ctl, complete, dfnew, cfnew, refresh, s)) != hipSuccess)
+    if ((e = launch_regblock(g, (const uint64_t *)DD, IX, (const int64_t *)(ws + Lo.off_iss), seg, totals, st, ctl,
+                             complete, dfnew, cfnew, refresh, s)) != hipSuccess)
       return e;
     mark();
     mark();
