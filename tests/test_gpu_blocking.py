@@ -187,3 +187,31 @@ def test_large_mixed_stream_blocking_digest(torch):
     d, ch = g.get_state()
     assert sha(d) == gold["die_free_sha256"] and sha(ch) == gold["chan_free_sha256"]
     g.close()
+
+
+@pytest.mark.parametrize("geo", [(2, 4, 1, 0), (2, 16, 2, 1), (1, 16, 4, 1), (3, 5, 3, 0)])
+def test_steady_stretches_break_anywhere(torch, geo):
+    """Heavily backlogged channels, where rounds repeat in closed form, with
+    stretches that end at many different rounds: issue times rise in steps,
+    some shorter than the backlog and some long enough for dies to go idle;
+    a third of the requests sit on a few dies, so queues run dry at
+    different times; a second call continues from the clocks left behind.
+    Die queues per channel 4, 32, 64 and 15 take 4, 2, 1 and 4 rounds per
+    lane in a steady batch."""
+    C, D, Pn, pp = geo
+    params = wl.geometry(C, D, Pn, flags=BLOCK | pp)
+    pages = C * D * Pn * 256
+    g, o = pair(params, [(wl.RANGE_BASE, pages * wl.PAGE)])
+    rng = np.random.default_rng(400 + 10 * C + D)
+    for call in range(2):
+        n = 40000
+        pg = rng.integers(0, pages, n)
+        hot = rng.random(n) < 0.3
+        pg[hot] = rng.integers(0, 2 * C, int(hot.sum()))
+        steps = np.zeros(n, dtype=np.int64)
+        at = np.sort(rng.choice(np.arange(1, n), 12, replace=False))
+        steps[at] = rng.choice([1_000, 50_000, 2_000_000, 20_000_000], at.size)
+        t0 = 0 if call == 0 else 400_000_000
+        issue = t0 + np.cumsum(steps)
+        addr = (np.uint64(wl.RANGE_BASE) + pg.astype(np.uint64) * np.uint64(wl.PAGE))
+        check_call(torch, g, o, addr, issue, f"steady stretches {geo} call {call}")

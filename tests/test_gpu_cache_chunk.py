@@ -230,3 +230,19 @@ def test_moe_capacity_stream_full_size(torch, frac, d):
     assert np.array_equal(hit.cpu().numpy(), wh)
     assert np.array_equal(cnt.cpu().numpy()[:5], o.counts())
     g.close()
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_random_chunked_caches(torch, seed):
+    """Random cache shapes, depths, chunk lengths and stream mixes, split
+    over three calls at random points."""
+    rng = np.random.default_rng(1000 + seed)
+    kind = ["uniform", "runs", "cycles", "descending", "hot"][seed % 5]
+    F = int(rng.integers(64, 3000))
+    d = int(rng.integers(0, min(63, F - 1) + 1))
+    R = int(rng.integers(max(F // 2, 70), 9000))
+    n = int(rng.integers(2000, 30000))
+    chunk = int(rng.integers(1, 6000))
+    s = np.asarray(streams(rng, kind, n, R), dtype=np.int64)
+    cuts = np.sort(rng.integers(0, n, 2))
+    run_both(torch, F, d, R, [s[:cuts[0]], s[cuts[0]:cuts[1]], s[cuts[1]:]], chunk, f"random{seed}-{kind}")
